@@ -1,0 +1,26 @@
+"""Compile the fp64 CPU oracle (oracle.c) into liboracle.so with gcc.
+
+Test infrastructure: only the tests, the smoke check and the benchmark's
+CPU-baseline leg load the result.  Generic x86-64 code (no -march=native),
+so the library built here also runs on another host.
+"""
+import os
+import subprocess
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+
+def build(verbose: bool = False) -> str:
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+           SRC, "-o", LIB + ".tmp", "-lm"]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

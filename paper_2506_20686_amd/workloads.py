@@ -1,0 +1,112 @@
+"""Seeded synthetic workloads for triangle attention.
+
+This module only draws random numbers and builds masks; it holds none of the
+method's arithmetic.  The GPU tests, the benchmark and the oracle tests all
+take their inputs from here, so both sides see bit-identical values.
+
+Recipe (the same for every workload): one CPU generator seeded with `seed`;
+tensors drawn in the order Q, K, V, G, B, dO as float32 standard normals
+scaled by their standard deviation, then rounded to the compute dtype (round
+to nearest even).  Randomness a workload needs beyond that (a random padding
+length) is drawn from the same generator afterwards.
+
+Masks are key masks: a padded token t (t >= n - n_pad) is never attended to
+as a key.  For the starting node the key index is the second pair axis
+(mask[a][b] = m[b]); for the ending node it is the first (mask[a][b] = m[a]).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional
+
+import torch
+
+STARTING, ENDING = 0, 1
+NODE_NAMES = {STARTING: "starting", ENDING: "ending"}
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    n: int
+    h: int
+    d: int
+    dtype: torch.dtype
+    nodes: tuple
+    bias_std: float = 1.0
+    pad_frac: float = 0.0        # fixed key padding: floor(pad_frac * n) tokens
+    rand_pad_frac: float = 0.0   # random key padding: Uniform{0..floor(rand_pad_frac * n)}
+    seed: int = 0
+
+    @property
+    def flops_fwd_bwd(self) -> float:
+        """Nominal fwd+bwd flop: 4 N^3 H d forward (Q K^T, P V) plus
+        10 N^3 H d backward (S recompute, dV, dP, dK, dQ)."""
+        return 14.0 * self.n ** 3 * self.h * self.d
+
+
+# Triangle-attention shapes of AF3 pair stacks: H = 4 heads of d = 32.
+WORKLOADS = {
+    "tri_start_fp32_n32": Workload("tri_start_fp32_n32", 32, 4, 32, torch.float32, (STARTING,)),
+    "tri_start_bf16_n256_pad10": Workload("tri_start_bf16_n256_pad10", 256, 4, 32, torch.bfloat16,
+                                          (STARTING,), pad_frac=0.10),
+    "tri_end_bf16_n384_randpad15": Workload("tri_end_bf16_n384_randpad15", 384, 4, 32,
+                                            torch.bfloat16, (ENDING,), rand_pad_frac=0.15),
+    "tri_bf16_n768": Workload("tri_bf16_n768", 768, 4, 32, torch.bfloat16, (STARTING, ENDING),
+                              bias_std=math.sqrt(2.0)),
+    "tri_start_bf16_n1536_pad5": Workload("tri_start_bf16_n1536_pad5", 1536, 4, 32, torch.bfloat16,
+                                          (STARTING,), pad_frac=0.05),
+}
+HEADLINE = "tri_bf16_n768"
+
+
+def key_mask(n: int, n_pad: int, node: int) -> torch.Tensor:
+    """[n, n] uint8 mask that excludes the last n_pad tokens as keys."""
+    m = (torch.arange(n) < n - n_pad).to(torch.uint8)
+    if node == STARTING:
+        return m[None, :].expand(n, n).contiguous()
+    return m[:, None].expand(n, n).contiguous()
+
+
+def pair_mask(n: int, n_pad: int) -> torch.Tensor:
+    """Token-pair mask m[a] * m[b]: padded rows then have no valid key."""
+    m = (torch.arange(n) < n - n_pad).to(torch.uint8)
+    return (m[:, None] * m[None, :]).contiguous()
+
+
+def random_mask(n: int, p_valid: float, gen: torch.Generator) -> torch.Tensor:
+    return (torch.rand((n, n), generator=gen) < p_valid).to(torch.uint8)
+
+
+def make_inputs(n: int, h: int, d: int, dtype: torch.dtype, seed: int = 0,
+                bias_std: float = 1.0, std: float = 1.0):
+    """Q, K, V, G [n,n,h,d], B [n,n,h], dO [n,n,h,d] on the CPU, plus the
+    generator (positioned after dO) for any further draws."""
+    gen = torch.Generator("cpu").manual_seed(seed)
+
+    def draw(shape, s):
+        return (torch.randn(shape, generator=gen, dtype=torch.float32) * s).to(dtype)
+
+    q = draw((n, n, h, d), std)
+    k = draw((n, n, h, d), std)
+    v = draw((n, n, h, d), std)
+    g = draw((n, n, h, d), std)
+    b = draw((n, n, h), bias_std)
+    do = draw((n, n, h, d), std)
+    return dict(q=q, k=k, v=v, g=g, bias=b, dout=do), gen
+
+
+def workload_inputs(w: Workload, node: Optional[int] = None):
+    """Inputs of a named workload for one node variant: a dict with q, k, v,
+    g, bias, dout, mask (uint8 [n,n]) and n_pad."""
+    node = w.nodes[0] if node is None else node
+    t, gen = make_inputs(w.n, w.h, w.d, w.dtype, w.seed, w.bias_std)
+    n_pad = int(math.floor(w.pad_frac * w.n))
+    if w.rand_pad_frac > 0:
+        hi = int(math.floor(w.rand_pad_frac * w.n))
+        n_pad = int(torch.randint(0, hi + 1, (1,), generator=gen).item())
+    t["mask"] = key_mask(w.n, n_pad, node)
+    t["n_pad"] = n_pad
+    t["node"] = node
+    return t
