@@ -1,0 +1,104 @@
+/*
+ * triattn: triangle self-attention (starting and ending node) for MI355X.
+ *
+ * The operation is MegaFold's memory-efficient 3D attention (arXiv
+ * 2506.20686, Section IV-A; forward and backward definitions in the appendix
+ * table "EvoAttention's forward and backward passes"), extended with the
+ * AF3 sigmoid gate.  For every pair (a, b) of an N x N pair map and head h:
+ *
+ *   starting node, row r = a, query q = b, keys k:
+ *     s_k = scale * <Q[r][q][h], K[r][k][h]> + bias[q][k][h],  valid iff mask[r][k]
+ *     out[r][q][h] = sigmoid(G[r][q][h]) * sum_k softmax(s)_k V[r][k][h]
+ *   ending node, row j = b, query i = a, keys k:
+ *     s_k = scale * <Q[i][j][h], K[k][j][h]> + bias[k][i][h],  valid iff mask[k][j]
+ *     out[i][j][h] = sigmoid(G[i][j][h]) * sum_k softmax(s)_k V[k][j][h]
+ *
+ * The softmax over keys is streamed (online max and sum) and the N^3 H logit
+ * tensor never exists in memory (Section IV-A); the forward saves one fp32
+ * log-sum-exp per (pair, head) for the backward pass, which recomputes the
+ * probabilities from it.  The bias gradient is a sum over the pair-row axis
+ * (appendix table); it is reduced in a fixed order, so results are bitwise
+ * reproducible (the paper's atomics are not).
+ *
+ * Conventions shared by every entry point
+ *   - All tensor pointers are DEVICE memory owned by the caller, C-contiguous
+ *     with the last index fastest:
+ *       q, k, v, g, out, dout, dq, dk, dv, dg : [n][n][h][d]   (dtype)
+ *       bias, dbias                             : [n][n][h]      (dtype)
+ *       lse                                     : [n][n][h]      (fp32)
+ *       mask                                    : [n][n]         (uint8, 0 = masked)
+ *     Tensor pointers must be 16-byte aligned.  mask may be NULL (all valid).
+ *   - A masked key gets weight exactly 0.  A query with no valid key gets
+ *     out = 0, lse = -inf and contributes nothing to any gradient.
+ *   - dtype TRIATTN_BF16: bfloat16 tensors, fp32 accumulation, outputs
+ *     rounded to nearest even.  TRIATTN_F32: fp32 throughout.
+ *   - d must be 32.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
+ *     positive (1/sqrt(d) is the usual choice).
+ *   - The library never allocates or frees memory and never synchronises:
+ *     work is enqueued on `stream` (a hipStream_t; NULL is the default stream)
+ *     and the caller supplies a device workspace of at least the size the
+ *     matching *_workspace_bytes call reports.  Outputs are fully
+ *     overwritten.  Calls that share a workspace must not overlap.
+ *   - Errors: every function returns a triattn_status.  Arguments are checked
+ *     before any HIP call is made, so an invalid call has no effect.  A HIP
+ *     launch failure returns TRIATTN_ERR_HIP.  Nothing aborts.
+ *   - Determinism: the same arguments on the same device give bitwise
+ *     identical results.
+ */
+#ifndef TRIATTN_H
+#define TRIATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TRIATTN_OK = 0,
+  TRIATTN_ERR_INVALID_ARG = 1, /* null pointer, bad enum, size or scale out of range */
+  TRIATTN_ERR_UNSUPPORTED = 2, /* a value the library does not implement (d != 32) */
+  TRIATTN_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  TRIATTN_ERR_HIP = 4          /* a HIP launch reported an error */
+} triattn_status;
+
+typedef enum { TRIATTN_STARTING = 0, TRIATTN_ENDING = 1 } triattn_node;
+typedef enum { TRIATTN_F32 = 0, TRIATTN_BF16 = 1 } triattn_dtype;
+
+/* Bytes of device workspace tri_attn_fwd needs for these sizes, written to
+ * *bytes.  Pure host arithmetic. */
+int tri_attn_fwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
+                                 size_t* bytes);
+
+/* Forward pass (Section IV-A: online-softmax streaming over key tiles,
+ * log-sum-exp saved).  Writes out [n][n][h][d] (dtype, gated) and lse
+ * [n][n][h] (fp32, natural log; -inf for a query with no valid key). */
+int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                 const void* q, const void* k, const void* v, const void* g, const void* bias,
+                 const uint8_t* mask, void* out, float* lse, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace tri_attn_bwd needs for these sizes. */
+int tri_attn_bwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
+                                 size_t* bytes);
+
+/* Backward pass of L = sum(dout * out) (appendix backward listing and
+ * table: D = rowsum(dO * O), dS = P (dP - D), dK/dV stage, dQ stage, bias
+ * gradient summed over rows in fixed order).  Takes the forward's inputs,
+ * its out and lse, and dout; writes dq, dk, dv, dg [n][n][h][d] and dbias
+ * [n][n][h], all in dtype.  The mask and scale get no gradient. */
+int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                 const void* q, const void* k, const void* v, const void* g, const void* bias,
+                 const uint8_t* mask, const void* out, const float* lse, const void* dout,
+                 void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
+                 size_t workspace_bytes, void* stream);
+
+/* Static, human-readable name of a status code ("unknown status" otherwise). */
+const char* tri_attn_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRIATTN_H */

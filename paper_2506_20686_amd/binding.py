@@ -1,0 +1,199 @@
+"""Python binding of libtriattn.so (ctypes).
+
+The functions named like the C entry points pass raw pointers through; the
+convenience wrappers fwd() / bwd() check torch tensors (device, dtype, shape,
+contiguity), allocate outputs and workspace with torch and call the library
+on torch's current stream.  All arithmetic happens in the library's HIP
+kernels; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtriattn.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
+STARTING, ENDING = 0, 1
+F32, BF16 = 0, 1
+HEAD_DIM = 32
+
+_LIB = None
+_vp, _i64, _f, _int, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_int, ctypes.c_size_t
+
+
+class TriAttnError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {tri_attn_status_string(status)} (status {status})")
+
+
+def lib():
+    """Load libtriattn.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2506_20686_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        L.tri_attn_fwd_workspace_bytes.argtypes = [_int, _int, _i64, _i64, _i64,
+                                                   ctypes.POINTER(_sz)]
+        L.tri_attn_bwd_workspace_bytes.argtypes = L.tri_attn_fwd_workspace_bytes.argtypes
+        L.tri_attn_fwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
+        L.tri_attn_bwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz, _vp]
+        L.tri_attn_status_string.argtypes = [_int]
+        L.tri_attn_status_string.restype = ctypes.c_char_p
+        for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
+                     "tri_attn_fwd", "tri_attn_bwd"):
+            getattr(L, name).restype = _int
+        _LIB = L
+    return _LIB
+
+
+# ---- the C entry points, same names -----------------------------------------------
+
+def tri_attn_status_string(status: int) -> str:
+    return lib().tri_attn_status_string(int(status)).decode()
+
+
+def tri_attn_fwd_workspace_bytes(node: int, dtype: int, n: int, h: int, d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_fwd_workspace_bytes(node, dtype, n, h, d, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_fwd_workspace_bytes")
+    return out.value
+
+
+def tri_attn_bwd_workspace_bytes(node: int, dtype: int, n: int, h: int, d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_bwd_workspace_bytes(node, dtype, n, h, d, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_bwd_workspace_bytes")
+    return out.value
+
+
+def tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, workspace,
+                 workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                              workspace, workspace_bytes, stream)
+
+
+def tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
+                 dv, dg, dbias, workspace, workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                              dout, dq, dk, dv, dg, dbias, workspace, workspace_bytes, stream)
+
+
+# ---- torch convenience wrappers -------------------------------------------------------
+
+_DTYPES = {torch.float32: F32, torch.bfloat16: BF16}
+
+
+def _check(name, t, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device or t.device.type != "cuda":
+        raise ValueError(f"{name} must be on {device} (got {t.device})")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _common(q, k, v, g, bias, mask):
+    if q.dim() != 4:
+        raise ValueError("q must be [n, n, h, d]")
+    n, n2, h, d = q.shape
+    if n != n2:
+        raise ValueError("q must be square in its two pair axes")
+    if q.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g)):
+        _check(name, t, (n, n, h, d), q.dtype, dev)
+    _check("bias", bias, (n, n, h), q.dtype, dev)
+    if mask is not None:
+        _check("mask", mask, (n, n), torch.uint8, dev)
+    return n, h, d, _DTYPES[q.dtype], dev
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(dev):
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def default_scale(d: int) -> float:
+    return 1.0 / math.sqrt(d)
+
+
+def fwd(q, k, v, g, bias, mask=None, node: int = STARTING, scale: Optional[float] = None,
+        workspace: Optional[torch.Tensor] = None):
+    """Triangle attention forward.  Returns (out [n,n,h,d], lse [n,n,h] fp32)."""
+    n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
+    scale = default_scale(d) if scale is None else float(scale)
+    out = torch.empty_like(q)
+    lse = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+    need = tri_attn_fwd_workspace_bytes(node, dt, n, h, d)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_attn_fwd(node, dt, n, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias),
+                      _ptr(mask), _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
+                      _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_fwd")
+    return out, lse
+
+
+def bwd(q, k, v, g, bias, out, lse, dout, mask=None, node: int = STARTING,
+        scale: Optional[float] = None, workspace: Optional[torch.Tensor] = None):
+    """Triangle attention backward.  Returns (dq, dk, dv, dg, dbias)."""
+    n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
+    _check("out", out, (n, n, h, d), q.dtype, dev)
+    _check("dout", dout, (n, n, h, d), q.dtype, dev)
+    _check("lse", lse, (n, n, h), torch.float32, dev)
+    scale = default_scale(d) if scale is None else float(scale)
+    dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
+    dbias = torch.empty_like(bias)
+    need = tri_attn_bwd_workspace_bytes(node, dt, n, h, d)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_attn_bwd(node, dt, n, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias),
+                      _ptr(mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
+                      _ptr(dv), _ptr(dg), _ptr(dbias), _ptr(workspace), workspace.numel(),
+                      _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_bwd")
+    return dq, dk, dv, dg, dbias
+
+
+class TriangleAttention(torch.autograd.Function):
+    """autograd wrapper: out = triangle_attention(q, k, v, g, bias; mask, node)."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, g, bias, mask=None, node=STARTING, scale=None):
+        out, lse = fwd(q, k, v, g, bias, mask, node, scale)
+        ctx.save_for_backward(q, k, v, g, bias, out, lse)
+        ctx.mask, ctx.node, ctx.scale = mask, node, scale
+        return out
+
+    @staticmethod
+    def backward(ctx, dout):
+        q, k, v, g, bias, out, lse = ctx.saved_tensors
+        grads = bwd(q, k, v, g, bias, out, lse, dout.contiguous(), ctx.mask, ctx.node, ctx.scale)
+        return (*grads, None, None, None)
+
+
+def triangle_attention(q, k, v, g, bias, mask=None, node: int = STARTING, scale=None):
+    return TriangleAttention.apply(q, k, v, g, bias, mask, node, scale)

@@ -1,0 +1,214 @@
+// C ABI of the triangle-attention library: argument checks, workspace
+// layout and launch sequencing.  Every check runs before the first HIP call.
+#include <math.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "kernels.h"
+#include "triattn.h"
+
+namespace {
+
+using triattn::Geom;
+
+constexpr int64_t MAX_N = 8192;
+constexpr int64_t MAX_H = 64;
+
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d) {
+  if (node != TRIATTN_STARTING && node != TRIATTN_ENDING) return TRIATTN_ERR_INVALID_ARG;
+  if (dtype != TRIATTN_F32 && dtype != TRIATTN_BF16) return TRIATTN_ERR_INVALID_ARG;
+  if (n < 1 || n > MAX_N || h < 1 || h > MAX_H || d < 1) return TRIATTN_ERR_INVALID_ARG;
+  if (d != triattn::HEAD_DIM) return TRIATTN_ERR_UNSUPPORTED;
+  return TRIATTN_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Row chunks of the bias-gradient reduction: enough workgroups to fill the
+// chip, at most 16 partial slabs.
+int db_row_chunks(int64_t n, int64_t h) {
+  const int64_t nblk = (n + 127) / 128;
+  const int64_t tiles = h * nblk * nblk;
+  int64_t c = (1024 + tiles - 1) / tiles;
+  if (c > 16) c = 16;
+  if (c > n) c = n;
+  if (c < 1) c = 1;
+  const int64_t rpc = (n + c - 1) / c;
+  return (int)((n + rpc - 1) / rpc);
+}
+
+struct Layout {
+  size_t bt, btT, kbits, lse2, dsum, da, dalo, slabs, total;
+  int nrc;
+};
+
+// Workspace layout (offsets in bytes, each 256-aligned):
+//   forward : bt [H][np][np] f32, kbits [n][np/32] u32
+//   backward: bt, btT [H][np][np] f32, kbits, lse2 and dsum [H][n][np] f32,
+//             dA [n][n][H][32] dtype (bf16: plus its low part, same size),
+//             slabs [nrc][H][np][np] f32
+Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
+  const size_t np = (size_t)((n + 31) / 32 * 32);
+  const size_t plane = (size_t)h * np * np * sizeof(float);
+  Layout L{};
+  size_t off = 0;
+  L.bt = off;
+  off += round256(plane);
+  if (bwd) {
+    L.btT = off;
+    off += round256(plane);
+  }
+  L.kbits = off;
+  off += round256((size_t)n * (np / 32) * sizeof(uint32_t));
+  if (bwd) {
+    const size_t rows = (size_t)h * n * np * sizeof(float);
+    L.lse2 = off;
+    off += round256(rows);
+    L.dsum = off;
+    off += round256(rows);
+    const size_t pair = (size_t)n * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4);
+    L.da = off;
+    off += round256(pair);
+    L.dalo = off;
+    if (dtype == TRIATTN_BF16) off += round256(pair);
+    L.nrc = db_row_chunks(n, h);
+    L.slabs = off;
+    off += round256((size_t)L.nrc * plane);
+  }
+  L.total = off;
+  return L;
+}
+
+Geom geom(int node, int64_t n, int64_t h, float scale) {
+  Geom g;
+  g.n = (int)n;
+  g.H = (int)h;
+  g.np = (int)((n + 31) / 32 * 32);
+  g.nkt = g.np / 32;
+  const int64_t pos = h * triattn::HEAD_DIM, row = n * pos;
+  g.sRow = node == TRIATTN_STARTING ? row : pos;
+  g.sPos = node == TRIATTN_STARTING ? pos : row;
+  g.lRow = node == TRIATTN_STARTING ? n * h : h;
+  g.lPos = node == TRIATTN_STARTING ? h : n * h;
+  g.scale = scale;
+  return g;
+}
+
+triattn::Prep prep_ptrs(const Layout& L, void* ws, bool bwd) {
+  char* b = (char*)ws;
+  return triattn::Prep{(float*)(b + L.bt), bwd ? (float*)(b + L.btT) : nullptr,
+                       (uint32_t*)(b + L.kbits)};
+}
+
+template <typename T>
+int run_fwd(int node, const Geom& g, const Layout& L, const void* q, const void* k,
+            const void* v, const void* gate, const void* bias, const uint8_t* mask, void* out,
+            float* lse, void* ws, hipStream_t s) {
+  const triattn::Prep p = prep_ptrs(L, ws, false);
+  if (triattn::launch_prep<T>(g, node, (const T*)bias, mask, p, s) != hipSuccess)
+    return TRIATTN_ERR_HIP;
+  if (triattn::launch_fwd<T>(g, p, (const T*)q, (const T*)k, (const T*)v, (const T*)gate,
+                             (T*)out, lse, s) != hipSuccess)
+    return TRIATTN_ERR_HIP;
+  return TRIATTN_OK;
+}
+
+template <typename T>
+int run_bwd(int node, const Geom& g, const Layout& L, const void* q, const void* k,
+            const void* v, const void* gate, const void* bias, const uint8_t* mask,
+            const void* out, const float* lse, const void* dout, void* dq, void* dk, void* dv,
+            void* dg, void* dbias, void* ws, hipStream_t s) {
+  const triattn::Prep p = prep_ptrs(L, ws, true);
+  char* b = (char*)ws;
+  const triattn::BwdWs w{(float*)(b + L.lse2), (float*)(b + L.dsum), (void*)(b + L.da),
+                         std::is_same<T, float>::value ? nullptr : (void*)(b + L.dalo),
+                         (float*)(b + L.slabs), L.nrc};
+  if (triattn::launch_prep<T>(g, node, (const T*)bias, mask, p, s) != hipSuccess)
+    return TRIATTN_ERR_HIP;
+  if (triattn::launch_bwd<T>(g, node, p, w, (const T*)q, (const T*)k, (const T*)v,
+                             (const T*)gate, (const T*)out, lse, (const T*)dout, (T*)dq, (T*)dk,
+                             (T*)dv, (T*)dg, (T*)dbias, s) != hipSuccess)
+    return TRIATTN_ERR_HIP;
+  return TRIATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_attn_fwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
+                                 size_t* bytes) {
+  const int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = plan(false, dtype, n, h).total;
+  return TRIATTN_OK;
+}
+
+int tri_attn_bwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
+                                 size_t* bytes) {
+  const int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = plan(true, dtype, n, h).total;
+  return TRIATTN_OK;
+}
+
+int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                 const void* q, const void* k, const void* v, const void* g, const void* bias,
+                 const uint8_t* mask, void* out, float* lse, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(false, dtype, n, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(node, n, h, scale);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == TRIATTN_BF16)
+    return run_fwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, workspace, s);
+  return run_fwd<float>(node, geo, L, q, k, v, g, bias, mask, out, lse, workspace, s);
+}
+
+int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                 const void* q, const void* k, const void* v, const void* g, const void* bias,
+                 const uint8_t* mask, const void* out, const float* lse, const void* dout,
+                 void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(true, dtype, n, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(node, n, h, scale);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == TRIATTN_BF16)
+    return run_bwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
+                                  dv, dg, dbias, workspace, s);
+  return run_bwd<float>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk, dv, dg,
+                        dbias, workspace, s);
+}
+
+const char* tri_attn_status_string(int status) {
+  switch (status) {
+    case TRIATTN_OK: return "ok";
+    case TRIATTN_ERR_INVALID_ARG: return "invalid argument";
+    case TRIATTN_ERR_UNSUPPORTED: return "unsupported argument value";
+    case TRIATTN_ERR_WORKSPACE: return "workspace missing or too small";
+    case TRIATTN_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

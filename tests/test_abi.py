@@ -1,0 +1,141 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes workspaces, and rejects invalid arguments before any
+HIP call (so none of these calls launches anything)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2506_20686_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "triattn.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2506_20686_amd import build
+        build.build()
+    return B.lib()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tri_attn_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert len(names) >= 5
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert B.tri_attn_status_string(B.OK) == "ok"
+    for s in (B.ERR_INVALID_ARG, B.ERR_UNSUPPORTED, B.ERR_WORKSPACE, B.ERR_HIP):
+        assert B.tri_attn_status_string(s) not in ("ok", "unknown status")
+    assert B.tri_attn_status_string(99) == "unknown status"
+
+
+def ws_bytes(fn, *args):
+    out = ctypes.c_size_t(0)
+    st = fn(*args, ctypes.byref(out))
+    return st, out.value
+
+
+@pytest.mark.parametrize("dtype", [B.F32, B.BF16])
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_workspace_sizes(lib, node, dtype):
+    el = 2 if dtype == B.BF16 else 4
+    for n, h in ((1, 1), (32, 4), (37, 1), (256, 4), (768, 4), (1536, 4)):
+        st, f = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, dtype, n, h, 32)
+        assert st == B.OK
+        np_ = (n + 31) // 32 * 32
+        assert f >= h * np_ * np_ * 4 + n * (np_ // 32) * 4
+        st, b = ws_bytes(lib.tri_attn_bwd_workspace_bytes, node, dtype, n, h, 32)
+        assert st == B.OK
+        assert b >= f + h * np_ * np_ * 4 + 2 * h * n * np_ * 4 + n * n * h * 32 * el
+        # O(N^2 H) memory: far below the N^3 H logits the method avoids
+        if n >= 768:
+            assert b < n ** 3 * h * el / 3
+
+
+def test_workspace_size_errors(lib):
+    f = lib.tri_attn_fwd_workspace_bytes
+    assert ws_bytes(f, 2, B.BF16, 8, 1, 32)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 0, 7, 8, 1, 32)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 0, B.BF16, 0, 1, 32)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 0, B.BF16, 8, 0, 32)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 0, B.BF16, 9000, 1, 32)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 0, B.BF16, 8, 1, 64)[0] == B.ERR_UNSUPPORTED
+    assert f(0, B.BF16, 8, 1, 32, None) == B.ERR_INVALID_ARG
+
+
+# Fake, 16-byte aligned, non-null addresses: every call below is invalid, so
+# the library must return before it would touch them.
+P = 0x10000
+
+
+def fwd_args(**over):
+    a = dict(node=0, dtype=B.BF16, n=16, h=2, d=32, scale=0.17, q=P, k=P, v=P, g=P, bias=P,
+             mask=None, out=P, lse=P, ws=P, wsb=1 << 30, stream=None)
+    a.update(over)
+    return (a["node"], a["dtype"], a["n"], a["h"], a["d"], a["scale"], a["q"], a["k"], a["v"],
+            a["g"], a["bias"], a["mask"], a["out"], a["lse"], a["ws"], a["wsb"], a["stream"])
+
+
+def bwd_args(**over):
+    a = dict(node=0, dtype=B.BF16, n=16, h=2, d=32, scale=0.17, q=P, k=P, v=P, g=P, bias=P,
+             mask=None, out=P, lse=P, dout=P, dq=P, dk=P, dv=P, dg=P, dbias=P, ws=P,
+             wsb=1 << 30, stream=None)
+    a.update(over)
+    return (a["node"], a["dtype"], a["n"], a["h"], a["d"], a["scale"], a["q"], a["k"], a["v"],
+            a["g"], a["bias"], a["mask"], a["out"], a["lse"], a["dout"], a["dq"], a["dk"],
+            a["dv"], a["dg"], a["dbias"], a["ws"], a["wsb"], a["stream"])
+
+
+FWD_BAD = [
+    (dict(node=5), B.ERR_INVALID_ARG), (dict(dtype=-1), B.ERR_INVALID_ARG),
+    (dict(n=0), B.ERR_INVALID_ARG), (dict(h=0), B.ERR_INVALID_ARG),
+    (dict(d=16), B.ERR_UNSUPPORTED), (dict(scale=0.0), B.ERR_INVALID_ARG),
+    (dict(scale=-1.0), B.ERR_INVALID_ARG), (dict(scale=float("nan")), B.ERR_INVALID_ARG),
+    (dict(scale=float("inf")), B.ERR_INVALID_ARG),
+    (dict(q=None), B.ERR_INVALID_ARG), (dict(k=None), B.ERR_INVALID_ARG),
+    (dict(v=None), B.ERR_INVALID_ARG), (dict(g=None), B.ERR_INVALID_ARG),
+    (dict(bias=None), B.ERR_INVALID_ARG), (dict(out=None), B.ERR_INVALID_ARG),
+    (dict(lse=None), B.ERR_INVALID_ARG), (dict(q=P + 2), B.ERR_INVALID_ARG),
+    (dict(lse=P + 4), B.ERR_INVALID_ARG),
+    (dict(ws=None), B.ERR_WORKSPACE), (dict(wsb=16), B.ERR_WORKSPACE),
+    (dict(ws=P + 8), B.ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("over,code", FWD_BAD)
+def test_fwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_fwd(*fwd_args(**over)) == code
+
+
+BWD_BAD = FWD_BAD + [
+    (dict(dout=None), B.ERR_INVALID_ARG), (dict(dq=None), B.ERR_INVALID_ARG),
+    (dict(dk=None), B.ERR_INVALID_ARG), (dict(dv=None), B.ERR_INVALID_ARG),
+    (dict(dg=None), B.ERR_INVALID_ARG), (dict(dbias=None), B.ERR_INVALID_ARG),
+    (dict(dbias=P + 2), B.ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("over,code", BWD_BAD)
+def test_bwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_bwd(*bwd_args(**over)) == code
+
+
+def test_undersized_workspace_reports_exact_requirement(lib):
+    for node in (0, 1):
+        st, need = ws_bytes(lib.tri_attn_bwd_workspace_bytes, node, B.BF16, 16, 2, 32)
+        assert st == B.OK
+        assert lib.tri_attn_bwd(*bwd_args(node=node, wsb=need - 1)) == B.ERR_WORKSPACE
+        st, need = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, 16, 2, 32)
+        assert lib.tri_attn_fwd(*fwd_args(node=node, wsb=need - 1)) == B.ERR_WORKSPACE
