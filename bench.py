@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Triangle-attention benchmark on one MI355X.
+
+One step = the whole hot path on one batch of synthetic input: forward and
+backward of triangle attention around the starting node and around the
+ending node, N = 768 tokens, H = 4 heads, d = 32, bf16 inputs with fp32
+accumulation, no padding (bias ~ N(0, 2)).  The metric is nominal fwd+bwd
+TFLOP/s (14 N^3 H d per node variant: 4 forward, 10 backward) and its
+fraction of the MI355X dense bf16 MFMA peak; peak HBM bytes are reported
+beside it.
+
+Prints ONE JSON line.  Inputs, outputs and workspaces are resident in HBM
+before the timed region; the timed region runs exactly --steps steps between
+two device synchronisations.  Per-kernel durations come from HIP events the
+library records on its launch stream during the same timed steps.
+
+The "cpu_baseline" leg times the fp64 oracle on the host cores on a bounded
+sample of the same workload (it is a reference point, not a target).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2516.6   # 256 CU x 2.4 GHz x 4096 dense bf16 flop/clk/CU
+MFMA_FP32_PEAK_TFLOPS = 157.3
+HBM_PEAK_GBS = 8000.0
+
+# Algorithmic MFMA flop per logit (per (row, query, key, head)) of each main
+# kernel: d-long dot products, 2 d flop each.  fwd: S, P V.  dq: S, dP, dQ.
+# dkdv: S, dP, dV, dK.  db: S, dP (it only reduces dS over rows).
+KERNEL_FLOP_PER_LOGIT_D = {"fwd": 4, "dq": 6, "dkdv": 8, "db": 4}
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None, help="workload name (default: the N=768 one)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample (0 disables it)")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    """Hash of the kernel sources; a traffic figure measured on other sources is stale."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2506_20686_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 --pmc summary, or
+    None if there is none or it was taken on different kernel sources."""
+    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"bytes_per_launch:\s*([0-9.eE+]+)", text)
+    s = re.search(r"source_hash:\s*([0-9a-f]+)", text)
+    if not m or not s or s.group(1) != kernel_source_hash():
+        return None
+    return float(m.group(1))
+
+
+def cpu_baseline(w, t, target_s):
+    """Time the fp64 oracle (as it stands) on rows of the starting node: the
+    forward and the per-row gradients (dQ, dK, dV, dG) of R rows, nominal
+    14 N^2 H d flop per row.  R is sized from a one-row trial run."""
+    import numpy as np
+
+    import oracle
+
+    arr = {k: np.ascontiguousarray(t[k].double().numpy()) for k in ("q", "k", "v", "g", "bias",
+                                                                    "dout")}
+    mask = t["mask"].numpy()
+
+    def run(rows):
+        t0 = time.perf_counter()
+        oracle.fwd(0, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], mask, rows=rows)
+        oracle.bwd(0, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], arr["dout"], mask,
+                   rows=rows, db_queries=[])
+        return time.perf_counter() - t0
+
+    one = run([0])
+    rows = max(1, min(w.n, int(target_s / max(one, 1e-3))))
+    sel = [int(i * w.n / rows) for i in range(rows)]
+    dt = run(sel)
+    flop = 14.0 * w.n ** 2 * w.h * w.d * rows
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(),
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"starting node of {w.name}: forward + per-row gradients (dQ, dK, dV, dG) "
+                      f"of {rows} of {w.n} rows, fp64, nominal 14*N^2*H*d flop per row; "
+                      f"dB (a row sum of the same dS) not included"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the row-sharded "
+              "design is described in DESIGN.md); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    from paper_2506_20686_amd import workloads as W
+
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2506_20686_amd import build
+        build.build()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    name = args.workload or W.HEADLINE
+    w = W.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    dt = B.BF16 if w.dtype == torch.bfloat16 else B.F32
+    scale = 1.0 / math.sqrt(w.d)
+    n, h, d = w.n, w.h, w.d
+
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)  # initialise the context before the memory counters
+    torch.cuda.reset_peak_memory_stats(dev)
+    host = {}
+    per_node = []
+    for node in w.nodes:
+        t = W.workload_inputs(w, node)
+        host[node] = t
+        x = {k: t[k].to(dev) for k in ("q", "k", "v", "g", "bias", "dout", "mask")}
+        x["out"] = torch.empty_like(x["q"])
+        x["lse"] = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+        for gname in ("dq", "dk", "dv", "dg"):
+            x[gname] = torch.empty_like(x["q"])
+        x["dbias"] = torch.empty_like(x["bias"])
+        per_node.append((node, x))
+    ws_bytes = max(max(B.tri_attn_fwd_workspace_bytes(nd, dt, n, h, d),
+                       B.tri_attn_bwd_workspace_bytes(nd, dt, n, h, d)) for nd in w.nodes)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda a: a.data_ptr()  # noqa: E731
+
+    def step():
+        for node, x in per_node:
+            st = B.tri_attn_fwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
+                                P(ws), ws_bytes, stream)
+            if st != B.OK:
+                raise B.TriAttnError(st, "tri_attn_fwd")
+            st = B.tri_attn_bwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
+                                P(x["dout"]), P(x["dq"]), P(x["dk"]), P(x["dv"]), P(x["dg"]),
+                                P(x["dbias"]), P(ws), ws_bytes, stream)
+            if st != B.OK:
+                raise B.TriAttnError(st, "tri_attn_bwd")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    B.tri_attn_timing_reset()
+    B.tri_attn_timing_enable(True)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize(dev)
+    t1 = time.perf_counter()
+    B.tri_attn_timing_enable(False)
+    ktimes = B.kernel_times()
+    peak_bytes = torch.cuda.max_memory_allocated(dev)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    flop_step = w.flops_fwd_bwd * len(w.nodes)
+    tflops = flop_step / (ms * 1e-3) / 1e12
+    peak = MFMA_BF16_PEAK_TFLOPS if dt == B.BF16 else MFMA_FP32_PEAK_TFLOPS
+
+    per_kernel = {k: {"avg_ms": round(v[0] / v[1], 5), "launches": v[1],
+                      "share": round(v[0] / max(1e-9, sum(x[0] for x in ktimes.values())), 4)}
+                  for k, v in ktimes.items() if v[1] > 0}
+    dom = max((k for k in per_kernel if k in KERNEL_FLOP_PER_LOGIT_D),
+              key=lambda k: ktimes[k][0])
+    avg_s = ktimes[dom][0] / ktimes[dom][1] * 1e-3
+    flop_launch = KERNEL_FLOP_PER_LOGIT_D[dom] * d * n ** 3 * h
+    achieved = flop_launch / avg_s / 1e12
+    traffic = recorded_traffic(dom, name)
+
+    out = {
+        "metric": "triangle-attn fwd+bwd TFLOP/s (% of bf16 MFMA peak) at N=768; peak HBM bytes",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if dt == B.BF16 else "f32",
+        "data": "synthetic (seeded normals; the paper's PDB-derived pair representations are "
+                "not available)",
+        "config": {"workload": name, "n": n, "heads": h, "head_dim": d,
+                   "nodes": [W.NODE_NAMES[x] for x in w.nodes], "mask": "all keys valid"
+                   if w.pad_frac == 0 and w.rand_pad_frac == 0 else "key padding",
+                   "bias_std": round(w.bias_std, 4), "parallelism": "none (1 GPU)"},
+        "pct_of_peak": round(100.0 * tflops / peak, 3),
+        "peak_hbm_bytes": int(peak_bytes),
+        "workspace_bytes": int(ws_bytes),
+        "naive_logits_bytes": int(n ** 3 * h * 2),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 3),
+                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 5),
+                     "traffic": traffic},
+        "per_kernel": per_kernel,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(w, host[w.nodes[0]], args.cpu_seconds)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -97,6 +97,23 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
 /* Static, human-readable name of a status code ("unknown status" otherwise). */
 const char* tri_attn_status_string(int status);
 
+/* Per-kernel timing, for benchmarks and profiling (not part of the paper's
+ * method).  While enabled, every entry point records a pair of HIP events
+ * on its stream around each kernel it launches.  The switch and the
+ * accumulated times are process-wide; enable it only while no other thread
+ * is calling the library.  Off by default. */
+int tri_attn_timing_enable(int on);
+
+/* Waits for the recorded events of kernel `index` (0, 1, ... in launch-site
+ * order; TRIATTN_ERR_INVALID_ARG past the last one) and returns its name
+ * (static string), the summed elapsed milliseconds and the launch count
+ * since the last reset.  TRIATTN_ERR_HIP if an event call failed. */
+int tri_attn_timing_read(int index, const char** name, double* total_ms, int64_t* launches);
+
+/* Clears the accumulated times and counts (after waiting for pending
+ * events); returns TRIATTN_ERR_HIP if an event call had failed. */
+int tri_attn_timing_reset(void);
+
 #ifdef __cplusplus
 }
 #endif

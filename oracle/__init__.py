@@ -39,7 +39,14 @@ def load(path):
     lib.oracle_bwd.argtypes = [ci, i64, i64, i64, dbl, _D, _D, _D, _D, _D, _U8, _D,
                                _D, _D, _D, _D, _D, _I64, i64, _I64, i64]
     lib.oracle_bwd.restype = None
+    lib.oracle_max_threads.argtypes = []
+    lib.oracle_max_threads.restype = ctypes.c_int
     return lib
+
+
+def max_threads() -> int:
+    """OpenMP threads the oracle runs on."""
+    return int(_lib().oracle_max_threads())
 
 
 def use_library(lib):

@@ -47,6 +47,7 @@
  * hand-derived fixtures.  The paper prints no numeric example.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -279,3 +280,6 @@ void oracle_bwd(int node, int64_t n, int64_t H, int64_t d, double scale, const d
   free(rl);
   free(ql);
 }
+
+/* Threads the oracle's parallel loops use (for reporting). */
+int oracle_max_threads(void) { return omp_get_max_threads(); }

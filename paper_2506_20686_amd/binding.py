@@ -48,8 +48,14 @@ def lib():
         L.tri_attn_bwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz, _vp]
         L.tri_attn_status_string.argtypes = [_int]
         L.tri_attn_status_string.restype = ctypes.c_char_p
+        L.tri_attn_timing_enable.argtypes = [_int]
+        L.tri_attn_timing_reset.argtypes = []
+        L.tri_attn_timing_read.argtypes = [_int, ctypes.POINTER(ctypes.c_char_p),
+                                           ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_int64)]
         for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
-                     "tri_attn_fwd", "tri_attn_bwd"):
+                     "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
+                     "tri_attn_timing_reset", "tri_attn_timing_read"):
             getattr(L, name).restype = _int
         _LIB = L
     return _LIB
@@ -89,6 +95,41 @@ def tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, 
     """Raw call: every tensor argument is an integer device address (or None)."""
     return lib().tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
                               dout, dq, dk, dv, dg, dbias, workspace, workspace_bytes, stream)
+
+
+def tri_attn_timing_enable(on: bool) -> None:
+    st = lib().tri_attn_timing_enable(1 if on else 0)
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_timing_enable")
+
+
+def tri_attn_timing_reset() -> None:
+    st = lib().tri_attn_timing_reset()
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_timing_reset")
+
+
+def tri_attn_timing_read(index: int):
+    """(name, total_ms, launches) of kernel `index`, or None past the last one."""
+    name, ms, cnt = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_int64()
+    st = lib().tri_attn_timing_read(index, ctypes.byref(name), ctypes.byref(ms),
+                                    ctypes.byref(cnt))
+    if st == ERR_INVALID_ARG:
+        return None
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_timing_read")
+    return name.value.decode(), ms.value, cnt.value
+
+
+def kernel_times():
+    """{kernel name: (total ms, launches)} accumulated since the last reset."""
+    out, i = {}, 0
+    while True:
+        r = tri_attn_timing_read(i)
+        if r is None:
+            return out
+        out[r[0]] = (r[1], r[2])
+        i += 1
 
 
 # ---- torch convenience wrappers -------------------------------------------------------

@@ -28,6 +28,7 @@
 
 #include "kernels.h"
 #include "stage.h"
+#include "timing.h"
 
 namespace triattn {
 
@@ -464,24 +465,40 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   T* da = (T*)ws.da;
   T* dalo = (T*)ws.dalo;
   const int64_t npair = (int64_t)g.n * g.n * g.H;
-  hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((npair + 255) / 256)), dim3(256), 0, s,
-                     g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+  {
+    KernelTimer t(K_BWD_PREP, s);
+    hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((npair + 255) / 256)), dim3(256), 0,
+                       s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+  }
   if (g.np > g.n) {
     const int64_t npad = (int64_t)g.H * g.n * (g.np - g.n);
+    KernelTimer t(K_BWD_PAD, s);
     hipLaunchKernelGGL(bwd_pad_kernel, dim3((unsigned)((npad + 255) / 256)), dim3(256), 0, s, g,
                        ws.lse2, ws.dsum);
   }
   BwdArgs<T> a{g, p.bt, p.btT, p.kbits, q, k, v, da, dalo, ws.lse2, ws.dsum, dq, dk, dv, ws.slabs,
                (g.n + BWD_BLK - 1) / BWD_BLK, ws.nrc, (g.n + ws.nrc - 1) / ws.nrc};
   const int64_t nrow = (int64_t)a.nblk * g.n * g.H;
-  // dq_kernel first: it produces D for the other two
-  hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
-  const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
-  hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(256), 0, s, a);
-  const int64_t nred = (int64_t)g.H * g.n * g.n;
-  hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0, s,
-                     g, node, ws.nrc, ws.slabs, dbias);
+  {
+    // dq_kernel first: it produces D for the other two
+    KernelTimer t(K_DQ, s);
+    hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+  }
+  {
+    KernelTimer t(K_DKDV, s);
+    hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+  }
+  {
+    const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
+    KernelTimer t(K_DB, s);
+    hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(256), 0, s, a);
+  }
+  {
+    const int64_t nred = (int64_t)g.H * g.n * g.n;
+    KernelTimer t(K_DB_REDUCE, s);
+    hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0, s,
+                       g, node, ws.nrc, ws.slabs, dbias);
+  }
   return hipGetLastError();
 }
 

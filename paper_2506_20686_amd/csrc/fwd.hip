@@ -16,6 +16,7 @@
 //  - key tiles that are fully masked for the row are skipped.
 #include "kernels.h"
 #include "stage.h"
+#include "timing.h"
 
 namespace triattn {
 
@@ -62,11 +63,17 @@ template <typename T>
 hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* mask, const Prep& p,
                        hipStream_t s) {
   const int64_t nb = ((int64_t)g.H * g.np * g.np + 255) / 256;
-  hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb), dim3(256), 0, s, g, node, bias,
-                     p.bt, p.btT);
+  {
+    KernelTimer t(K_PREP_BIAS, s);
+    hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb), dim3(256), 0, s, g, node, bias,
+                       p.bt, p.btT);
+  }
   const int64_t nk = ((int64_t)g.n * g.nkt + 255) / 256;
-  hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)nk), dim3(256), 0, s, g, node, mask,
-                     p.kbits);
+  {
+    KernelTimer t(K_PREP_KBITS, s);
+    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)nk), dim3(256), 0, s, g, node, mask,
+                       p.kbits);
+  }
   return hipGetLastError();
 }
 
@@ -196,7 +203,10 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   const int64_t nwg = (int64_t)a.nqb * g.n * g.H;
-  hipLaunchKernelGGL(fwd_kernel<T>, dim3((unsigned)nwg), dim3(256), 0, s, a);
+  {
+    KernelTimer t(K_FWD, s);
+    hipLaunchKernelGGL(fwd_kernel<T>, dim3((unsigned)nwg), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -1,0 +1,123 @@
+// Opt-in per-kernel timing: when enabled, each kernel launch of the library
+// is bracketed by two HIP events recorded on the launch's stream; reading
+// the timings waits for those events and accumulates their elapsed times
+// per kernel.  Off by default, in which case the brackets cost one branch.
+#include <mutex>
+#include <vector>
+
+#include "timing.h"
+#include "triattn.h"
+
+namespace triattn {
+
+namespace {
+
+const char* const kNames[K_COUNT] = {"prep_bias", "prep_kbits", "fwd",  "bwd_prep",
+                                     "bwd_pad",   "dq",         "dkdv", "db",
+                                     "db_reduce"};
+
+struct Pending {
+  int id;
+  hipEvent_t a, b;
+};
+
+struct State {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;  // created events not in use
+  std::vector<Pending> pending;  // recorded, not yet read
+  double ms[K_COUNT] = {};
+  int64_t launches[K_COUNT] = {};
+  int status = TRIATTN_OK;
+};
+
+State& st() {
+  static State s;
+  return s;
+}
+
+bool take(State& s, hipEvent_t* e) {
+  if (!s.pool.empty()) {
+    *e = s.pool.back();
+    s.pool.pop_back();
+    return true;
+  }
+  return hipEventCreate(e) == hipSuccess;
+}
+
+void drain(State& s) {
+  for (const Pending& p : s.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess)
+      s.status = TRIATTN_ERR_HIP;
+    s.ms[p.id] += ms;
+    s.launches[p.id] += 1;
+    s.pool.push_back(p.a);
+    s.pool.push_back(p.b);
+  }
+  s.pending.clear();
+}
+
+}  // namespace
+
+KernelTimer::KernelTimer(KernelId id, hipStream_t stream) : id_(id), stream_(stream) {
+  State& s = st();
+  if (!s.on) return;
+  std::lock_guard<std::mutex> lock(s.mu);
+  if (!take(s, &a_) || !take(s, &b_) || hipEventRecord(a_, stream_) != hipSuccess) {
+    s.status = TRIATTN_ERR_HIP;
+    return;
+  }
+  armed_ = true;
+}
+
+KernelTimer::~KernelTimer() {
+  if (!armed_) return;
+  State& s = st();
+  std::lock_guard<std::mutex> lock(s.mu);
+  if (hipEventRecord(b_, stream_) != hipSuccess) {
+    s.status = TRIATTN_ERR_HIP;
+    return;
+  }
+  s.pending.push_back(Pending{id_, a_, b_});
+  if (s.pending.size() >= 4096) drain(s);
+}
+
+}  // namespace triattn
+
+extern "C" {
+
+int tri_attn_timing_enable(int on) {
+  triattn::State& s = triattn::st();
+  std::lock_guard<std::mutex> lock(s.mu);
+  s.on = on != 0;
+  return TRIATTN_OK;
+}
+
+int tri_attn_timing_reset(void) {
+  triattn::State& s = triattn::st();
+  std::lock_guard<std::mutex> lock(s.mu);
+  triattn::drain(s);
+  for (int i = 0; i < triattn::K_COUNT; ++i) {
+    s.ms[i] = 0.0;
+    s.launches[i] = 0;
+  }
+  const int r = s.status;
+  s.status = TRIATTN_OK;
+  return r;
+}
+
+int tri_attn_timing_read(int index, const char** name, double* total_ms, int64_t* launches) {
+  if (index < 0 || index >= triattn::K_COUNT || name == nullptr || total_ms == nullptr ||
+      launches == nullptr)
+    return TRIATTN_ERR_INVALID_ARG;
+  triattn::State& s = triattn::st();
+  std::lock_guard<std::mutex> lock(s.mu);
+  triattn::drain(s);
+  *name = triattn::kNames[index];
+  *total_ms = s.ms[index];
+  *launches = s.launches[index];
+  return s.status;
+}
+
+}  // extern "C"
