@@ -37,20 +37,21 @@ constexpr bool kSplitDA = std::is_same<T, bf16>::value;
 
 // ---- elementwise preparation -------------------------------------------------------
 
+// Four threads per (pair, head): thread t handles channels 8 (t % 4) .. +7,
+// so every load and store is 16 contiguous bytes and a wave covers 16 whole
+// (pair, head) rows.
 template <typename T>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T* out,
                                                        const float* lse, const T* gate,
                                                        const T* dout, T* dg, T* da,
                                                        T* dalo, float* lse2) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (a, b, h)
+  const int64_t tix = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t idx = tix >> 2;  // (a, b, h)
   const int64_t total = (int64_t)G.n * G.n * G.H;
   if (idx >= total) return;
-  const int h = (int)(idx % G.H);
-  const int64_t pair = idx / G.H;
-  const int a = (int)(pair / G.n), b = (int)(pair % G.n);
-  const int64_t base = idx * HEAD_DIM;
+  const int64_t base = idx * HEAD_DIM + 8 * (tix & 3);
 #pragma unroll
-  for (int j = 0; j < HEAD_DIM / 4; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const f32x4 go = load4(dout + base + 4 * j), oo = load4(out + base + 4 * j);
     const f32x4 gg = load4(gate + base + 4 * j);
     f32x4 dgv, dav;
@@ -69,10 +70,14 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
       store4(dalo + base + 4 * j, lo);
     }
   }
-  const int row = node == 0 ? a : b, qi = node == 0 ? b : a;
-  const int64_t at = ((int64_t)h * G.n + row) * G.np + qi;
-  const float l = lse[idx];
-  lse2[at] = l == neg_inf() ? pos_inf() : l * LOG2E;
+  if ((tix & 3) == 0) {
+    const int h = (int)(idx % G.H);
+    const int64_t pair = idx / G.H;
+    const int a = (int)(pair / G.n), b = (int)(pair % G.n);
+    const int row = node == 0 ? a : b, qi = node == 0 ? b : a;
+    const float l = lse[idx];
+    lse2[((int64_t)h * G.n + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
+  }
 }
 
 // Queries n .. np-1 of every row: no valid key (+inf) and D = 0.
@@ -85,8 +90,6 @@ __global__ __launch_bounds__(256) void bwd_pad_kernel(Geom G, float* lse2, float
   lse2[at] = pos_inf();
   dsum[at] = 0.f;
 }
-
-// ---- dK, dV ------------------------------------------------------------------------
 
 constexpr int BWD_WAVES = 4;
 constexpr int BWD_BLK = BWD_WAVES * TILE;
@@ -107,29 +110,172 @@ struct BwdArgs {
   int rpc;   // rows per chunk (db)
 };
 
+// ---- dQ (and D) ----------------------------------------------------------------------
+
+// Per (row, head, 128 queries): stream the row's keys in blocks of 64 (K, K^T
+// and V staged in LDS, double-buffered).  dQ = scale (X - D Y) with
+// X = sum_k P dP K, Y = sum_k P K and D = sum_k P dP, all from one pass.
 template <typename T>
-__global__ __launch_bounds__(256) void dkdv_kernel(BwdArgs<T> a) {
+__global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int kb = w % a.nblk, rh = w / a.nblk;
+  const int qb = w % a.nblk, rh = w / a.nblk;
   const int r = rh % G.n, h = rh / G.n;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int kt = kb * BWD_WAVES + wave;  // this wave's key tile; lane <-> key
+  const int q0 = qb * BWD_BLK + wave * TILE;
+  const bool active = q0 < G.n;
+  const int q = q0 + l32;  // lane <-> query
+  const bool qok = q < G.n;
+
+  __shared__ __align__(16) T ks[2 * ROW_TILE];    // K   [key][channel]
+  __shared__ __align__(16) T kT[2 * TRANS_TILE];  // K^T [channel][key]
+  __shared__ __align__(16) T vs[2 * ROW_TILE];    // V   [key][channel]
+
+  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const T* kr = a.k + rowbase;
+  const T* vr = a.v + rowbase;
+  const int last = G.n - 1;
+  typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+  float l2 = pos_inf();
+  zero_frags<T>(dalf);
+  if (qok) {
+    row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
+    row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
+    if constexpr (kSplitDA<T>) row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    l2 = a.lse2[((int64_t)h * G.n + r) * G.np + q];
+  } else {
+    zero_frags<T>(qf);
+    zero_frags<T>(daf);
+  }
+  const float c1 = G.scale * LOG2E;
+  f32x16 xt = {}, yt = {};
+  float dpart = 0.f;
+  const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
+  const int nblk = (G.nkt + 1) >> 1;
+  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
+  auto bias_tile = [&](int kt) { return load_quads(bq + min(kt, G.nkt - 1) * TILE); };
+
+  auto sub_tile = [&](const T* ksb, const T* kTb, const T* vsb, const f32x16& bias, uint32_t bits,
+                      int u) {
+    // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
+    typename M::frag af[M::KCH];
+    row_frags(ksb + (32 * u + l32) * LDS_ROW, g, af);
+    f32x16 s = M::mma(af[0], qf[0], bias);
+#pragma unroll
+    for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], qf[t], s);
+    if (bits != 0xffffffffu) mask_rows(s, bits, g);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2));
+    // dP^T = V dA^T, then P dP and its running sum D
+    row_frags(vsb + (32 * u + l32) * LDS_ROW, g, af);
+    f32x16 dp = M::mma(af[0], daf[0], f32x16{});
+#pragma unroll
+    for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], daf[t], dp);
+    if constexpr (kSplitDA<T>) {
+#pragma unroll
+      for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      dp[v] *= s[v];
+      dpart += dp[v];
+    }
+    // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the keys)
+    typename M::frag pf[M::PCH], xf[M::PCH];
+    quad_frags(kTb + l32 * LDS_TROW + 32 * u, g, xf);
+    acc_frags(dp, pf);
+#pragma unroll
+    for (int t = 0; t < M::PCH; ++t) xt = M::mma(xf[t], pf[t], xt);
+    acc_frags(s, pf);
+#pragma unroll
+    for (int t = 0; t < M::PCH; ++t) yt = M::mma(xf[t], pf[t], yt);
+  };
+
+  PairPiece<T> kp;
+  RowPiece<T> vp;
+  uint64_t bb = block_bits(kb, G.nkt, 0);
+  kp.load(kr, G.sPos, 0, last, tid);
+  vp.load(vr, G.sPos, 0, last, tid);
+  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
+  kp.validate(tid, bb);
+  kp.store_rows(ks, tid);
+  kp.store_trans(kT, tid);
+  vp.store(vs, tid, bb);
+  __syncthreads();
+  int buf = 0;
+  for (int b = 0; b < nblk; ++b) {
+    const int bn = min(b + 1, nblk - 1);
+    const uint64_t bbn = block_bits(kb, G.nkt, bn);
+    kp.load(kr, G.sPos, bn * SPAN, last, tid);
+    vp.load(vr, G.sPos, bn * SPAN, last, tid);
+    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
+    if (active) {
+      const T* ksb = ks + buf * ROW_TILE;
+      const T* kTb = kT + buf * TRANS_TILE;
+      const T* vsb = vs + buf * ROW_TILE;
+      if ((uint32_t)bb) sub_tile(ksb, kTb, vsb, b0, (uint32_t)bb, 0);
+      if ((uint32_t)(bb >> 32)) sub_tile(ksb, kTb, vsb, b1, (uint32_t)(bb >> 32), 1);
+    }
+    if (b + 1 < nblk) {
+      kp.validate(tid, bbn);
+      kp.store_rows(ks + (buf ^ 1) * ROW_TILE, tid);
+      kp.store_trans(kT + (buf ^ 1) * TRANS_TILE, tid);
+      vp.store(vs + (buf ^ 1) * ROW_TILE, tid, bbn);
+    }
+    __syncthreads();
+    b0 = n0;
+    b1 = n1;
+    bb = bbn;
+    buf ^= 1;
+  }
+  if (!active) return;
+  const float dsum = wave_xor32_sum(dpart);
+  if (!qok) return;
+  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = dsum;
+  const int64_t base = rowbase + (int64_t)q * G.sPos;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    f32x4 x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
+    store4(a.dq + base + 8 * j + 4 * g, x);
+  }
+}
+
+// ---- dK, dV --------------------------------------------------------------------------
+
+// Per (row, head, 128 keys; wave <-> 32 keys, lane <-> key): stream the row's
+// queries in blocks of 64 (Q, Q^T, dA, dA^T, the low part of dA, lse2 and -D
+// staged in LDS, double-buffered).  The paper's first backward stage.
+template <typename T>
+__global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
+  using M = Mma<T>;
+  const Geom& G = a.g;
+  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int kbk = w % a.nblk, rh = w / a.nblk;
+  const int r = rh % G.n, h = rh / G.n;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int kt = kbk * BWD_WAVES + wave;  // this wave's key tile
   const bool active = kt < G.nkt;
   const uint32_t bits = active ? a.kbits[(int64_t)r * G.nkt + kt] : 0u;
   const int key = kt * TILE + l32;
   const bool kvalid = (bits >> l32) & 1u;
+  const bool work = bits != 0u;  // some key of this wave is valid for the row
 
-  __shared__ __align__(16) T qs[TILE * LDS_ROW];       // Q tile   [query][channel]
-  __shared__ __align__(16) T qT[HEAD_DIM * LDS_ROW];   // Q^T tile [channel][query]
-  __shared__ __align__(16) T das[TILE * LDS_ROW];      // dA tile
-  __shared__ __align__(16) T daT[HEAD_DIM * LDS_ROW];  // dA^T tile
-  __shared__ __align__(16) T dalos[kSplitDA<T> ? TILE * LDS_ROW : 1];  // low part of dA
-  __shared__ __align__(16) float l2s[TILE];            // lse2 of the tile's queries
-  __shared__ __align__(16) float nds[TILE];            // -D of the tile's queries
+  __shared__ __align__(16) T qs[2 * ROW_TILE];      // Q    [query][channel]
+  __shared__ __align__(16) T qT[2 * TRANS_TILE];    // Q^T  [channel][query]
+  __shared__ __align__(16) T das[2 * ROW_TILE];     // dA
+  __shared__ __align__(16) T daT[2 * TRANS_TILE];   // dA^T
+  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * ROW_TILE : 1];  // low part of dA
+  __shared__ __align__(16) float l2s[2 * SPAN];     // lse2 of the block's queries
+  __shared__ __align__(16) float nds[2 * SPAN];     // -D of the block's queries
 
   const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const T* qr = a.q + rowbase;
+  const T* dar = a.da + rowbase;
+  const T* dalr = kSplitDA<T> ? a.dalo + rowbase : nullptr;
+  const int last = G.n - 1;
   typename M::frag kf[M::KCH], vf[M::KCH];
   if (kvalid) {
     row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
@@ -140,75 +286,99 @@ __global__ __launch_bounds__(256) void dkdv_kernel(BwdArgs<T> a) {
   }
   const float c1 = G.scale * LOG2E;
   f32x16 dkt = {}, dvt = {};
+  // the lane's key row of the key-major bias (row 0 for idle waves)
   const float* bk = a.btT + ((int64_t)h * G.np + (active ? key : 0)) * G.np + 4 * g;
   const float* l2row = a.lse2 + ((int64_t)h * G.n + r) * G.np;
   const float* drow = a.dsum + ((int64_t)h * G.n + r) * G.np;
+  const int nblk = (G.nkt + 1) >> 1;  // query blocks of 64
+  const float kmask = kvalid ? 0.f : neg_inf();
+  auto bias_tile = [&](int t) {
+    f32x16 x = load_quads(bk + min(t, G.nkt - 1) * TILE);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) x[v] += kmask;  // -inf for a masked key
+    return x;
+  };
 
-  for (int qt = 0; qt < G.nkt; ++qt) {
-    __syncthreads();
-    const uint32_t qbits = range_bits(qt * TILE, G.n);
-    if (tid < 128) {
-      stage_tile<true, true>(a.q + rowbase, G.sPos, qt * TILE, qbits, tid, qs, qT);
-      if constexpr (kSplitDA<T>)
-        stage_tile<true, false>(a.dalo + rowbase, G.sPos, qt * TILE, qbits, tid, dalos,
-                                (T*)nullptr);
-    } else {
-      stage_tile<true, true>(a.da + rowbase, G.sPos, qt * TILE, qbits, tid - 128, das, daT);
-    }
-    if (tid < TILE) l2s[tid] = l2row[qt * TILE + tid];
-    else if (tid < 2 * TILE) nds[tid - TILE] = -drow[qt * TILE + tid - TILE];
-    __syncthreads();
-    if (bits == 0u) continue;  // every key of this wave is masked for the row
-
+  PairPiece<T> qp, dap;
+  RowPiece<T> dlp;
+  float sv = 0.f;  // thread < 64: lse2 of query tid; 64 <= thread < 128: -D of query tid-64
+  const int sq = tid & 63;
+  auto load_block = [&](int b) {
+    qp.load(qr, G.sPos, b * SPAN, last, tid);
+    dap.load(dar, G.sPos, b * SPAN, last, tid);
+    if constexpr (kSplitDA<T>) dlp.load(dalr, G.sPos, b * SPAN, last, tid);
+    const int qi = min(b * SPAN + sq, G.np - 1);
+    sv = tid < SPAN ? l2row[qi] : -drow[qi];
+  };
+  auto store_block = [&](int b, int bf) {
+    const uint64_t vb = range_bits64(b * SPAN, G.n);
+    qp.validate(tid, vb);
+    dap.validate(tid, vb);
+    qp.store_rows(qs + bf * ROW_TILE, tid);
+    qp.store_trans(qT + bf * TRANS_TILE, tid);
+    dap.store_rows(das + bf * ROW_TILE, tid);
+    dap.store_trans(daT + bf * TRANS_TILE, tid);
+    if constexpr (kSplitDA<T>) dlp.store(dals + bf * ROW_TILE, tid, vb);
+    const bool in = b * SPAN + sq < G.np;  // queries n..np-1 carry +inf / 0 already
+    if (tid < SPAN)
+      l2s[bf * SPAN + sq] = in ? sv : pos_inf();
+    else if (tid < 2 * SPAN)
+      nds[bf * SPAN + sq] = in ? sv : 0.f;
+  };
+  auto sub_tile = [&](int bf, const f32x16& bias, int u) {
+    const T* qsb = qs + bf * ROW_TILE;
     // S = bias + Q K^T (lane <-> key, registers <-> queries)
-    f32x16 s;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = *(const f32x4*)(bk + qt * TILE + 8 * j);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) s[4 * j + e] = kvalid ? x[e] : neg_inf();
-    }
     typename M::frag af[M::KCH];
-    row_frags(qs + l32 * LDS_ROW, g, af);
+    row_frags(qsb + (32 * u + l32) * LDS_ROW, g, af);
+    f32x16 s = M::mma(af[0], kf[0], bias);
 #pragma unroll
-    for (int t = 0; t < M::KCH; ++t) s = M::mma(af[t], kf[t], s);
-    // P = exp2(S * scale * log2 e - lse2[query])
+    for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], kf[t], s);
+    // P = exp2(S scale log2 e - lse2[query])
+    const f32x16 l2 = load_quads(l2s + bf * SPAN + 32 * u + 4 * g);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 l2 = *(const f32x4*)(l2s + 8 * j + 4 * g);
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        s[4 * j + e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[4 * j + e], c1, -l2[e]));
-    }
+    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2[v]));
     // dP - D = dA V^T - D, then dS = P (dP - D)
-    f32x16 dp;
+    row_frags(das + bf * ROW_TILE + (32 * u + l32) * LDS_ROW, g, af);
+    f32x16 dp = M::mma(af[0], vf[0], load_quads(nds + bf * SPAN + 32 * u + 4 * g));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = *(const f32x4*)(nds + 8 * j + 4 * g);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dp[4 * j + e] = x[e];
-    }
-    row_frags(das + l32 * LDS_ROW, g, af);
-#pragma unroll
-    for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], vf[t], dp);
+    for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], vf[t], dp);
     if constexpr (kSplitDA<T>) {
-      row_frags(dalos + l32 * LDS_ROW, g, af);
+      row_frags(dals + bf * ROW_TILE + (32 * u + l32) * LDS_ROW, g, af);
 #pragma unroll
       for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], vf[t], dp);
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v) dp[v] *= s[v];
-
-    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the tile's queries)
+    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the block's queries)
     typename M::frag pf[M::PCH], xf[M::PCH];
     acc_frags(s, pf);
-    quad_frags(daT + l32 * LDS_ROW, g, xf);
+    quad_frags(daT + bf * TRANS_TILE + l32 * LDS_TROW + 32 * u, g, xf);
 #pragma unroll
     for (int t = 0; t < M::PCH; ++t) dvt = M::mma(xf[t], pf[t], dvt);
     acc_frags(dp, pf);
-    quad_frags(qT + l32 * LDS_ROW, g, xf);
+    quad_frags(qT + bf * TRANS_TILE + l32 * LDS_TROW + 32 * u, g, xf);
 #pragma unroll
     for (int t = 0; t < M::PCH; ++t) dkt = M::mma(xf[t], pf[t], dkt);
+  };
+
+  load_block(0);
+  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
+  store_block(0, 0);
+  __syncthreads();
+  int buf = 0;
+  for (int b = 0; b < nblk; ++b) {
+    const int bn = min(b + 1, nblk - 1);
+    load_block(bn);
+    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
+    if (work) {
+      sub_tile(buf, b0, 0);
+      if (2 * b + 1 < G.nkt) sub_tile(buf, b1, 1);
+    }
+    if (b + 1 < nblk) store_block(bn, buf ^ 1);
+    __syncthreads();
+    b0 = n0;
+    b1 = n1;
+    buf ^= 1;
   }
   if (!active || key >= G.n) return;
   const int64_t base = rowbase + (int64_t)key * G.sPos;
@@ -226,216 +396,138 @@ __global__ __launch_bounds__(256) void dkdv_kernel(BwdArgs<T> a) {
   }
 }
 
-// ---- dQ ----------------------------------------------------------------------------
+// ---- dBias ---------------------------------------------------------------------------
 
+constexpr int DB_WAVES = 8;  // 4 query tiles x 2 key halves
+
+// One workgroup: 128 queries x 128 keys of one head, summed over the rows of
+// one row chunk.  Wave w owns query tile w % 4 (lane <-> query) and key tiles
+// 2 (w / 4), 2 (w / 4) + 1.  Per row the block's K and V (128 keys each) are
+// staged in LDS, double-buffered, and each wave prefetches the next row's Q,
+// dA, lse2 and D.  The bias tiles stay in registers for all rows.
 template <typename T>
-__global__ __launch_bounds__(256) void dq_kernel(BwdArgs<T> a) {
+__global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int qb = w % a.nblk, rh = w / a.nblk;
-  const int r = rh % G.n, h = rh / G.n;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int q0 = qb * BWD_BLK + wave * TILE;
-  const bool active = q0 < G.n;
-  const int q = q0 + l32;  // lane <-> query
-  const bool qok = q < G.n;
-
-  __shared__ __align__(16) T ks[TILE * LDS_ROW];      // K   [key][channel]
-  __shared__ __align__(16) T kT[HEAD_DIM * LDS_ROW];  // K^T [channel][key]
-  __shared__ __align__(16) T vs[TILE * LDS_ROW];      // V   [key][channel]
-
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
-  typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
-  float l2 = pos_inf();
-  zero_frags<T>(dalf);
-  if (qok) {
-    row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
-    row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
-    if constexpr (kSplitDA<T>) row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
-    l2 = a.lse2[((int64_t)h * G.n + r) * G.np + q];
-  } else {
-    zero_frags<T>(qf);
-    zero_frags<T>(daf);
-  }
-  const float c1 = G.scale * LOG2E;
-  // dQ = scale sum_k P (dP - D) K = scale (X - D Y) with X = sum_k P dP K,
-  // Y = sum_k P K and D = sum_k P dP, all accumulated in this one pass.
-  f32x16 xt = {}, yt = {};
-  float dpart = 0.f;
-  const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
-  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
-
-  for (int kt = 0; kt < G.nkt; ++kt) {
-    const uint32_t bits = kb[kt];
-    if (bits == 0u) continue;
-    __syncthreads();
-    if (tid < 128)
-      stage_tile<true, true>(a.k + rowbase, G.sPos, kt * TILE, bits, tid, ks, kT);
-    else
-      stage_tile<true, false>(a.v + rowbase, G.sPos, kt * TILE, bits, tid - 128, vs, (T*)nullptr);
-    __syncthreads();
-    if (!active) continue;
-
-    // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
-    f32x16 s;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = *(const f32x4*)(bq + kt * TILE + 8 * j);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) s[4 * j + e] = x[e];
-    }
-    typename M::frag af[M::KCH];
-    row_frags(ks + l32 * LDS_ROW, g, af);
-#pragma unroll
-    for (int t = 0; t < M::KCH; ++t) s = M::mma(af[t], qf[t], s);
-    if (bits != 0xffffffffu) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        if (!((bits >> acc_row(v, g)) & 1u)) s[v] = neg_inf();
-    }
-#pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2));
-    // dP^T = V dA^T, then P dP and its running sum D
-    row_frags(vs + l32 * LDS_ROW, g, af);
-    f32x16 dp = {};
-#pragma unroll
-    for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], daf[t], dp);
-    if constexpr (kSplitDA<T>) {
-#pragma unroll
-      for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
-    }
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      dp[v] *= s[v];
-      dpart += dp[v];
-    }
-    // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the tile's keys)
-    typename M::frag pf[M::PCH], xf[M::PCH];
-    quad_frags(kT + l32 * LDS_ROW, g, xf);
-    acc_frags(dp, pf);
-#pragma unroll
-    for (int t = 0; t < M::PCH; ++t) xt = M::mma(xf[t], pf[t], xt);
-    acc_frags(s, pf);
-#pragma unroll
-    for (int t = 0; t < M::PCH; ++t) yt = M::mma(xf[t], pf[t], yt);
-  }
-  if (!active) return;
-  const float dsum = wave_xor32_sum(dpart);
-  if (!qok) return;
-  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = dsum;
-  const int64_t base = rowbase + (int64_t)q * G.sPos;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    f32x4 x;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
-    store4(a.dq + base + 8 * j + 4 * g, x);
-  }
-}
-
-// ---- dBias -------------------------------------------------------------------------
-
-// One workgroup: 128 queries (wave <-> 32 queries, lane <-> query) x 128
-// keys (4 tiles) of one head, summed over the rows of one row chunk.
-template <typename T>
-__global__ __launch_bounds__(256) void db_kernel(BwdArgs<T> a) {
-  using M = Mma<T>;
-  const Geom& G = a.g;
-  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int kb = w % a.nblk;
+  const int kbk = w % a.nblk;
   const int qb = (w / a.nblk) % a.nblk;
   const int rc = (w / (a.nblk * a.nblk)) % a.nrc;
   const int h = w / (a.nblk * a.nblk * a.nrc);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int q0 = qb * BWD_BLK + wave * TILE;
-  if (q0 >= G.n) return;  // no barriers in this kernel
+  const int q0 = qb * BWD_BLK + (wave & 3) * TILE;
+  const int kh = wave >> 2;  // key half of the block
+  const bool active = q0 < G.n;
   const int q = q0 + l32;
   const bool qok = q < G.n;
+  const int qc = min(q, G.n - 1);  // clamped: loads stay in bounds
   const float c1 = G.scale * LOG2E;
 
-  f32x16 binit[BWD_WAVES], acc[BWD_WAVES];
-  const float* bq = a.bt + ((int64_t)h * G.np + q) * G.np + 4 * g;
-#pragma unroll
-  for (int st = 0; st < BWD_WAVES; ++st) {
-    acc[st] = f32x16{};
-    const int kt = kb * BWD_WAVES + st;
-    if (kt < G.nkt) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 x = *(const f32x4*)(bq + kt * TILE + 8 * j);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) binit[st][4 * j + e] = x[e];
-      }
-    }
-  }
+  __shared__ __align__(16) T ks[2 * 2 * ROW_TILE];  // K rows of the block's 128 keys, 2 buffers
+  __shared__ __align__(16) T vs[2 * 2 * ROW_TILE];  // V rows
 
+  const int kt0 = kbk * BWD_WAVES;  // first key tile of the block
+  const int last = G.n - 1;
+  f32x16 binit[2], acc[2];
+  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    acc[u] = f32x16{};
+    binit[u] = load_quads(bq + min(kt0 + 2 * kh + u, G.nkt - 1) * TILE);
+  }
+  auto row_bits = [&](int r, int half) -> uint64_t {
+    return block_bits(a.kbits + (int64_t)r * G.nkt, G.nkt, (kt0 >> 1) + half);
+  };
   const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
-  for (int r = r0; r < r1; ++r) {
+
+  // threads 0..255 stage K, 256..511 stage V; two 64-key halves each
+  const int st_t = tid & 255;
+  const T* stsrc = tid >= 256 ? a.v : a.k;
+  T* stdst = tid >= 256 ? vs : ks;
+  RowPiece<T> kvp[2];
+  typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+  typename M::frag nqf[M::KCH], ndaf[M::KCH], ndalf[M::KCH];
+  float l2 = pos_inf(), nd = 0.f, nl2 = pos_inf(), nnd = 0.f;
+  zero_frags<T>(ndalf);
+  zero_frags<T>(dalf);
+  auto load_row = [&](int r) {
     const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
-    typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
-    float l2 = pos_inf(), nd = 0.f;
-    zero_frags<T>(dalf);
-    if (qok) {
-      row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
-      row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
-      if constexpr (kSplitDA<T>) row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
-      const int64_t at = ((int64_t)h * G.n + r) * G.np + q;
-      l2 = a.lse2[at];
-      nd = -a.dsum[at];
-    } else {
-      zero_frags<T>(qf);
-      zero_frags<T>(daf);
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+      kvp[half].load(stsrc + rowbase, G.sPos, (kt0 + 2 * half) * TILE, last, st_t);
+    const int64_t qa = rowbase + (int64_t)qc * G.sPos;
+    row_frags(a.q + qa, g, nqf);
+    row_frags(a.da + qa, g, ndaf);
+    if constexpr (kSplitDA<T>) row_frags(a.dalo + qa, g, ndalf);
+    const int64_t at = ((int64_t)h * G.n + r) * G.np + qc;
+    nl2 = a.lse2[at];
+    nnd = -a.dsum[at];
+  };
+  auto store_row = [&](int r, int bf) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+      kvp[half].store(stdst + (2 * bf + half) * ROW_TILE, st_t, row_bits(r, half));
+#pragma unroll
+    for (int t = 0; t < M::KCH; ++t) {
+      qf[t] = nqf[t];
+      daf[t] = ndaf[t];
+      dalf[t] = ndalf[t];
     }
-    if (__all(l2 == pos_inf())) continue;  // no query of the wave has a valid key
-    f32x16 ndv;
+    l2 = qok ? nl2 : pos_inf();  // a clamped lane attends to nothing
+    nd = nnd;
+  };
+
+  if (r0 < r1) {
+    load_row(r0);
+    store_row(r0, 0);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int r = r0; r < r1; ++r) {
+    const int rn = min(r + 1, r1 - 1);
+    const uint64_t bb = row_bits(r, kh);  // this wave's two key tiles
+    load_row(rn);
+    if (active && bb != 0ull && !__all(l2 == pos_inf())) {
+      const f32x16 ndv = splat16(nd);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) ndv[v] = nd;
+      for (int u = 0; u < 2; ++u) {
+        const uint32_t bits = (uint32_t)(bb >> (32 * u));
+        if (bits == 0u) continue;
+        const int off = (2 * buf + kh) * ROW_TILE + (32 * u + l32) * LDS_ROW;
+        typename M::frag af[M::KCH];
+        row_frags(ks + off, g, af);
+        f32x16 s = M::mma(af[0], qf[0], binit[u]);
 #pragma unroll
-    for (int st = 0; st < BWD_WAVES; ++st) {
-      const int kt = kb * BWD_WAVES + st;
-      if (kt >= G.nkt) continue;
-      const uint32_t bits = a.kbits[(int64_t)r * G.nkt + kt];
-      if (bits == 0u) continue;
-      const int key = kt * TILE + l32;  // A-operand row of this lane
-      typename M::frag kf[M::KCH], vf[M::KCH];
-      if ((bits >> l32) & 1u) {
-        row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
-        row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
-      } else {
-        zero_frags<T>(kf);
-        zero_frags<T>(vf);
-      }
-      f32x16 s = binit[st];
+        for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], qf[t], s);
+        if (bits != 0xffffffffu) mask_rows(s, bits, g);
+        row_frags(vs + off, g, af);
+        f32x16 dp = M::mma(af[0], daf[0], ndv);
 #pragma unroll
-      for (int t = 0; t < M::KCH; ++t) s = M::mma(kf[t], qf[t], s);
-      if (bits != 0xffffffffu) {
+        for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], daf[t], dp);
+        if constexpr (kSplitDA<T>) {
+#pragma unroll
+          for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
+        }
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          if (!((bits >> acc_row(v, g)) & 1u)) s[v] = neg_inf();
+          acc[u][v] += __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2)) * dp[v];
       }
-      f32x16 dp = ndv;
-#pragma unroll
-      for (int t = 0; t < M::KCH; ++t) dp = M::mma(vf[t], daf[t], dp);
-      if constexpr (kSplitDA<T>) {
-#pragma unroll
-        for (int t = 0; t < M::KCH; ++t) dp = M::mma(vf[t], dalf[t], dp);
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        acc[st][v] += __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2)) * dp[v];
     }
+    if (r + 1 < r1) store_row(rn, buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
   }
+  if (!active) return;
   float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + q) * G.np + 4 * g;
 #pragma unroll
-  for (int st = 0; st < BWD_WAVES; ++st) {
-    const int kt = kb * BWD_WAVES + st;
+  for (int u = 0; u < 2; ++u) {
+    const int kt = kt0 + 2 * kh + u;
     if (kt >= G.nkt) continue;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       f32x4 x;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = acc[st][4 * j + e];
+      for (int e = 0; e < 4; ++e) x[e] = acc[u][4 * j + e];
       *(f32x4*)(slab + kt * TILE + 8 * j) = x;
     }
   }
@@ -467,8 +559,8 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   const int64_t npair = (int64_t)g.n * g.n * g.H;
   {
     KernelTimer t(K_BWD_PREP, s);
-    hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((npair + 255) / 256)), dim3(256), 0,
-                       s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+    hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((4 * npair + 255) / 256)), dim3(256),
+                       0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
   }
   if (g.np > g.n) {
     const int64_t npad = (int64_t)g.H * g.n * (g.np - g.n);
@@ -491,7 +583,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
-    hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
   }
   {
     const int64_t nred = (int64_t)g.H * g.n * g.n;

@@ -32,6 +32,7 @@ typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int HEAD_DIM = 32;  // d: channels per head
 constexpr int TILE = 32;      // rows / columns of one MFMA tile
@@ -125,6 +126,23 @@ __device__ inline void acc_frags(const f32x16& a, float (&f)[Mma<float>::PCH]) {
 // Row index (within the tile) of accumulator register v for lane half g.
 __device__ inline int acc_row(int v, int g) { return 8 * (v >> 2) + 4 * g + (v & 3); }
 
+// Set accumulator entries whose row bit in `bits` (bit i = row i of the
+// tile) is clear to -inf.  Only used on tiles with some masked row.
+__device__ inline void mask_rows(f32x16& s, uint32_t bits, int g) {
+  const uint32_t b = bits >> (4 * g);
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    if (!((b >> (8 * (v >> 2) + (v & 3))) & 1u)) s[v] = -__builtin_inff();
+}
+
+// Maximum of the 16 accumulator entries of a lane.
+__device__ inline float max16(const f32x16& s) {
+  float m = fmaxf(s[0], s[1]);
+#pragma unroll
+  for (int v = 2; v < 16; v += 2) m = fmaxf(m, fmaxf(s[v], s[v + 1]));
+  return m;
+}
+
 // Four consecutive elements <-> fp32.
 __device__ inline f32x4 load4(const bf16* p) {
   bf16x4 x = *(const bf16x4*)p;
@@ -148,7 +166,18 @@ __device__ inline int xcd_swizzle(int b, int total) {
   return (b % XCD) * per + b / XCD;
 }
 
-__device__ inline float wave_xor32_max(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-__device__ inline float wave_xor32_sum(float x) { return x + __shfl_xor(x, 32); }
+// Combine lane l with lane l ^ 32.  v_permlane32_swap(x, x) leaves
+// (x[l], x[l ^ 32]) in the two results, in one order or the other, so a
+// symmetric combination of them needs no select.
+__device__ inline float wave_xor32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float wave_xor32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 }  // namespace triattn

@@ -13,7 +13,12 @@
 //    initial MFMA accumulator, so adding it costs no vector instruction, and
 //    the softmax runs in base 2 with scale * log2(e) folded into one FMA;
 //  - the sigmoid gate is applied in the epilogue;
-//  - key tiles that are fully masked for the row are skipped.
+//  - key tiles that are fully masked for the row are skipped;
+//  - keys stream in blocks of 64 through double-buffered LDS: the next
+//    block's loads are issued before the current block is computed, one
+//    barrier per block;
+//  - the running max is only raised when it grows by more than 2^8, so the
+//    rescale of the accumulator is rare.
 #include "kernels.h"
 #include "stage.h"
 #include "timing.h"
@@ -81,6 +86,10 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
 
 constexpr int FWD_WAVES = 4;
 constexpr int FWD_QBLK = FWD_WAVES * TILE;  // queries per workgroup
+// The running max only moves when a lane's block max exceeds it by more than
+// this (log2 units), so unnormalised weights stay <= 2^8 and most blocks skip
+// the rescale of the accumulator.  Any stale max gives the same result.
+constexpr float STALE_MAX_SLACK = 8.f;
 
 template <typename T>
 struct FwdArgs {
@@ -94,7 +103,7 @@ struct FwdArgs {
 };
 
 template <typename T>
-__global__ __launch_bounds__(256) void fwd_kernel(FwdArgs<T> a) {
+__global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   using M = Mma<T>;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
@@ -106,10 +115,13 @@ __global__ __launch_bounds__(256) void fwd_kernel(FwdArgs<T> a) {
   const int q = q0 + l32;
   const bool qok = q < G.n;
 
-  __shared__ __align__(16) T ks[TILE * LDS_ROW];      // K tile  [key][channel]
-  __shared__ __align__(16) T vt[HEAD_DIM * LDS_ROW];  // V^T tile [channel][key]
+  __shared__ __align__(16) T ks[2 * ROW_TILE];    // K block   [key][channel], 2 buffers
+  __shared__ __align__(16) T vt[2 * TRANS_TILE];  // V^T block [channel][key], 2 buffers
 
   const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const T* kr = a.k + rowbase;
+  const T* vr = a.v + rowbase;
+  const int last = G.n - 1;
   typename M::frag qf[M::KCH];
   if (qok)
     row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
@@ -120,62 +132,76 @@ __global__ __launch_bounds__(256) void fwd_kernel(FwdArgs<T> a) {
   float m = neg_inf(), lsum = 0.f;
   f32x16 o = {};
   const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
+  const int nblk = (G.nkt + 1) >> 1;
+  // the lane's query row of the bias map (row 0 for idle waves: loads stay in bounds)
   const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
+  auto bias_tile = [&](int kt) { return load_quads(bq + min(kt, G.nkt - 1) * TILE); };
 
-  for (int kt = 0; kt < G.nkt; ++kt) {
-    const uint32_t bits = kb[kt];
-    if (bits == 0u) continue;  // no valid key in this tile (same for every wave)
-    __syncthreads();
-    if (tid < 128)
-      stage_tile<true, false>(a.k + rowbase, G.sPos, kt * TILE, bits, tid, ks, (T*)nullptr);
-    else
-      stage_tile<false, true>(a.v + rowbase, G.sPos, kt * TILE, bits, tid - 128, (T*)nullptr, vt);
-    __syncthreads();
-    if (!active) continue;
-
-    // s^T = bias + K Q^T for this lane's query and the tile's 32 keys
-    f32x16 s;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = *(const f32x4*)(bq + kt * TILE + 8 * j);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) s[4 * j + e] = x[e];
-    }
+  // one 32-key sub-tile: logits, online softmax (base 2, stale max), P V
+  auto sub_tile = [&](const T* ksb, const T* vtb, const f32x16& bias, uint32_t bits, int u) {
     typename M::frag kf[M::KCH];
-    row_frags(ks + l32 * LDS_ROW, g, kf);
+    row_frags(ksb + (32 * u + l32) * LDS_ROW, g, kf);
+    f32x16 s = M::mma(kf[0], qf[0], bias);  // s^T = bias + K Q^T
 #pragma unroll
-    for (int t = 0; t < M::KCH; ++t) s = M::mma(kf[t], qf[t], s);
-    if (bits != 0xffffffffu) {
+    for (int t = 1; t < M::KCH; ++t) s = M::mma(kf[t], qf[t], s);
+    if (bits != 0xffffffffu) mask_rows(s, bits, g);
+    const float mx = wave_xor32_max(max16(s)) * c1;
+    if (__any(mx > m + STALE_MAX_SLACK)) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      lsum *= alpha;
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        if (!((bits >> acc_row(v, g)) & 1u)) s[v] = neg_inf();
+      for (int v = 0; v < 16; ++v) o[v] *= alpha;
+      m = mnew;
     }
-
-    // online softmax in base 2: logit2 = s * scale * log2(e)
-    float mx = s[0];
-#pragma unroll
-    for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[v]);
-    mx = wave_xor32_max(mx);
-    const float mnew = fmaxf(m, mx * c1);
-    const float mu = mnew == neg_inf() ? 0.f : mnew;
-    const float alpha = __builtin_amdgcn_exp2f(m - mu);
     float ps = 0.f;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -mu));
+      s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m));
       ps += s[v];
     }
-    lsum = lsum * alpha + ps;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) o[v] *= alpha;
-    m = mnew;
-
-    // O^T += V^T P^T
+    lsum += ps;
     typename M::frag pf[M::PCH], vf[M::PCH];
     acc_frags(s, pf);
-    quad_frags(vt + l32 * LDS_ROW, g, vf);
+    quad_frags(vtb + l32 * LDS_TROW + 32 * u, g, vf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) o = M::mma(vf[t], pf[t], o);
+    for (int t = 0; t < M::PCH; ++t) o = M::mma(vf[t], pf[t], o);  // O^T += V^T P^T
+  };
+
+  RowPiece<T> kp;
+  PairPiece<T> vp;
+  uint64_t bb = block_bits(kb, G.nkt, 0);
+  kp.load(kr, G.sPos, 0, last, tid);
+  vp.load(vr, G.sPos, 0, last, tid);
+  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
+  kp.store(ks, tid, bb);
+  vp.validate(tid, bb);
+  vp.store_trans(vt, tid);
+  __syncthreads();
+  int buf = 0;
+  for (int b = 0; b < nblk; ++b) {
+    // issue the next block's loads (the last block reloads itself, unused)
+    const int bn = min(b + 1, nblk - 1);
+    const uint64_t bbn = block_bits(kb, G.nkt, bn);
+    kp.load(kr, G.sPos, bn * SPAN, last, tid);
+    vp.load(vr, G.sPos, bn * SPAN, last, tid);
+    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
+    if (active) {
+      const T* ksb = ks + buf * ROW_TILE;
+      const T* vtb = vt + buf * TRANS_TILE;
+      if ((uint32_t)bb) sub_tile(ksb, vtb, b0, (uint32_t)bb, 0);
+      if ((uint32_t)(bb >> 32)) sub_tile(ksb, vtb, b1, (uint32_t)(bb >> 32), 1);
+    }
+    if (b + 1 < nblk) {
+      kp.store(ks + (buf ^ 1) * ROW_TILE, tid, bbn);
+      vp.validate(tid, bbn);
+      vp.store_trans(vt + (buf ^ 1) * TRANS_TILE, tid);
+    }
+    __syncthreads();
+    b0 = n0;
+    b1 = n1;
+    bb = bbn;
+    buf ^= 1;
   }
   if (!active) return;
 

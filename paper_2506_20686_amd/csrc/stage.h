@@ -1,61 +1,155 @@
-// LDS staging of 32 x 32 operand tiles (one head of 32 consecutive pair
-// positions of one row), shared by the waves of a workgroup.
+// Staging of operand blocks (64 consecutive pair positions x 32 channels of
+// one row and head) from HBM through registers into LDS.  A workgroup of 256
+// threads moves one block per call; loads for the next block are issued
+// before the current block is computed and stored to the other LDS buffer
+// after it, so HBM latency hides behind the MFMA/VALU work.
+//
+// Loads never depend on the validity of a position: the position is clamped
+// into [0, last] (every address stays in bounds) and invalid positions are
+// replaced by zeros only when the piece is stored to LDS.  Conditional loads
+// would make the compiler wait for them right away.
 #pragma once
 
 #include "common.h"
 
 namespace triattn {
 
-// Padded LDS row length (elements): 32 data + 8 pad keeps every row 16-byte
-// aligned and spreads consecutive rows over different banks.
-constexpr int LDS_ROW = HEAD_DIM + 8;
+constexpr int SPAN = 64;               // positions per staged block
+constexpr int LDS_ROW = HEAD_DIM + 8;  // row-major tile [position][channel]: 80-byte rows (bf16)
+// Transposed tile [channel][position].  The row stride is an odd multiple of
+// 8 bytes (136 bytes for bf16, 272 for fp32), so the quad reads of 32
+// consecutive rows fall on 32 different bank pairs.
+constexpr int LDS_TROW = SPAN + 4;
+constexpr int ROW_TILE = SPAN * LDS_ROW;
+constexpr int TRANS_TILE = HEAD_DIM * LDS_TROW;
 
-// 128 threads (u = 0..127) copy positions start .. start+31 of one row:
-// thread u moves positions p, p+1 (p = 2 (u / 8)) x channels c0 .. c0+3
-// (c0 = 4 (u % 8)).  Positions whose bit in `valid` is clear are written as
-// zeros.  ROW writes tile[p][c] (row-major), TRANS writes tileT[c][p].
-template <bool ROW, bool TRANS, typename T>
-__device__ inline void stage_tile(const T* src, int64_t sPos, int start, uint32_t valid, int u,
-                                  T* tile, T* tileT);
+template <typename T>
+struct Vec;
+template <>
+struct Vec<bf16> {
+  using v4 = bf16x4;
+};
+template <>
+struct Vec<float> {
+  using v4 = f32x4;
+};
 
-template <bool ROW, bool TRANS>
-__device__ inline void stage_tile(const bf16* src, int64_t sPos, int start, uint32_t valid,
-                                  int u, bf16* tile, bf16* tileT) {
-  const int p = 2 * (u >> 3), c0 = 4 * (u & 7);
-  bf16x4 x0 = {}, x1 = {};
-  if ((valid >> p) & 1u) x0 = *(const bf16x4*)(src + (int64_t)(start + p) * sPos + c0);
-  if ((valid >> (p + 1)) & 1u) x1 = *(const bf16x4*)(src + (int64_t)(start + p + 1) * sPos + c0);
-  if (ROW) {
-    *(bf16x4*)(tile + p * LDS_ROW + c0) = x0;
-    *(bf16x4*)(tile + (p + 1) * LDS_ROW + c0) = x1;
+__device__ inline bool bit64(uint64_t b, int i) { return (b >> i) & 1ull; }
+
+// One position x 8 channels: thread t holds position t / 4, channels
+// 8 (t % 4) .. +7.  Feeds a row-major tile.
+template <typename T>
+struct RowPiece;
+
+template <>
+struct RowPiece<bf16> {
+  bf16x8 x;
+  __device__ inline void load(const bf16* src, int64_t sPos, int start, int last, int t) {
+    const int p = min(start + (t >> 2), last);
+    x = *(const bf16x8*)(src + (int64_t)p * sPos + 8 * (t & 3));
   }
-  if (TRANS) {
+  __device__ inline void store(bf16* tile, int t, uint64_t valid) const {
+    const bf16x8 v = bit64(valid, t >> 2) ? x : bf16x8{};
+    *(bf16x8*)(tile + (t >> 2) * LDS_ROW + 8 * (t & 3)) = v;
+  }
+};
+
+template <>
+struct RowPiece<float> {
+  f32x4 lo, hi;
+  __device__ inline void load(const float* src, int64_t sPos, int start, int last, int t) {
+    const int p = min(start + (t >> 2), last);
+    const float* s = src + (int64_t)p * sPos + 8 * (t & 3);
+    lo = *(const f32x4*)s;
+    hi = *(const f32x4*)(s + 4);
+  }
+  __device__ inline void store(float* tile, int t, uint64_t valid) const {
+    const bool ok = bit64(valid, t >> 2);
+    float* d = tile + (t >> 2) * LDS_ROW + 8 * (t & 3);
+    *(f32x4*)d = ok ? lo : f32x4{};
+    *(f32x4*)(d + 4) = ok ? hi : f32x4{};
+  }
+};
+
+// Two positions x 4 channels: thread t holds positions p, p + 1 with
+// p = 2 (t / 8) and channels 4 (t % 8) .. +3.  Feeds a row-major tile, a
+// transposed tile, or both.  Call validate() before storing.
+template <typename T>
+struct PairPiece {
+  using V4 = typename Vec<T>::v4;
+  V4 x0, x1;
+  __device__ inline void load(const T* src, int64_t sPos, int start, int last, int t) {
+    const int p = start + 2 * (t >> 3), c0 = 4 * (t & 7);
+    x0 = *(const V4*)(src + (int64_t)min(p, last) * sPos + c0);
+    x1 = *(const V4*)(src + (int64_t)min(p + 1, last) * sPos + c0);
+  }
+  __device__ inline void validate(int t, uint64_t valid) {
+    const int p = 2 * (t >> 3);
+    if (!bit64(valid, p)) x0 = V4{};
+    if (!bit64(valid, p + 1)) x1 = V4{};
+  }
+  __device__ inline void store_rows(T* tile, int t) const {
+    const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
+    *(V4*)(tile + p * LDS_ROW + c0) = x0;
+    *(V4*)(tile + (p + 1) * LDS_ROW + c0) = x1;
+  }
+  __device__ inline void store_trans(T* tileT, int t) const;
+};
+
+// Interleave the two positions' bf16 channels into 32-bit words with integer
+// ops (channel j of positions p and p + 1 form one word).
+template <>
+__device__ inline void PairPiece<bf16>::store_trans(bf16* tileT, int t) const {
+  const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
+  const u32x2 a = __builtin_bit_cast(u32x2, x0), b = __builtin_bit_cast(u32x2, x1);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) *(bf16x2*)(tileT + (c0 + j) * LDS_ROW + p) = bf16x2{x0[j], x1[j]};
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t x = a[j >> 1], y = b[j >> 1];
+    const uint32_t w = (j & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
+    *(uint32_t*)(tileT + (c0 + j) * LDS_TROW + p) = w;
   }
 }
-
-template <bool ROW, bool TRANS>
-__device__ inline void stage_tile(const float* src, int64_t sPos, int start, uint32_t valid,
-                                  int u, float* tile, float* tileT) {
-  const int p = 2 * (u >> 3), c0 = 4 * (u & 7);
-  f32x4 x0 = {}, x1 = {};
-  if ((valid >> p) & 1u) x0 = *(const f32x4*)(src + (int64_t)(start + p) * sPos + c0);
-  if ((valid >> (p + 1)) & 1u) x1 = *(const f32x4*)(src + (int64_t)(start + p + 1) * sPos + c0);
-  if (ROW) {
-    *(f32x4*)(tile + p * LDS_ROW + c0) = x0;
-    *(f32x4*)(tile + (p + 1) * LDS_ROW + c0) = x1;
-  }
-  if (TRANS) {
+template <>
+__device__ inline void PairPiece<float>::store_trans(float* tileT, int t) const {
+  const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) *(f32x2*)(tileT + (c0 + j) * LDS_ROW + p) = f32x2{x0[j], x1[j]};
-  }
+  for (int j = 0; j < 4; ++j) *(f32x2*)(tileT + (c0 + j) * LDS_TROW + p) = f32x2{x0[j], x1[j]};
 }
 
-// Bits of positions start .. start+31 that lie inside [0, n).
-__device__ inline uint32_t range_bits(int start, int n) {
+// Bits of positions start .. start+63 that lie inside [0, n).
+__device__ inline uint64_t range_bits64(int start, int n) {
   const int m = n - start;
-  return m >= 32 ? 0xffffffffu : (m <= 0 ? 0u : ((1u << m) - 1u));
+  return m >= 64 ? ~0ull : (m <= 0 ? 0ull : ((1ull << m) - 1ull));
+}
+
+// Key-valid bits of 64-key block b of a row: words 2 b and 2 b + 1 of the
+// row's key bits (a word past the last tile counts as empty; the reads stay
+// in bounds).
+__device__ inline uint64_t block_bits(const uint32_t* kb, int nkt, int b) {
+  const int t = 2 * b;
+  const uint32_t lo = kb[min(t, nkt - 1)];
+  const uint32_t hi = kb[min(t + 1, nkt - 1)];
+  return (t < nkt ? (uint64_t)lo : 0ull) | (t + 1 < nkt ? (uint64_t)hi << 32 : 0ull);
+}
+
+// Accumulator registers <- the four quads this lane owns of a 32-wide run of
+// fp32 (elements 8 j + 4 g .. +3).  `p` must already point at element 4 g.
+__device__ inline f32x16 load_quads(const float* p) {
+  f32x16 s;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const f32x4 x = *(const f32x4*)(p + 8 * j);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[4 * j + e] = x[e];
+  }
+  return s;
+}
+
+__device__ inline f32x16 splat16(float x) {
+  f32x16 s;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) s[v] = x;
+  return s;
 }
 
 }  // namespace triattn
