@@ -153,8 +153,10 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   float dpart = 0.f;
   const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
   const int nblk = (G.nkt + 1) >> 1;
-  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
-  auto bias_tile = [&](int kt) { return load_quads(bq + min(kt, G.nkt - 1) * TILE); };
+  const int qt = active ? q0 / TILE : 0;
+  auto bias_tile = [&](int kt) {
+    return load_frag_tile(frag_tile(a.bt, h, qt, min(kt, G.nkt - 1), G.nkt), lane);
+  };
 
   auto sub_tile = [&](const T* ksb, const T* kTb, const T* vsb, const f32x16& bias, uint32_t bits,
                       int u) {
@@ -286,14 +288,13 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   }
   const float c1 = G.scale * LOG2E;
   f32x16 dkt = {}, dvt = {};
-  // the lane's key row of the key-major bias (row 0 for idle waves)
-  const float* bk = a.btT + ((int64_t)h * G.np + (active ? key : 0)) * G.np + 4 * g;
+  const int ktc = active ? kt : 0;  // key tile of the key-major bias (0 for idle waves)
   const float* l2row = a.lse2 + ((int64_t)h * G.n + r) * G.np;
   const float* drow = a.dsum + ((int64_t)h * G.n + r) * G.np;
   const int nblk = (G.nkt + 1) >> 1;  // query blocks of 64
   const float kmask = kvalid ? 0.f : neg_inf();
   auto bias_tile = [&](int t) {
-    f32x16 x = load_quads(bk + min(t, G.nkt - 1) * TILE);
+    f32x16 x = load_frag_tile(frag_tile(a.btT, h, ktc, min(t, G.nkt - 1), G.nkt), lane);
 #pragma unroll
     for (int v = 0; v < 16; ++v) x[v] += kmask;  // -inf for a masked key
     return x;
@@ -429,11 +430,12 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   const int kt0 = kbk * BWD_WAVES;  // first key tile of the block
   const int last = G.n - 1;
   f32x16 binit[2], acc[2];
-  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
+  const int qt = active ? q0 / TILE : 0;
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     acc[u] = f32x16{};
-    binit[u] = load_quads(bq + min(kt0 + 2 * kh + u, G.nkt - 1) * TILE);
+    binit[u] =
+        load_frag_tile(frag_tile(a.bt, h, qt, min(kt0 + 2 * kh + u, G.nkt - 1), G.nkt), lane);
   }
   auto row_bits = [&](int r, int half) -> uint64_t {
     return block_bits(a.kbits + (int64_t)r * G.nkt, G.nkt, (kt0 >> 1) + half);

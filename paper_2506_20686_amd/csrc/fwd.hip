@@ -27,16 +27,23 @@ namespace triattn {
 
 // ---- preparation ------------------------------------------------------------------
 
-// bt[h][x][y] = bias(query x, key y, h) / scale and btT[h][x][y] =
-// bias(query y, key x, h) / scale over the zero-padded np x np map.  The
-// starting node reads bias[q][k][h], the ending node bias[k][q][h].
+// bias / scale over the zero-padded np x np map, in accumulator order (see
+// frag_tile): x = 32 t1 + l % 32 is the lane's column, y = 32 t2 + 8 j +
+// 4 (l / 32) + e its row.  bt holds bias(query x, key y) for the kernels
+// whose lanes own queries; btT holds bias(query y, key x) for the kernel
+// whose lanes own keys.  The starting node reads bias[q][k][h], the ending
+// node bias[k][q][h].
 template <typename T>
 __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const T* bias,
                                                         float* bt, float* btT) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t np = G.np, total = (int64_t)G.H * np * np;
   if (idx >= total) return;
-  const int y = (int)(idx % np), x = (int)((idx / np) % np), h = (int)(idx / (np * np));
+  const int nt = G.nkt;
+  const int e = (int)(idx & 3), l = (int)((idx >> 2) & 63), j = (int)((idx >> 8) & 3);
+  const int64_t tt = idx >> 10;
+  const int t2 = (int)(tt % nt), t1 = (int)((tt / nt) % nt), h = (int)(tt / ((int64_t)nt * nt));
+  const int x = 32 * t1 + (l & 31), y = 32 * t2 + 8 * j + 4 * (l >> 5) + e;
   const int n = G.n;
   auto at = [&](int qi, int ki) -> int64_t {
     return node == 0 ? ((int64_t)qi * n + ki) * G.H + h : ((int64_t)ki * n + qi) * G.H + h;
@@ -133,9 +140,11 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   f32x16 o = {};
   const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
   const int nblk = (G.nkt + 1) >> 1;
-  // the lane's query row of the bias map (row 0 for idle waves: loads stay in bounds)
-  const float* bq = a.bt + ((int64_t)h * G.np + (active ? q : 0)) * G.np + 4 * g;
-  auto bias_tile = [&](int kt) { return load_quads(bq + min(kt, G.nkt - 1) * TILE); };
+  // bias tiles of this wave's queries (tile 0 for idle waves: loads stay in bounds)
+  const int qt = active ? q0 / TILE : 0;
+  auto bias_tile = [&](int kt) {
+    return load_frag_tile(frag_tile(a.bt, h, qt, min(kt, G.nkt - 1), G.nkt), lane);
+  };
 
   // one 32-key sub-tile: logits, online softmax (base 2, stale max), P V
   auto sub_tile = [&](const T* ksb, const T* vtb, const f32x16& bias, uint32_t bits, int u) {

@@ -24,8 +24,9 @@ struct Geom {
 
 // Workspace pieces (device pointers), see api.hip for sizes.
 struct Prep {
-  float* bt;       // [H][np][np]  bias(q, k) / scale, query-major (zero padded)
-  float* btT;      // [H][np][np]  the same, key-major (backward only; may be null)
+  float* bt;       // [H][np/32][np/32][1024] bias(q, k) / scale in accumulator order,
+                   //   lanes <-> queries (zero padded)
+  float* btT;      // the same with lanes <-> keys (backward only; may be null)
   uint32_t* kbits; // [n][nkt]     bit e of word t: key 32 t + e is valid for that row
 };
 

@@ -145,6 +145,25 @@ __device__ inline f32x16 load_quads(const float* p) {
   return s;
 }
 
+// Bias maps in accumulator order.  The 32 x 32 values of tile (t1, t2) of a
+// head are stored as [j][lane][e] (j, e = 0..3), lane l holding register
+// 4 j + e of the accumulator (its column is 32 t1 + l % 32, its row
+// 32 t2 + 8 j + 4 (l / 32) + e).  A wave then reads each j as one 1 KB
+// contiguous run instead of 32 scattered rows.
+__device__ inline const float* frag_tile(const float* map, int h, int t1, int t2, int nt) {
+  return map + (((int64_t)h * nt + t1) * nt + t2) * 1024;
+}
+__device__ inline f32x16 load_frag_tile(const float* tile, int lane) {
+  f32x16 s;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const f32x4 x = *(const f32x4*)(tile + (j * 64 + lane) * 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s[4 * j + e] = x[e];
+  }
+  return s;
+}
+
 __device__ inline f32x16 splat16(float x) {
   f32x16 s;
 #pragma unroll
