@@ -199,25 +199,26 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   uint64_t bb = block_bits(kb, G.nkt, 0);
   kp.load(kr, G.sPos, 0, last, tid);
   vp.load(vr, G.sPos, 0, last, tid);
-  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
+  f32x16 bA0 = bias_tile(0), bA1 = bias_tile(1), bB0, bB1;
   kp.validate(tid, bb);
   kp.store_rows(ks, tid);
   kp.store_trans(kT, tid);
   vp.store(vs, tid, bb);
   __syncthreads();
-  int buf = 0;
-  for (int b = 0; b < nblk; ++b) {
+  auto step = [&](int b, const f32x16& c0, const f32x16& c1, f32x16& n0, f32x16& n1) {
     const int bn = min(b + 1, nblk - 1);
     const uint64_t bbn = block_bits(kb, G.nkt, bn);
     kp.load(kr, G.sPos, bn * SPAN, last, tid);
     vp.load(vr, G.sPos, bn * SPAN, last, tid);
-    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
+    n0 = bias_tile(2 * bn);
+    n1 = bias_tile(2 * bn + 1);
+    const int buf = b & 1;
     if (active) {
       const T* ksb = ks + buf * ROW_TILE;
       const T* kTb = kT + buf * TRANS_TILE;
       const T* vsb = vs + buf * ROW_TILE;
-      if ((uint32_t)bb) sub_tile(ksb, kTb, vsb, b0, (uint32_t)bb, 0);
-      if ((uint32_t)(bb >> 32)) sub_tile(ksb, kTb, vsb, b1, (uint32_t)(bb >> 32), 1);
+      if ((uint32_t)bb) sub_tile(ksb, kTb, vsb, c0, (uint32_t)bb, 0);
+      if ((uint32_t)(bb >> 32)) sub_tile(ksb, kTb, vsb, c1, (uint32_t)(bb >> 32), 1);
     }
     if (b + 1 < nblk) {
       kp.validate(tid, bbn);
@@ -226,10 +227,12 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
       vp.store(vs + (buf ^ 1) * ROW_TILE, tid, bbn);
     }
     __syncthreads();
-    b0 = n0;
-    b1 = n1;
     bb = bbn;
-    buf ^= 1;
+  };
+  for (int b = 0; b < nblk; b += 2) {
+    step(b, bA0, bA1, bB0, bB1);
+    if (b + 1 >= nblk) break;
+    step(b + 1, bB0, bB1, bA0, bA1);
   }
   if (!active) return;
   const float dsum = wave_xor32_sum(dpart);
@@ -363,23 +366,26 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   };
 
   load_block(0);
-  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
+  f32x16 bA0 = bias_tile(0), bA1 = bias_tile(1), bB0, bB1;
   store_block(0, 0);
   __syncthreads();
-  int buf = 0;
-  for (int b = 0; b < nblk; ++b) {
+  auto step = [&](int b, const f32x16& c0, const f32x16& c1, f32x16& n0, f32x16& n1) {
     const int bn = min(b + 1, nblk - 1);
     load_block(bn);
-    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
+    n0 = bias_tile(2 * bn);
+    n1 = bias_tile(2 * bn + 1);
+    const int buf = b & 1;
     if (work) {
-      sub_tile(buf, b0, 0);
-      if (2 * b + 1 < G.nkt) sub_tile(buf, b1, 1);
+      sub_tile(buf, c0, 0);
+      if (2 * b + 1 < G.nkt) sub_tile(buf, c1, 1);
     }
     if (b + 1 < nblk) store_block(bn, buf ^ 1);
     __syncthreads();
-    b0 = n0;
-    b1 = n1;
-    buf ^= 1;
+  };
+  for (int b = 0; b < nblk; b += 2) {
+    step(b, bA0, bA1, bB0, bB1);
+    if (b + 1 >= nblk) break;
+    step(b + 1, bB0, bB1, bA0, bA1);
   }
   if (!active || key >= G.n) return;
   const int64_t base = rowbase + (int64_t)key * G.sPos;
@@ -400,12 +406,14 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
 // ---- dBias ---------------------------------------------------------------------------
 
 constexpr int DB_WAVES = 8;  // 4 query tiles x 2 key halves
+constexpr int DB_ROWS = 2 * SPAN;  // keys (and queries) per workgroup block
 
 // One workgroup: 128 queries x 128 keys of one head, summed over the rows of
 // one row chunk.  Wave w owns query tile w % 4 (lane <-> query) and key tiles
-// 2 (w / 4), 2 (w / 4) + 1.  Per row the block's K and V (128 keys each) are
-// staged in LDS, double-buffered, and each wave prefetches the next row's Q,
-// dA, lse2 and D.  The bias tiles stay in registers for all rows.
+// 2 (w / 4), 2 (w / 4) + 1.  Per row, K and V of the 128 keys and Q, dA (and
+// its low part), lse2 and -D of the 128 queries are loaded with coalesced
+// 16-byte pieces (issued before the previous row's compute) and staged in
+// LDS.  The bias tiles stay in registers for all rows.
 template <typename T>
 __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
@@ -416,18 +424,22 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   const int rc = (w / (a.nblk * a.nblk)) % a.nrc;
   const int h = w / (a.nblk * a.nblk * a.nrc);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int q0 = qb * BWD_BLK + (wave & 3) * TILE;
+  const int qw = (wave & 3) * TILE;  // this wave's queries within the block
+  const int q0 = qb * DB_ROWS + qw;
   const int kh = wave >> 2;  // key half of the block
   const bool active = q0 < G.n;
-  const int q = q0 + l32;
-  const bool qok = q < G.n;
-  const int qc = min(q, G.n - 1);  // clamped: loads stay in bounds
   const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) T ks[2 * 2 * ROW_TILE];  // K rows of the block's 128 keys, 2 buffers
-  __shared__ __align__(16) T vs[2 * 2 * ROW_TILE];  // V rows
+  __shared__ __align__(16) T ks[2 * ROW_TILE];   // K  [key][channel] of the 128 keys
+  __shared__ __align__(16) T vs[2 * ROW_TILE];   // V
+  __shared__ __align__(16) T qs[2 * ROW_TILE];   // Q  [query][channel] of the 128 queries
+  __shared__ __align__(16) T das[2 * ROW_TILE];  // dA
+  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * ROW_TILE : 1];
+  __shared__ __align__(16) float l2s[DB_ROWS];   // lse2 of the queries (+inf: none valid)
+  __shared__ __align__(16) float nds[DB_ROWS];   // -D
 
   const int kt0 = kbk * BWD_WAVES;  // first key tile of the block
+  const int kstart = kt0 * TILE, qstart = qb * DB_ROWS;
   const int last = G.n - 1;
   f32x16 binit[2], acc[2];
   const int qt = active ? q0 / TILE : 0;
@@ -442,60 +454,56 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   };
   const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
 
-  // threads 0..255 stage K, 256..511 stage V; two 64-key halves each
-  const int st_t = tid & 255;
-  const T* stsrc = tid >= 256 ? a.v : a.k;
-  T* stdst = tid >= 256 ? vs : ks;
-  RowPiece<T> kvp[2];
-  typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
-  typename M::frag nqf[M::KCH], ndaf[M::KCH], ndalf[M::KCH];
-  float l2 = pos_inf(), nd = 0.f, nl2 = pos_inf(), nnd = 0.f;
-  zero_frags<T>(ndalf);
-  zero_frags<T>(dalf);
+  // thread -> (half of the 128 positions, piece index within the half)
+  const int half = tid >> 8, pt = tid & 255;
+  const uint64_t qvalid = range_bits64(qstart + SPAN * half, G.n);
+  RowPiece<T> kp, vp, qp, dap, dlp;
+  float sv = 0.f;  // thread < 128: lse2 of query tid; 128 <= thread < 256: -D of query tid-128
+  const int sq = min(qstart + (tid & 127), G.np - 1);
   auto load_row = [&](int r) {
     const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
-#pragma unroll
-    for (int half = 0; half < 2; ++half)
-      kvp[half].load(stsrc + rowbase, G.sPos, (kt0 + 2 * half) * TILE, last, st_t);
-    const int64_t qa = rowbase + (int64_t)qc * G.sPos;
-    row_frags(a.q + qa, g, nqf);
-    row_frags(a.da + qa, g, ndaf);
-    if constexpr (kSplitDA<T>) row_frags(a.dalo + qa, g, ndalf);
-    const int64_t at = ((int64_t)h * G.n + r) * G.np + qc;
-    nl2 = a.lse2[at];
-    nnd = -a.dsum[at];
+    kp.load(a.k + rowbase, G.sPos, kstart + SPAN * half, last, pt);
+    vp.load(a.v + rowbase, G.sPos, kstart + SPAN * half, last, pt);
+    qp.load(a.q + rowbase, G.sPos, qstart + SPAN * half, last, pt);
+    dap.load(a.da + rowbase, G.sPos, qstart + SPAN * half, last, pt);
+    if constexpr (kSplitDA<T>) dlp.load(a.dalo + rowbase, G.sPos, qstart + SPAN * half, last, pt);
+    const int64_t at = ((int64_t)h * G.n + r) * G.np + sq;
+    sv = tid < DB_ROWS ? a.lse2[at] : -a.dsum[at];
   };
-  auto store_row = [&](int r, int bf) {
-#pragma unroll
-    for (int half = 0; half < 2; ++half)
-      kvp[half].store(stdst + (2 * bf + half) * ROW_TILE, st_t, row_bits(r, half));
-#pragma unroll
-    for (int t = 0; t < M::KCH; ++t) {
-      qf[t] = nqf[t];
-      daf[t] = ndaf[t];
-      dalf[t] = ndalf[t];
-    }
-    l2 = qok ? nl2 : pos_inf();  // a clamped lane attends to nothing
-    nd = nnd;
+  auto store_row = [&](int r) {
+    const uint64_t kv = row_bits(r, half);
+    kp.store(ks + half * ROW_TILE, pt, kv);
+    vp.store(vs + half * ROW_TILE, pt, kv);
+    qp.store(qs + half * ROW_TILE, pt, qvalid);
+    dap.store(das + half * ROW_TILE, pt, qvalid);
+    if constexpr (kSplitDA<T>) dlp.store(dals + half * ROW_TILE, pt, qvalid);
+    const bool in = qstart + (tid & 127) < G.n;
+    if (tid < DB_ROWS)
+      l2s[tid] = in ? sv : pos_inf();
+    else if (tid < 2 * DB_ROWS)
+      nds[tid - DB_ROWS] = in ? sv : 0.f;
   };
 
   if (r0 < r1) {
     load_row(r0);
-    store_row(r0, 0);
+    store_row(r0);
   }
   __syncthreads();
-  int buf = 0;
   for (int r = r0; r < r1; ++r) {
-    const int rn = min(r + 1, r1 - 1);
     const uint64_t bb = row_bits(r, kh);  // this wave's two key tiles
-    load_row(rn);
+    load_row(min(r + 1, r1 - 1));         // the last row reloads itself, unused
+    const float l2 = l2s[qw + l32];
     if (active && bb != 0ull && !__all(l2 == pos_inf())) {
-      const f32x16 ndv = splat16(nd);
+      typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+      row_frags(qs + (qw + l32) * LDS_ROW, g, qf);
+      row_frags(das + (qw + l32) * LDS_ROW, g, daf);
+      if constexpr (kSplitDA<T>) row_frags(dals + (qw + l32) * LDS_ROW, g, dalf);
+      const f32x16 ndv = splat16(nds[qw + l32]);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const uint32_t bits = (uint32_t)(bb >> (32 * u));
         if (bits == 0u) continue;
-        const int off = (2 * buf + kh) * ROW_TILE + (32 * u + l32) * LDS_ROW;
+        const int off = (SPAN * kh + 32 * u + l32) * LDS_ROW;
         typename M::frag af[M::KCH];
         row_frags(ks + off, g, af);
         f32x16 s = M::mma(af[0], qf[0], binit[u]);
@@ -515,12 +523,12 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
           acc[u][v] += __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2)) * dp[v];
       }
     }
-    if (r + 1 < r1) store_row(rn, buf ^ 1);
+    __syncthreads();  // everyone is done with row r's tiles
+    if (r + 1 < r1) store_row(r + 1);
     __syncthreads();
-    buf ^= 1;
   }
   if (!active) return;
-  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + q) * G.np + 4 * g;
+  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + q0 + l32) * G.np + 4 * g;
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int kt = kt0 + 2 * kh + u;

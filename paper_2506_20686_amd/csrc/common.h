@@ -135,13 +135,50 @@ __device__ inline void mask_rows(f32x16& s, uint32_t bits, int g) {
     if (!((b >> (8 * (v >> 2) + (v & 3))) & 1u)) s[v] = -__builtin_inff();
 }
 
-// Maximum of the 16 accumulator entries of a lane.
+// Maximum of the 16 accumulator entries of a lane (a chain of 3-input maxes).
 __device__ inline float max16(const f32x16& s) {
-  float m = fmaxf(s[0], s[1]);
+  float m = fmaxf(fmaxf(s[0], s[1]), s[2]);
 #pragma unroll
-  for (int v = 2; v < 16; v += 2) m = fmaxf(m, fmaxf(s[v], s[v + 1]));
-  return m;
+  for (int v = 3; v < 15; v += 2) m = fmaxf(fmaxf(m, s[v]), s[v + 1]);
+  return fmaxf(m, s[15]);
 }
+
+// Tree reductions (short dependency chains) over one or two accumulators.
+__device__ inline float max32(const f32x16& a, const f32x16& b) {
+  float t[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    t[i] = fmaxf(fmaxf(a[4 * i], a[4 * i + 1]), fmaxf(a[4 * i + 2], a[4 * i + 3]));
+    t[4 + i] = fmaxf(fmaxf(b[4 * i], b[4 * i + 1]), fmaxf(b[4 * i + 2], b[4 * i + 3]));
+  }
+  return fmaxf(fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3])),
+               fmaxf(fmaxf(t[4], t[5]), fmaxf(t[6], t[7])));
+}
+__device__ inline float sum16(const f32x16& a) {
+  float t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) t[i] = (a[4 * i] + a[4 * i + 1]) + (a[4 * i + 2] + a[4 * i + 3]);
+  return (t[0] + t[1]) + (t[2] + t[3]);
+}
+
+// A-operand that sums a B operand's contraction slots into accumulator row 0:
+// row 0 is all ones, the other rows are zero.  D += ones_row0 * B then adds
+// sum_k B[k][n] to register 0 of the lanes of half g = 0 (row 0), and leaves
+// the other rows at zero.  Moves a per-lane row sum from the VALU to the MFMA.
+template <typename F>
+__device__ inline F ones_row0(int l32);
+template <>
+__device__ inline bf16x8 ones_row0<bf16x8>(int l32) {
+  const bf16 v = l32 == 0 ? (bf16)1.f : (bf16)0.f;
+  return bf16x8{v, v, v, v, v, v, v, v};
+}
+template <>
+__device__ inline float ones_row0<float>(int l32) {
+  return l32 == 0 ? 1.f : 0.f;
+}
+
+// Hardware reciprocal (about 1 ulp), for normalisation and the sigmoid.
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // Four consecutive elements <-> fp32.
 __device__ inline f32x4 load4(const bf16* p) {

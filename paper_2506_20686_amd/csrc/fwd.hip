@@ -93,6 +93,7 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
 
 constexpr int FWD_WAVES = 4;
 constexpr int FWD_QBLK = FWD_WAVES * TILE;  // queries per workgroup
+constexpr int FWD_ROWS = 2;                 // rows per workgroup (they share the bias tiles)
 // The running max only moves when a lane's block max exceeds it by more than
 // this (log2 units), so unnormalised weights stay <= 2^8 and most blocks skip
 // the rescale of the accumulator.  Any stale max gives the same result.
@@ -109,135 +110,241 @@ struct FwdArgs {
   int nqb;  // query blocks per row
 };
 
+// Online-softmax state of one (row, 32 queries) pair of a wave.  The row
+// sums of P accumulate on the MFMA: register 0 of the lanes of half 0 of
+// `l` holds sum_k P for the lane's query (see ones_row0).
+struct SoftmaxState {
+  float m;
+  f32x16 l;
+  f32x16 o;  // O^T accumulator: registers <-> channels, lane <-> query
+};
+
 template <typename T>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   using M = Mma<T>;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int qb = w % a.nqb, rh = w / a.nqb;
-  const int r = rh % G.n, h = rh / G.n;
+  const int nrp = (G.n + FWD_ROWS - 1) / FWD_ROWS;
+  const int r0 = (rh % nrp) * FWD_ROWS, h = rh / nrp;
+  const bool row1 = FWD_ROWS > 1 && r0 + 1 < G.n;  // the second row exists
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int q0 = qb * FWD_QBLK + wave * TILE;  // first query of this wave
   const bool active = q0 < G.n;
   const int q = q0 + l32;
   const bool qok = q < G.n;
 
-  __shared__ __align__(16) T ks[2 * ROW_TILE];    // K block   [key][channel], 2 buffers
-  __shared__ __align__(16) T vt[2 * TRANS_TILE];  // V^T block [channel][key], 2 buffers
+  // K block [key][channel] and V^T block [channel][key] of both rows, 2 buffers
+  __shared__ __align__(16) T ks[2 * FWD_ROWS * ROW_TILE];
+  __shared__ __align__(16) T vt[2 * FWD_ROWS * TRANS_TILE];
 
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
-  const T* kr = a.k + rowbase;
-  const T* vr = a.v + rowbase;
   const int last = G.n - 1;
-  typename M::frag qf[M::KCH];
-  if (qok)
-    row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
-  else
-    zero_frags<T>(qf);
+  int64_t rowbase[FWD_ROWS];
+  typename M::frag qf[FWD_ROWS][M::KCH];
+  const uint32_t* kb[FWD_ROWS];
+  SoftmaxState st[FWD_ROWS];
+#pragma unroll
+  for (int i = 0; i < FWD_ROWS; ++i) {
+    const int r = min(r0 + i, last);
+    rowbase[i] = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+    kb[i] = a.kbits + (int64_t)r * G.nkt;
+    if (qok)
+      row_frags(a.q + rowbase[i] + (int64_t)q * G.sPos, g, qf[i]);
+    else
+      zero_frags<T>(qf[i]);
+    st[i].m = neg_inf();
+    st[i].l = f32x16{};
+    st[i].o = f32x16{};
+  }
 
   const float c1 = G.scale * LOG2E;
-  float m = neg_inf(), lsum = 0.f;
-  f32x16 o = {};
-  const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
   const int nblk = (G.nkt + 1) >> 1;
   // bias tiles of this wave's queries (tile 0 for idle waves: loads stay in bounds)
   const int qt = active ? q0 / TILE : 0;
   auto bias_tile = [&](int kt) {
     return load_frag_tile(frag_tile(a.bt, h, qt, min(kt, G.nkt - 1), G.nkt), lane);
   };
+  // key bits of block b for both rows (the second row's are zero if it does not exist)
+  auto bits_of = [&](int b, uint64_t(&bb)[FWD_ROWS]) {
+    bb[0] = block_bits(kb[0], G.nkt, b);
+    if constexpr (FWD_ROWS > 1) bb[1] = row1 ? block_bits(kb[1], G.nkt, b) : 0ull;
+  };
+  const typename M::frag ones = ones_row0<typename M::frag>(l32);
 
-  // one 32-key sub-tile: logits, online softmax (base 2, stale max), P V
-  auto sub_tile = [&](const T* ksb, const T* vtb, const f32x16& bias, uint32_t bits, int u) {
+  // raise the running max to include mx (log2 units) and rescale the state
+  auto rescale = [&](SoftmaxState& S, float mx) {
+    const float mnew = fmaxf(S.m, mx);
+    const float alpha = __builtin_amdgcn_exp2f(S.m - mnew);
+    S.l[0] *= alpha;  // rows 1..31 of l stay zero
+#pragma unroll
+    for (int v = 0; v < 16; ++v) S.o[v] *= alpha;
+    S.m = mnew;
+  };
+
+  // one 32-key sub-tile of one row: logits, online softmax (base 2, stale max), P V
+  auto sub_tile = [&](SoftmaxState& S, const typename M::frag(&qfr)[M::KCH], const T* ksb,
+                      const T* vtb, const f32x16& bias, uint32_t bits, int u) {
     typename M::frag kf[M::KCH];
     row_frags(ksb + (32 * u + l32) * LDS_ROW, g, kf);
-    f32x16 s = M::mma(kf[0], qf[0], bias);  // s^T = bias + K Q^T
+    f32x16 s = M::mma(kf[0], qfr[0], bias);  // s^T = bias + K Q^T
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) s = M::mma(kf[t], qf[t], s);
+    for (int t = 1; t < M::KCH; ++t) s = M::mma(kf[t], qfr[t], s);
     if (bits != 0xffffffffu) mask_rows(s, bits, g);
     const float mx = wave_xor32_max(max16(s)) * c1;
-    if (__any(mx > m + STALE_MAX_SLACK)) {
-      const float mnew = fmaxf(m, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-      lsum *= alpha;
+    if (__any(mx > S.m + STALE_MAX_SLACK)) rescale(S, mx);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) o[v] *= alpha;
-      m = mnew;
-    }
-    float ps = 0.f;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m));
-      ps += s[v];
-    }
-    lsum += ps;
+    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -S.m));
     typename M::frag pf[M::PCH], vf[M::PCH];
     acc_frags(s, pf);
     quad_frags(vtb + l32 * LDS_TROW + 32 * u, g, vf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) o = M::mma(vf[t], pf[t], o);  // O^T += V^T P^T
+    for (int t = 0; t < M::PCH; ++t) {
+      S.o = M::mma(vf[t], pf[t], S.o);  // O^T += V^T P^T
+      S.l = M::mma(ones, pf[t], S.l);   // row sums of P
+    }
   };
 
-  RowPiece<T> kp;
-  PairPiece<T> vp;
-  uint64_t bb = block_bits(kb, G.nkt, 0);
-  kp.load(kr, G.sPos, 0, last, tid);
-  vp.load(vr, G.sPos, 0, last, tid);
-  f32x16 b0 = bias_tile(0), b1 = bias_tile(1);
-  kp.store(ks, tid, bb);
-  vp.validate(tid, bb);
-  vp.store_trans(vt, tid);
+  // A full 64-key block (every key valid in both rows): one straight-line
+  // stretch -- all logit MFMAs, then the maxes, one (rare) rescale per row,
+  // then exp / sums / bf16 packing interleaved with the P V MFMAs -- so the
+  // scheduler can overlap the two rows' and sub-tiles' independent work.
+  auto full_block = [&](int buf, const f32x16& c0, const f32x16& c1b) {
+    f32x16 s[FWD_ROWS][2];
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) {
+      const T* ksb = ks + (buf * FWD_ROWS + i) * ROW_TILE;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        typename M::frag kf[M::KCH];
+        row_frags(ksb + (32 * u + l32) * LDS_ROW, g, kf);
+        s[i][u] = M::mma(kf[0], qf[i][0], u ? c1b : c0);
+#pragma unroll
+        for (int t = 1; t < M::KCH; ++t) s[i][u] = M::mma(kf[t], qf[i][t], s[i][u]);
+      }
+    }
+    float mx[FWD_ROWS];
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) mx[i] = wave_xor32_max(max32(s[i][0], s[i][1])) * c1;
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i)
+      if (__any(mx[i] > st[i].m + STALE_MAX_SLACK)) rescale(st[i], mx[i]);
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) {
+      SoftmaxState& S = st[i];
+      const T* vtb = vt + (buf * FWD_ROWS + i) * TRANS_TILE;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          s[i][u][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i][u][v], c1, -S.m));
+        typename M::frag pf[M::PCH], vf[M::PCH];
+        acc_frags(s[i][u], pf);
+        quad_frags(vtb + l32 * LDS_TROW + 32 * u, g, vf);
+#pragma unroll
+        for (int t = 0; t < M::PCH; ++t) {
+          S.o = M::mma(vf[t], pf[t], S.o);
+          S.l = M::mma(ones, pf[t], S.l);
+        }
+      }
+    }
+  };
+
+  // staging: each row's block is 256 K pieces and 256 V pieces (64 positions
+  // x 32 channels); thread tid moves FWD_ROWS consecutive pieces of row srow
+  constexpr int TPR = 256 / FWD_ROWS;  // threads per staged row
+  RowPiece<T> kp[FWD_ROWS];
+  PairPiece<T> vp[FWD_ROWS];
+  const int srow = tid / TPR;
+  const int sp0 = FWD_ROWS * (tid % TPR);
+  const T* skr = a.k + rowbase[srow];
+  const T* svr = a.v + rowbase[srow];
+  auto stage_load = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) {
+      kp[i].load(skr, G.sPos, b * SPAN, last, sp0 + i);
+      vp[i].load(svr, G.sPos, b * SPAN, last, sp0 + i);
+    }
+  };
+  auto stage_store = [&](int buf, const uint64_t(&bb)[FWD_ROWS]) {
+    T* kd = ks + (buf * FWD_ROWS + srow) * ROW_TILE;
+    T* vd = vt + (buf * FWD_ROWS + srow) * TRANS_TILE;
+    const uint64_t v = bb[srow];
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) {
+      kp[i].store(kd, sp0 + i, v);
+      vp[i].validate(sp0 + i, v);
+      vp[i].store_trans(vd, sp0 + i);
+    }
+  };
+
+  uint64_t bb[FWD_ROWS];
+  bits_of(0, bb);
+  stage_load(0);
+  f32x16 bA0 = bias_tile(0), bA1 = bias_tile(1), bB0, bB1;
+  stage_store(0, bb);
   __syncthreads();
-  int buf = 0;
-  for (int b = 0; b < nblk; ++b) {
-    // issue the next block's loads (the last block reloads itself, unused)
+  auto step = [&](int b, const f32x16& c0, const f32x16& c1b, f32x16& n0, f32x16& n1) {
     const int bn = min(b + 1, nblk - 1);
-    const uint64_t bbn = block_bits(kb, G.nkt, bn);
-    kp.load(kr, G.sPos, bn * SPAN, last, tid);
-    vp.load(vr, G.sPos, bn * SPAN, last, tid);
-    const f32x16 n0 = bias_tile(2 * bn), n1 = bias_tile(2 * bn + 1);
-    if (active) {
-      const T* ksb = ks + buf * ROW_TILE;
-      const T* vtb = vt + buf * TRANS_TILE;
-      if ((uint32_t)bb) sub_tile(ksb, vtb, b0, (uint32_t)bb, 0);
-      if ((uint32_t)(bb >> 32)) sub_tile(ksb, vtb, b1, (uint32_t)(bb >> 32), 1);
+    uint64_t bbn[FWD_ROWS];
+    bits_of(bn, bbn);
+    stage_load(bn);
+    n0 = bias_tile(2 * bn);
+    n1 = bias_tile(2 * bn + 1);
+    const int buf = b & 1;
+    bool full = bb[0] == ~0ull;
+    if constexpr (FWD_ROWS > 1) full = full && (!row1 || bb[1] == ~0ull);
+    if (active && full) {
+      full_block(buf, c0, c1b);
+    } else if (active) {
+#pragma unroll
+      for (int i = 0; i < FWD_ROWS; ++i) {
+        const T* ksb = ks + (buf * FWD_ROWS + i) * ROW_TILE;
+        const T* vtb = vt + (buf * FWD_ROWS + i) * TRANS_TILE;
+        if ((uint32_t)bb[i]) sub_tile(st[i], qf[i], ksb, vtb, c0, (uint32_t)bb[i], 0);
+        if ((uint32_t)(bb[i] >> 32))
+          sub_tile(st[i], qf[i], ksb, vtb, c1b, (uint32_t)(bb[i] >> 32), 1);
+      }
     }
-    if (b + 1 < nblk) {
-      kp.store(ks + (buf ^ 1) * ROW_TILE, tid, bbn);
-      vp.validate(tid, bbn);
-      vp.store_trans(vt + (buf ^ 1) * TRANS_TILE, tid);
-    }
+    if (b + 1 < nblk) stage_store(buf ^ 1, bbn);
     __syncthreads();
-    b0 = n0;
-    b1 = n1;
-    bb = bbn;
-    buf ^= 1;
+#pragma unroll
+    for (int i = 0; i < FWD_ROWS; ++i) bb[i] = bbn[i];
+  };
+  for (int b = 0; b < nblk; b += 2) {
+    step(b, bA0, bA1, bB0, bB1);
+    if (b + 1 >= nblk) break;
+    step(b + 1, bB0, bB1, bA0, bA1);
   }
-  if (!active) return;
+  if (!active || !qok) return;
 
   // epilogue: normalise, gate, store; lse = ln(sum exp) = (m + log2 l) ln 2
-  const float lt = wave_xor32_sum(lsum);
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (!qok) return;
-  const int64_t base = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c0 = 8 * j + 4 * g;
-    const f32x4 gv = load4(a.gate + base + c0);
-    f32x4 ov;
+  for (int i = 0; i < FWD_ROWS; ++i) {
+    if (i == 1 && !row1) break;
+    const SoftmaxState& S = st[i];
+    const float lt = wave_xor32_sum(S.l[0]);  // half 1 holds zeros in register 0
+    const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
+    const int64_t base = rowbase[i] + (int64_t)q * G.sPos;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) ov[e] = o[4 * j + e] * inv / (1.f + __expf(-gv[e]));
-    store4(a.out + base + c0, ov);
+    for (int j = 0; j < 4; ++j) {
+      const int c0 = 8 * j + 4 * g;
+      const f32x4 gv = load4(a.gate + base + c0);
+      f32x4 ov;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ov[e] = S.o[4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+      store4(a.out + base + c0, ov);
+    }
+    if (g == 0)
+      a.lse[(int64_t)(r0 + i) * G.lRow + (int64_t)q * G.lPos + h] =
+          lt > 0.f ? (S.m + log2f(lt)) * LN2 : neg_inf();
   }
-  if (g == 0)
-    a.lse[(int64_t)r * G.lRow + (int64_t)q * G.lPos + h] =
-        lt > 0.f ? (m + log2f(lt)) * LN2 : neg_inf();
 }
 
 template <typename T>
 hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, const T* v,
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
-  const int64_t nwg = (int64_t)a.nqb * g.n * g.H;
+  const int64_t nwg = (int64_t)a.nqb * ((g.n + FWD_ROWS - 1) / FWD_ROWS) * g.H;
   {
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL(fwd_kernel<T>, dim3((unsigned)nwg), dim3(256), 0, s, a);

@@ -45,11 +45,11 @@ template <>
 struct RowPiece<bf16> {
   bf16x8 x;
   __device__ inline void load(const bf16* src, int64_t sPos, int start, int last, int t) {
-    const int p = min(start + (t >> 2), last);
+    const int p = start + SPAN - 1 <= last ? start + (t >> 2) : min(start + (t >> 2), last);
     x = *(const bf16x8*)(src + (int64_t)p * sPos + 8 * (t & 3));
   }
   __device__ inline void store(bf16* tile, int t, uint64_t valid) const {
-    const bf16x8 v = bit64(valid, t >> 2) ? x : bf16x8{};
+    const bf16x8 v = (valid == ~0ull || bit64(valid, t >> 2)) ? x : bf16x8{};
     *(bf16x8*)(tile + (t >> 2) * LDS_ROW + 8 * (t & 3)) = v;
   }
 };
@@ -64,7 +64,7 @@ struct RowPiece<float> {
     hi = *(const f32x4*)(s + 4);
   }
   __device__ inline void store(float* tile, int t, uint64_t valid) const {
-    const bool ok = bit64(valid, t >> 2);
+    const bool ok = valid == ~0ull || bit64(valid, t >> 2);
     float* d = tile + (t >> 2) * LDS_ROW + 8 * (t & 3);
     *(f32x4*)d = ok ? lo : f32x4{};
     *(f32x4*)(d + 4) = ok ? hi : f32x4{};
@@ -84,6 +84,7 @@ struct PairPiece {
     x1 = *(const V4*)(src + (int64_t)min(p + 1, last) * sPos + c0);
   }
   __device__ inline void validate(int t, uint64_t valid) {
+    if (valid == ~0ull) return;  // the common full block: no selects
     const int p = 2 * (t >> 3);
     if (!bit64(valid, p)) x0 = V4{};
     if (!bit64(valid, p + 1)) x1 = V4{};
