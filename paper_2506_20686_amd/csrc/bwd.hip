@@ -26,6 +26,7 @@
 //              chunk order.  No atomics, so the result is reproducible.
 #include <type_traits>
 
+#include "dma.h"
 #include "kernels.h"
 #include "stage.h"
 #include "timing.h"
@@ -543,6 +544,167 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   }
 }
 
+// bf16 bias gradient with asynchronous LDS staging (see dma.h).  Same work
+// split as db_kernel (128 queries x 128 keys of one head, summed over the
+// rows of one chunk; wave w owns query tile w % 4 and key tiles
+// 2 (w / 4) + 0, 1), but per row K, V, Q, dA, its low part, lse2 and -D land
+// in LDS by DMA through a ring of three slots, two rows ahead, so the rows
+// stream without register staging or vector instructions for the copies.
+constexpr int DBD_BLK = 128;                  // queries (and keys) per workgroup block
+constexpr int DBD_OP = DBD_BLK * 64;          // 8 KB: one operand block of a row
+constexpr int DBD_LD = 5 * DBD_OP;            // offset of lse2 (512 B) and -D... (512 B)
+constexpr int DBD_SLOT = 5 * DBD_OP + 1024;   // K, V, Q, dA, dA low, lse2, D
+constexpr int DBD_SLOTS = 3;
+constexpr int DBD_OPS = 6;                    // DMA ops per thread per row
+
+__global__ __launch_bounds__(512, 1) void db_dma_kernel(BwdArgs<bf16> a) {
+  using M = Mma<bf16>;
+  using F = bf16x8;
+  const Geom& G = a.g;
+  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int kbk = w % a.nblk;
+  const int qb = (w / a.nblk) % a.nblk;
+  const int rc = (w / (a.nblk * a.nblk)) % a.nrc;
+  const int h = w / (a.nblk * a.nblk * a.nrc);
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  // the wave index is uniform: say so, so that what derives from it stays scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qtl = wave & 3, kh = wave >> 2;
+  const int qstart = qb * DBD_BLK, kstart = kbk * DBD_BLK;
+  const int q = qstart + qtl * TILE + l32;  // this lane's query
+  const bool active = qstart + qtl * TILE < G.n;
+  const bool qok = q < G.n;
+  const int kt0 = kbk * 4 + 2 * kh;  // this wave's first key tile
+  const int last = G.n - 1;
+  const float c1 = G.scale * LOG2E;
+
+  __shared__ __align__(16) char smem[DBD_SLOTS * DBD_SLOT];
+
+  // ---- DMA lanes: operand op j moves position tid / 4 of the 128, chunk
+  // slot tid % 4; the lse2 / -D op moves 128 bytes per wave (lanes 0..7)
+  const int dp = tid >> 2, dc = (tid & 3) ^ swz(dp);
+  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t kofs = (int64_t)min(kstart + dp, last) * G.sPos + 8 * dc + hb;
+  const int64_t qofs = (int64_t)min(qstart + dp, last) * G.sPos + 8 * dc + hb;
+  const int lq = min(qstart + 32 * (wave & 3) + 4 * lane, G.np - 4);  // lse2 / D lanes
+  const float* ldsrc = wave < 4 ? a.lse2 : a.dsum;
+  auto issue = [&](int r, int slot) {
+    char* sl = smem + slot * DBD_SLOT + 1024 * wave;
+    const int64_t rb = (int64_t)r * G.sRow;
+    dma16(a.k + rb + kofs, sl);
+    dma16(a.v + rb + kofs, sl + DBD_OP);
+    dma16(a.q + rb + qofs, sl + 2 * DBD_OP);
+    dma16(a.da + rb + qofs, sl + 3 * DBD_OP);
+    dma16(a.dalo + rb + qofs, sl + 4 * DBD_OP);
+    if (lane < 8)
+      dma16(ldsrc + ((int64_t)h * G.n + r) * G.np + lq,
+            smem + slot * DBD_SLOT + DBD_LD + 128 * wave);
+  };
+
+  // ---- LDS read addresses (slot 0)
+  const uint32_t base = lds_addr(smem);
+  const int sw = swz(l32);
+  const uint32_t qpos = (uint32_t)(qtl * TILE + l32) * 64;
+  const uint32_t rq0 = base + qpos + 16 * (g ^ sw), rq1 = base + qpos + 16 * ((2 + g) ^ sw);
+  const uint32_t kpos = (uint32_t)(2 * kh * TILE + l32) * 64;
+  const uint32_t rk0 = base + kpos + 16 * (g ^ sw), rk1 = base + kpos + 16 * ((2 + g) ^ sw);
+  const uint32_t rl = base + DBD_LD + (qtl * TILE + l32) * 4;
+
+  f32x16 binit[2], acc[2];
+  const int qt = active ? qstart / TILE + qtl : 0;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    acc[u] = f32x16{};
+    binit[u] = load_frag_tile(frag_tile(a.bt, h, qt, min(kt0 + u, G.nkt - 1), G.nkt), lane);
+  }
+  // The bias tiles are plain register loads; let them complete before any
+  // DMA is issued.  With loads of both kinds outstanding the compiler cannot
+  // count them apart and would wait for all DMAs at every use of binit.
+  wait_vm<0>();
+  const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
+  const int nr = r1 - r0;
+  // key bits of this wave's two key tiles in row r (a tile past the end is empty)
+  auto kbits = [&](int r, int u) -> uint32_t {
+    const int t = kt0 + u;
+    return t < G.nkt ? const_load(a.kbits + (int64_t)r * G.nkt + t) : 0u;
+  };
+  // key bits of the whole 128-key block (for zeroing V rows of invalid keys)
+  auto blk_full = [&](int r) {
+    bool f = true;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int t = kbk * 4 + j;
+      f = f && (t >= G.nkt || const_load(a.kbits + (int64_t)r * G.nkt + t) == 0xffffffffu);
+    }
+    return f;
+  };
+
+  if (nr > 0) {
+    issue(r0, 0);
+    issue(r0 + min(1, nr - 1), 1);
+  }
+  for (int i = 0; i < nr; ++i) {
+    const int r = r0 + i, slot = i % DBD_SLOTS;
+    const uint32_t so = slot * DBD_SLOT;
+    wait_vm<DBD_OPS>();  // row r has landed (row r + 1 may be in flight)
+    lds_barrier();
+    if (!blk_full(r)) {
+      // zero V rows of keys invalid for the row (P = 0 there, and 0 times a
+      // non-finite dP would not be); thread t: key t / 4, 16 bytes
+      const int key = kstart + dp;
+      const int t = key >> 5;
+      const uint32_t wbits = t < G.nkt ? const_load(a.kbits + (int64_t)r * G.nkt + t) : 0u;
+      if (!((wbits >> (key & 31)) & 1u))
+        *(f32x4*)(smem + so + DBD_OP + 16 * tid) = f32x4{};
+      __syncthreads();
+    }
+    // row r + 2 into the slot of row r - 1 (a copy of the last row past the
+    // end keeps the wait counts uniform)
+    issue(r0 + min(i + 2, nr - 1), (i + 2) % DBD_SLOTS);
+    if (!active) continue;
+    const uint32_t b0 = kbits(r, 0), b1 = kbits(r, 1);
+    if ((b0 | b1) == 0u) continue;
+    float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + so);
+    const float nd = -*(const TRIATTN_LDS float*)(uintptr_t)(rl + so + 512);
+    if (!qok) l2 = pos_inf();
+    const F qf0 = lds_load16<F>(rq0 + so + 2 * DBD_OP), qf1 = lds_load16<F>(rq1 + so + 2 * DBD_OP);
+    const F d0 = lds_load16<F>(rq0 + so + 3 * DBD_OP), d1 = lds_load16<F>(rq1 + so + 3 * DBD_OP);
+    const F e0 = lds_load16<F>(rq0 + so + 4 * DBD_OP), e1 = lds_load16<F>(rq1 + so + 4 * DBD_OP);
+    const f32x16 ndv = splat16(nd);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const uint32_t bits = u ? b1 : b0;
+      const uint32_t ko = so + u * TILE * 64;
+      const F k0 = lds_load16<F>(rk0 + ko), k1 = lds_load16<F>(rk1 + ko);
+      f32x16 sv = M::mma(k1, qf1, M::mma(k0, qf0, binit[u]));  // S^T = bias + K Q^T
+      if (bits != 0xffffffffu) mask_rows(sv, bits, g);
+      const F v0 = lds_load16<F>(rk0 + ko + DBD_OP), v1 = lds_load16<F>(rk1 + ko + DBD_OP);
+      f32x16 dpv = M::mma(v0, d0, ndv);  // dP^T - D = V dA^T - D (hi and lo parts of dA)
+      dpv = M::mma(v1, d1, dpv);
+      dpv = M::mma(v0, e0, dpv);
+      dpv = M::mma(v1, e1, dpv);
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        acc[u][v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
+    }
+  }
+  wait_vm<0>();  // the copies past the end must land before the workgroup ends
+  if (!active) return;
+  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + qstart + qtl * TILE + l32) * G.np + 4 * g;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int kt = kt0 + u;
+    if (kt >= G.nkt) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      f32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = acc[u][4 * j + e];
+      *(f32x4*)(slab + kt * TILE + 8 * j) = x;
+    }
+  }
+}
+
 // dbias at (query q, key k, head h) = sum of the slabs in chunk order; the
 // starting node stores it at [q][k][h], the ending node at [k][q][h].
 template <typename T>
@@ -593,7 +755,10 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
-    hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+    if constexpr (std::is_same<T, bf16>::value)
+      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)ndb), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
   }
   {
     const int64_t nred = (int64_t)g.H * g.n * g.n;

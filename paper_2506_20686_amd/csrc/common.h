@@ -143,17 +143,23 @@ __device__ inline float max16(const f32x16& s) {
   return fmaxf(m, s[15]);
 }
 
-// Tree reductions (short dependency chains) over one or two accumulators.
+// Maximum of 32 values (two accumulators) as a tree of 3-input maxes: 16
+// instructions, depth 4.
+__device__ inline float max3f(float a, float b, float c) { return fmaxf(a, fmaxf(b, c)); }
 __device__ inline float max32(const f32x16& a, const f32x16& b) {
-  float t[8];
+  float t[12];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    t[i] = fmaxf(fmaxf(a[4 * i], a[4 * i + 1]), fmaxf(a[4 * i + 2], a[4 * i + 3]));
-    t[4 + i] = fmaxf(fmaxf(b[4 * i], b[4 * i + 1]), fmaxf(b[4 * i + 2], b[4 * i + 3]));
+  for (int i = 0; i < 5; ++i) {
+    t[i] = max3f(a[3 * i], a[3 * i + 1], a[3 * i + 2]);
+    t[5 + i] = max3f(b[3 * i], b[3 * i + 1], b[3 * i + 2]);
   }
-  return fmaxf(fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3])),
-               fmaxf(fmaxf(t[4], t[5]), fmaxf(t[6], t[7])));
+  t[10] = a[15];
+  t[11] = b[15];
+  const float u0 = max3f(t[0], t[1], t[2]), u1 = max3f(t[3], t[4], t[5]);
+  const float u2 = max3f(t[6], t[7], t[8]), u3 = max3f(t[9], t[10], t[11]);
+  return fmaxf(max3f(u0, u1, u2), u3);
 }
+// Tree sum of the 16 entries of a lane.
 __device__ inline float sum16(const f32x16& a) {
   float t[4];
 #pragma unroll

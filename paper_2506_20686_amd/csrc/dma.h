@@ -1,0 +1,159 @@
+// Asynchronous staging of bf16 operand blocks through LDS on gfx950.
+//
+// A block is 64 consecutive pair positions x 32 channels of one (row, head):
+// 64 positions x 64 bytes = 4 KB.  It is copied HBM -> LDS with
+// global_load_lds_dwordx4 (each lane moves 16 bytes straight into LDS, no
+// registers, no vector instructions), three blocks in flight per buffer
+// ring, so the load latency hides behind two blocks of compute.
+//
+// LDS layout of a block: row-major [position][4 chunks of 8 channels], the
+// chunk slots of position p permuted by XOR with (p >> 1) & 3.  The DMA
+// writes a wave's 64 lanes to 1 KB of consecutive LDS, so the permutation is
+// applied on the global side: the lane that fills slot s of position p loads
+// chunk s ^ swz(p).  Readers then see
+//   - row fragments (8 consecutive channels of one position per lane,
+//     ds_read_b128) of 8 consecutive positions on 8 different bank groups;
+//   - transposed fragments (4 consecutive positions of one channel per lane,
+//     ds_read_b64_tr_b16) with the 4 positions of a lane group on different
+//     bank groups.
+//
+// Waits: a DMA counts in vmcnt like any vector load and completes in issue
+// order.  Before a block is read the waves wait until at most the ops issued
+// after it are outstanding, then meet at a barrier.  The compiler neither
+// knows that a DMA writes the LDS a later ds_read reads nor may it wait on
+// the DMAs by itself, so the waits are explicit and the transposed reads are
+// issued with inline assembly (the builtin makes the compiler wait for every
+// outstanding load first).
+#pragma once
+
+#include "common.h"
+
+namespace triattn {
+
+#define TRIATTN_LDS __attribute__((address_space(3)))
+
+constexpr int DBLK_POS = 64;                  // positions per block
+constexpr int DBLK_BYTES = DBLK_POS * 64;     // 4 KB
+constexpr int DBLK_ELEMS = DBLK_BYTES / 2;
+
+__device__ inline int swz(int p) { return (p >> 1) & 3; }
+
+// Byte offset of channels 8 c .. 8 c + 7 of position p in a block.
+__device__ inline int blk_off(int p, int c) { return p * 64 + 16 * (c ^ swz(p)); }
+
+// Copy one block (positions start .. start + 63 of a row, clamped to `last`
+// so every address is in bounds) into LDS.  `part` (0..3) selects the
+// quarter of the block, positions 16 part .. 16 part + 15, that this wave
+// moves; four waves (or four calls) move a whole block.  `dst` is the
+// block's LDS base (same for the whole wave).
+__device__ inline void dma_block_part(const bf16* row, int64_t sPos, int start, int last,
+                                      bf16* dst, int part, int lane) {
+  const int p = 16 * part + (lane >> 2);
+  const int c = (lane & 3) ^ swz(p);
+  const int pos = min(start + p, last);
+  __builtin_amdgcn_global_load_lds(row + (int64_t)pos * sPos + 8 * c,
+                                   (TRIATTN_LDS void*)((char*)dst + 1024 * part), 16, 0, 0);
+}
+
+// One 16-byte DMA lane: `src` is this lane's global address, `dst_wave` the
+// LDS address of the wave's 1 KB destination (lane i lands at + 16 i).
+__device__ inline void dma16(const void* src, void* dst_wave) {
+  __builtin_amdgcn_global_load_lds(src, (TRIATTN_LDS void*)dst_wave, 16, 0, 0);
+}
+
+// 16-byte LDS load from a 32-bit LDS byte address.
+template <typename V>
+__device__ inline V lds_load16(uint32_t addr) {
+  return *(const TRIATTN_LDS V*)(uintptr_t)addr;
+}
+
+// s_waitcnt vmcnt(N) (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// and lgkmcnt left at their maxima).
+template <int N>
+__device__ inline void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier that orders LDS accesses (the compiler may not move
+// memory operations across it) without waiting for outstanding loads.
+__device__ inline void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Row fragments for the 32x32x16 bf16 MFMA (A row / B column = position p of
+// the block): chunk t holds channels 16 t + 8 g .. +7.
+__device__ inline void blk_row_frags(const bf16* blk, int p, int g, bf16x8 (&f)[2]) {
+  const char* b = (const char*)blk;
+  f[0] = *(const bf16x8*)(b + blk_off(p, g));
+  f[1] = *(const bf16x8*)(b + blk_off(p, 2 + g));
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// ds_read_b64_tr_b16: in each group of 16 lanes, lane 4 e + j supplies the
+// 8 bytes at its address (4 consecutive channels of one position), and lane
+// i receives element i % 4 of lane 4 e + i / 4's data as its element e.
+template <int OFF = 0>
+__device__ inline s16x4 ds_read_tr(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset range");
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
+// LDS byte address (32-bit) of a pointer into shared memory.
+__device__ inline uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const TRIATTN_LDS void*)p;
+}
+
+// Per-lane address of the transposed fragment reads of a block: lane l
+// (16-lane group G = l / 16, index j = l % 4 within its row of 4, e = l % 16
+// / 4) supplies channels 16 (G % 2) + 4 j .. +3 of position base + e, where
+// base = 4 (G / 2) + 16 t (+ 8 for the second half) + key offset.  The
+// result of the pair of reads is the A/B fragment whose lane l holds channel
+// l % 32 and positions {16 t + 4 g + 0..3, 16 t + 8 + 4 g + 0..3}, g = l / 32:
+// the quad order of an accumulator-fed operand (see quad_frags).
+struct TrAddr {
+  int pe;    // e + 4 (G / 2): position offset of this lane's source row
+  int cch;   // logical chunk 2 (G % 2) + j / 2
+  int half;  // byte offset 8 (j % 2) inside the chunk
+  __device__ inline explicit TrAddr(int lane) {
+    const int G = lane >> 4, i = lane & 15, j = i & 3, e = i >> 2;
+    pe = e + 4 * (G >> 1);
+    cch = 2 * (G & 1) + (j >> 1);
+    half = 8 * (j & 1);
+  }
+  // byte offset for source position p0 + pe
+  __device__ inline int off(int p0) const {
+    const int p = p0 + pe;
+    return blk_off(p, cch) + half;
+  }
+};
+
+// Transposed fragments of positions 32 u .. 32 u + 31 of a block (the
+// contraction index of an accumulator-fed product), for both 16-position
+// chunks t = 0, 1.  The caller must wait for lgkmcnt before using them
+// (tr_wait).
+__device__ inline void blk_tr_frags(uint32_t blk, const TrAddr& ta, int u, s16x4 (&r)[4]) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    r[2 * t] = ds_read_tr(blk + ta.off(32 * u + 16 * t));
+    r[2 * t + 1] = ds_read_tr(blk + ta.off(32 * u + 16 * t + 8));
+  }
+}
+
+// Wait for all outstanding LDS reads, tied to the registers they fill so
+// that no use of them is scheduled before the wait.
+__device__ inline void tr_wait(s16x4 (&r)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
+}
+
+__device__ inline bf16x8 tr_frag(const s16x4 (&r)[4], int t) {
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(r[2 * t], r[2 * t + 1], 0, 1, 2, 3,
+                                                            4, 5, 6, 7));
+}
+
+}  // namespace triattn

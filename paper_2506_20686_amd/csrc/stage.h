@@ -126,10 +126,17 @@ __device__ inline uint64_t range_bits64(int start, int n) {
 // Key-valid bits of 64-key block b of a row: words 2 b and 2 b + 1 of the
 // row's key bits (a word past the last tile counts as empty; the reads stay
 // in bounds).
+// The words are read through the constant address space: the key bits are
+// written by an earlier kernel and only read here, so the compiler may use
+// scalar loads (a vector load of a uniform value would make it wait for
+// every outstanding vector load before the value can be moved to a scalar).
+__device__ inline uint32_t const_load(const uint32_t* p) {
+  return *(const __attribute__((address_space(4))) uint32_t*)p;
+}
 __device__ inline uint64_t block_bits(const uint32_t* kb, int nkt, int b) {
   const int t = 2 * b;
-  const uint32_t lo = kb[min(t, nkt - 1)];
-  const uint32_t hi = kb[min(t + 1, nkt - 1)];
+  const uint32_t lo = const_load(kb + min(t, nkt - 1));
+  const uint32_t hi = const_load(kb + min(t + 1, nkt - 1));
   return (t < nkt ? (uint64_t)lo : 0ull) | (t + 1 < nkt ? (uint64_t)hi << 32 : 0ull);
 }
 

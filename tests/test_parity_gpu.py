@@ -203,4 +203,7 @@ def test_peak_memory_is_quadratic():
     # outputs (out + 4 gradients of pair size, lse, dbias) + workspace
     bound = 5 * pair + n * n * h * 6 + ws + (64 << 20)
     assert peak <= bound, (peak, bound)
-    assert peak < n ** 3 * h * 2 / 3  # far below the N^3 H bf16 logits (3.6 GB)
+    # the whole backward (outputs, workspace, partial bias-gradient slabs)
+    # stays well below the N^3 H bf16 logit tensor alone (3.6 GB at N = 768;
+    # the ratio falls as 1 / N for larger N)
+    assert peak < 0.4 * n ** 3 * h * 2
