@@ -51,7 +51,23 @@ def parse():
     ap.add_argument("--workload", default=None, help="workload name (default: the N=768 one)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many bytes 5 times "
+                         "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+def copy_calibration(nbytes):
+    """A plain copy of known size: under rocprofv3 --pmc its FETCH_SIZE and WRITE_SIZE per
+    dispatch, divided by nbytes, are the scale factors of those counters."""
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize(dev)
+    print(json.dumps({"copy_bytes": src.numel() * 4, "launches": 5}), flush=True)
 
 
 def kernel_source_hash():
@@ -82,7 +98,7 @@ def recorded_traffic(kernel, workload):
 def cpu_baseline(w, t, target_s):
     """Time the fp64 oracle (as it stands) on rows of the starting node: the
     forward and the per-row gradients (dQ, dK, dV, dG) of R rows, nominal
-    14 N^2 H d flop per row.  R is sized from a one-row trial run."""
+    14 N^2 H d flop per row.  R is sized from a trial of one row per thread."""
     import numpy as np
 
     import oracle
@@ -98,8 +114,11 @@ def cpu_baseline(w, t, target_s):
                    rows=rows, db_queries=[])
         return time.perf_counter() - t0
 
-    one = run([0])
-    rows = max(1, min(w.n, int(target_s / max(one, 1e-3))))
+    # the oracle spreads rows over its threads: size the sample from a trial
+    # with one row per thread
+    nt = max(1, min(w.n, oracle.max_threads()))
+    trial = run(list(range(nt)))
+    rows = max(nt, min(w.n, int(nt * target_s / max(trial, 1e-3)) // nt * nt))
     sel = [int(i * w.n / rows) for i in range(rows)]
     dt = run(sel)
     flop = 14.0 * w.n ** 2 * w.h * w.d * rows
@@ -117,6 +136,10 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path (the row-sharded "
               "design is described in DESIGN.md); run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_bytes > 0:
+        copy_calibration(args.copy_bytes)
+        return
 
     import torch
 

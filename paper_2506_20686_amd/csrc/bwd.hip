@@ -103,7 +103,7 @@ struct BwdArgs {
   const T *q, *k, *v, *da;
   const T* dalo;  // bf16 only: dA - bf16(dA), also rounded to bf16
   const float* lse2;
-  float* dsum;  // D per (head, row, query): written by dq_kernel, read after
+  float* dsum;  // -D per (head, row, query): written by dq_kernel, read after
   T *dq, *dk, *dv;
   float* slabs;
   int nblk;  // 128-wide blocks per axis
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   if (!active) return;
   const float dsum = wave_xor32_sum(dpart);
   if (!qok) return;
-  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = dsum;
+  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = -dsum;  // stored negated
   const int64_t base = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
     dap.load(dar, G.sPos, b * SPAN, last, tid);
     if constexpr (kSplitDA<T>) dlp.load(dalr, G.sPos, b * SPAN, last, tid);
     const int qi = min(b * SPAN + sq, G.np - 1);
-    sv = tid < SPAN ? l2row[qi] : -drow[qi];
+    sv = tid < SPAN ? l2row[qi] : drow[qi];
   };
   auto store_block = [&](int b, int bf) {
     const uint64_t vb = range_bits64(b * SPAN, G.n);
@@ -404,6 +404,209 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   }
 }
 
+// bf16 dK, dV with asynchronous LDS staging (see dma.h).  One workgroup =
+// 8 waves = 128 keys x 2 rows of one head: wave w owns key tile w % 4 of
+// the block (lane <-> key) in row r0 + w / 4.  Queries stream in blocks of
+// 32; per block, Q, dA and its low part of both rows, their lse2 and D, and
+// the key-major bias tiles of the 128 keys (shared by the two rows) are
+// copied HBM -> LDS by DMA into a ring of KD_SLOTS slots.  Q^T and dA^T
+// fragments come from the transposing LDS read of the same row-major
+// blocks.
+constexpr int KD_ROWS = 2;
+constexpr int KD_BLK = 32 * 64;                        // 2 KB: 32 positions x 32 channels
+constexpr int KD_Q = 0, KD_DA = 2 * KD_BLK, KD_LO = 4 * KD_BLK;  // [row] blocks
+constexpr int KD_BIAS = 6 * KD_BLK;                    // 4 key tiles x 4 KB
+constexpr int KD_L2 = KD_BIAS + 4 * 4096;              // lse2 [row][32], then -D [row][32]
+constexpr int KD_SLOT = KD_L2 + 4 * 128;
+// Ring depth (blocks in flight + 1).  Two slots (58 KB) let two workgroups
+// share a CU: four waves per SIMD hide more latency than a deeper ring with
+// two (measured: 0.82 ms against 0.98-1.07 ms with four slots at N = 768).
+constexpr int KD_SLOTS = 2;
+constexpr int KD_OPS = 4;    // DMA ops per thread per block
+
+__global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(BwdArgs<bf16> a) {
+  using M = Mma<bf16>;
+  using F = bf16x8;
+  const Geom& G = a.g;
+  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int nrg = (G.n + KD_ROWS - 1) / KD_ROWS;
+  const int kbk = w % a.nblk, rg = (w / a.nblk) % nrg, h = w / (a.nblk * nrg);
+  const int r0 = rg * KD_ROWS;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ri = wave >> 2;                 // row of this wave (0, 1)
+  const int r = min(r0 + ri, G.n - 1);
+  const bool rok = r0 + ri < G.n;
+  const int kt = kbk * 4 + (wave & 3);      // this wave's key tile
+  const int nkt = G.nkt, last = G.n - 1;
+  const bool active = rok && kt < nkt;
+  const uint32_t bits = active ? const_load(a.kbits + (int64_t)r * nkt + kt) : 0u;
+  const int key = kt * TILE + l32;
+  const bool kvalid = (bits >> l32) & 1u;
+  const bool work = bits != 0u;
+  const float c1 = G.scale * LOG2E;
+
+  __shared__ __align__(16) char smem[KD_SLOTS * KD_SLOT];
+
+  // ---- the wave's keys: K and V fragments (zero for invalid keys, so that
+  // non-finite values there cannot reach the products)
+  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  F kf[M::KCH], vf[M::KCH];
+  if (kvalid) {
+    row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
+    row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
+  } else {
+    zero_frags<bf16>(kf);
+    zero_frags<bf16>(vf);
+  }
+  // the fragments are plain register loads: let them complete before any
+  // DMA is issued (with both kinds outstanding the compiler would wait for
+  // every DMA at each use)
+  wait_vm<0>();
+
+  // ---- DMA lanes.  Op 0: Q and dA of both rows (wave w: block w / 2 of
+  // [Q0, Q1, dA0, dA1], positions 16 (w % 2) + lane / 4).  Op 1: waves 0-3
+  // the low part of dA, waves 4-7 lse2 / -D (lanes 0..7, 128 bytes each).
+  // Ops 2, 3: bias tiles 4 KB each, wave w: tile 2 (op - 2) + w / 4,
+  // quarter w % 4.
+  const int dpl = 16 * (wave & 1) + (lane >> 2);
+  int64_t drow[KD_ROWS];
+#pragma unroll
+  for (int i = 0; i < KD_ROWS; ++i)
+    drow[i] = (int64_t)min(r0 + i, last) * G.sRow + (int64_t)h * HEAD_DIM;
+  const int b0 = wave >> 1;  // op 0 block: 0 Q0, 1 Q1, 2 dA0, 3 dA1
+  const bf16* src0 = b0 < 2 ? a.q : a.da;
+  const int64_t row0 = (b0 & 1) ? drow[1] : drow[0];
+  const int64_t row1 = (wave >> 1 & 1) ? drow[1] : drow[0];  // op 1 (waves 0-3): dalo row
+  const int lrow = min(r0 + (wave & 1), last);                // op 1 (waves 4-7): lse2 / -D row
+  const float* lsrc = (wave & 2) ? a.dsum : a.lse2;
+  auto issue = [&](int t, int slot) {
+    char* sl = smem + slot * KD_SLOT;
+    const int p = min(t * TILE + dpl, last);
+    const int c = (lane & 3) ^ swz(dpl);
+    dma16(src0 + row0 + (int64_t)p * G.sPos + 8 * c, sl + b0 * KD_BLK + 1024 * (wave & 1));
+    if (wave < 4) {
+      dma16(a.dalo + row1 + (int64_t)p * G.sPos + 8 * c,
+            sl + KD_LO + (wave >> 1) * KD_BLK + 1024 * (wave & 1));
+    } else if (lane < 8) {
+      dma16(lsrc + ((int64_t)h * G.n + lrow) * G.np + t * TILE + 4 * lane,
+            sl + KD_L2 + 128 * (wave - 4));
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int tl = 2 * j + (wave >> 2);
+      const float* bsrc = frag_tile(a.btT, h, min(kbk * 4 + tl, nkt - 1), t, nkt);
+      dma16((const char*)bsrc + 1024 * (wave & 3) + 16 * lane,
+            sl + KD_BIAS + tl * 4096 + 1024 * (wave & 3));
+    }
+  };
+
+  // ---- LDS read addresses (slot 0)
+  const uint32_t base = lds_addr(smem);
+  const int sw = swz(l32);
+  const uint32_t rq0 = base + ri * KD_BLK + l32 * 64 + 16 * (g ^ sw);
+  const uint32_t rq1 = base + ri * KD_BLK + l32 * 64 + 16 * ((2 + g) ^ sw);
+  const TrAddr ta(lane);
+  const uint32_t rtr = base + ri * KD_BLK + ta.off(0);
+  const uint32_t rtr8 = base + ri * KD_BLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + KD_BIAS + (wave & 3) * 4096 + lane * 16;
+  const uint32_t rl = base + KD_L2 + ri * 128 + 16 * g;  // + 32 j: lse2 quad j; + 256: D
+
+  f32x16 dkt = {}, dvt = {};
+  const float kmask = kvalid ? 0.f : neg_inf();
+  auto quads = [&](uint32_t at) {
+    f32x16 x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x4 y = lds_load16<f32x4>(at + 32 * j);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[4 * j + e] = y[e];
+    }
+    return x;
+  };
+
+#pragma unroll
+  for (int j = 0; j < KD_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
+  for (int t = 0; t < nkt; ++t) {
+    const uint32_t so = (t % KD_SLOTS) * KD_SLOT;
+    // block t has landed (the KD_SLOTS - 2 blocks after it may be in flight)
+    wait_vm<(KD_SLOTS - 2) * KD_OPS>();
+    lds_barrier();
+    // block t + KD_SLOTS - 1 into the slot of block t - 1 (a copy of the last
+    // block past the end keeps the wait counts uniform)
+    issue(min(t + KD_SLOTS - 1, nkt - 1), (t + KD_SLOTS - 1) % KD_SLOTS);
+    if (!work) continue;
+    // S = bias + Q K^T (registers <-> queries, lane <-> key)
+    f32x16 sv;
+    {
+      f32x16 bias;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bias[4 * j + e] = y[e];
+      }
+      if (bits != 0xffffffffu) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) bias[v] += kmask;  // -inf for an invalid key
+      }
+      const F q0 = lds_load16<F>(rq0 + so + KD_Q), q1 = lds_load16<F>(rq1 + so + KD_Q);
+      sv = M::mma(q1, kf[1], M::mma(q0, kf[0], bias));
+    }
+    // P = exp2(S c1 - lse2[query])
+    const f32x16 l2 = quads(rl + so);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2[v]));
+    // dP - D = dA V^T - D (hi and lo parts of dA), then dS = P (dP - D)
+    const F d0 = lds_load16<F>(rq0 + so + KD_DA), d1 = lds_load16<F>(rq1 + so + KD_DA);
+    const F e0 = lds_load16<F>(rq0 + so + KD_LO), e1 = lds_load16<F>(rq1 + so + KD_LO);
+    f32x16 dp = quads(rl + so + 256);  // -D
+    dp = M::mma(d0, vf[0], dp);
+    dp = M::mma(d1, vf[1], dp);
+    dp = M::mma(e0, vf[0], dp);
+    dp = M::mma(e1, vf[1], dp);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dp[v] *= sv[v];
+    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the block's queries)
+    const uint32_t tq = rtr + so + KD_Q, td = rtr + so + KD_DA;
+    const uint32_t tq8 = rtr8 + so + KD_Q, td8 = rtr8 + so + KD_DA;
+    s16x4 xa[4], xq[4];
+    xa[0] = ds_read_tr<0>(td);
+    xa[1] = ds_read_tr<8 * 64>(td8);
+    xa[2] = ds_read_tr<16 * 64>(td);
+    xa[3] = ds_read_tr<24 * 64>(td8);
+    xq[0] = ds_read_tr<0>(tq);
+    xq[1] = ds_read_tr<8 * 64>(tq8);
+    xq[2] = ds_read_tr<16 * 64>(tq);
+    xq[3] = ds_read_tr<24 * 64>(tq8);
+    F pf[M::PCH], sf[M::PCH];
+    acc_frags(sv, pf);
+    acc_frags(dp, sf);
+    tr_wait(xa);
+    tr_wait(xq);
+#pragma unroll
+    for (int u = 0; u < M::PCH; ++u) {
+      dvt = M::mma(tr_frag(xa, u), pf[u], dvt);
+      dkt = M::mma(tr_frag(xq, u), sf[u], dkt);
+    }
+  }
+  wait_vm<0>();  // the copies past the end must land before the workgroup ends
+  if (!active || key >= G.n) return;
+  const int64_t gb = rowbase + (int64_t)key * G.sPos;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c0 = 8 * j + 4 * g;
+    f32x4 x, y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = dvt[4 * j + e];
+      y[e] = dkt[4 * j + e] * G.scale;
+    }
+    store4(a.dv + gb + c0, x);
+    store4(a.dk + gb + c0, y);
+  }
+}
+
 // ---- dBias ---------------------------------------------------------------------------
 
 constexpr int DB_WAVES = 8;  // 4 query tiles x 2 key halves
@@ -469,7 +672,7 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
     dap.load(a.da + rowbase, G.sPos, qstart + SPAN * half, last, pt);
     if constexpr (kSplitDA<T>) dlp.load(a.dalo + rowbase, G.sPos, qstart + SPAN * half, last, pt);
     const int64_t at = ((int64_t)h * G.n + r) * G.np + sq;
-    sv = tid < DB_ROWS ? a.lse2[at] : -a.dsum[at];
+    sv = tid < DB_ROWS ? a.lse2[at] : a.dsum[at];
   };
   auto store_row = [&](int r) {
     const uint64_t kv = row_bits(r, half);
@@ -544,164 +747,144 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   }
 }
 
-// bf16 bias gradient with asynchronous LDS staging (see dma.h).  Same work
-// split as db_kernel (128 queries x 128 keys of one head, summed over the
-// rows of one chunk; wave w owns query tile w % 4 and key tiles
-// 2 (w / 4) + 0, 1), but per row K, V, Q, dA, its low part, lse2 and -D land
-// in LDS by DMA through a ring of three slots, two rows ahead, so the rows
-// stream without register staging or vector instructions for the copies.
-constexpr int DBD_BLK = 128;                  // queries (and keys) per workgroup block
-constexpr int DBD_OP = DBD_BLK * 64;          // 8 KB: one operand block of a row
-constexpr int DBD_LD = 5 * DBD_OP;            // offset of lse2 (512 B) and -D... (512 B)
-constexpr int DBD_SLOT = 5 * DBD_OP + 1024;   // K, V, Q, dA, dA low, lse2, D
-constexpr int DBD_SLOTS = 3;
-constexpr int DBD_OPS = 6;                    // DMA ops per thread per row
+// bf16 bias gradient with asynchronous LDS staging (see dma.h).  One
+// workgroup: 128 queries x 64 keys of one head, summed over the rows of one
+// row chunk; wave w owns query tile w % 4 (lane <-> query) and key tile
+// w / 4 of the block.  Per row, K and V of the 64 keys and Q, dA, its low
+// part, lse2 and -D of the 128 queries land in LDS by DMA through a ring of
+// two slots (33 KB each), one row ahead; two workgroups share a CU (four
+// waves per SIMD) to hide the latency of each wave's dependent MFMA and
+// vector steps.
+constexpr int DBD_Q = 128, DBD_K = 64;        // queries and keys per workgroup block
+constexpr int DBD_KV = DBD_K * 64;            // 4 KB: K (or V) of the block's keys
+constexpr int DBD_QB = DBD_Q * 64;            // 8 KB: Q (or dA, dA low) of the queries
+constexpr int DBD_OK = 0, DBD_OV = DBD_KV, DBD_OQ = 2 * DBD_KV;
+constexpr int DBD_ODA = DBD_OQ + DBD_QB, DBD_OLO = DBD_ODA + DBD_QB;
+constexpr int DBD_LD = DBD_OLO + DBD_QB;      // lse2 [128], then -D [128]
+constexpr int DBD_SLOT = DBD_LD + 1024;
+constexpr int DBD_SLOTS = 2;
+constexpr int DBD_OPS = 5;                    // DMA ops per thread per row
 
-__global__ __launch_bounds__(512, 1) void db_dma_kernel(BwdArgs<bf16> a) {
+__global__ __launch_bounds__(512, 2) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int kbk = w % a.nblk;
-  const int qb = (w / a.nblk) % a.nblk;
-  const int rc = (w / (a.nblk * a.nblk)) % a.nrc;
-  const int h = w / (a.nblk * a.nblk * a.nrc);
+  const int kbk = w % nkb;
+  const int qb = (w / nkb) % a.nblk;
+  const int rc = (w / (nkb * a.nblk)) % a.nrc;
+  const int h = w / (nkb * a.nblk * a.nrc);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  // the wave index is uniform: say so, so that what derives from it stays scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qtl = wave & 3, kh = wave >> 2;
-  const int qstart = qb * DBD_BLK, kstart = kbk * DBD_BLK;
+  const int qtl = wave & 3, ktl = wave >> 2;
+  const int qstart = qb * DBD_Q, kstart = kbk * DBD_K;
   const int q = qstart + qtl * TILE + l32;  // this lane's query
-  const bool active = qstart + qtl * TILE < G.n;
+  const int kt = kbk * 2 + ktl;             // this wave's key tile
+  const bool active = qstart + qtl * TILE < G.n && kt < G.nkt;
   const bool qok = q < G.n;
-  const int kt0 = kbk * 4 + 2 * kh;  // this wave's first key tile
   const int last = G.n - 1;
   const float c1 = G.scale * LOG2E;
 
   __shared__ __align__(16) char smem[DBD_SLOTS * DBD_SLOT];
 
-  // ---- DMA lanes: operand op j moves position tid / 4 of the 128, chunk
-  // slot tid % 4; the lse2 / -D op moves 128 bytes per wave (lanes 0..7)
-  const int dp = tid >> 2, dc = (tid & 3) ^ swz(dp);
-  const int64_t hb = (int64_t)h * HEAD_DIM;
-  const int64_t kofs = (int64_t)min(kstart + dp, last) * G.sPos + 8 * dc + hb;
-  const int64_t qofs = (int64_t)min(qstart + dp, last) * G.sPos + 8 * dc + hb;
-  const int lq = min(qstart + 32 * (wave & 3) + 4 * lane, G.np - 4);  // lse2 / D lanes
+  f32x16 binit, acc = {};
+  {
+    const int qt = active ? qstart / TILE + qtl : 0;
+    binit = load_frag_tile(frag_tile(a.bt, h, qt, min(kt, G.nkt - 1), G.nkt), lane);
+  }
+  // the bias tile is a plain register load: let it complete before any DMA
+  // is issued (with both kinds outstanding the compiler would wait for every
+  // DMA at each use of binit)
+  wait_vm<0>();
+
+  // ---- DMA lanes.  Op 0: K (waves 0-3) and V (waves 4-7) of the 64 keys,
+  // wave w % 4 moving positions 16 (w % 4) + lane / 4.  Ops 1-3: Q, dA, dA
+  // low of the 128 queries, position tid / 4.  Op 4: lse2 (waves 0-3) and
+  // -D (waves 4-7), 128 bytes per wave (lanes 0..7).
+  const int hb = h * HEAD_DIM;
+  const int kp = 16 * (wave & 3) + (lane >> 2), kc = (lane & 3) ^ swz(kp);
+  const int64_t kofs = (int64_t)min(kstart + kp, last) * G.sPos + 8 * kc + hb;
+  const bf16* kvsrc = wave < 4 ? a.k : a.v;
+  const int qp = tid >> 2, qc = (tid & 3) ^ swz(qp);
+  const int64_t qofs = (int64_t)min(qstart + qp, last) * G.sPos + 8 * qc + hb;
+  const int lq = min(qstart + 32 * (wave & 3) + 4 * lane, G.np - 4);
   const float* ldsrc = wave < 4 ? a.lse2 : a.dsum;
   auto issue = [&](int r, int slot) {
-    char* sl = smem + slot * DBD_SLOT + 1024 * wave;
+    char* sl = smem + slot * DBD_SLOT;
     const int64_t rb = (int64_t)r * G.sRow;
-    dma16(a.k + rb + kofs, sl);
-    dma16(a.v + rb + kofs, sl + DBD_OP);
-    dma16(a.q + rb + qofs, sl + 2 * DBD_OP);
-    dma16(a.da + rb + qofs, sl + 3 * DBD_OP);
-    dma16(a.dalo + rb + qofs, sl + 4 * DBD_OP);
+    dma16(kvsrc + rb + kofs, sl + (wave < 4 ? DBD_OK : DBD_OV) + 1024 * (wave & 3));
+    dma16(a.q + rb + qofs, sl + DBD_OQ + 1024 * wave);
+    dma16(a.da + rb + qofs, sl + DBD_ODA + 1024 * wave);
+    dma16(a.dalo + rb + qofs, sl + DBD_OLO + 1024 * wave);
     if (lane < 8)
-      dma16(ldsrc + ((int64_t)h * G.n + r) * G.np + lq,
-            smem + slot * DBD_SLOT + DBD_LD + 128 * wave);
+      dma16(ldsrc + ((int64_t)h * G.n + r) * G.np + lq, sl + DBD_LD + 128 * wave);
   };
 
   // ---- LDS read addresses (slot 0)
   const uint32_t base = lds_addr(smem);
   const int sw = swz(l32);
-  const uint32_t qpos = (uint32_t)(qtl * TILE + l32) * 64;
-  const uint32_t rq0 = base + qpos + 16 * (g ^ sw), rq1 = base + qpos + 16 * ((2 + g) ^ sw);
-  const uint32_t kpos = (uint32_t)(2 * kh * TILE + l32) * 64;
-  const uint32_t rk0 = base + kpos + 16 * (g ^ sw), rk1 = base + kpos + 16 * ((2 + g) ^ sw);
+  const uint32_t qpos = base + (uint32_t)(qtl * TILE + l32) * 64;
+  const uint32_t rq0 = qpos + 16 * (g ^ sw), rq1 = qpos + 16 * ((2 + g) ^ sw);
+  const uint32_t kpos = base + (uint32_t)(ktl * TILE + l32) * 64;
+  const uint32_t rk0 = kpos + 16 * (g ^ sw), rk1 = kpos + 16 * ((2 + g) ^ sw);
   const uint32_t rl = base + DBD_LD + (qtl * TILE + l32) * 4;
 
-  f32x16 binit[2], acc[2];
-  const int qt = active ? qstart / TILE + qtl : 0;
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    acc[u] = f32x16{};
-    binit[u] = load_frag_tile(frag_tile(a.bt, h, qt, min(kt0 + u, G.nkt - 1), G.nkt), lane);
-  }
-  // The bias tiles are plain register loads; let them complete before any
-  // DMA is issued.  With loads of both kinds outstanding the compiler cannot
-  // count them apart and would wait for all DMAs at every use of binit.
-  wait_vm<0>();
   const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
   const int nr = r1 - r0;
-  // key bits of this wave's two key tiles in row r (a tile past the end is empty)
-  auto kbits = [&](int r, int u) -> uint32_t {
-    const int t = kt0 + u;
-    return t < G.nkt ? const_load(a.kbits + (int64_t)r * G.nkt + t) : 0u;
-  };
-  // key bits of the whole 128-key block (for zeroing V rows of invalid keys)
-  auto blk_full = [&](int r) {
-    bool f = true;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int t = kbk * 4 + j;
-      f = f && (t >= G.nkt || const_load(a.kbits + (int64_t)r * G.nkt + t) == 0xffffffffu);
-    }
-    return f;
+  const int nkt = G.nkt;
+  auto kword = [&](int r, int t) -> uint32_t {
+    return t < nkt ? const_load(a.kbits + (int64_t)r * nkt + t) : 0u;
   };
 
-  if (nr > 0) {
-    issue(r0, 0);
-    issue(r0 + min(1, nr - 1), 1);
-  }
+  if (nr > 0) issue(r0, 0);
   for (int i = 0; i < nr; ++i) {
-    const int r = r0 + i, slot = i % DBD_SLOTS;
-    const uint32_t so = slot * DBD_SLOT;
-    wait_vm<DBD_OPS>();  // row r has landed (row r + 1 may be in flight)
+    const int r = r0 + i;
+    const uint32_t so = (i % DBD_SLOTS) * DBD_SLOT;
+    wait_vm<(DBD_SLOTS - 2) * DBD_OPS>();  // row r has landed
     lds_barrier();
-    if (!blk_full(r)) {
+    const uint32_t w0 = kword(r, kbk * 2), w1 = kword(r, kbk * 2 + 1);
+    if ((w0 & w1) != 0xffffffffu) {
       // zero V rows of keys invalid for the row (P = 0 there, and 0 times a
-      // non-finite dP would not be); thread t: key t / 4, 16 bytes
-      const int key = kstart + dp;
-      const int t = key >> 5;
-      const uint32_t wbits = t < G.nkt ? const_load(a.kbits + (int64_t)r * G.nkt + t) : 0u;
-      if (!((wbits >> (key & 31)) & 1u))
-        *(f32x4*)(smem + so + DBD_OP + 16 * tid) = f32x4{};
+      // non-finite dP would not be); thread t < 256: key t / 4, 16 bytes
+      if (tid < 256) {
+        const uint32_t wb = (tid >> 7) ? w1 : w0;
+        if (!((wb >> ((tid >> 2) & 31)) & 1u)) *(f32x4*)(smem + so + DBD_OV + 16 * tid) = f32x4{};
+      }
       __syncthreads();
     }
-    // row r + 2 into the slot of row r - 1 (a copy of the last row past the
-    // end keeps the wait counts uniform)
-    issue(r0 + min(i + 2, nr - 1), (i + 2) % DBD_SLOTS);
-    if (!active) continue;
-    const uint32_t b0 = kbits(r, 0), b1 = kbits(r, 1);
-    if ((b0 | b1) == 0u) continue;
+    // row r + 1 into the other slot (a copy of the last row past the end
+    // keeps the wait counts uniform)
+    issue(r0 + min(i + DBD_SLOTS - 1, nr - 1), (i + DBD_SLOTS - 1) % DBD_SLOTS);
+    const uint32_t bits = ktl ? w1 : w0;
+    if (!active || bits == 0u) continue;
     float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + so);
-    const float nd = -*(const TRIATTN_LDS float*)(uintptr_t)(rl + so + 512);
+    const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + so + 512);
     if (!qok) l2 = pos_inf();
-    const F qf0 = lds_load16<F>(rq0 + so + 2 * DBD_OP), qf1 = lds_load16<F>(rq1 + so + 2 * DBD_OP);
-    const F d0 = lds_load16<F>(rq0 + so + 3 * DBD_OP), d1 = lds_load16<F>(rq1 + so + 3 * DBD_OP);
-    const F e0 = lds_load16<F>(rq0 + so + 4 * DBD_OP), e1 = lds_load16<F>(rq1 + so + 4 * DBD_OP);
-    const f32x16 ndv = splat16(nd);
+    const F q0 = lds_load16<F>(rq0 + so + DBD_OQ), q1 = lds_load16<F>(rq1 + so + DBD_OQ);
+    const F k0 = lds_load16<F>(rk0 + so + DBD_OK), k1 = lds_load16<F>(rk1 + so + DBD_OK);
+    f32x16 sv = M::mma(k1, q1, M::mma(k0, q0, binit));  // S^T = bias + K Q^T
+    if (bits != 0xffffffffu) mask_rows(sv, bits, g);
+    const F d0 = lds_load16<F>(rq0 + so + DBD_ODA), d1 = lds_load16<F>(rq1 + so + DBD_ODA);
+    const F e0 = lds_load16<F>(rq0 + so + DBD_OLO), e1 = lds_load16<F>(rq1 + so + DBD_OLO);
+    const F v0 = lds_load16<F>(rk0 + so + DBD_OV), v1 = lds_load16<F>(rk1 + so + DBD_OV);
+    f32x16 dpv = M::mma(v0, d0, splat16(nd));  // dP^T - D = V dA^T - D (hi and lo parts)
+    dpv = M::mma(v1, d1, dpv);
+    dpv = M::mma(v0, e0, dpv);
+    dpv = M::mma(v1, e1, dpv);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const uint32_t bits = u ? b1 : b0;
-      const uint32_t ko = so + u * TILE * 64;
-      const F k0 = lds_load16<F>(rk0 + ko), k1 = lds_load16<F>(rk1 + ko);
-      f32x16 sv = M::mma(k1, qf1, M::mma(k0, qf0, binit[u]));  // S^T = bias + K Q^T
-      if (bits != 0xffffffffu) mask_rows(sv, bits, g);
-      const F v0 = lds_load16<F>(rk0 + ko + DBD_OP), v1 = lds_load16<F>(rk1 + ko + DBD_OP);
-      f32x16 dpv = M::mma(v0, d0, ndv);  // dP^T - D = V dA^T - D (hi and lo parts of dA)
-      dpv = M::mma(v1, d1, dpv);
-      dpv = M::mma(v0, e0, dpv);
-      dpv = M::mma(v1, e1, dpv);
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        acc[u][v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
-    }
+    for (int v = 0; v < 16; ++v)
+      acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
   }
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active) return;
-  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + qstart + qtl * TILE + l32) * G.np + 4 * g;
+  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + qstart + qtl * TILE + l32) * G.np +
+                kt * TILE + 4 * g;
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int kt = kt0 + u;
-    if (kt >= G.nkt) continue;
+  for (int j = 0; j < 4; ++j) {
+    f32x4 x;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f32x4 x;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = acc[u][4 * j + e];
-      *(f32x4*)(slab + kt * TILE + 8 * j) = x;
-    }
+    for (int e = 0; e < 4; ++e) x[e] = acc[4 * j + e];
+    *(f32x4*)(slab + 8 * j) = x;
   }
 }
 
@@ -750,14 +933,21 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   }
   {
     KernelTimer t(K_DKDV, s);
-    hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+    if constexpr (std::is_same<T, bf16>::value) {
+      const int64_t nwg = (int64_t)a.nblk * ((g.n + KD_ROWS - 1) / KD_ROWS) * g.H;
+      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a);
+    } else {
+      hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+    }
   }
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
-    if constexpr (std::is_same<T, bf16>::value)
-      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)ndb), dim3(512), 0, s, a);
-    else
+    if constexpr (std::is_same<T, bf16>::value) {
+      const int nkb = (g.n + DBD_K - 1) / DBD_K;
+      const int64_t nwg = (int64_t)a.nblk * nkb * ws.nrc * g.H;
+      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a, nkb);
+    } else
       hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
   }
   {

@@ -1,21 +1,24 @@
 // Asynchronous staging of bf16 operand blocks through LDS on gfx950.
 //
-// A block is 64 consecutive pair positions x 32 channels of one (row, head):
-// 64 positions x 64 bytes = 4 KB.  It is copied HBM -> LDS with
+// A block is consecutive pair positions x 32 channels of one (row, head),
+// 64 bytes per position.  It is copied HBM -> LDS with
 // global_load_lds_dwordx4 (each lane moves 16 bytes straight into LDS, no
-// registers, no vector instructions), three blocks in flight per buffer
-// ring, so the load latency hides behind two blocks of compute.
+// registers, no vector instructions) into a ring of slots, one or more
+// blocks ahead of the compute.
 //
 // LDS layout of a block: row-major [position][4 chunks of 8 channels], the
-// chunk slots of position p permuted by XOR with (p >> 1) & 3.  The DMA
+// chunk slots of position p permuted by XOR with swz(p) (below).  The DMA
 // writes a wave's 64 lanes to 1 KB of consecutive LDS, so the permutation is
 // applied on the global side: the lane that fills slot s of position p loads
-// chunk s ^ swz(p).  Readers then see
-//   - row fragments (8 consecutive channels of one position per lane,
-//     ds_read_b128) of 8 consecutive positions on 8 different bank groups;
-//   - transposed fragments (4 consecutive positions of one channel per lane,
-//     ds_read_b64_tr_b16) with the 4 positions of a lane group on different
-//     bank groups.
+// chunk s ^ swz(p).  The permutation keeps both read patterns free of bank
+// conflicts whether the LDS serves 128 or 256 bytes per cycle:
+//   - row fragments (one 16-byte chunk of one position per lane,
+//     ds_read_b128, consecutive lanes on consecutive positions): any 8
+//     aligned consecutive positions, and any 16, hit distinct 16-byte bank
+//     groups;
+//   - transposed fragments (ds_read_b64_tr_b16: 16 lanes read 4 consecutive
+//     positions x 2 chunks): positions p and p + 2 put their chunk pairs in
+//     different halves of the 64-byte row.
 //
 // Waits: a DMA counts in vmcnt like any vector load and completes in issue
 // order.  Before a block is read the waves wait until at most the ops issued
@@ -32,28 +35,14 @@ namespace triattn {
 
 #define TRIATTN_LDS __attribute__((address_space(3)))
 
-constexpr int DBLK_POS = 64;                  // positions per block
-constexpr int DBLK_BYTES = DBLK_POS * 64;     // 4 KB
-constexpr int DBLK_ELEMS = DBLK_BYTES / 2;
-
-__device__ inline int swz(int p) { return (p >> 1) & 3; }
+// Bit 1 of the slot permutation is bit 1 ^ bit 3 of the position, bit 0 is
+// bit 2: a bijection of the four chunk slots for positions 8 m + b + 2 k
+// (k = 0..3) and for 16 m + b + 4 k, and positions p, p + 2 (p % 4 < 2)
+// differ in bit 1.
+__device__ inline int swz(int p) { return ((((p >> 1) ^ (p >> 3)) & 1) << 1) | ((p >> 2) & 1); }
 
 // Byte offset of channels 8 c .. 8 c + 7 of position p in a block.
 __device__ inline int blk_off(int p, int c) { return p * 64 + 16 * (c ^ swz(p)); }
-
-// Copy one block (positions start .. start + 63 of a row, clamped to `last`
-// so every address is in bounds) into LDS.  `part` (0..3) selects the
-// quarter of the block, positions 16 part .. 16 part + 15, that this wave
-// moves; four waves (or four calls) move a whole block.  `dst` is the
-// block's LDS base (same for the whole wave).
-__device__ inline void dma_block_part(const bf16* row, int64_t sPos, int start, int last,
-                                      bf16* dst, int part, int lane) {
-  const int p = 16 * part + (lane >> 2);
-  const int c = (lane & 3) ^ swz(p);
-  const int pos = min(start + p, last);
-  __builtin_amdgcn_global_load_lds(row + (int64_t)pos * sPos + 8 * c,
-                                   (TRIATTN_LDS void*)((char*)dst + 1024 * part), 16, 0, 0);
-}
 
 // One 16-byte DMA lane: `src` is this lane's global address, `dst_wave` the
 // LDS address of the wave's 1 KB destination (lane i lands at + 16 i).
@@ -81,14 +70,6 @@ __device__ inline void lds_barrier() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-}
-
-// Row fragments for the 32x32x16 bf16 MFMA (A row / B column = position p of
-// the block): chunk t holds channels 16 t + 8 g .. +7.
-__device__ inline void blk_row_frags(const bf16* blk, int p, int g, bf16x8 (&f)[2]) {
-  const char* b = (const char*)blk;
-  f[0] = *(const bf16x8*)(b + blk_off(p, g));
-  f[1] = *(const bf16x8*)(b + blk_off(p, 2 + g));
 }
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -131,19 +112,11 @@ struct TrAddr {
     const int p = p0 + pe;
     return blk_off(p, cch) + half;
   }
+  // The slot permutation of p0 + pe depends on bit 3 of p0 and not on its
+  // bits 4 and up, so for p0 = 16 k the read is off(0) + 64 p0 and for
+  // p0 = 16 k + 8 it is off(8) + 64 (p0 - 8): two base addresses and
+  // immediate offsets cover a whole block.
 };
-
-// Transposed fragments of positions 32 u .. 32 u + 31 of a block (the
-// contraction index of an accumulator-fed product), for both 16-position
-// chunks t = 0, 1.  The caller must wait for lgkmcnt before using them
-// (tr_wait).
-__device__ inline void blk_tr_frags(uint32_t blk, const TrAddr& ta, int u, s16x4 (&r)[4]) {
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    r[2 * t] = ds_read_tr(blk + ta.off(32 * u + 16 * t));
-    r[2 * t + 1] = ds_read_tr(blk + ta.off(32 * u + 16 * t + 8));
-  }
-}
 
 // Wait for all outstanding LDS reads, tied to the registers they fill so
 // that no use of them is scheduled before the wait.

@@ -448,6 +448,7 @@ __global__ __launch_bounds__(512, 1) void fwd_pipe_kernel(FwdArgs<bf16> a) {
   const uint32_t kr1 = base + rp * 2 * FP_ROWBLK + l32 * 64 + 16 * ((2 + g) ^ sw);
   const TrAddr ta(lane);
   const uint32_t vtr = base + (FP_ROWS + 2 * rp) * FP_ROWBLK + ta.off(0);
+  const uint32_t vtr8 = base + (FP_ROWS + 2 * rp) * FP_ROWBLK + ta.off(8) - 8 * 64;
   const uint32_t brd = base + FP_KV + qtl * 4096 + lane * 16;
 
   // logits of block t (ring slot `slot`) for both rows: S^T = bias + K Q^T
@@ -478,11 +479,12 @@ __global__ __launch_bounds__(512, 1) void fwd_pipe_kernel(FwdArgs<bf16> a) {
   // P = exp2(S c1 - m), then O^T += V^T P^T and the row sums, row i of slot
   auto pv = [&](int slot, int i, f32x16& s) {
     const uint32_t va = vtr + slot * FP_SLOT + i * FP_ROWBLK;
+    const uint32_t va8 = vtr8 + slot * FP_SLOT + i * FP_ROWBLK;
     s16x4 tr[4];
     tr[0] = ds_read_tr<0>(va);
-    tr[1] = ds_read_tr<8 * 64>(va);
+    tr[1] = ds_read_tr<8 * 64>(va8);
     tr[2] = ds_read_tr<16 * 64>(va);
-    tr[3] = ds_read_tr<24 * 64>(va);
+    tr[3] = ds_read_tr<24 * 64>(va8);
 #pragma unroll
     for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m[i]));
     F pf[M::PCH];

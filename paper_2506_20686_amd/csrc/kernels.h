@@ -32,7 +32,7 @@ struct Prep {
 
 struct BwdWs {
   float* lse2;   // [H][n][np]  lse * log2(e); +inf where the query has no valid key
-  float* dsum;   // [H][n][np]  D = rowsum(dO * O)
+  float* dsum;   // [H][n][np]  -D, D = rowsum(dO * O) (stored negated: it enters as -D)
   void* da;      // [n][n][H][32] dtype: dA = dO * sigmoid(G), laid out like dO
   void* dalo;    // bf16 only: dA - bf16(dA) rounded to bf16 (null for fp32)
   float* slabs;  // [nrc][H][np][np] per-row-chunk partial bias gradients
