@@ -249,6 +249,178 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   }
 }
 
+// bf16 dQ (and D) with asynchronous LDS staging (see dma.h).  One workgroup
+// = 4 waves = 64 queries x 2 rows of one head: wave w owns query tile w % 2
+// (lane <-> query) of row r0 + w / 2.  Keys stream in blocks of 32; per
+// block, K and V of both rows and the query-major bias tiles of the 64
+// queries (shared by the two rows) are copied HBM -> LDS by DMA into a ring
+// of three slots, two blocks ahead.  K^T fragments for the dQ products come
+// from the transposing LDS read of the row-major K block.  Three workgroups
+// share a CU (48 KB of LDS each).
+constexpr int QD_BLK = 32 * 64;                     // 2 KB: 32 keys x 32 channels
+constexpr int QD_K = 0, QD_V = 2 * QD_BLK;          // [row] blocks
+constexpr int QD_BIAS = 4 * QD_BLK;                 // 2 query tiles x 4 KB
+constexpr int QD_SLOT = QD_BIAS + 2 * 4096;
+constexpr int QD_SLOTS = 3;
+constexpr int QD_OPS = 4;                           // DMA ops per thread per block
+
+__global__ __launch_bounds__(256, 3) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
+  using M = Mma<bf16>;
+  using F = bf16x8;
+  const Geom& G = a.g;
+  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int nrg = (G.n + 1) / 2;
+  const int qb = w % nqb, rg = (w / nqb) % nrg, h = w / (nqb * nrg);
+  const int r0 = rg * 2;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qtl = wave & 1, ri = wave >> 1;
+  const int r = min(r0 + ri, G.n - 1);
+  const bool rok = r0 + ri < G.n;
+  const int q0 = qb * 64 + qtl * TILE;
+  const int q = q0 + l32;
+  const bool active = rok && q0 < G.n;
+  const bool qok = q < G.n;
+  const int nkt = G.nkt, last = G.n - 1;
+  const float c1 = G.scale * LOG2E;
+
+  __shared__ __align__(16) char smem[QD_SLOTS * QD_SLOT];
+
+  // ---- this lane's query: Q, dA (hi, lo) fragments and lse2
+  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  F qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+  float l2 = pos_inf();
+  if (qok) {
+    row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
+    row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
+    row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    l2 = a.lse2[((int64_t)h * G.n + r) * G.np + q];
+  } else {
+    zero_frags<bf16>(qf);
+    zero_frags<bf16>(daf);
+    zero_frags<bf16>(dalf);
+  }
+  // plain register loads: let them complete before any DMA is issued (with
+  // both kinds outstanding the compiler would wait for every DMA at each use)
+  wait_vm<0>();
+
+  // ---- DMA lanes.  Ops 0, 1: K, V of both rows (wave w: row w / 2,
+  // positions 16 (w % 2) + lane / 4).  Ops 2, 3: bias tile j of the 64
+  // queries, quarter w.
+  const int dri = wave >> 1;
+  const int dp = 16 * (wave & 1) + (lane >> 2), dc = (lane & 3) ^ swz(dp);
+  const int64_t drb = (int64_t)min(r0 + dri, last) * G.sRow + (int64_t)h * HEAD_DIM + 8 * dc;
+  auto issue = [&](int t, int slot) {
+    char* sl = smem + slot * QD_SLOT;
+    const int64_t o = drb + (int64_t)min(t * TILE + dp, last) * G.sPos;
+    dma16(a.k + o, sl + QD_K + dri * QD_BLK + 1024 * (wave & 1));
+    dma16(a.v + o, sl + QD_V + dri * QD_BLK + 1024 * (wave & 1));
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const float* bsrc = frag_tile(a.bt, h, min(qb * 2 + j, nkt - 1), t, nkt);
+      dma16((const char*)bsrc + 1024 * wave + 16 * lane, sl + QD_BIAS + j * 4096 + 1024 * wave);
+    }
+  };
+
+  // ---- LDS read addresses (slot 0)
+  const uint32_t base = lds_addr(smem);
+  const int sw = swz(l32);
+  const uint32_t rk0 = base + ri * QD_BLK + l32 * 64 + 16 * (g ^ sw);
+  const uint32_t rk1 = base + ri * QD_BLK + l32 * 64 + 16 * ((2 + g) ^ sw);
+  const TrAddr ta(lane);
+  const uint32_t rtr = base + QD_K + ri * QD_BLK + ta.off(0);
+  const uint32_t rtr8 = base + QD_K + ri * QD_BLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + QD_BIAS + qtl * 4096 + lane * 16;
+
+  f32x16 xt = {}, yt = {};
+  float dpart = 0.f;
+
+#pragma unroll
+  for (int j = 0; j < QD_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
+  for (int t = 0; t < nkt; ++t) {
+    const uint32_t so = (t % QD_SLOTS) * QD_SLOT;
+    wait_vm<(QD_SLOTS - 2) * QD_OPS>();  // block t has landed
+    lds_barrier();
+    // key bits of both rows: the same in every wave, so the branch below (it
+    // holds a barrier) is uniform across the workgroup
+    const uint32_t w0 = const_load(a.kbits + (int64_t)r0 * nkt + t);
+    const uint32_t w1 = r0 + 1 < G.n ? const_load(a.kbits + (int64_t)(r0 + 1) * nkt + t) : 0u;
+    if ((w0 & (r0 + 1 < G.n ? w1 : 0xffffffffu)) != 0xffffffffu) {
+      // zero V rows of keys invalid for a row (P = 0 there, and 0 times a
+      // non-finite dP would not be); thread t < 128: row t / 64, key t / 2 % 32
+      if (tid < 128) {
+        const uint32_t wb = (tid >> 6) ? w1 : w0;
+        if (!((wb >> ((tid >> 1) & 31)) & 1u))
+          *(f32x4*)(smem + so + QD_V + 32 * tid) = f32x4{},
+                   *(f32x4*)(smem + so + QD_V + 32 * tid + 16) = f32x4{};
+      }
+      __syncthreads();
+    }
+    // block t + QD_SLOTS - 1 into the slot of block t - 1
+    issue(min(t + QD_SLOTS - 1, nkt - 1), (t + QD_SLOTS - 1) % QD_SLOTS);
+    const uint32_t bits = ri ? w1 : w0;
+    if (!active || bits == 0u) continue;
+    // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
+    f32x16 sv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sv[4 * j + e] = y[e];
+    }
+    {
+      const F k0 = lds_load16<F>(rk0 + so + QD_K), k1 = lds_load16<F>(rk1 + so + QD_K);
+      sv = M::mma(k1, qf[1], M::mma(k0, qf[0], sv));
+    }
+    if (bits != 0xffffffffu) mask_rows(sv, bits, g);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2));
+    // dP^T = V dA^T (hi and lo parts), then P dP and its running sum D
+    f32x16 dp;
+    {
+      const F v0 = lds_load16<F>(rk0 + so + QD_V), v1 = lds_load16<F>(rk1 + so + QD_V);
+      dp = M::mma(v0, daf[0], f32x16{});
+      dp = M::mma(v1, daf[1], dp);
+      dp = M::mma(v0, dalf[0], dp);
+      dp = M::mma(v1, dalf[1], dp);
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      dp[v] *= sv[v];
+      dpart += dp[v];
+    }
+    // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the block's keys)
+    const uint32_t tk = rtr + so, tk8 = rtr8 + so;
+    s16x4 xk[4];
+    xk[0] = ds_read_tr<0>(tk);
+    xk[1] = ds_read_tr<8 * 64>(tk8);
+    xk[2] = ds_read_tr<16 * 64>(tk);
+    xk[3] = ds_read_tr<24 * 64>(tk8);
+    F pf[M::PCH], xf[M::PCH];
+    acc_frags(dp, xf);
+    acc_frags(sv, pf);
+    tr_wait(xk);
+#pragma unroll
+    for (int u = 0; u < M::PCH; ++u) {
+      xt = M::mma(tr_frag(xk, u), xf[u], xt);
+      yt = M::mma(tr_frag(xk, u), pf[u], yt);
+    }
+  }
+  wait_vm<0>();  // the copies past the end must land before the workgroup ends
+  if (!active) return;
+  const float dsum = wave_xor32_sum(dpart);
+  if (!qok) return;
+  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = -dsum;  // stored negated
+  const int64_t gb = rowbase + (int64_t)q * G.sPos;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    f32x4 x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
+    store4(a.dq + gb + 8 * j + 4 * g, x);
+  }
+}
+
 // ---- dK, dV --------------------------------------------------------------------------
 
 // Per (row, head, 128 keys; wave <-> 32 keys, lane <-> key): stream the row's
@@ -927,9 +1099,15 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
                (g.n + BWD_BLK - 1) / BWD_BLK, ws.nrc, (g.n + ws.nrc - 1) / ws.nrc};
   const int64_t nrow = (int64_t)a.nblk * g.n * g.H;
   {
-    // dq_kernel first: it produces D for the other two
+    // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
-    hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+    if constexpr (std::is_same<T, bf16>::value) {
+      const int nqb = (g.n + 63) / 64;
+      const int64_t nwg = (int64_t)nqb * ((g.n + 1) / 2) * g.H;
+      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(256), 0, s, a, nqb);
+    } else {
+      hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+    }
   }
   {
     KernelTimer t(K_DKDV, s);
