@@ -343,270 +343,172 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   }
 }
 
-// bf16 forward: asynchronous LDS staging (see dma.h) and a software
-// pipeline.  One workgroup = 8 waves = 128 queries x 4 rows of one head:
-// waves 0-3 take rows r0, r0 + 1 and waves 4-7 rows r0 + 2, r0 + 3, wave
-// w % 4 the queries 32 (w % 4) .. +31.  Keys stream in blocks of 32; per
-// block, K and V of the four rows and the bias tiles of the 128 queries
-// (shared by the four rows) are copied HBM -> LDS by DMA into a ring of four
-// slots, three blocks ahead.  While a wave computes exp / P V of block b it
-// already issues the logit MFMAs of block b + 1 (whose data landed one
-// iteration earlier), so the matrix cores run under the vector work instead
-// of after it.  Every operand reaches LDS without registers or vector
-// instructions; V^T fragments come from the transposing LDS load; the only
-// vmcnt waits are the explicit ones for the next block.
-constexpr int FP_WAVES = 8;
-constexpr int FP_ROWS = 4;                              // rows per workgroup
-constexpr int FP_POS = 32;                              // keys per block
-constexpr int FP_ROWBLK = FP_POS * 64;                  // 2 KB: one row's K (or V) block
-constexpr int FP_KV = 2 * FP_ROWS * FP_ROWBLK;          // 16 KB: K rows 0..3, V rows 0..3
-constexpr int FP_SLOT = FP_KV + 4 * 4096;               // + bias tiles of the 4 query tiles
-constexpr int FP_SLOTS = 4;
-constexpr int FP_DMA_OPS = 4;                           // DMA ops per thread per block
+// bf16 forward with asynchronous LDS staging (see dma.h).  One workgroup =
+// 8 waves = 128 queries x 2 rows of one head (wave w: query tile w % 4 of
+// row r0 + w / 4, one row per wave).  Keys stream in blocks of 32 through a
+// three-slot DMA ring (K and V of both rows, the bias tiles of the 128
+// queries, shared by the rows: 24 KB per slot), two blocks ahead.  89 VGPRs
+// and 72 KB of LDS let two workgroups share a CU: four waves per SIMD hide
+// the latency of each wave's dependent MFMA / exp steps (a variant with two
+// rows per wave and a software-pipelined loop, at two waves per SIMD, was
+// 25% slower).
+constexpr int FO_ROWS = 2;
+constexpr int FO_ROWBLK = 32 * 64;                     // 2 KB: one row's K (or V) block
+constexpr int FO_KV = 2 * FO_ROWS * FO_ROWBLK;         // 8 KB: K0, K1, V0, V1
+constexpr int FO_SLOT = FO_KV + 4 * 4096;              // + bias tiles of the 4 query tiles
+constexpr int FO_SLOTS = 3;
+constexpr int FO_OPS = 3;                              // DMA ops per thread per block
 
-__global__ __launch_bounds__(512, 1) void fwd_pipe_kernel(FwdArgs<bf16> a) {
+__global__ __launch_bounds__(512, 4) void fwd_dma_kernel(FwdArgs<bf16> a) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int nrg = (G.n + FP_ROWS - 1) / FP_ROWS;
+  const int nrg = (G.n + FO_ROWS - 1) / FO_ROWS;
   const int qb = w % a.nqb, rg = (w / a.nqb) % nrg, h = w / (a.nqb * nrg);
-  const int r0 = rg * FP_ROWS;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int qtl = wave & 3, rp = wave >> 2;  // query tile of the block, row pair
+  const int r0 = rg * FO_ROWS;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qtl = wave & 3, ri = wave >> 2;
+  const int row = r0 + ri;                  // this wave's row
+  const bool rok = row < G.n;
   const int q0 = qb * FWD_QBLK + qtl * TILE;
-  const bool active = q0 < G.n;
+  const bool active = rok && q0 < G.n;
   const int q = q0 + l32;
   const bool qok = q < G.n;
   const int nkt = G.nkt, last = G.n - 1;
+  const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) char smem[FP_SLOTS * FP_SLOT];
+  __shared__ __align__(16) char smem[FO_SLOTS * FO_SLOT];
 
-  int64_t rowbase[FP_ROWS];  // the four rows (clamped into range, for the DMA)
-#pragma unroll
-  for (int i = 0; i < FP_ROWS; ++i)
-    rowbase[i] = (int64_t)min(r0 + i, last) * G.sRow + (int64_t)h * HEAD_DIM;
-  // key-valid bits of block t of row r0 + i (zero for rows past the end)
-  auto bits = [&](int i, int t) -> uint32_t {
-    return r0 + i < G.n ? const_load(a.kbits + (int64_t)(r0 + i) * nkt + t) : 0u;
-  };
+  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t myrow = (int64_t)min(row, last) * G.sRow + hb;
+  F qf[M::KCH];
+  if (active && qok)
+    row_frags(a.q + myrow + (int64_t)q * G.sPos, g, qf);
+  else
+    zero_frags<bf16>(qf);
+  // plain register loads: let them complete before any DMA is issued (with
+  // both kinds outstanding the compiler would wait for every DMA at each use)
+  wait_vm<0>();
 
-  // ---- DMA lanes.  Ops 0, 1: K, V of all four rows (thread t: row t / 128,
-  // position (t % 128) / 4, chunk slot t % 4).  Ops 2, 3: bias tiles
-  // 2 j + t / 256, 16 bytes (t % 256) of each.
-  const int drow = wave >> 1;
+  // ---- DMA lanes.  Op 0: K and V of both rows (wave w: block w / 2 of
+  // [K0, K1, V0, V1], positions 16 (w % 2) + lane / 4).  Ops 1, 2: bias
+  // tiles 2 (op - 1) + w / 4, quarter w % 4.
+  const int db = wave >> 1;
   const int dp = 16 * (wave & 1) + (lane >> 2), dc = (lane & 3) ^ swz(dp);
-  const int64_t drb = drow == 0 ? rowbase[0] : drow == 1 ? rowbase[1] : drow == 2 ? rowbase[2]
-                                                                                  : rowbase[3];
+  const bf16* dsrc = db < 2 ? a.k : a.v;
+  const int64_t drb = (int64_t)min(r0 + (db & 1), last) * G.sRow + hb + 8 * dc;
   auto issue = [&](int t, int slot) {
-    char* sl = smem + slot * FP_SLOT;
-    const int64_t o = drb + (int64_t)min(t * FP_POS + dp, last) * G.sPos + 8 * dc;
-    dma16(a.k + o, sl + drow * FP_ROWBLK + 1024 * (wave & 1));
-    dma16(a.v + o, sl + (FP_ROWS + drow) * FP_ROWBLK + 1024 * (wave & 1));
+    char* sl = smem + slot * FO_SLOT;
+    dma16(dsrc + drb + (int64_t)min(t * TILE + dp, last) * G.sPos,
+          sl + db * FO_ROWBLK + 1024 * (wave & 1));
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int tile = 2 * j + (wave >> 2);
       const float* src = frag_tile(a.bt, h, min(qb * 4 + tile, nkt - 1), t, nkt);
       dma16((const char*)src + 1024 * (wave & 3) + 16 * lane,
-            sl + FP_KV + tile * 4096 + 1024 * (wave & 3));
+            sl + FO_KV + tile * 4096 + 1024 * (wave & 3));
     }
   };
+  // key bits of block t of row r0 + i (zero for a row past the end)
+  auto bits = [&](int i, int t) -> uint32_t {
+    return r0 + i < G.n ? const_load(a.kbits + (int64_t)(r0 + i) * nkt + t) : 0u;
+  };
 
-  // ---- this wave's rows and state
-  int64_t myrow[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) myrow[i] = rp ? rowbase[2 + i] : rowbase[i];
-  F qf[2][M::KCH];
-  float m[2];
-  f32x16 o[2];
-  // row sums of P of row i accumulate on the MFMA in accumulator row i of
-  // `lsum` (register i of the lanes of half 0): ones_i has ones in row i only
-  f32x16 lsum = {};
-  F ones[2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    if (qok)
-      row_frags(a.q + myrow[i] + (int64_t)q * G.sPos, g, qf[i]);
-    else
-      zero_frags<bf16>(qf[i]);
-    m[i] = neg_inf();
-    o[i] = f32x16{};
-    const bf16 x = l32 == i ? (bf16)1.f : (bf16)0.f;
-    ones[i] = F{x, x, x, x, x, x, x, x};
-  }
-  const float c1 = G.scale * LOG2E;
-  // The query fragments are plain register loads; let them complete before
-  // any DMA is issued.  With loads of both kinds outstanding the compiler
-  // cannot count them apart and would wait for all DMAs at every use of qf.
-  wait_vm<0>();
-
-  // ---- LDS read addresses (slot 0, the wave's first row; the rest is an
-  // offset)
+  // ---- LDS read addresses (slot 0)
   const uint32_t base = lds_addr(smem);
   const int sw = swz(l32);
-  const uint32_t kr0 = base + rp * 2 * FP_ROWBLK + l32 * 64 + 16 * (g ^ sw);
-  const uint32_t kr1 = base + rp * 2 * FP_ROWBLK + l32 * 64 + 16 * ((2 + g) ^ sw);
+  const uint32_t rk0 = base + ri * FO_ROWBLK + l32 * 64 + 16 * (g ^ sw);
+  const uint32_t rk1 = base + ri * FO_ROWBLK + l32 * 64 + 16 * ((2 + g) ^ sw);
   const TrAddr ta(lane);
-  const uint32_t vtr = base + (FP_ROWS + 2 * rp) * FP_ROWBLK + ta.off(0);
-  const uint32_t vtr8 = base + (FP_ROWS + 2 * rp) * FP_ROWBLK + ta.off(8) - 8 * 64;
-  const uint32_t brd = base + FP_KV + qtl * 4096 + lane * 16;
+  const uint32_t rv = base + (2 + ri) * FO_ROWBLK + ta.off(0);
+  const uint32_t rv8 = base + (2 + ri) * FO_ROWBLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + FO_KV + qtl * 4096 + lane * 16;
 
-  // logits of block t (ring slot `slot`) for both rows: S^T = bias + K Q^T
-  auto logits = [&](int slot, f32x16 (&s)[2]) {
-    const uint32_t so = slot * FP_SLOT;
-    f32x16 bias;
+  float m = neg_inf();
+  f32x16 o = {}, lsum = {};  // O^T; row sums of P in accumulator row 0 (see ones_row0)
+  const F ones = ones_row0<F>(l32);
+
+#pragma unroll
+  for (int j = 0; j < FO_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
+  for (int t = 0; t < nkt; ++t) {
+    const uint32_t so = (t % FO_SLOTS) * FO_SLOT;
+    wait_vm<(FO_SLOTS - 2) * FO_OPS>();  // block t has landed
+    lds_barrier();
+    const uint32_t w0 = bits(0, t), w1 = bits(1, t);
+    if ((w0 & (r0 + 1 < G.n ? w1 : 0xffffffffu)) != 0xffffffffu) {
+      // zero the V rows of keys invalid for a row (weight 0, and 0 times a
+      // non-finite value would not be); thread t < 128: row t / 64, key t / 2 % 32
+      if (tid < 128) {
+        const uint32_t wb = (tid >> 6) ? w1 : w0;
+        if (!((wb >> ((tid >> 1) & 31)) & 1u)) {
+          char* z = smem + so + 2 * FO_ROWBLK + 32 * tid;
+          *(f32x4*)z = f32x4{};
+          *(f32x4*)(z + 16) = f32x4{};
+        }
+      }
+      __syncthreads();
+    }
+    // block t + FO_SLOTS - 1 into the slot of block t - 1 (a copy of the last
+    // block past the end keeps the wait counts uniform)
+    issue(min(t + FO_SLOTS - 1, nkt - 1), (t + FO_SLOTS - 1) % FO_SLOTS);
+    const uint32_t wb = ri ? w1 : w0;
+    if (!active || wb == 0u) continue;
+    f32x16 s;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const f32x4 y = lds_load16<f32x4>(brd + so + 1024 * j);
+      const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) bias[4 * j + e] = y[e];
+      for (int e = 0; e < 4; ++e) s[4 * j + e] = y[e];
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const F k0 = lds_load16<F>(kr0 + so + i * FP_ROWBLK);
-      const F k1 = lds_load16<F>(kr1 + so + i * FP_ROWBLK);
-      s[i] = M::mma(k1, qf[i][1], M::mma(k0, qf[i][0], bias));
+    {
+      const F k0 = lds_load16<F>(rk0 + so), k1 = lds_load16<F>(rk1 + so);
+      s = M::mma(k1, qf[1], M::mma(k0, qf[0], s));  // S^T = bias + K Q^T
     }
-  };
-  auto rescale = [&](int i, float mx) {
-    const float mnew = fmaxf(m[i], mx);
-    const float alpha = __builtin_amdgcn_exp2f(m[i] - mnew);
-    lsum[i] *= alpha;
+    if (wb != 0xffffffffu) mask_rows(s, wb, g);
+    const float mx = wave_xor32_max(max16(s)) * c1;
+    if (__any(mx > m + STALE_MAX_SLACK)) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      lsum[0] *= alpha;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) o[i][v] *= alpha;
-    m[i] = mnew;
-  };
-  // P = exp2(S c1 - m), then O^T += V^T P^T and the row sums, row i of slot
-  auto pv = [&](int slot, int i, f32x16& s) {
-    const uint32_t va = vtr + slot * FP_SLOT + i * FP_ROWBLK;
-    const uint32_t va8 = vtr8 + slot * FP_SLOT + i * FP_ROWBLK;
+      for (int v = 0; v < 16; ++v) o[v] *= alpha;
+      m = mnew;
+    }
     s16x4 tr[4];
-    tr[0] = ds_read_tr<0>(va);
-    tr[1] = ds_read_tr<8 * 64>(va8);
-    tr[2] = ds_read_tr<16 * 64>(va);
-    tr[3] = ds_read_tr<24 * 64>(va8);
+    tr[0] = ds_read_tr<0>(rv + so);
+    tr[1] = ds_read_tr<8 * 64>(rv8 + so);
+    tr[2] = ds_read_tr<16 * 64>(rv + so);
+    tr[3] = ds_read_tr<24 * 64>(rv8 + so);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m[i]));
+    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m));
     F pf[M::PCH];
     acc_frags(s, pf);
     tr_wait(tr);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) {
-      o[i] = M::mma(tr_frag(tr, t), pf[t], o[i]);  // O^T += V^T P^T
-      lsum = M::mma(ones[i], pf[t], lsum);         // row sums of P
+    for (int u = 0; u < M::PCH; ++u) {
+      o = M::mma(tr_frag(tr, u), pf[u], o);  // O^T += V^T P^T
+      lsum = M::mma(ones, pf[u], lsum);      // row sums of P
     }
-  };
-  // zero the V rows of keys that are invalid for a row (weight 0, and 0
-  // times a non-finite value would not be 0); thread t: row t / 128,
-  // position (t % 128) / 4, 16 bytes
-  auto zero_invalid = [&](int slot, const uint32_t (&wb)[FP_ROWS]) {
-    const uint32_t word = drow == 0 ? wb[0] : drow == 1 ? wb[1] : drow == 2 ? wb[2] : wb[3];
-    if (!((word >> dp) & 1u))
-      *(f32x4*)(smem + slot * FP_SLOT + (FP_ROWS + drow) * FP_ROWBLK + 16 * (tid & 127)) =
-          f32x4{};
-  };
-  auto all_valid = [&](const uint32_t (&wb)[FP_ROWS]) {
-    bool f = true;
-#pragma unroll
-    for (int i = 0; i < FP_ROWS; ++i) f = f && (r0 + i >= G.n || wb[i] == 0xffffffffu);
-    return f;
-  };
-
-  // ---- prologue: blocks 0, 1, 2 in flight; logits of block 0
-  uint32_t wc[FP_ROWS];  // key bits of the current block
-#pragma unroll
-  for (int i = 0; i < FP_ROWS; ++i) wc[i] = bits(i, 0);
-  issue(0, 0);
-  issue(min(1, nkt - 1), 1);
-  issue(min(2, nkt - 1), 2);
-  wait_vm<2 * FP_DMA_OPS>();
-  lds_barrier();
-  if (!all_valid(wc)) {
-    zero_invalid(0, wc);
-    __syncthreads();
-  }
-  // logits of the current and the next block (two sets used in turn) and
-  // the maxima (log2 units) of the current block's
-  f32x16 sA[2], sB[2];
-  float mA[2], mB[2];
-  auto row_max = [&](f32x16 (&s)[2], const uint32_t (&wb)[FP_ROWS], float (&mx)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint32_t wi = rp ? wb[2 + i] : wb[i];
-      if (wi != 0xffffffffu) mask_rows(s[i], wi, g);
-      mx[i] = wave_xor32_max(max16(s[i])) * c1;
-    }
-  };
-  if (active) {
-    logits(0, sA);
-    row_max(sA, wc, mA);
-  }
-
-  // one block: t's exp / P V with block t + 1's logits issued alongside
-  auto iter = [&](int t, f32x16 (&sc)[2], f32x16 (&sn)[2], float (&mc)[2], float (&mn)[2]) {
-    const int slot = t & 3, nslot = (t + 1) & 3;
-    const bool more = t + 1 < nkt;
-    // block t + 1 must have landed; only block t + 2 (issued in the last
-    // iteration) may still be in flight
-    wait_vm<FP_DMA_OPS>();
-    lds_barrier();
-    uint32_t wn[FP_ROWS];
-#pragma unroll
-    for (int i = 0; i < FP_ROWS; ++i) wn[i] = more ? bits(i, t + 1) : 0u;
-    if (more && !all_valid(wn)) {
-      zero_invalid(nslot, wn);
-      __syncthreads();
-    }
-    // block t + 3 (a copy of the last block past the end keeps the wait
-    // counts uniform; its slot held block t - 1, which every wave is done with)
-    issue(min(t + 3, nkt - 1), (t + 3) & 3);
-    if (active) {
-      const uint32_t w0 = rp ? wc[2] : wc[0], w1 = rp ? wc[3] : wc[1];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        if (__any(mc[i] > m[i] + STALE_MAX_SLACK)) rescale(i, mc[i]);
-      // past the last block this reads a copy of the last block: harmless
-      logits(nslot, sn);
-      if (w0 == 0xffffffffu && w1 == 0xffffffffu) {
-        pv(slot, 0, sc[0]);
-        pv(slot, 1, sc[1]);
-      } else {
-        if (w0) pv(slot, 0, sc[0]);
-        if (w1) pv(slot, 1, sc[1]);
-      }
-      row_max(sn, wn, mn);
-    }
-#pragma unroll
-    for (int i = 0; i < FP_ROWS; ++i) wc[i] = wn[i];
-  };
-  for (int t = 0; t < nkt; t += 2) {
-    iter(t, sA, sB, mA, mB);
-    if (t + 1 >= nkt) break;
-    iter(t + 1, sB, sA, mB, mA);
   }
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active || !qok) return;
-
+  const float lt = wave_xor32_sum(lsum[0]);  // half 1 holds zero in register 0
+  const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
+  const int64_t gbase = myrow + (int64_t)q * G.sPos;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = r0 + 2 * rp + i;
-    if (r >= G.n) break;
-    const float lt = wave_xor32_sum(lsum[i]);  // half 1 holds zeros in registers 0, 1
-    const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
-    const int64_t gbase = myrow[i] + (int64_t)q * G.sPos;
+  for (int j = 0; j < 4; ++j) {
+    const int c0 = 8 * j + 4 * g;
+    const f32x4 gv = load4(a.gate + gbase + c0);
+    f32x4 ov;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c0 = 8 * j + 4 * g;
-      const f32x4 gv = load4(a.gate + gbase + c0);
-      f32x4 ov;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ov[e] = o[i][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
-      store4(a.out + gbase + c0, ov);
-    }
-    if (g == 0)
-      a.lse[(int64_t)r * G.lRow + (int64_t)q * G.lPos + h] =
-          lt > 0.f ? (m[i] + log2f(lt)) * LN2 : neg_inf();
+    for (int e = 0; e < 4; ++e) ov[e] = o[4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+    store4(a.out + gbase + c0, ov);
   }
+  if (g == 0)
+    a.lse[(int64_t)row * G.lRow + (int64_t)q * G.lPos + h] =
+        lt > 0.f ? (m + log2f(lt)) * LN2 : neg_inf();
 }
 
 template <typename T>
@@ -614,9 +516,9 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   if constexpr (std::is_same<T, bf16>::value) {
-    const int64_t nwg = (int64_t)a.nqb * ((g.n + FP_ROWS - 1) / FP_ROWS) * g.H;
+    const int64_t nwg = (int64_t)a.nqb * ((g.n + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL(fwd_pipe_kernel, dim3((unsigned)nwg), dim3(64 * FP_WAVES), 0, s, a);
+    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a);
   } else {
     const int64_t nwg = (int64_t)a.nqb * ((g.n + FWD_ROWS - 1) / FWD_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
