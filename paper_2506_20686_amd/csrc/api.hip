@@ -41,13 +41,13 @@ int db_row_chunks(int64_t n, int64_t h) {
 }
 
 struct Layout {
-  size_t bt, btT, kbits, lse2, dsum, da, dalo, slabs, total;
+  size_t bt, btT, kbits, rowfull, lse2, dsum, da, dalo, slabs, total;
   int nrc;
 };
 
 // Workspace layout (offsets in bytes, each 256-aligned):
-//   forward : bt [H][np][np] f32, kbits [n][np/32] u32
-//   backward: bt, btT [H][np][np] f32, kbits, lse2 and dsum [H][n][np] f32,
+//   forward : bt [H][np][np] f32, kbits [n][np/32] u32, rowfull [n] u32
+//   backward: bt, btT [H][np][np] f32, kbits, rowfull, lse2 and dsum [H][n][np] f32,
 //             dA [n][n][H][32] dtype (bf16: plus its low part, same size),
 //             slabs [nrc][H][np][np] f32
 Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
@@ -63,6 +63,8 @@ Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
   }
   L.kbits = off;
   off += round256((size_t)n * (np / 32) * sizeof(uint32_t));
+  L.rowfull = off;
+  off += round256((size_t)n * sizeof(uint32_t));
   if (bwd) {
     const size_t rows = (size_t)h * n * np * sizeof(float);
     L.lse2 = off;
@@ -100,7 +102,7 @@ Geom geom(int node, int64_t n, int64_t h, float scale) {
 triattn::Prep prep_ptrs(const Layout& L, void* ws, bool bwd) {
   char* b = (char*)ws;
   return triattn::Prep{(float*)(b + L.bt), bwd ? (float*)(b + L.btT) : nullptr,
-                       (uint32_t*)(b + L.kbits)};
+                       (uint32_t*)(b + L.kbits), (uint32_t*)(b + L.rowfull)};
 }
 
 template <typename T>

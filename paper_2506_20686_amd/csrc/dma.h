@@ -50,6 +50,27 @@ __device__ inline void dma16(const void* src, void* dst_wave) {
   __builtin_amdgcn_global_load_lds(src, (TRIATTN_LDS void*)dst_wave, 16, 0, 0);
 }
 
+// Buffer resource over the bytes [base, end) (gfx9 raw buffer, stride 0).
+// A lane whose offset falls past `end` reads zeros, so the ragged tail of a
+// tensor needs no clamped addresses.  The record count saturates at 4 GiB - 1;
+// callers keep each lane's offset below 2^32 by moving `base` with the tile.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ inline rsrc_t buf_rsrc(const void* base, const void* end) {
+  // callers keep base <= end; the test on the high word stays scalar
+  const uint64_t len = (uint64_t)((const char*)end - (const char*)base);
+  const uint32_t nr = (len >> 32) != 0 ? 0xffffffffu : (uint32_t)len;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)nr,
+                                           0x00020000);
+}
+
+// One 16-byte DMA lane through a buffer resource: lane i's 16 bytes at
+// `voff` land at dst_wave + 16 i.  The resource (and so the per-tile advance)
+// lives in scalar registers; the lane offset is fixed for the whole loop.
+__device__ inline void dma16b(rsrc_t r, uint32_t voff, void* dst_wave) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (TRIATTN_LDS void*)dst_wave, 16, (int)voff, 0, 0,
+                                           0);
+}
+
 // 16-byte LDS load from a 32-bit LDS byte address.
 template <typename V>
 __device__ inline V lds_load16(uint32_t addr) {

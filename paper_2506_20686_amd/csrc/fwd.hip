@@ -4,8 +4,9 @@
 // and save the log-sum-exp.  Also the per-call preparation kernels.
 //
 // Differences from the paper's Triton kernel, for gfx950:
-//  - one workgroup = 4 waves = 128 queries of one (row, head); the K and V
-//    tiles of the row are staged once in LDS and shared by the 4 waves;
+//  - one bf16 workgroup = 8 waves = 128 queries x 4 rows of one head; the
+//    K and V tiles of the rows and the bias tiles of the queries (shared by
+//    the rows) are copied into LDS by DMA and shared by the waves;
 //  - logits are formed transposed (S^T = K Q^T) so that each lane owns one
 //    query: the running max/sum are per-lane scalars and the output
 //    accumulator O^T = V^T P^T is rescaled with one multiply per register;
@@ -13,10 +14,8 @@
 //    initial MFMA accumulator, so adding it costs no vector instruction, and
 //    the softmax runs in base 2 with scale * log2(e) folded into one FMA;
 //  - the sigmoid gate is applied in the epilogue;
-//  - key tiles that are fully masked for the row are skipped;
-//  - keys stream in blocks of 64 through double-buffered LDS: the next
-//    block's loads are issued before the current block is computed, one
-//    barrier per block;
+//  - key tiles that are fully masked for the row are skipped, and rows with
+//    every key valid take a loop without mask steps;
 //  - the running max is only raised when it grows by more than 2^8, so the
 //    rescale of the accumulator is rare.
 #include <type_traits>
@@ -57,21 +56,26 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const 
 }
 
 // kbits[row][t]: bit e set iff key 32 t + e < n and mask(row, key) != 0.
-// The starting node reads mask[row][key], the ending node mask[key][row].
+// rowfull[row] = 1 iff every key < n is valid for the row.  One workgroup
+// per row, thread t builds word t (nkt <= 256 for n <= 8192).  The starting
+// node reads mask[row][key], the ending node mask[key][row].
 __global__ __launch_bounds__(256) void prep_kbits_kernel(Geom G, int node, const uint8_t* mask,
-                                                         uint32_t* kbits) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)G.n * G.nkt) return;
-  const int row = (int)(idx / G.nkt), t = (int)(idx % G.nkt), n = G.n;
-  uint32_t bits = 0;
-  for (int e = 0; e < 32; ++e) {
-    const int key = 32 * t + e;
-    if (key >= n) break;
-    const bool ok = mask == nullptr ||
-                    mask[node == 0 ? (int64_t)row * n + key : (int64_t)key * n + row] != 0;
-    bits |= (ok ? 1u : 0u) << e;
+                                                         uint32_t* kbits, uint32_t* rowfull) {
+  const int row = blockIdx.x, t = threadIdx.x, n = G.n;
+  uint32_t bits = 0, want = 0;
+  if (t < G.nkt) {
+    for (int e = 0; e < 32; ++e) {
+      const int key = 32 * t + e;
+      if (key >= n) break;
+      const bool ok = mask == nullptr ||
+                      mask[node == 0 ? (int64_t)row * n + key : (int64_t)key * n + row] != 0;
+      bits |= (ok ? 1u : 0u) << e;
+      want |= 1u << e;
+    }
+    kbits[(int64_t)row * G.nkt + t] = bits;
   }
-  kbits[idx] = bits;
+  const int full = __syncthreads_and(bits == want);
+  if (t == 0) rowfull[row] = full ? 1u : 0u;
 }
 
 template <typename T>
@@ -83,11 +87,10 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
     hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb), dim3(256), 0, s, g, node, bias,
                        p.bt, p.btT);
   }
-  const int64_t nk = ((int64_t)g.n * g.nkt + 255) / 256;
   {
     KernelTimer t(K_PREP_KBITS, s);
-    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)nk), dim3(256), 0, s, g, node, mask,
-                       p.kbits);
+    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.n), dim3(256), 0, s, g, node, mask,
+                       p.kbits, p.rowfull);
   }
   return hipGetLastError();
 }
@@ -107,6 +110,7 @@ struct FwdArgs {
   Geom g;
   const float* bt;
   const uint32_t* kbits;
+  const uint32_t* rowfull;
   const T *q, *k, *v, *gate;
   T* out;
   float* lse;
@@ -344,22 +348,38 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
 }
 
 // bf16 forward with asynchronous LDS staging (see dma.h).  One workgroup =
-// 8 waves = 128 queries x 2 rows of one head (wave w: query tile w % 4 of
-// row r0 + w / 4, one row per wave).  Keys stream in blocks of 32 through a
-// three-slot DMA ring (K and V of both rows, the bias tiles of the 128
-// queries, shared by the rows: 24 KB per slot), two blocks ahead.  89 VGPRs
-// and 72 KB of LDS let two workgroups share a CU: four waves per SIMD hide
-// the latency of each wave's dependent MFMA / exp steps (a variant with two
-// rows per wave and a software-pipelined loop, at two waves per SIMD, was
-// 25% slower).
-constexpr int FO_ROWS = 2;
-constexpr int FO_ROWBLK = 32 * 64;                     // 2 KB: one row's K (or V) block
-constexpr int FO_KV = 2 * FO_ROWS * FO_ROWBLK;         // 8 KB: K0, K1, V0, V1
-constexpr int FO_SLOT = FO_KV + 4 * 4096;              // + bias tiles of the 4 query tiles
-constexpr int FO_SLOTS = 3;
-constexpr int FO_OPS = 3;                              // DMA ops per thread per block
+// 8 waves = 128 queries x 4 rows of one head; wave w owns query tiles
+// 2 (w % 2) and 2 (w % 2) + 1 of row r0 + w / 2, so every K and V fragment
+// it reads from LDS serves two query tiles.  Keys stream in tiles of 32
+// through a double-buffered DMA ring: per slot the K and V tiles of the 4
+// rows (16 KB) and the bias tiles of the 4 query tiles, shared by the rows
+// (16 KB).  64 KB of LDS and at most 128 VGPRs let two workgroups share a
+// CU (four waves per SIMD).
+//
+// The loop is unrolled by the ring length, so every LDS read has a constant
+// slot offset, and the DMAs go through buffer resources whose base moves
+// with the tile: no vector instruction is spent on addresses.  A workgroup
+// whose rows have every key valid (every row of an unmasked problem) runs a
+// loop without any mask step.
+constexpr int FO_ROWS = 4;
+constexpr int FO_QT = 2;                            // query tiles per wave
+constexpr int FO_ROWBLK = 32 * 64;                  // one row's K (or V) tile: 32 keys x 64 B
+constexpr int FO_V0 = FO_ROWS * FO_ROWBLK;          // V tiles follow the K tiles
+constexpr int FO_BIAS = 2 * FO_ROWS * FO_ROWBLK;    // then the 4 bias tiles (fp32, 4 KB each)
+constexpr int FO_SLOT = FO_BIAS + 4 * 4096;         // 32 KB
+constexpr int FO_SLOTS = 2;
 
-__global__ __launch_bounds__(512, 4) void fwd_dma_kernel(FwdArgs<bf16> a) {
+template <int S>
+using slot_c = std::integral_constant<int, S>;
+
+// Bits of the keys of tile t that lie below n (all 32 except in a ragged last tile).
+__device__ inline uint32_t in_range_bits(int t, int n) {
+  const int m = n - 32 * t;
+  return m >= 32 ? 0xffffffffu : (m <= 0 ? 0u : (1u << m) - 1u);
+}
+
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void fwd_dma_kernel(FwdArgs<bf16> a) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -369,152 +389,247 @@ __global__ __launch_bounds__(512, 4) void fwd_dma_kernel(FwdArgs<bf16> a) {
   const int r0 = rg * FO_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qtl = wave & 3, ri = wave >> 2;
-  const int row = r0 + ri;                  // this wave's row
+  const int qh = wave & 1, ri = wave >> 1;
+  const int row = r0 + ri;  // this wave's row
   const bool rok = row < G.n;
-  const int q0 = qb * FWD_QBLK + qtl * TILE;
-  const bool active = rok && q0 < G.n;
-  const int q = q0 + l32;
-  const bool qok = q < G.n;
   const int nkt = G.nkt, last = G.n - 1;
   const float c1 = G.scale * LOG2E;
+  const int nrows = min(FO_ROWS, G.n - r0);  // rows of this group that exist
 
   __shared__ __align__(16) char smem[FO_SLOTS * FO_SLOT];
 
   const int64_t hb = (int64_t)h * HEAD_DIM;
   const int64_t myrow = (int64_t)min(row, last) * G.sRow + hb;
-  F qf[M::KCH];
-  if (active && qok)
-    row_frags(a.q + myrow + (int64_t)q * G.sPos, g, qf);
-  else
-    zero_frags<bf16>(qf);
+  // query tiles 2 qh + i of the block: lane <-> query
+  int qv[FO_QT];
+  bool act[FO_QT];
+  F qf[FO_QT][M::KCH];
+#pragma unroll
+  for (int i = 0; i < FO_QT; ++i) {
+    const int q0 = qb * FWD_QBLK + (FO_QT * qh + i) * TILE;
+    qv[i] = q0 + l32;
+    act[i] = rok && q0 < G.n;
+    if (act[i] && qv[i] < G.n)
+      row_frags(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
+    else
+      zero_frags<bf16>(qf[i]);
+  }
+  const bool active = act[0];  // tile 1 active implies tile 0 active
+  bool rows_full = true;
+  for (int i = 0; i < nrows; ++i) rows_full = rows_full && const_load(a.rowfull + r0 + i) != 0u;
   // plain register loads: let them complete before any DMA is issued (with
   // both kinds outstanding the compiler would wait for every DMA at each use)
   wait_vm<0>();
 
-  // ---- DMA lanes.  Op 0: K and V of both rows (wave w: block w / 2 of
-  // [K0, K1, V0, V1], positions 16 (w % 2) + lane / 4).  Ops 1, 2: bias
-  // tiles 2 (op - 1) + w / 4, quarter w % 4.
-  const int db = wave >> 1;
-  const int dp = 16 * (wave & 1) + (lane >> 2), dc = (lane & 3) ^ swz(dp);
-  const bf16* dsrc = db < 2 ? a.k : a.v;
-  const int64_t drb = (int64_t)min(r0 + (db & 1), last) * G.sRow + hb + 8 * dc;
-  auto issue = [&](int t, int slot) {
-    char* sl = smem + slot * FO_SLOT;
-    dma16(dsrc + drb + (int64_t)min(t * TILE + dp, last) * G.sPos,
-          sl + db * FO_ROWBLK + 1024 * (wave & 1));
+  // ---- DMA lanes.  Ops 0, 1: K or V tile of one row (wave w: K of row w
+  // for w < 4, V of row w - 4 otherwise), keys 16 op + lane / 4.  Ops 2, 3:
+  // bias tiles 2 (op - 2) + w / 4, quarter w % 4.  Lane offsets are fixed;
+  // the source pointers advance by one tile per issue (scalar registers
+  // only).  Tiles past the last are issued with an empty resource: they
+  // write zeros into a slot that is never read again and keep the wait
+  // counts uniform.
+  const int dblk = wave;  // K0..K3, V0..V3
+  const int dp = lane >> 2;
+  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const bf16* dsrc = dblk < 4 ? a.k : a.v;
+  const bf16* dptr = dsrc + (int64_t)min(r0 + (dblk & 3), last) * G.sRow + hb;
+  const bf16* const dend = dsrc + tensor;
+  uint32_t dvoff[2];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int tile = 2 * j + (wave >> 2);
-      const float* src = frag_tile(a.bt, h, min(qb * 4 + tile, nkt - 1), t, nkt);
-      dma16((const char*)src + 1024 * (wave & 3) + 16 * lane,
-            sl + FO_KV + tile * 4096 + 1024 * (wave & 3));
+  for (int j = 0; j < 2; ++j) {
+    const int p = 16 * j + dp;
+    dvoff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
+  }
+  const int64_t tstep = (int64_t)TILE * G.sPos;
+  const float* bptr = a.bt + ((int64_t)h * nkt + (int64_t)qb * 4) * nkt * 1024;
+  const float* const bend = a.bt + (int64_t)G.H * nkt * nkt * 1024;
+  const int bt0 = wave >> 2, bt1 = 2 + (wave >> 2);  // bias tiles this wave copies
+  const uint32_t bvoff0 =
+      (uint32_t)(((int64_t)bt0 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
+  const uint32_t bvoff1 =
+      (uint32_t)(((int64_t)bt1 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
+  char* const kvdst = smem + dblk * FO_ROWBLK;
+  char* const bdst0 = smem + FO_BIAS + bt0 * 4096 + 1024 * (wave & 3);
+  char* const bdst1 = smem + FO_BIAS + bt1 * 4096 + 1024 * (wave & 3);
+  int issued = 0;
+  auto issue = [&](int slot) {
+    const bool real = issued < nkt;
+    const rsrc_t rk = real ? buf_rsrc(dptr, dend) : buf_rsrc(dptr, dptr);
+    dma16b(rk, dvoff[0], kvdst + slot * FO_SLOT);
+    dma16b(rk, dvoff[1], kvdst + slot * FO_SLOT + 1024);
+    const rsrc_t rb = real ? buf_rsrc(bptr, bend) : buf_rsrc(bptr, bptr);
+    dma16b(rb, bvoff0, bdst0 + slot * FO_SLOT);
+    dma16b(rb, bvoff1, bdst1 + slot * FO_SLOT);
+    if (issued + 1 < nkt) {
+      dptr += tstep;
+      bptr += 1024;
     }
-  };
-  // key bits of block t of row r0 + i (zero for a row past the end)
-  auto bits = [&](int i, int t) -> uint32_t {
-    return r0 + i < G.n ? const_load(a.kbits + (int64_t)(r0 + i) * nkt + t) : 0u;
+    ++issued;
   };
 
-  // ---- LDS read addresses (slot 0)
+  // ---- LDS read addresses (slot 0; the slot adds a constant)
   const uint32_t base = lds_addr(smem);
   const int sw = swz(l32);
   const uint32_t rk0 = base + ri * FO_ROWBLK + l32 * 64 + 16 * (g ^ sw);
   const uint32_t rk1 = base + ri * FO_ROWBLK + l32 * 64 + 16 * ((2 + g) ^ sw);
   const TrAddr ta(lane);
-  const uint32_t rv = base + (2 + ri) * FO_ROWBLK + ta.off(0);
-  const uint32_t rv8 = base + (2 + ri) * FO_ROWBLK + ta.off(8) - 8 * 64;
-  const uint32_t rb = base + FO_KV + qtl * 4096 + lane * 16;
+  const uint32_t rv = base + FO_V0 + ri * FO_ROWBLK + ta.off(0);
+  const uint32_t rv8 = base + FO_V0 + ri * FO_ROWBLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + FO_BIAS + FO_QT * qh * 4096 + lane * 16;
 
-  float m = neg_inf();
-  f32x16 o = {}, lsum = {};  // O^T; row sums of P in accumulator row 0 (see ones_row0)
-  const F ones = ones_row0<F>(l32);
-
+  float m[FO_QT];
+  f32x16 o[FO_QT];
+  float ls0[FO_QT], ls1[FO_QT];  // this lane's share of sum_k P (its 16 keys of each tile)
 #pragma unroll
-  for (int j = 0; j < FO_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
-  for (int t = 0; t < nkt; ++t) {
-    const uint32_t so = (t % FO_SLOTS) * FO_SLOT;
-    wait_vm<(FO_SLOTS - 2) * FO_OPS>();  // block t has landed
-    lds_barrier();
-    const uint32_t w0 = bits(0, t), w1 = bits(1, t);
-    if ((w0 & (r0 + 1 < G.n ? w1 : 0xffffffffu)) != 0xffffffffu) {
-      // zero the V rows of keys invalid for a row (weight 0, and 0 times a
-      // non-finite value would not be); thread t < 128: row t / 64, key t / 2 % 32
-      if (tid < 128) {
-        const uint32_t wb = (tid >> 6) ? w1 : w0;
-        if (!((wb >> ((tid >> 1) & 31)) & 1u)) {
-          char* z = smem + so + 2 * FO_ROWBLK + 32 * tid;
-          *(f32x4*)z = f32x4{};
-          *(f32x4*)(z + 16) = f32x4{};
+  for (int i = 0; i < FO_QT; ++i) {
+    m[i] = neg_inf();
+    o[i] = f32x16{};
+    ls0[i] = ls1[i] = 0.f;
+  }
+  const bf16x2 one2 = {(bf16)1.f, (bf16)1.f};
+
+  // zero the V rows of keys invalid for a row in ring slot S (weight 0, and
+  // 0 times a non-finite value would not be); thread t < 128: row t / 32, key t % 32
+  auto zero_invalid_v = [&](auto slot, const uint32_t (&wr)[FO_ROWS]) {
+    constexpr int S = decltype(slot)::value;
+    if (tid < 128) {
+      const int rr = tid >> 5;
+      const uint32_t wb = rr == 0 ? wr[0] : rr == 1 ? wr[1] : rr == 2 ? wr[2] : wr[3];
+      if (!((wb >> (tid & 31)) & 1u)) {
+        char* z = smem + S * FO_SLOT + FO_V0 + rr * FO_ROWBLK + 64 * (tid & 31);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) *(f32x4*)(z + 16 * e) = f32x4{};
+      }
+    }
+  };
+
+  // the loop; FULL: every key of every row of the group is valid
+  auto run = [&](auto full_c) {
+    constexpr bool FULL = decltype(full_c)::value;
+    auto step = [&](int t, auto slot) {
+      constexpr int S = decltype(slot)::value;
+      uint32_t wr[FO_ROWS];  // key bits of tile t per row (0 for a row past the end)
+#pragma unroll
+      for (int i = 0; i < FO_ROWS; ++i)
+        wr[i] = i < nrows ? (FULL ? in_range_bits(t, G.n)
+                                  : const_load(a.kbits + (int64_t)(r0 + i) * nkt + t))
+                          : 0u;
+      wait_vm<0>();  // tile t has landed
+      lds_barrier();
+      if (!FULL) {
+        bool full = true;
+#pragma unroll
+        for (int i = 0; i < FO_ROWS; ++i) full = full && (i >= nrows || wr[i] == 0xffffffffu);
+        if (!full) {
+          zero_invalid_v(slot, wr);
+          __syncthreads();
         }
       }
-      __syncthreads();
+      issue(S ^ 1);  // tile t + 1 into the other slot
+      const uint32_t wb = ri == 0 ? wr[0] : ri == 1 ? wr[1] : ri == 2 ? wr[2] : wr[3];
+      if (!active || wb == 0u) return;
+      const F k0 = lds_load16<F>(rk0 + S * FO_SLOT), k1 = lds_load16<F>(rk1 + S * FO_SLOT);
+      f32x16 s[FO_QT];
+#pragma unroll
+      for (int i = 0; i < FO_QT; ++i) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 y = lds_load16<f32x4>(rb + S * FO_SLOT + i * 4096 + 1024 * j);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
+        }
+        s[i] = M::mma(k1, qf[i][1], M::mma(k0, qf[i][0], s[i]));  // S^T = bias + K Q^T
+      }
+      s16x4 tr[4];
+      tr[0] = ds_read_tr<S * FO_SLOT>(rv);
+      tr[1] = ds_read_tr<S * FO_SLOT + 8 * 64>(rv8);
+      tr[2] = ds_read_tr<S * FO_SLOT + 16 * 64>(rv);
+      tr[3] = ds_read_tr<S * FO_SLOT + 24 * 64>(rv8);
+#pragma unroll
+      for (int i = 0; i < FO_QT; ++i) {
+        if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
+        const float mx = wave_xor32_max(max16(s[i])) * c1;
+        if (__any(mx > m[i] + STALE_MAX_SLACK)) {
+          const float mnew = fmaxf(m[i], mx);
+          const float alpha = __builtin_amdgcn_exp2f(m[i] - mnew);
+          ls0[i] *= alpha;
+          ls1[i] *= alpha;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[i][v] *= alpha;
+          m[i] = mnew;
+        }
+      }
+      F pf[FO_QT][M::PCH];
+#pragma unroll
+      for (int i = 0; i < FO_QT; ++i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          s[i][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i][v], c1, -m[i]));
+        acc_frags(s[i], pf[i]);
+      }
+      tr_wait(tr);
+#pragma unroll
+      for (int i = 0; i < FO_QT; ++i) {
+#pragma unroll
+        for (int u = 0; u < M::PCH; ++u) o[i] = M::mma(tr_frag(tr, u), pf[i][u], o[i]);
+      }
+      // row sums of the bf16 P the MFMA used: dot products with (1, 1)
+#pragma unroll
+      for (int i = 0; i < FO_QT; ++i) {
+#pragma unroll
+        for (int u = 0; u < M::PCH; ++u) {
+          ls0[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 0, 1), one2, ls0[i], false);
+          ls1[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 2, 3), one2, ls1[i], false);
+          ls0[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 4, 5), one2, ls0[i], false);
+          ls1[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 6, 7), one2, ls1[i], false);
+        }
+      }
+    };
+    issue(0);
+    for (int t = 0; t < nkt; t += FO_SLOTS) {
+      step(t, slot_c<0>{});
+      if (t + 1 >= nkt) break;
+      step(t + 1, slot_c<1>{});
     }
-    // block t + FO_SLOTS - 1 into the slot of block t - 1 (a copy of the last
-    // block past the end keeps the wait counts uniform)
-    issue(min(t + FO_SLOTS - 1, nkt - 1), (t + FO_SLOTS - 1) % FO_SLOTS);
-    const uint32_t wb = ri ? w1 : w0;
-    if (!active || wb == 0u) continue;
-    f32x16 s;
+  };
+  if (rows_full)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
+
+  wait_vm<0>();  // the copies past the end must land before the workgroup ends
+  if (!active) return;
+#pragma unroll
+  for (int i = 0; i < FO_QT; ++i) {
+    const float lt = wave_xor32_sum(ls0[i] + ls1[i]);  // the lane halves hold 16 keys each
+    if (!act[i] || qv[i] >= G.n) continue;
+    const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
+    const int64_t gbase = myrow + (int64_t)qv[i] * G.sPos;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
+      const int c0 = 8 * j + 4 * g;
+      const f32x4 gv = load4(a.gate + gbase + c0);
+      f32x4 ov;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) s[4 * j + e] = y[e];
+      for (int e = 0; e < 4; ++e)
+        ov[e] = o[i][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+      store4(a.out + gbase + c0, ov);
     }
-    {
-      const F k0 = lds_load16<F>(rk0 + so), k1 = lds_load16<F>(rk1 + so);
-      s = M::mma(k1, qf[1], M::mma(k0, qf[0], s));  // S^T = bias + K Q^T
-    }
-    if (wb != 0xffffffffu) mask_rows(s, wb, g);
-    const float mx = wave_xor32_max(max16(s)) * c1;
-    if (__any(mx > m + STALE_MAX_SLACK)) {
-      const float mnew = fmaxf(m, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-      lsum[0] *= alpha;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[v] *= alpha;
-      m = mnew;
-    }
-    s16x4 tr[4];
-    tr[0] = ds_read_tr<0>(rv + so);
-    tr[1] = ds_read_tr<8 * 64>(rv8 + so);
-    tr[2] = ds_read_tr<16 * 64>(rv + so);
-    tr[3] = ds_read_tr<24 * 64>(rv8 + so);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -m));
-    F pf[M::PCH];
-    acc_frags(s, pf);
-    tr_wait(tr);
-#pragma unroll
-    for (int u = 0; u < M::PCH; ++u) {
-      o = M::mma(tr_frag(tr, u), pf[u], o);  // O^T += V^T P^T
-      lsum = M::mma(ones, pf[u], lsum);      // row sums of P
-    }
+    if (g == 0)
+      a.lse[(int64_t)row * G.lRow + (int64_t)qv[i] * G.lPos + h] =
+          lt > 0.f ? (m[i] + log2f(lt)) * LN2 : neg_inf();
   }
-  wait_vm<0>();  // the copies past the end must land before the workgroup ends
-  if (!active || !qok) return;
-  const float lt = wave_xor32_sum(lsum[0]);  // half 1 holds zero in register 0
-  const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
-  const int64_t gbase = myrow + (int64_t)q * G.sPos;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c0 = 8 * j + 4 * g;
-    const f32x4 gv = load4(a.gate + gbase + c0);
-    f32x4 ov;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) ov[e] = o[4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
-    store4(a.out + gbase + c0, ov);
-  }
-  if (g == 0)
-    a.lse[(int64_t)row * G.lRow + (int64_t)q * G.lPos + h] =
-        lt > 0.f ? (m + log2f(lt)) * LN2 : neg_inf();
 }
+
 
 template <typename T>
 hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, const T* v,
                       const T* gate, T* out, float* lse, hipStream_t s) {
-  FwdArgs<T> a{g, p.bt, p.kbits, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
+  FwdArgs<T> a{g, p.bt, p.kbits, p.rowfull, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   if constexpr (std::is_same<T, bf16>::value) {
     const int64_t nwg = (int64_t)a.nqb * ((g.n + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);

@@ -28,6 +28,7 @@ struct Prep {
                    //   lanes <-> queries (zero padded)
   float* btT;      // the same with lanes <-> keys (backward only; may be null)
   uint32_t* kbits; // [n][nkt]     bit e of word t: key 32 t + e is valid for that row
+  uint32_t* rowfull;  // [n]     1 iff every key < n is valid for that row, else 0
 };
 
 struct BwdWs {
