@@ -27,12 +27,12 @@ int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Row chunks of the bias-gradient reduction: about 4608 workgroups of
-// 128 queries x 64 keys (nine rounds of two per CU on 256 CUs), at most 16
+// Row chunks of the bias-gradient reduction: about 2304 workgroups of
+// 128 queries x 128 keys (nine rounds of one per CU on 256 CUs), at most 16
 // partial slabs.
 int db_row_chunks(int64_t n, int64_t h) {
-  const int64_t tiles = h * ((n + 127) / 128) * ((n + 63) / 64);
-  int64_t c = (4608 + tiles - 1) / tiles;
+  const int64_t tiles = h * ((n + 127) / 128) * ((n + 127) / 128);
+  int64_t c = (2304 + tiles - 1) / tiles;
   if (c > 16) c = 16;
   if (c > n) c = n;
   if (c < 1) c = 1;

@@ -100,6 +100,7 @@ struct BwdArgs {
   Geom g;
   const float *bt, *btT;
   const uint32_t* kbits;
+  const uint32_t* rowfull;
   const T *q, *k, *v, *da;
   const T* dalo;  // bf16 only: dA - bf16(dA), also rounded to bf16
   const float* lse2;
@@ -250,49 +251,65 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
 }
 
 // bf16 dQ (and D) with asynchronous LDS staging (see dma.h).  One workgroup
-// = 4 waves = 64 queries x 2 rows of one head: wave w owns query tile w % 2
-// (lane <-> query) of row r0 + w / 2.  Keys stream in blocks of 32; per
-// block, K and V of both rows and the query-major bias tiles of the 64
-// queries (shared by the two rows) are copied HBM -> LDS by DMA into a ring
-// of QD_SLOTS slots.  K^T fragments for the dQ products come from the
-// transposing LDS read of the row-major K block.
-constexpr int QD_BLK = 32 * 64;                     // 2 KB: 32 keys x 32 channels
-constexpr int QD_K = 0, QD_V = 2 * QD_BLK;          // [row] blocks
-constexpr int QD_BIAS = 4 * QD_BLK;                 // 2 query tiles x 4 KB
-constexpr int QD_SLOT = QD_BIAS + 2 * 4096;
-// Two slots (32 KB) let four workgroups share a CU, four waves per SIMD
-// (measured 0.73 ms against 0.81-0.85 ms with three slots and three waves
-// per SIMD at N = 768).
-constexpr int QD_SLOTS = 2;
-constexpr int QD_OPS = 4;                           // DMA ops per thread per block
+// = QD_ROWS x QD_QT waves = 32 QD_QT queries x QD_ROWS rows of one head:
+// wave w owns query tile w % QD_QT (lane <-> query) of row r0 + w / QD_QT.
+// Keys stream in tiles of 32; per tile, K and V of the rows and the
+// query-major bias tiles of the queries (shared by the rows) are copied
+// HBM -> LDS by DMA into a ring of QD_SLOTS slots.  K^T fragments for the
+// dQ products come from the transposing LDS read of the row-major K tile.
+// The DMAs go through buffer resources advanced in scalar registers, and
+// the loop is unrolled by the ring length, so no vector instruction is
+// spent on addresses.
+#ifndef QD_ROWS_CFG
+#define QD_ROWS_CFG 2
+#endif
+#ifndef QD_QT_CFG
+#define QD_QT_CFG 2
+#endif
+#ifndef QD_SLOTS_CFG
+#define QD_SLOTS_CFG 2
+#endif
+constexpr int QD_ROWS = QD_ROWS_CFG, QD_QT = QD_QT_CFG, QD_SLOTS = QD_SLOTS_CFG;
+constexpr int QD_WAVES = QD_ROWS * QD_QT;
+constexpr int QD_BLK = 32 * 64;                         // 2 KB: 32 keys x 32 channels
+constexpr int QD_K = 0, QD_V = QD_ROWS * QD_BLK;        // [row] tiles
+constexpr int QD_BIAS = 2 * QD_ROWS * QD_BLK;           // QD_QT query tiles x 4 KB
+constexpr int QD_SLOT = QD_BIAS + QD_QT * 4096;
+constexpr int QD_UNITS = 4 * (QD_ROWS + QD_QT);         // 1 KB DMA units per tile
+constexpr int QD_OPS = QD_UNITS / QD_WAVES;             // DMA ops per thread per tile
+static_assert(QD_UNITS % QD_WAVES == 0, "DMA units must split evenly over the waves");
+static_assert(QD_SLOTS * QD_SLOT <= 65536, "slot offsets must fit the LDS immediate");
 
-__global__ __launch_bounds__(256, 4) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
+__global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4, 4))) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int nrg = (G.n + 1) / 2;
+  const int nrg = (G.n + QD_ROWS - 1) / QD_ROWS;
   const int qb = w % nqb, rg = (w / nqb) % nrg, h = w / (nqb * nrg);
-  const int r0 = rg * 2;
+  const int r0 = rg * QD_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qtl = wave & 1, ri = wave >> 1;
-  const int r = min(r0 + ri, G.n - 1);
+  const int qtl = wave % QD_QT, ri = wave / QD_QT;
+  const int last = G.n - 1;
+  const int r = min(r0 + ri, last);
   const bool rok = r0 + ri < G.n;
-  const int q0 = qb * 64 + qtl * TILE;
+  const int q0 = qb * 32 * QD_QT + qtl * TILE;
   const int q = q0 + l32;
   const bool active = rok && q0 < G.n;
   const bool qok = q < G.n;
-  const int nkt = G.nkt, last = G.n - 1;
+  const int nkt = G.nkt;
+  const int nrows = min(QD_ROWS, G.n - r0);  // rows of this group that exist
   const float c1 = G.scale * LOG2E;
 
   __shared__ __align__(16) char smem[QD_SLOTS * QD_SLOT];
 
   // ---- this lane's query: Q, dA (hi, lo) fragments and lse2
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t rowbase = (int64_t)r * G.sRow + hb;
   F qf[M::KCH], daf[M::KCH], dalf[M::KCH];
   float l2 = pos_inf();
-  if (qok) {
+  if (active && qok) {
     row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
     row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
     row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
@@ -302,26 +319,56 @@ __global__ __launch_bounds__(256, 4) void dq_dma_kernel(BwdArgs<bf16> a, int nqb
     zero_frags<bf16>(daf);
     zero_frags<bf16>(dalf);
   }
+  bool rows_full = true;
+  for (int i = 0; i < nrows; ++i) rows_full = rows_full && const_load(a.rowfull + r0 + i) != 0u;
   // plain register loads: let them complete before any DMA is issued (with
   // both kinds outstanding the compiler would wait for every DMA at each use)
   wait_vm<0>();
 
-  // ---- DMA lanes.  Ops 0, 1: K, V of both rows (wave w: row w / 2,
-  // positions 16 (w % 2) + lane / 4).  Ops 2, 3: bias tile j of the 64
-  // queries, quarter w.
-  const int dri = wave >> 1;
-  const int dp = 16 * (wave & 1) + (lane >> 2), dc = (lane & 3) ^ swz(dp);
-  const int64_t drb = (int64_t)min(r0 + dri, last) * G.sRow + (int64_t)h * HEAD_DIM + 8 * dc;
-  auto issue = [&](int t, int slot) {
-    char* sl = smem + slot * QD_SLOT;
-    const int64_t o = drb + (int64_t)min(t * TILE + dp, last) * G.sPos;
-    dma16(a.k + o, sl + QD_K + dri * QD_BLK + 1024 * (wave & 1));
-    dma16(a.v + o, sl + QD_V + dri * QD_BLK + 1024 * (wave & 1));
+  // ---- DMA lanes.  Unit u = QD_OPS w + j of wave w: u < 4 QD_ROWS: half
+  // u % 2 (keys 16 (u % 2) + lane / 4) of tile u / 2 of [K rows, V rows];
+  // otherwise quarter v % 4 of bias tile v / 4, v = u - 4 QD_ROWS.  Lane
+  // offsets are fixed; the source bases advance by one key tile per issue.
+  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int64_t tstep = (int64_t)TILE * G.sPos;
+  const void* src[QD_OPS];
+  const void* srcend[QD_OPS];
+  int64_t adv[QD_OPS];  // bytes per tile
+  uint32_t voff[QD_OPS];
+  char* dst[QD_OPS];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const float* bsrc = frag_tile(a.bt, h, min(qb * 2 + j, nkt - 1), t, nkt);
-      dma16((const char*)bsrc + 1024 * wave + 16 * lane, sl + QD_BIAS + j * 4096 + 1024 * wave);
+  for (int j = 0; j < QD_OPS; ++j) {
+    const int u = QD_OPS * wave + j;
+    if (u < 4 * QD_ROWS) {
+      const int blk = u >> 1, half = u & 1;
+      const bf16* t = blk < QD_ROWS ? a.k : a.v;
+      const int p = 16 * half + (lane >> 2);
+      src[j] = t + (int64_t)min(r0 + blk % QD_ROWS, last) * G.sRow + hb;
+      srcend[j] = t + tensor;
+      adv[j] = tstep * 2;
+      voff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
+      dst[j] = smem + blk * QD_BLK + 1024 * half;
+    } else {
+      const int v = u - 4 * QD_ROWS, tl = v >> 2, qu = v & 3;
+      src[j] = a.bt + ((int64_t)h * nkt + qb * QD_QT + tl) * nkt * 1024;
+      srcend[j] = a.bt + (int64_t)G.H * nkt * nkt * 1024;
+      adv[j] = 4096;
+      voff[j] = (uint32_t)(1024 * qu + 16 * lane);
+      dst[j] = smem + QD_BIAS + tl * 4096 + 1024 * qu;
     }
+  }
+  int issued = 0;
+  auto issue = [&](int slot) {
+    // tiles past the last copy nothing (empty resources) but keep the wait
+    // counts uniform
+    const bool real = issued < nkt;
+#pragma unroll
+    for (int j = 0; j < QD_OPS; ++j) {
+      dma16b(real ? buf_rsrc(src[j], srcend[j]) : buf_rsrc(src[j], src[j]), voff[j],
+             dst[j] + slot * QD_SLOT);
+      if (issued + 1 < nkt) src[j] = (const char*)src[j] + adv[j];
+    }
+    ++issued;
   };
 
   // ---- LDS read addresses (slot 0)
@@ -337,77 +384,106 @@ __global__ __launch_bounds__(256, 4) void dq_dma_kernel(BwdArgs<bf16> a, int nqb
   f32x16 xt = {}, yt = {};
   float dpart = 0.f;
 
+  // the loop; FULL: every key of every row of the group is valid
+  auto run = [&](auto full_c) {
+    constexpr bool FULL = decltype(full_c)::value;
+    auto step = [&](int t, auto slot) {
+      constexpr int S = decltype(slot)::value;
+      constexpr uint32_t so = S * QD_SLOT;
+      uint32_t wr[QD_ROWS];  // key bits of tile t per row (0 for a row past the end)
 #pragma unroll
-  for (int j = 0; j < QD_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
-  for (int t = 0; t < nkt; ++t) {
-    const uint32_t so = (t % QD_SLOTS) * QD_SLOT;
-    wait_vm<(QD_SLOTS - 2) * QD_OPS>();  // block t has landed
-    lds_barrier();
-    // key bits of both rows: the same in every wave, so the branch below (it
-    // holds a barrier) is uniform across the workgroup
-    const uint32_t w0 = const_load(a.kbits + (int64_t)r0 * nkt + t);
-    const uint32_t w1 = r0 + 1 < G.n ? const_load(a.kbits + (int64_t)(r0 + 1) * nkt + t) : 0u;
-    if ((w0 & (r0 + 1 < G.n ? w1 : 0xffffffffu)) != 0xffffffffu) {
-      // zero V rows of keys invalid for a row (P = 0 there, and 0 times a
-      // non-finite dP would not be); thread t < 128: row t / 64, key t / 2 % 32
-      if (tid < 128) {
-        const uint32_t wb = (tid >> 6) ? w1 : w0;
-        if (!((wb >> ((tid >> 1) & 31)) & 1u))
-          *(f32x4*)(smem + so + QD_V + 32 * tid) = f32x4{},
-                   *(f32x4*)(smem + so + QD_V + 32 * tid + 16) = f32x4{};
+      for (int i = 0; i < QD_ROWS; ++i)
+        wr[i] = i < nrows ? (FULL ? in_range_bits(t, G.n)
+                                  : const_load(a.kbits + (int64_t)(r0 + i) * nkt + t))
+                          : 0u;
+      wait_vm<(QD_SLOTS - 2) * QD_OPS>();  // tile t has landed
+      lds_barrier();
+      if (!FULL) {
+        bool full = true;
+#pragma unroll
+        for (int i = 0; i < QD_ROWS; ++i) full = full && (i >= nrows || wr[i] == 0xffffffffu);
+        if (!full) {
+          // zero V rows of keys invalid for a row (P = 0 there, and 0 times a
+          // non-finite dP would not be); thread t < 32 QD_ROWS: row t / 32, key t % 32
+          if (tid < 32 * QD_ROWS) {
+            uint32_t wb = 0;
+#pragma unroll
+            for (int i = 0; i < QD_ROWS; ++i)
+              if ((tid >> 5) == i) wb = wr[i];
+            if (!((wb >> (tid & 31)) & 1u)) {
+              char* z = smem + so + QD_V + (tid >> 5) * QD_BLK + 64 * (tid & 31);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) *(f32x4*)(z + 16 * e) = f32x4{};
+            }
+          }
+          __syncthreads();
+        }
       }
-      __syncthreads();
-    }
-    // block t + QD_SLOTS - 1 into the slot of block t - 1
-    issue(min(t + QD_SLOTS - 1, nkt - 1), (t + QD_SLOTS - 1) % QD_SLOTS);
-    const uint32_t bits = ri ? w1 : w0;
-    if (!active || bits == 0u) continue;
-    // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
-    f32x16 sv;
+      issue((S + QD_SLOTS - 1) % QD_SLOTS);  // tile t + QD_SLOTS - 1 into the slot of tile t - 1
+      uint32_t bits = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
+      for (int i = 0; i < QD_ROWS; ++i)
+        if (ri == i) bits = wr[i];
+      if (!active || bits == 0u) return;
+      // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
+      f32x16 sv;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sv[4 * j + e] = y[e];
-    }
-    {
-      const F k0 = lds_load16<F>(rk0 + so + QD_K), k1 = lds_load16<F>(rk1 + so + QD_K);
-      sv = M::mma(k1, qf[1], M::mma(k0, qf[0], sv));
-    }
-    if (bits != 0xffffffffu) mask_rows(sv, bits, g);
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2));
-    // dP^T = V dA^T (hi and lo parts), then P dP and its running sum D
-    f32x16 dp;
-    {
-      const F v0 = lds_load16<F>(rk0 + so + QD_V), v1 = lds_load16<F>(rk1 + so + QD_V);
-      dp = M::mma(v0, daf[0], f32x16{});
-      dp = M::mma(v1, daf[1], dp);
-      dp = M::mma(v0, dalf[0], dp);
-      dp = M::mma(v1, dalf[1], dp);
-    }
+        for (int e = 0; e < 4; ++e) sv[4 * j + e] = y[e];
+      }
+      {
+        const F k0 = lds_load16<F>(rk0 + so + QD_K), k1 = lds_load16<F>(rk1 + so + QD_K);
+        sv = M::mma(k1, qf[1], M::mma(k0, qf[0], sv));
+      }
+      if (bits != 0xffffffffu) mask_rows(sv, bits, g);
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      dp[v] *= sv[v];
-      dpart += dp[v];
-    }
-    // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the block's keys)
-    const uint32_t tk = rtr + so, tk8 = rtr8 + so;
-    s16x4 xk[4];
-    xk[0] = ds_read_tr<0>(tk);
-    xk[1] = ds_read_tr<8 * 64>(tk8);
-    xk[2] = ds_read_tr<16 * 64>(tk);
-    xk[3] = ds_read_tr<24 * 64>(tk8);
-    F pf[M::PCH], xf[M::PCH];
-    acc_frags(dp, xf);
-    acc_frags(sv, pf);
-    tr_wait(xk);
+      for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2));
+      // dP^T = V dA^T (hi and lo parts), then P dP and its running sum D
+      f32x16 dp;
+      {
+        const F v0 = lds_load16<F>(rk0 + so + QD_V), v1 = lds_load16<F>(rk1 + so + QD_V);
+        dp = M::mma(v0, daf[0], f32x16{});
+        dp = M::mma(v1, daf[1], dp);
+        dp = M::mma(v0, dalf[0], dp);
+        dp = M::mma(v1, dalf[1], dp);
+      }
 #pragma unroll
-    for (int u = 0; u < M::PCH; ++u) {
-      xt = M::mma(tr_frag(xk, u), xf[u], xt);
-      yt = M::mma(tr_frag(xk, u), pf[u], yt);
+      for (int v = 0; v < 16; ++v) {
+        dp[v] *= sv[v];
+        dpart += dp[v];
+      }
+      // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the tile's keys)
+      s16x4 xk[4];
+      xk[0] = ds_read_tr<so>(rtr);
+      xk[1] = ds_read_tr<so + 8 * 64>(rtr8);
+      xk[2] = ds_read_tr<so + 16 * 64>(rtr);
+      xk[3] = ds_read_tr<so + 24 * 64>(rtr8);
+      F pf[M::PCH], xf[M::PCH];
+      acc_frags(dp, xf);
+      acc_frags(sv, pf);
+      tr_wait(xk);
+#pragma unroll
+      for (int u = 0; u < M::PCH; ++u) {
+        xt = M::mma(tr_frag(xk, u), xf[u], xt);
+        yt = M::mma(tr_frag(xk, u), pf[u], yt);
+      }
+    };
+#pragma unroll
+    for (int j = 0; j < QD_SLOTS - 1; ++j) issue(j);
+    for (int t = 0; t < nkt; t += QD_SLOTS) {
+      step(t, slot_c<0>{});
+      if (t + 1 >= nkt) break;
+      step(t + 1, slot_c<1 % QD_SLOTS>{});
+      if (QD_SLOTS < 3 || t + 2 >= nkt) continue;
+      step(t + 2, slot_c<2 % QD_SLOTS>{});
     }
-  }
+  };
+  if (rows_full)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active) return;
   const float dsum = wave_xor32_sum(dpart);
@@ -422,6 +498,7 @@ __global__ __launch_bounds__(256, 4) void dq_dma_kernel(BwdArgs<bf16> a, int nqb
     store4(a.dq + gb + 8 * j + 4 * g, x);
   }
 }
+
 
 // ---- dK, dV --------------------------------------------------------------------------
 
@@ -579,26 +656,40 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
 }
 
 // bf16 dK, dV with asynchronous LDS staging (see dma.h).  One workgroup =
-// 8 waves = 128 keys x 2 rows of one head: wave w owns key tile w % 4 of
-// the block (lane <-> key) in row r0 + w / 4.  Queries stream in blocks of
-// 32; per block, Q, dA and its low part of both rows, their lse2 and D, and
-// the key-major bias tiles of the 128 keys (shared by the two rows) are
-// copied HBM -> LDS by DMA into a ring of KD_SLOTS slots.  Q^T and dA^T
-// fragments come from the transposing LDS read of the same row-major
-// blocks.
-constexpr int KD_ROWS = 2;
+// 16 waves = 128 keys x 4 rows of one head: wave w owns key tile w % 4 of
+// the block (lane <-> key) in row r0 + w / 4.  Queries stream in tiles of
+// 32; per tile, Q, dA and its low part of the 4 rows, their lse2 and -D,
+// and the key-major bias tiles of the 128 keys (shared by the rows), 41 KB,
+// are copied HBM -> LDS by DMA into a three-slot ring, two tiles ahead.
+// One workgroup per CU runs four waves per SIMD.  Q^T and dA^T fragments
+// come from the transposing LDS read of the same row-major tiles.  The
+// DMAs go through buffer resources advanced in scalar registers, and the
+// loop is unrolled by the ring length, so no vector instruction is spent on
+// addresses.
+#ifndef KD_ROWS_CFG
+#define KD_ROWS_CFG 2
+#endif
+#ifndef KD_SLOTS_CFG
+#define KD_SLOTS_CFG 2
+#endif
+constexpr int KD_ROWS = KD_ROWS_CFG;
+constexpr int KD_WAVES = 4 * KD_ROWS;
+constexpr int KD_HALF = KD_WAVES / 2;              // waves per half of the DMA lanes
 constexpr int KD_BLK = 32 * 64;                        // 2 KB: 32 positions x 32 channels
-constexpr int KD_Q = 0, KD_DA = 2 * KD_BLK, KD_LO = 4 * KD_BLK;  // [row] blocks
-constexpr int KD_BIAS = 6 * KD_BLK;                    // 4 key tiles x 4 KB
-constexpr int KD_L2 = KD_BIAS + 4 * 4096;              // lse2 [row][32], then -D [row][32]
-constexpr int KD_SLOT = KD_L2 + 4 * 128;
-// Ring depth (blocks in flight + 1).  Two slots (58 KB) let two workgroups
-// share a CU: four waves per SIMD hide more latency than a deeper ring with
-// two (measured: 0.82 ms against 0.98-1.07 ms with four slots at N = 768).
-constexpr int KD_SLOTS = 2;
-constexpr int KD_OPS = 4;    // DMA ops per thread per block
+constexpr int KD_SLOTS = KD_SLOTS_CFG;
+constexpr int KD_BOPS = 16 / KD_WAVES;                 // bias DMA ops per wave per tile
+constexpr int KD_OPS = 2 + KD_BOPS;                    // DMA ops per thread per tile
+// LDS regions, each holding its piece of every ring slot (so that slot
+// offsets stay small enough for the immediate field of LDS instructions):
+// Q, dA and dA low [slot][row] tiles, bias [slot][key tile] (4 KB each),
+// lse2 / -D [slot][2][row][32].
+constexpr int KD_TS = KD_ROWS * KD_BLK;                // 8 KB: one slot of a tile region
+constexpr int KD_Q = 0, KD_DA = KD_SLOTS * KD_TS, KD_LO = 2 * KD_SLOTS * KD_TS;
+constexpr int KD_BIAS = 3 * KD_SLOTS * KD_TS, KD_BS = 4 * 4096;
+constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
+constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 123 KB
 
-__global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(BwdArgs<bf16> a) {
+__global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -608,11 +699,12 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
   const int r0 = rg * KD_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int ri = wave >> 2;                 // row of this wave (0, 1)
-  const int r = min(r0 + ri, G.n - 1);
+  const int ri = wave >> 2;                 // row of this wave (0..3)
+  const int last = G.n - 1;
+  const int r = min(r0 + ri, last);
   const bool rok = r0 + ri < G.n;
   const int kt = kbk * 4 + (wave & 3);      // this wave's key tile
-  const int nkt = G.nkt, last = G.n - 1;
+  const int nkt = G.nkt;
   const bool active = rok && kt < nkt;
   const uint32_t bits = active ? const_load(a.kbits + (int64_t)r * nkt + kt) : 0u;
   const int key = kt * TILE + l32;
@@ -620,11 +712,12 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
   const bool work = bits != 0u;
   const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) char smem[KD_SLOTS * KD_SLOT];
+  __shared__ __align__(16) char smem[KD_LDS];
 
   // ---- the wave's keys: K and V fragments (zero for invalid keys, so that
   // non-finite values there cannot reach the products)
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t rowbase = (int64_t)r * G.sRow + hb;
   F kf[M::KCH], vf[M::KCH];
   if (kvalid) {
     row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
@@ -638,41 +731,63 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
   // every DMA at each use)
   wait_vm<0>();
 
-  // ---- DMA lanes.  Op 0: Q and dA of both rows (wave w: block w / 2 of
-  // [Q0, Q1, dA0, dA1], positions 16 (w % 2) + lane / 4).  Op 1: waves 0-3
-  // the low part of dA, waves 4-7 lse2 / -D (lanes 0..7, 128 bytes each).
-  // Ops 2, 3: bias tiles 4 KB each, wave w: tile 2 (op - 2) + w / 4,
-  // quarter w % 4.
-  const int dpl = 16 * (wave & 1) + (lane >> 2);
-  int64_t drow[KD_ROWS];
+  // ---- DMA lanes (lane offsets fixed, bases advanced per tile in scalar
+  // registers).  Op 0: Q (waves 0-7) or dA (waves 8-15) of row (w % 8) / 2,
+  // positions 16 (w % 2) + lane / 4.  Op 1: the low part of dA of row
+  // w / 2 (waves 0-7), or lse2 (waves 8-11) / -D (waves 12-15) of row w % 4,
+  // 128 bytes (lanes 0..7).  Op 2: bias tile w / 4, quarter w % 4.
+  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int p16 = 16 * (wave & 1) + (lane >> 2);
+  const uint32_t pvoff = (uint32_t)(((int64_t)p16 * G.sPos + hb + 8 * ((lane & 3) ^ swz(p16))) * 2);
+  const int64_t tstep = (int64_t)TILE * G.sPos;  // elements per query tile
+  const int orow = (wave % KD_HALF) >> 1;       // op 0 / op 1 (dA low) row
+  const bf16* src0 = wave < KD_HALF ? a.q : a.da;
+  const bf16* p0 = src0 + (int64_t)min(r0 + orow, last) * G.sRow;
+  const bf16* p1 = a.dalo + (int64_t)min(r0 + orow, last) * G.sRow;
+  char* const dst0 = smem + (wave < KD_HALF ? KD_Q : KD_DA) + orow * KD_BLK + 1024 * (wave & 1);
+  constexpr int dst0_stride = KD_TS;
+  const bool lo_op = wave < KD_HALF;
+  const int lidx = wave - KD_HALF;                 // lse2 rows, then -D rows
+  const float* pl = (lidx < KD_ROWS ? a.lse2 : a.dsum) +
+                    ((int64_t)h * G.n + min(r0 + lidx % KD_ROWS, last)) * G.np;
+  const float* const plend = pl + G.np;
+  char* const dst1 = lo_op ? smem + KD_LO + orow * KD_BLK + 1024 * (wave & 1)
+                           : smem + KD_L2 + 128 * lidx;
+  const int dst1_stride = lo_op ? KD_TS : KD_LS;
+  const uint32_t lvoff = 16u * (uint32_t)lane;
+  // bias op j of wave w: quarter (KD_BOPS w + j) % 4 of key tile (KD_BOPS w + j) / 4
+  const float* pb = a.btT + ((int64_t)h * nkt + kbk * 4) * nkt * 1024;
+  const float* const pbend = a.btT + (int64_t)G.H * nkt * nkt * 1024;
+  uint32_t bvoff[KD_BOPS];
+  char* dst2[KD_BOPS];
 #pragma unroll
-  for (int i = 0; i < KD_ROWS; ++i)
-    drow[i] = (int64_t)min(r0 + i, last) * G.sRow + (int64_t)h * HEAD_DIM;
-  const int b0 = wave >> 1;  // op 0 block: 0 Q0, 1 Q1, 2 dA0, 3 dA1
-  const bf16* src0 = b0 < 2 ? a.q : a.da;
-  const int64_t row0 = (b0 & 1) ? drow[1] : drow[0];
-  const int64_t row1 = (wave >> 1 & 1) ? drow[1] : drow[0];  // op 1 (waves 0-3): dalo row
-  const int lrow = min(r0 + (wave & 1), last);                // op 1 (waves 4-7): lse2 / -D row
-  const float* lsrc = (wave & 2) ? a.dsum : a.lse2;
-  auto issue = [&](int t, int slot) {
-    char* sl = smem + slot * KD_SLOT;
-    const int p = min(t * TILE + dpl, last);
-    const int c = (lane & 3) ^ swz(dpl);
-    dma16(src0 + row0 + (int64_t)p * G.sPos + 8 * c, sl + b0 * KD_BLK + 1024 * (wave & 1));
-    if (wave < 4) {
-      dma16(a.dalo + row1 + (int64_t)p * G.sPos + 8 * c,
-            sl + KD_LO + (wave >> 1) * KD_BLK + 1024 * (wave & 1));
-    } else if (lane < 8) {
-      dma16(lsrc + ((int64_t)h * G.n + lrow) * G.np + t * TILE + 4 * lane,
-            sl + KD_L2 + 128 * (wave - 4));
-    }
+  for (int j = 0; j < KD_BOPS; ++j) {
+    const int u = KD_BOPS * wave + j, tl = u >> 2;
+    bvoff[j] = (uint32_t)(((int64_t)tl * nkt * 1024 + 256 * (u & 3)) * 4 + 16 * lane);
+    dst2[j] = smem + KD_BIAS + tl * 4096 + 1024 * (u & 3);
+  }
+  int issued = 0;
+  auto issue = [&](int slot) {
+    // tiles past the last copy nothing (empty resources) but keep the wait
+    // counts uniform
+    const bool real = issued < nkt;
+    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff,
+           dst0 + slot * dst0_stride);
+    if (lo_op)
+      dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff,
+             dst1 + slot * dst1_stride);
+    else if (lane < 8)
+      dma16b(real ? buf_rsrc(pl, plend) : buf_rsrc(pl, pl), lvoff, dst1 + slot * dst1_stride);
+    const rsrc_t rbias = real ? buf_rsrc(pb, pbend) : buf_rsrc(pb, pb);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int tl = 2 * j + (wave >> 2);
-      const float* bsrc = frag_tile(a.btT, h, min(kbk * 4 + tl, nkt - 1), t, nkt);
-      dma16((const char*)bsrc + 1024 * (wave & 3) + 16 * lane,
-            sl + KD_BIAS + tl * 4096 + 1024 * (wave & 3));
+    for (int j = 0; j < KD_BOPS; ++j) dma16b(rbias, bvoff[j], dst2[j] + slot * KD_BS);
+    if (issued + 1 < nkt) {
+      p0 += tstep;
+      p1 += tstep;
+      pl += TILE;
+      pb += 1024;
     }
+    ++issued;
   };
 
   // ---- LDS read addresses (slot 0)
@@ -683,8 +798,9 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
   const TrAddr ta(lane);
   const uint32_t rtr = base + ri * KD_BLK + ta.off(0);
   const uint32_t rtr8 = base + ri * KD_BLK + ta.off(8) - 8 * 64;
+  const uint32_t rta = rtr + KD_DA, rta8 = rtr8 + KD_DA;
   const uint32_t rb = base + KD_BIAS + (wave & 3) * 4096 + lane * 16;
-  const uint32_t rl = base + KD_L2 + ri * 128 + 16 * g;  // + 32 j: lse2 quad j; + 256: D
+  const uint32_t rl = base + KD_L2 + ri * 128 + 16 * g;  // + 32 j: lse2 quad j; + 512: -D
 
   f32x16 dkt = {}, dvt = {};
   const float kmask = kvalid ? 0.f : neg_inf();
@@ -699,24 +815,20 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
     return x;
   };
 
-#pragma unroll
-  for (int j = 0; j < KD_SLOTS - 1; ++j) issue(min(j, nkt - 1), j);
-  for (int t = 0; t < nkt; ++t) {
-    const uint32_t so = (t % KD_SLOTS) * KD_SLOT;
-    // block t has landed (the KD_SLOTS - 2 blocks after it may be in flight)
-    wait_vm<(KD_SLOTS - 2) * KD_OPS>();
+  auto step = [&](auto slot) {
+    constexpr int S = decltype(slot)::value;
+    constexpr uint32_t so = S * KD_TS;  // slot offset inside the Q, dA and dA-low regions
+    wait_vm<(KD_SLOTS - 2) * KD_OPS>();  // tile t has landed (tiles after it may be in flight)
     lds_barrier();
-    // block t + KD_SLOTS - 1 into the slot of block t - 1 (a copy of the last
-    // block past the end keeps the wait counts uniform)
-    issue(min(t + KD_SLOTS - 1, nkt - 1), (t + KD_SLOTS - 1) % KD_SLOTS);
-    if (!work) continue;
+    issue((S + KD_SLOTS - 1) % KD_SLOTS);  // tile t + KD_SLOTS - 1 into the slot of tile t - 1
+    if (!work) return;
     // S = bias + Q K^T (registers <-> queries, lane <-> key)
     f32x16 sv;
     {
       f32x16 bias;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const f32x4 y = lds_load16<f32x4>(rb + so + 1024 * j);
+        const f32x4 y = lds_load16<f32x4>(rb + S * KD_BS + 1024 * j);
 #pragma unroll
         for (int e = 0; e < 4; ++e) bias[4 * j + e] = y[e];
       }
@@ -728,31 +840,29 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
       sv = M::mma(q1, kf[1], M::mma(q0, kf[0], bias));
     }
     // P = exp2(S c1 - lse2[query])
-    const f32x16 l2 = quads(rl + so);
+    const f32x16 l2 = quads(rl + S * KD_LS);
 #pragma unroll
     for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2[v]));
     // dP - D = dA V^T - D (hi and lo parts of dA), then dS = P (dP - D)
     const F d0 = lds_load16<F>(rq0 + so + KD_DA), d1 = lds_load16<F>(rq1 + so + KD_DA);
     const F e0 = lds_load16<F>(rq0 + so + KD_LO), e1 = lds_load16<F>(rq1 + so + KD_LO);
-    f32x16 dp = quads(rl + so + 256);  // -D
+    f32x16 dp = quads(rl + S * KD_LS + KD_ROWS * 128);  // -D
     dp = M::mma(d0, vf[0], dp);
     dp = M::mma(d1, vf[1], dp);
     dp = M::mma(e0, vf[0], dp);
     dp = M::mma(e1, vf[1], dp);
 #pragma unroll
     for (int v = 0; v < 16; ++v) dp[v] *= sv[v];
-    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the block's queries)
-    const uint32_t tq = rtr + so + KD_Q, td = rtr + so + KD_DA;
-    const uint32_t tq8 = rtr8 + so + KD_Q, td8 = rtr8 + so + KD_DA;
+    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the tile's queries)
     s16x4 xa[4], xq[4];
-    xa[0] = ds_read_tr<0>(td);
-    xa[1] = ds_read_tr<8 * 64>(td8);
-    xa[2] = ds_read_tr<16 * 64>(td);
-    xa[3] = ds_read_tr<24 * 64>(td8);
-    xq[0] = ds_read_tr<0>(tq);
-    xq[1] = ds_read_tr<8 * 64>(tq8);
-    xq[2] = ds_read_tr<16 * 64>(tq);
-    xq[3] = ds_read_tr<24 * 64>(tq8);
+    xa[0] = ds_read_tr<so>(rta);
+    xa[1] = ds_read_tr<so + 8 * 64>(rta8);
+    xa[2] = ds_read_tr<so + 16 * 64>(rta);
+    xa[3] = ds_read_tr<so + 24 * 64>(rta8);
+    xq[0] = ds_read_tr<so + KD_Q>(rtr);
+    xq[1] = ds_read_tr<so + KD_Q + 8 * 64>(rtr8);
+    xq[2] = ds_read_tr<so + KD_Q + 16 * 64>(rtr);
+    xq[3] = ds_read_tr<so + KD_Q + 24 * 64>(rtr8);
     F pf[M::PCH], sf[M::PCH];
     acc_frags(sv, pf);
     acc_frags(dp, sf);
@@ -763,6 +873,16 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
       dvt = M::mma(tr_frag(xa, u), pf[u], dvt);
       dkt = M::mma(tr_frag(xq, u), sf[u], dkt);
     }
+  };
+
+#pragma unroll
+  for (int j = 0; j < KD_SLOTS - 1; ++j) issue(j);
+  for (int t = 0; t < nkt; t += KD_SLOTS) {
+    step(slot_c<0>{});
+    if (t + 1 >= nkt) break;
+    step(slot_c<1 % KD_SLOTS>{});
+    if (KD_SLOTS < 3 || t + 2 >= nkt) continue;
+    step(slot_c<2 % KD_SLOTS>{});
   }
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active || key >= G.n) return;
@@ -780,6 +900,7 @@ __global__ __launch_bounds__(512, KD_SLOTS <= 2 ? 2 : 1) void dkdv_dma_kernel(Bw
     store4(a.dk + gb + c0, y);
   }
 }
+
 
 // ---- dBias ---------------------------------------------------------------------------
 
@@ -922,41 +1043,45 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
 }
 
 // bf16 bias gradient with asynchronous LDS staging (see dma.h).  One
-// workgroup: 128 queries x 64 keys of one head, summed over the rows of one
-// row chunk; wave w owns query tile w % 4 (lane <-> query) and key tile
-// w / 4 of the block.  Per row, K and V of the 64 keys and Q, dA, its low
-// part, lse2 and -D of the 128 queries land in LDS by DMA through a ring of
-// two slots (33 KB each), one row ahead; two workgroups share a CU (four
-// waves per SIMD) to hide the latency of each wave's dependent MFMA and
-// vector steps.
-constexpr int DBD_Q = 128, DBD_K = 64;        // queries and keys per workgroup block
-constexpr int DBD_KV = DBD_K * 64;            // 4 KB: K (or V) of the block's keys
+// workgroup = 16 waves = 128 queries x 128 keys of one head, summed over
+// the rows of one row chunk; wave w owns query tile w % 4 (lane <-> query)
+// and key tile w / 4 of the block.  Per row, K and V of the 128 keys and Q,
+// dA, its low part, lse2 and -D of the 128 queries (41 KB) land in LDS by
+// DMA through a three-slot ring, two rows ahead, and are shared by the 16
+// waves; one workgroup per CU runs four waves per SIMD.  The DMAs go
+// through buffer resources whose bases advance by one row in scalar
+// registers, so no vector instruction is spent on addresses, and the bias
+// tile of each wave stays in registers for all rows.
+constexpr int DBD_Q = 128, DBD_K = 128;       // queries and keys per workgroup block
+constexpr int DBD_WAVES = 16;
+constexpr int DBD_KV = DBD_K * 64;            // 8 KB: K (or V) of the block's keys
 constexpr int DBD_QB = DBD_Q * 64;            // 8 KB: Q (or dA, dA low) of the queries
 constexpr int DBD_OK = 0, DBD_OV = DBD_KV, DBD_OQ = 2 * DBD_KV;
 constexpr int DBD_ODA = DBD_OQ + DBD_QB, DBD_OLO = DBD_ODA + DBD_QB;
 constexpr int DBD_LD = DBD_OLO + DBD_QB;      // lse2 [128], then -D [128]
 constexpr int DBD_SLOT = DBD_LD + 1024;
-constexpr int DBD_SLOTS = 2;
-constexpr int DBD_OPS = 5;                    // DMA ops per thread per row
+constexpr int DBD_SLOTS = 3;
+constexpr int DBD_OPS = 3;                    // DMA ops per thread per row
 
-__global__ __launch_bounds__(512, 2) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
+__global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int nqb = (G.n + DBD_Q - 1) / DBD_Q;
   const int kbk = w % nkb;
-  const int qb = (w / nkb) % a.nblk;
-  const int rc = (w / (nkb * a.nblk)) % a.nrc;
-  const int h = w / (nkb * a.nblk * a.nrc);
+  const int qb = (w / nkb) % nqb;
+  const int rc = (w / (nkb * nqb)) % a.nrc;
+  const int h = w / (nkb * nqb * a.nrc);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qtl = wave & 3, ktl = wave >> 2;
   const int qstart = qb * DBD_Q, kstart = kbk * DBD_K;
   const int q = qstart + qtl * TILE + l32;  // this lane's query
-  const int kt = kbk * 2 + ktl;             // this wave's key tile
+  const int kt = kstart / TILE + ktl;       // this wave's key tile
   const bool active = qstart + qtl * TILE < G.n && kt < G.nkt;
   const bool qok = q < G.n;
-  const int last = G.n - 1;
+  const int nkt = G.nkt;
   const float c1 = G.scale * LOG2E;
 
   __shared__ __align__(16) char smem[DBD_SLOTS * DBD_SLOT];
@@ -964,34 +1089,59 @@ __global__ __launch_bounds__(512, 2) void db_dma_kernel(BwdArgs<bf16> a, int nkb
   f32x16 binit, acc = {};
   {
     const int qt = active ? qstart / TILE + qtl : 0;
-    binit = load_frag_tile(frag_tile(a.bt, h, qt, min(kt, G.nkt - 1), G.nkt), lane);
+    binit = load_frag_tile(frag_tile(a.bt, h, qt, min(kt, nkt - 1), nkt), lane);
   }
   // the bias tile is a plain register load: let it complete before any DMA
   // is issued (with both kinds outstanding the compiler would wait for every
   // DMA at each use of binit)
   wait_vm<0>();
 
-  // ---- DMA lanes.  Op 0: K (waves 0-3) and V (waves 4-7) of the 64 keys,
-  // wave w % 4 moving positions 16 (w % 4) + lane / 4.  Ops 1-3: Q, dA, dA
-  // low of the 128 queries, position tid / 4.  Op 4: lse2 (waves 0-3) and
-  // -D (waves 4-7), 128 bytes per wave (lanes 0..7).
+  // ---- DMA lanes (lane offsets fixed, row bases in scalar registers).
+  // Op 0: K (waves 0-7) or V (waves 8-15) of the 128 keys, keys
+  // 16 (w % 8) + lane / 4.  Op 1: Q (waves 0-7) or dA (waves 8-15) of the
+  // 128 queries.  Op 2: the low part of dA (waves 0-7), lse2 (waves 8-11)
+  // or -D (waves 12-15), 128 bytes per wave (lanes 0..7).
+  const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
+  const int nr = max(r1 - r0, 0);
+  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
   const int hb = h * HEAD_DIM;
-  const int kp = 16 * (wave & 3) + (lane >> 2), kc = (lane & 3) ^ swz(kp);
-  const int64_t kofs = (int64_t)min(kstart + kp, last) * G.sPos + 8 * kc + hb;
-  const bf16* kvsrc = wave < 4 ? a.k : a.v;
-  const int qp = tid >> 2, qc = (tid & 3) ^ swz(qp);
-  const int64_t qofs = (int64_t)min(qstart + qp, last) * G.sPos + 8 * qc + hb;
-  const int lq = min(qstart + 32 * (wave & 3) + 4 * lane, G.np - 4);
-  const float* ldsrc = wave < 4 ? a.lse2 : a.dsum;
+  const int pp = 16 * (wave & 7) + (lane >> 2);  // position (key or query) of this lane
+  const int pc = (lane & 3) ^ swz(pp);
+  const bf16* src0 = wave < 8 ? a.k : a.v;
+  const bf16* src1 = wave < 8 ? a.q : a.da;
+  const uint32_t voff0 =
+      (uint32_t)(((int64_t)(kstart + pp) * G.sPos + hb + 8 * pc) * 2);
+  const uint32_t voff1 =
+      (uint32_t)(((int64_t)(qstart + pp) * G.sPos + hb + 8 * pc) * 2);
+  // op 2: dA low (waves 0-7, same lane offsets as op 1) or lse2 / -D rows
+  const bool lo_op = wave < 8;
+  const float* lrow = (wave < 12 ? a.lse2 : a.dsum) + (int64_t)h * G.n * G.np;
+  const uint32_t voff2 =
+      lo_op ? voff1 : (uint32_t)((qstart + 32 * (wave & 3) + 4 * lane) * 4);
+  char* const dst0 = smem + (wave < 8 ? DBD_OK : DBD_OV) + 1024 * (wave & 7);
+  char* const dst1 = smem + (wave < 8 ? DBD_OQ : DBD_ODA) + 1024 * (wave & 7);
+  char* const dst2 = lo_op ? smem + DBD_OLO + 1024 * wave
+                           : smem + DBD_LD + 128 * (wave - 8);
   auto issue = [&](int r, int slot) {
-    char* sl = smem + slot * DBD_SLOT;
-    const int64_t rb = (int64_t)r * G.sRow;
-    dma16(kvsrc + rb + kofs, sl + (wave < 4 ? DBD_OK : DBD_OV) + 1024 * (wave & 3));
-    dma16(a.q + rb + qofs, sl + DBD_OQ + 1024 * wave);
-    dma16(a.da + rb + qofs, sl + DBD_ODA + 1024 * wave);
-    dma16(a.dalo + rb + qofs, sl + DBD_OLO + 1024 * wave);
-    if (lane < 8)
-      dma16(ldsrc + ((int64_t)h * G.n + r) * G.np + lq, sl + DBD_LD + 128 * wave);
+    // rows past the chunk copy nothing (empty resources) but keep the wait
+    // counts uniform
+    const bool real = r < r1;
+    const int64_t rb = (int64_t)min(r, G.n - 1) * G.sRow;
+    const bf16* p0 = src0 + rb;
+    const bf16* p1 = src1 + rb;
+    const bf16* p2 = a.dalo + rb;
+    const float* pl = lrow + (int64_t)min(r, G.n - 1) * G.np;
+    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff0,
+           dst0 + slot * DBD_SLOT);
+    dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff1,
+           dst1 + slot * DBD_SLOT);
+    if (lo_op) {
+      dma16b(real ? buf_rsrc(p2, a.dalo + tensor) : buf_rsrc(p2, p2), voff2,
+             dst2 + slot * DBD_SLOT);
+    } else if (lane < 8) {
+      dma16b(real ? buf_rsrc(pl, pl + G.np) : buf_rsrc(pl, pl), voff2,
+             dst2 + slot * DBD_SLOT);
+    }
   };
 
   // ---- LDS read addresses (slot 0)
@@ -1002,52 +1152,67 @@ __global__ __launch_bounds__(512, 2) void db_dma_kernel(BwdArgs<bf16> a, int nkb
   const uint32_t kpos = base + (uint32_t)(ktl * TILE + l32) * 64;
   const uint32_t rk0 = kpos + 16 * (g ^ sw), rk1 = kpos + 16 * ((2 + g) ^ sw);
   const uint32_t rl = base + DBD_LD + (qtl * TILE + l32) * 4;
+  const uint32_t* kbrow = a.kbits + kstart / TILE;
 
-  const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
-  const int nr = r1 - r0;
-  const int nkt = G.nkt;
-  auto kword = [&](int r, int t) -> uint32_t {
-    return t < nkt ? const_load(a.kbits + (int64_t)r * nkt + t) : 0u;
-  };
-
-  if (nr > 0) issue(r0, 0);
-  for (int i = 0; i < nr; ++i) {
-    const int r = r0 + i;
-    const uint32_t so = (i % DBD_SLOTS) * DBD_SLOT;
-    wait_vm<(DBD_SLOTS - 2) * DBD_OPS>();  // row r has landed
+  auto step = [&](int r, auto slot) {
+    constexpr int S = decltype(slot)::value;
+    const uint32_t wb = kt < nkt ? const_load(kbrow + (int64_t)r * nkt + ktl) : 0u;
+    wait_vm<DBD_OPS>();  // row r has landed (only row r + 1 is still in flight)
     lds_barrier();
-    const uint32_t w0 = kword(r, kbk * 2), w1 = kword(r, kbk * 2 + 1);
-    if ((w0 & w1) != 0xffffffffu) {
-      // zero V rows of keys invalid for the row (P = 0 there, and 0 times a
-      // non-finite dP would not be); thread t < 256: key t / 4, 16 bytes
-      if (tid < 256) {
-        const uint32_t wb = (tid >> 7) ? w1 : w0;
-        if (!((wb >> ((tid >> 2) & 31)) & 1u)) *(f32x4*)(smem + so + DBD_OV + 16 * tid) = f32x4{};
+    {
+      // key bits of the block's 4 tiles: the same in every wave, so the
+      // branch below (it holds a barrier) is uniform across the workgroup
+      uint32_t all = 0xffffffffu;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        all &= kstart / TILE + j < nkt ? const_load(kbrow + (int64_t)r * nkt + j) : 0xffffffffu;
+      if (all != 0xffffffffu) {
+        // zero V rows of keys invalid for the row (P = 0 there, and 0 times
+        // a non-finite dP would not be); thread t < 512: key t / 4, 16 bytes
+        if (tid < 512) {
+          const int j = tid >> 7;
+          const uint32_t b = kstart / TILE + j < nkt ? const_load(kbrow + (int64_t)r * nkt + j) : 0u;
+          if (!((b >> ((tid >> 2) & 31)) & 1u))
+            *(f32x4*)(smem + S * DBD_SLOT + DBD_OV + 16 * tid) = f32x4{};
+        }
+        __syncthreads();
       }
-      __syncthreads();
     }
-    // row r + 1 into the other slot (a copy of the last row past the end
-    // keeps the wait counts uniform)
-    issue(r0 + min(i + DBD_SLOTS - 1, nr - 1), (i + DBD_SLOTS - 1) % DBD_SLOTS);
-    const uint32_t bits = ktl ? w1 : w0;
-    if (!active || bits == 0u) continue;
-    float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + so);
-    const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + so + 512);
+    issue(r + 2, (S + 2) % DBD_SLOTS);  // row r + 2 into the slot of row r - 1
+    if (!active || wb == 0u) return;
+    float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT);
+    const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT + 512);
     if (!qok) l2 = pos_inf();
-    const F q0 = lds_load16<F>(rq0 + so + DBD_OQ), q1 = lds_load16<F>(rq1 + so + DBD_OQ);
-    const F k0 = lds_load16<F>(rk0 + so + DBD_OK), k1 = lds_load16<F>(rk1 + so + DBD_OK);
+    const F q0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OQ);
+    const F q1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OQ);
+    const F k0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OK);
+    const F k1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OK);
     f32x16 sv = M::mma(k1, q1, M::mma(k0, q0, binit));  // S^T = bias + K Q^T
-    if (bits != 0xffffffffu) mask_rows(sv, bits, g);
-    const F d0 = lds_load16<F>(rq0 + so + DBD_ODA), d1 = lds_load16<F>(rq1 + so + DBD_ODA);
-    const F e0 = lds_load16<F>(rq0 + so + DBD_OLO), e1 = lds_load16<F>(rq1 + so + DBD_OLO);
-    const F v0 = lds_load16<F>(rk0 + so + DBD_OV), v1 = lds_load16<F>(rk1 + so + DBD_OV);
-    f32x16 dpv = M::mma(v0, d0, splat16(nd));  // dP^T - D = V dA^T - D (hi and lo parts)
+    if (wb != 0xffffffffu) mask_rows(sv, wb, g);
+    const F d0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_ODA);
+    const F d1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_ODA);
+    const F e0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OLO);
+    const F e1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OLO);
+    const F v0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OV);
+    const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
+    f32x16 dpv = splat16(nd);  // dP^T - D = V dA^T - D (hi and lo parts)
+    dpv = M::mma(v0, d0, dpv);
     dpv = M::mma(v1, d1, dpv);
     dpv = M::mma(v0, e0, dpv);
     dpv = M::mma(v1, e1, dpv);
 #pragma unroll
     for (int v = 0; v < 16; ++v)
       acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
+  };
+
+  issue(r0, 0);
+  issue(r0 + 1, 1);
+  for (int i = 0; i < nr; i += DBD_SLOTS) {
+    step(r0 + i, slot_c<0>{});
+    if (i + 1 >= nr) break;
+    step(r0 + i + 1, slot_c<1>{});
+    if (i + 2 >= nr) break;
+    step(r0 + i + 2, slot_c<2>{});
   }
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active) return;
@@ -1061,6 +1226,7 @@ __global__ __launch_bounds__(512, 2) void db_dma_kernel(BwdArgs<bf16> a, int nkb
     *(f32x4*)(slab + 8 * j) = x;
   }
 }
+
 
 // dbias at (query q, key k, head h) = sum of the slabs in chunk order; the
 // starting node stores it at [q][k][h], the ending node at [k][q][h].
@@ -1097,16 +1263,16 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     hipLaunchKernelGGL(bwd_pad_kernel, dim3((unsigned)((npad + 255) / 256)), dim3(256), 0, s, g,
                        ws.lse2, ws.dsum);
   }
-  BwdArgs<T> a{g, p.bt, p.btT, p.kbits, q, k, v, da, dalo, ws.lse2, ws.dsum, dq, dk, dv, ws.slabs,
+  BwdArgs<T> a{g, p.bt, p.btT, p.kbits, p.rowfull, q, k, v, da, dalo, ws.lse2, ws.dsum, dq, dk, dv, ws.slabs,
                (g.n + BWD_BLK - 1) / BWD_BLK, ws.nrc, (g.n + ws.nrc - 1) / ws.nrc};
   const int64_t nrow = (int64_t)a.nblk * g.n * g.H;
   {
     // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
     if constexpr (std::is_same<T, bf16>::value) {
-      const int nqb = (g.n + 63) / 64;
-      const int64_t nwg = (int64_t)nqb * ((g.n + 1) / 2) * g.H;
-      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(256), 0, s, a, nqb);
+      const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
+      const int64_t nwg = (int64_t)nqb * ((g.n + QD_ROWS - 1) / QD_ROWS) * g.H;
+      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(64 * QD_WAVES), 0, s, a, nqb);
     } else {
       hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
     }
@@ -1115,7 +1281,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     KernelTimer t(K_DKDV, s);
     if constexpr (std::is_same<T, bf16>::value) {
       const int64_t nwg = (int64_t)a.nblk * ((g.n + KD_ROWS - 1) / KD_ROWS) * g.H;
-      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a);
+      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(64 * KD_WAVES), 0, s, a);
     } else {
       hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
     }
@@ -1125,8 +1291,8 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     KernelTimer t(K_DB, s);
     if constexpr (std::is_same<T, bf16>::value) {
       const int nkb = (g.n + DBD_K - 1) / DBD_K;
-      const int64_t nwg = (int64_t)a.nblk * nkb * ws.nrc * g.H;
-      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a, nkb);
+      const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
+      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg), dim3(64 * DBD_WAVES), 0, s, a, nkb);
     } else
       hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
   }

@@ -29,6 +29,8 @@
 // outstanding load first).
 #pragma once
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace triattn {
@@ -69,6 +71,17 @@ __device__ inline rsrc_t buf_rsrc(const void* base, const void* end) {
 __device__ inline void dma16b(rsrc_t r, uint32_t voff, void* dst_wave) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (TRIATTN_LDS void*)dst_wave, 16, (int)voff, 0, 0,
                                            0);
+}
+
+// Ring slot index as a compile-time constant (loops unrolled by the ring
+// length give every LDS access a constant slot offset).
+template <int S>
+using slot_c = std::integral_constant<int, S>;
+
+// Bits of the keys of tile t that lie below n (all 32 except in a ragged last tile).
+__device__ inline uint32_t in_range_bits(int t, int n) {
+  const int m = n - 32 * t;
+  return m >= 32 ? 0xffffffffu : (m <= 0 ? 0u : (1u << m) - 1u);
 }
 
 // 16-byte LDS load from a 32-bit LDS byte address.

@@ -369,15 +369,6 @@ constexpr int FO_BIAS = 2 * FO_ROWS * FO_ROWBLK;    // then the 4 bias tiles (fp
 constexpr int FO_SLOT = FO_BIAS + 4 * 4096;         // 32 KB
 constexpr int FO_SLOTS = 2;
 
-template <int S>
-using slot_c = std::integral_constant<int, S>;
-
-// Bits of the keys of tile t that lie below n (all 32 except in a ragged last tile).
-__device__ inline uint32_t in_range_bits(int t, int n) {
-  const int m = n - 32 * t;
-  return m >= 32 ? 0xffffffffu : (m <= 0 ? 0u : (1u << m) - 1u);
-}
-
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void fwd_dma_kernel(FwdArgs<bf16> a) {
   using M = Mma<bf16>;
