@@ -1229,20 +1229,28 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
 
 
 // dbias at (query q, key k, head h) = sum of the slabs in chunk order; the
-// starting node stores it at [q][k][h], the ending node at [k][q][h].
+// starting node stores it at [q][k][h], the ending node at [k][q][h].  One
+// thread per (h, q, 4 consecutive keys): every slab read is 16 contiguous
+// bytes (the slab rows are np long, a multiple of 32).
 template <typename T>
 __global__ __launch_bounds__(256) void db_reduce_kernel(Geom G, int node, int nrc,
                                                         const float* slabs, T* dbias) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (h, q, k), k fastest
-  const int64_t n = G.n;
-  if (idx >= (int64_t)G.H * n * n) return;
-  const int k = (int)(idx % n), q = (int)((idx / n) % n), h = (int)(idx / (n * n));
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (h, q, k / 4), k fastest
+  const int64_t n = G.n, nk4 = (n + 3) / 4;
+  if (idx >= (int64_t)G.H * n * nk4) return;
+  const int k0 = (int)(idx % nk4) * 4, q = (int)((idx / nk4) % n), h = (int)(idx / (n * nk4));
   const int64_t plane = (int64_t)G.np * G.np;
-  const float* p = slabs + (int64_t)h * plane + (int64_t)q * G.np + k;
-  float s = 0.f;
-  for (int c = 0; c < nrc; ++c) s += p[(int64_t)c * G.H * plane];
-  const int64_t at = node == 0 ? ((int64_t)q * n + k) * G.H + h : ((int64_t)k * n + q) * G.H + h;
-  dbias[at] = (T)s;
+  const float* p = slabs + (int64_t)h * plane + (int64_t)q * G.np + k0;
+  f32x4 s = *(const f32x4*)p;
+  for (int c = 1; c < nrc; ++c) s += *(const f32x4*)(p + (int64_t)c * G.H * plane);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int k = k0 + e;
+    if (k >= n) break;
+    const int64_t at =
+        node == 0 ? ((int64_t)q * n + k) * G.H + h : ((int64_t)k * n + q) * G.H + h;
+    dbias[at] = (T)s[e];
+  }
 }
 
 template <typename T>
@@ -1297,7 +1305,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
       hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
   }
   {
-    const int64_t nred = (int64_t)g.H * g.n * g.n;
+    const int64_t nred = (int64_t)g.H * g.n * ((g.n + 3) / 4);
     KernelTimer t(K_DB_REDUCE, s);
     hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0, s,
                        g, node, ws.nrc, ws.slabs, dbias);
