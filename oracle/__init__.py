@@ -121,3 +121,49 @@ def bwd(node, q, k, v, g, bias, dout, mask=None, scale=None, rows=None, db_queri
                       _ptr(bias), _ptr(m, _U8), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
                       _ptr(dg), _ptr(db), _ptr(rl, _I64), nr, _ptr(ql, _I64), nq)
     return dq, dk, dv, dg, db
+
+
+# ---- fused layer-norm + linear projection (ln_linear.c) ----------------------------
+
+def _lnl_decl(lib):
+    i64, dbl = ctypes.c_int64, ctypes.c_double
+    lib.oracle_lnl_fwd.argtypes = [i64, i64, i64, dbl, _D, _D, _D, _D, _D, _D, _D, _I64, i64]
+    lib.oracle_lnl_fwd.restype = None
+    lib.oracle_lnl_bwd.argtypes = [i64, i64, i64, dbl, _D, _D, _D, _D, _D, _D, _D, _D, _D,
+                                   _I64, i64]
+    lib.oracle_lnl_bwd.restype = None
+    return lib
+
+
+def lnl_fwd(x, gamma, beta, w, eps=1e-5, rows=None):
+    """Layer-norm over the last axis of x [M, K], then o2 = o1 W (W [K, N]).
+    Returns (o2 [M, N], mean [M], rstd [M]) in float64; rows restricts the
+    work to those rows (other entries NaN)."""
+    x, gamma, beta, w = (_f64(t) for t in (x, gamma, beta, w))
+    M, K = x.shape
+    N = w.shape[1]
+    o2 = np.full((M, N), np.nan)
+    mean = np.full(M, np.nan)
+    rstd = np.full(M, np.nan)
+    rl, nr = _list(rows)
+    _lnl_decl(_lib()).oracle_lnl_fwd(M, K, N, float(eps), _ptr(x), _ptr(gamma), _ptr(beta),
+                                     _ptr(w), _ptr(o2), _ptr(mean), _ptr(rstd), _ptr(rl, _I64), nr)
+    return o2, mean, rstd
+
+
+def lnl_bwd(x, gamma, beta, w, do2, eps=1e-5, rows=None, sums=True):
+    """Backward of sum(do2 * o2): returns (dx [M, K], dw [K, N], dgamma [K],
+    dbeta [K]) in float64.  rows restricts dx to those rows; sums=False skips
+    the sums over rows (dw, dgamma, dbeta are then None)."""
+    x, gamma, beta, w, do2 = (_f64(t) for t in (x, gamma, beta, w, do2))
+    M, K = x.shape
+    N = w.shape[1]
+    dx = np.full((M, K), np.nan)
+    dw = np.full((K, N), np.nan) if sums else None
+    dgamma = np.full(K, np.nan) if sums else None
+    dbeta = np.full(K, np.nan) if sums else None
+    rl, nr = _list(rows)
+    _lnl_decl(_lib()).oracle_lnl_bwd(M, K, N, float(eps), _ptr(x), _ptr(gamma), _ptr(beta),
+                                     _ptr(w), _ptr(do2), _ptr(dx), _ptr(dw), _ptr(dgamma),
+                                     _ptr(dbeta), _ptr(rl, _I64), nr)
+    return dx, dw, dgamma, dbeta

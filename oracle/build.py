@@ -1,4 +1,5 @@
-"""Compile the fp64 CPU oracle (oracle.c) into liboracle.so with gcc.
+"""Compile the fp64 CPU oracle (oracle.c: triangle attention; ln_linear.c:
+fused layer-norm + linear projection) into liboracle.so with gcc.
 
 Test infrastructure: only the tests, the smoke check and the benchmark's
 CPU-baseline leg load the result.  Generic x86-64 code (no -march=native),
@@ -9,12 +10,13 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "oracle.c")
+SRC_LNL = os.path.join(HERE, "ln_linear.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 
 def build(verbose: bool = False) -> str:
     cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
-           SRC, "-o", LIB + ".tmp", "-lm"]
+           SRC, SRC_LNL, "-o", LIB + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

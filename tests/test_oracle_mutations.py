@@ -72,3 +72,54 @@ def test_pins_catch_mutation(name, tmp_path):
     finally:
         oracle.use_library(prev)
     assert caught, f"no pin caught mutation {name}"
+
+
+# ---- the fused layer-norm + linear oracle (ln_linear.c) -------------------------------
+
+import test_oracle_ln_linear as lnl_pins  # noqa: E402
+
+LNL_MUTATIONS = {
+    "unbiased_variance": ("  var /= (double)K;", "  var /= (double)(K - 1);"),
+    "mean_not_subtracted": ("    xhat[k] = (x[k] - mean) * rstd;", "    xhat[k] = x[k] * rstd;"),
+    "beta_dropped": ("    o1[k] = xhat[k] * gamma[k] + beta[k];", "    o1[k] = xhat[k] * gamma[k];"),
+    "c1_dropped": ("rstd * (wdy[k] - c1 * xhat[k] - c2)", "rstd * (wdy[k] - c2)"),
+    "c2_dropped": ("rstd * (wdy[k] - c1 * xhat[k] - c2)", "rstd * (wdy[k] - c1 * xhat[k])"),
+    "rstd_missing_in_dx": ("rstd * (wdy[k] - c1 * xhat[k] - c2)", "(wdy[k] - c1 * xhat[k] - c2)"),
+    "gamma_missing_in_wdy": ("      wdy[k] = d1 * gamma[k];", "      wdy[k] = d1;"),
+    "dw_uses_xhat": ("        dw[k * N + n] += o1 * do2[m * N + n];",
+                     "        dw[k * N + n] += xhat * do2[m * N + n];"),
+    "dgamma_uses_o1": ("      dg += d1 * xhat;", "      dg += d1 * o1;"),
+    "w_transposed_in_do1": ("      for (int64_t n = 0; n < N; ++n) d1 += do2[m * N + n] * w[k * N + n];",
+                            "      for (int64_t n = 0; n < N; ++n) d1 += do2[m * N + n] * w[n * K + k % N];"),
+}
+
+LNL_PIN_TESTS = [
+    (lnl_pins.test_forward_and_backward_match_torch, dict(m=5, k=4, n=3, seed=0)),
+    (lnl_pins.test_backward_matches_central_finite_differences, dict()),
+    (lnl_pins.test_row_shift_and_scale_invariance, dict()),
+    (lnl_pins.test_zero_gamma_gives_beta_projection_and_no_input_gradient, dict()),
+    (lnl_pins.test_closed_form_two_features, dict()),
+]
+
+
+@pytest.mark.parametrize("name", sorted(LNL_MUTATIONS))
+def test_lnl_pins_catch_mutation(name, tmp_path):
+    old, new = LNL_MUTATIONS[name]
+    src = open(obuild.SRC_LNL).read()
+    assert src.count(old) == 1, f"mutation anchor for {name} not found exactly once"
+    bad = tmp_path / "ln_linear_mut.c"
+    bad.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mut.so"
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-std=c11", obuild.SRC,
+                    str(bad), "-o", str(lib), "-lm"], check=True)
+    prev = oracle.use_library(oracle.load(str(lib)))
+    caught = []
+    try:
+        for fn, kw in LNL_PIN_TESTS:
+            try:
+                fn(**kw)
+            except AssertionError:
+                caught.append(fn.__name__)
+    finally:
+        oracle.use_library(prev)
+    assert caught, f"no pin caught mutation {name}"
