@@ -94,6 +94,30 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
                  size_t workspace_bytes, void* stream);
 
+/* Fused layer-norm + linear projection (Section IV, fused layer-norm &
+ * linear projection; forward formulas in the appendix table of fused
+ * operators): the step that produces the attention inputs from the pair
+ * representation.  For every row of x [m][k]:
+ *   o1 = (x - mean) * rstd * gamma + beta,  rstd = 1 / sqrt(var + eps),
+ *        mean and var (biased) over the row's k features;
+ *   o2 = o1 W,  W [k][ncols],  ncols = cols[0] + ... + cols[n_out - 1].
+ * o2's columns are written into n_out row-major tensors: outs[i] receives
+ * columns cols[0] + ... + cols[i - 1] onwards as [m][cols[i]] (for triangle
+ * attention: Q, K, V, G [n*n][h*d] and the bias logits [n*n][h]).  mean and
+ * rstd [m] (fp32) are saved for the backward pass.
+ *   dtype: TRIATTN_BF16 only (x, gamma [k], beta [k], w and the outputs;
+ *          fp32 statistics and accumulation); TRIATTN_ERR_UNSUPPORTED else.
+ *   k must be 128; 1 <= n_out <= 8; every cols[i] a positive multiple of 4
+ *   and ncols <= 1024; m >= 1; eps finite and >= 0.
+ *   cols and outs are host arrays; tensor pointers are device memory,
+ *   16-byte aligned.  Same workspace, stream and error rules as above. */
+int tri_ln_linear_fwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
+                                      const int64_t* cols, size_t* bytes);
+int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, float eps,
+                      const void* x, const void* gamma, const void* beta, const void* w,
+                      void* const* outs, float* mean, float* rstd, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code ("unknown status" otherwise). */
 const char* tri_attn_status_string(int status);
 

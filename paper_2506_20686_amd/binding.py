@@ -53,9 +53,15 @@ def lib():
         L.tri_attn_timing_read.argtypes = [_int, ctypes.POINTER(ctypes.c_char_p),
                                            ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_int64)]
+        _i64p = ctypes.POINTER(_i64)
+        L.tri_ln_linear_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _int, _i64p,
+                                                        ctypes.POINTER(_sz)]
+        L.tri_ln_linear_fwd.argtypes = [_int, _i64, _i64, _int, _i64p, _f, _vp, _vp, _vp, _vp,
+                                        ctypes.POINTER(_vp), _vp, _vp, _vp, _sz, _vp]
         for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
                      "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
-                     "tri_attn_timing_reset", "tri_attn_timing_read"):
+                     "tri_attn_timing_reset", "tri_attn_timing_read",
+                     "tri_ln_linear_fwd_workspace_bytes", "tri_ln_linear_fwd"):
             getattr(L, name).restype = _int
         _LIB = L
     return _LIB
@@ -95,6 +101,28 @@ def tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, 
     """Raw call: every tensor argument is an integer device address (or None)."""
     return lib().tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
                               dout, dq, dk, dv, dg, dbias, workspace, workspace_bytes, stream)
+
+
+def _cols_arr(cols):
+    return (_i64 * len(cols))(*[int(c) for c in cols])
+
+
+def tri_ln_linear_fwd_workspace_bytes(dtype: int, m: int, k: int, cols) -> int:
+    out = _sz(0)
+    st = lib().tri_ln_linear_fwd_workspace_bytes(dtype, m, k, len(cols), _cols_arr(cols),
+                                                 ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_ln_linear_fwd_workspace_bytes")
+    return out.value
+
+
+def tri_ln_linear_fwd(dtype, m, k, cols, eps, x, gamma, beta, w, outs, mean, rstd, workspace,
+                      workspace_bytes, stream) -> int:
+    """Raw call: tensor arguments are integer device addresses; cols and outs
+    are Python sequences (passed as host arrays)."""
+    outs_arr = (_vp * len(outs))(*outs)
+    return lib().tri_ln_linear_fwd(dtype, m, k, len(cols), _cols_arr(cols), eps, x, gamma, beta,
+                                   w, outs_arr, mean, rstd, workspace, workspace_bytes, stream)
 
 
 def tri_attn_timing_enable(on: bool) -> None:
@@ -238,3 +266,33 @@ class TriangleAttention(torch.autograd.Function):
 
 def triangle_attention(q, k, v, g, bias, mask=None, node: int = STARTING, scale=None):
     return TriangleAttention.apply(q, k, v, g, bias, mask, node, scale)
+
+
+# ---- fused layer-norm + linear projection ---------------------------------------------
+
+def ln_linear_fwd(x, gamma, beta, w, cols, eps: float = 1e-5,
+                  workspace: Optional[torch.Tensor] = None):
+    """o2 = layer_norm(x) * gamma + beta, then @ w, split column-wise into
+    len(cols) tensors [m, cols[i]].  x [m, k] bf16.  Returns (outs, mean,
+    rstd)."""
+    if x.dim() != 2:
+        raise ValueError("x must be [m, k]")
+    m, k = x.shape
+    dev = x.device
+    ncols = int(sum(cols))
+    _check("x", x, (m, k), torch.bfloat16, dev)
+    _check("gamma", gamma, (k,), torch.bfloat16, dev)
+    _check("beta", beta, (k,), torch.bfloat16, dev)
+    _check("w", w, (k, ncols), torch.bfloat16, dev)
+    outs = [torch.empty((m, int(c)), dtype=torch.bfloat16, device=dev) for c in cols]
+    mean = torch.empty(m, dtype=torch.float32, device=dev)
+    rstd = torch.empty(m, dtype=torch.float32, device=dev)
+    need = tri_ln_linear_fwd_workspace_bytes(BF16, m, k, cols)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_ln_linear_fwd(BF16, m, k, cols, float(eps), _ptr(x), _ptr(gamma), _ptr(beta),
+                           _ptr(w), [o.data_ptr() for o in outs], _ptr(mean), _ptr(rstd),
+                           _ptr(workspace), workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_ln_linear_fwd")
+    return outs, mean, rstd

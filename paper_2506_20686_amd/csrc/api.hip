@@ -202,6 +202,86 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                         dbias, workspace, s);
 }
 
+// ---- fused layer-norm + linear projection ---------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+int lnl_check(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, int64_t* ncols) {
+  if (dtype != TRIATTN_F32 && dtype != TRIATTN_BF16) return TRIATTN_ERR_INVALID_ARG;
+  if (m < 1 || m > ((int64_t)1 << 31) || k < 1 || n_out < 1 || cols == nullptr)
+    return TRIATTN_ERR_INVALID_ARG;
+  if (n_out > triattn::LNL_MAX_OUT) return TRIATTN_ERR_UNSUPPORTED;
+  int64_t total = 0;
+  for (int i = 0; i < n_out; ++i) {
+    if (cols[i] < 1) return TRIATTN_ERR_INVALID_ARG;
+    if (cols[i] % 4 != 0) return TRIATTN_ERR_UNSUPPORTED;
+    total += cols[i];
+  }
+  if (total > 1024) return TRIATTN_ERR_UNSUPPORTED;
+  if (dtype != TRIATTN_BF16 || k != triattn::LNL_K) return TRIATTN_ERR_UNSUPPORTED;
+  *ncols = total;
+  return TRIATTN_OK;
+}
+
+size_t lnl_np(int64_t ncols) { return (size_t)((ncols + 31) / 32 * 32); }
+
+}  // namespace
+
+extern "C" {
+
+int tri_ln_linear_fwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
+                                      const int64_t* cols, size_t* bytes) {
+  int64_t ncols = 0;
+  const int st = lnl_check(dtype, m, k, n_out, cols, &ncols);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = round256(lnl_np(ncols) * triattn::LNL_K * sizeof(triattn::bf16));
+  return TRIATTN_OK;
+}
+
+int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, float eps,
+                      const void* x, const void* gamma, const void* beta, const void* w,
+                      void* const* outs, float* mean, float* rstd, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  int64_t ncols = 0;
+  int st = lnl_check(dtype, m, k, n_out, cols, &ncols);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(eps) && eps >= 0.f) || outs == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {x, gamma, beta, w, mean, rstd};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  for (int i = 0; i < n_out; ++i)
+    if (outs[i] == nullptr || !aligned16(outs[i])) return TRIATTN_ERR_INVALID_ARG;
+  size_t need = 0;
+  tri_ln_linear_fwd_workspace_bytes(dtype, m, k, n_out, cols, &need);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < need)
+    return TRIATTN_ERR_WORKSPACE;
+  triattn::LnlArgs a{};
+  a.m = m;
+  a.ncols = (int)ncols;
+  a.np = (int)lnl_np(ncols);
+  a.n_out = n_out;
+  int64_t c = 0;
+  for (int i = 0; i < n_out; ++i) {
+    a.start[i] = (int)c;
+    a.out[i] = (triattn::bf16*)outs[i];
+    c += cols[i];
+  }
+  for (int i = n_out; i <= triattn::LNL_MAX_OUT; ++i) a.start[i] = (int)ncols;
+  a.eps = eps;
+  a.x = (const triattn::bf16*)x;
+  a.gamma = (const triattn::bf16*)gamma;
+  a.beta = (const triattn::bf16*)beta;
+  a.mean = mean;
+  a.rstd = rstd;
+  if (triattn::launch_lnl_fwd(a, (triattn::bf16*)workspace, (const triattn::bf16*)w,
+                              (hipStream_t)stream) != hipSuccess)
+    return TRIATTN_ERR_HIP;
+  return TRIATTN_OK;
+}
+
 const char* tri_attn_status_string(int status) {
   switch (status) {
     case TRIATTN_OK: return "ok";

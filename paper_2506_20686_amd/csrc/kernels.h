@@ -51,4 +51,23 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& w, co
                       const T* k, const T* v, const T* gate, const T* out, const float* lse,
                       const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, hipStream_t s);
 
+// ---- fused layer-norm + linear projection (lnl.hip) ---------------------------------
+constexpr int LNL_K = 128;       // features per row (the pair channel width)
+constexpr int LNL_MAX_OUT = 8;   // output tensors o2's columns are split into
+
+struct LnlArgs {
+  int64_t m;                     // rows
+  int ncols;                     // output columns N (sum of the outputs' widths)
+  int np;                        // N rounded up to a multiple of 32
+  int n_out;                     // output tensors
+  int start[LNL_MAX_OUT + 1];    // first column of each output; start[n_out] = N
+  float eps;
+  const bf16 *x, *gamma, *beta;  // x [m][K], gamma and beta [K]
+  const bf16* wt;                // W^T [np][K] (prepared in the workspace)
+  bf16* out[LNL_MAX_OUT];        // output i: [m][start[i + 1] - start[i]]
+  float *mean, *rstd;            // [m], saved for the backward
+};
+
+hipError_t launch_lnl_fwd(const LnlArgs& a, bf16* wt, const bf16* w, hipStream_t s);
+
 }  // namespace triattn

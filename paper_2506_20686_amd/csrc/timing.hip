@@ -12,9 +12,10 @@ namespace triattn {
 
 namespace {
 
-const char* const kNames[K_COUNT] = {"prep_bias", "prep_kbits", "fwd",  "bwd_prep",
-                                     "bwd_pad",   "dq",         "dkdv", "db",
-                                     "db_reduce"};
+const char* const kNames[K_COUNT] = {"prep_bias",   "prep_kbits", "fwd",        "bwd_prep",
+                                     "bwd_pad",     "dq",         "dkdv",       "db",
+                                     "db_reduce",   "lnl_prep",   "lnl_fwd",    "lnl_bwd_dx",
+                                     "lnl_bwd_dw",  "lnl_reduce"};
 
 struct Pending {
   int id;

@@ -110,3 +110,30 @@ def workload_inputs(w: Workload, node: Optional[int] = None):
     t["n_pad"] = n_pad
     t["node"] = node
     return t
+
+
+# ---- fused layer-norm + linear projection ------------------------------------------------
+
+# The attention's input projection of an AF3 pair stack: the pair
+# representation [n*n][c_z = 128] is normalised and projected to Q, K, V, G
+# (h*d = 128 columns each) and the bias logits (h = 4 columns).
+LNL_K = 128
+LNL_COLS = (128, 128, 128, 128, 4)
+
+
+def lnl_inputs(m: int, cols=LNL_COLS, seed: int = 0, k: int = LNL_K):
+    """x [m, k] ~ N(0.3, 1.5^2); gamma ~ 1 + 0.2 N(0, 1); beta ~ 0.2 N(0, 1);
+    W [k, sum(cols)] ~ N(0, 1/k); do2 [m, sum(cols)] ~ N(0, 1); drawn in that
+    order from one CPU generator, rounded to bf16."""
+    gen = torch.Generator("cpu").manual_seed(seed)
+    ncols = int(sum(cols))
+
+    def draw(shape, std=1.0, mean=0.0):
+        return (torch.randn(*shape, generator=gen) * std + mean).to(torch.bfloat16)
+
+    x = draw((m, k), 1.5, 0.3)
+    gamma = draw((k,), 0.2, 1.0)
+    beta = draw((k,), 0.2)
+    w = draw((k, ncols), 1.0 / math.sqrt(k))
+    do2 = draw((m, ncols))
+    return dict(x=x, gamma=gamma, beta=beta, w=w, do2=do2, cols=tuple(cols))

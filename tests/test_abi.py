@@ -24,7 +24,7 @@ def lib():
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(tri_attn_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(tri_(?:attn|ln_linear)_\w+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol(lib):
@@ -139,3 +139,47 @@ def test_undersized_workspace_reports_exact_requirement(lib):
         assert lib.tri_attn_bwd(*bwd_args(node=node, wsb=need - 1)) == B.ERR_WORKSPACE
         st, need = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, 16, 2, 32)
         assert lib.tri_attn_fwd(*fwd_args(node=node, wsb=need - 1)) == B.ERR_WORKSPACE
+
+
+# ---- fused layer-norm + linear projection ----------------------------------------------
+
+COLS = [128, 128, 128, 128, 4]
+
+
+def lnl_args(**over):
+    a = dict(dtype=B.BF16, m=1000, k=128, cols=COLS, eps=1e-5, x=P, gamma=P, beta=P, w=P,
+             outs=[P] * len(over.get("cols", COLS)), mean=P, rstd=P, ws=P, wsb=1 << 30,
+             stream=None)
+    a.update(over)
+    cols = (ctypes.c_int64 * len(a["cols"]))(*a["cols"])
+    outs = None if a["outs"] is None else (ctypes.c_void_p * len(a["outs"]))(*a["outs"])
+    return (a["dtype"], a["m"], a["k"], len(a["cols"]), cols, a["eps"], a["x"], a["gamma"],
+            a["beta"], a["w"], outs, a["mean"], a["rstd"], a["ws"], a["wsb"], a["stream"])
+
+
+def test_ln_linear_workspace_size(lib):
+    for cols in ([128], [4], COLS, [512, 512]):
+        got = B.tri_ln_linear_fwd_workspace_bytes(B.BF16, 5000, 128, cols)
+        np_ = (sum(cols) + 31) // 32 * 32
+        assert got >= np_ * 128 * 2
+
+
+LNL_BAD = [
+    (dict(dtype=-1), B.ERR_INVALID_ARG), (dict(dtype=B.F32), B.ERR_UNSUPPORTED),
+    (dict(m=0), B.ERR_INVALID_ARG), (dict(k=64), B.ERR_UNSUPPORTED),
+    (dict(k=0), B.ERR_INVALID_ARG), (dict(cols=[128, 6]), B.ERR_UNSUPPORTED),
+    (dict(cols=[128, 0]), B.ERR_INVALID_ARG), (dict(cols=[512, 516]), B.ERR_UNSUPPORTED),
+    (dict(cols=[4] * 9), B.ERR_UNSUPPORTED), (dict(eps=-1.0), B.ERR_INVALID_ARG),
+    (dict(eps=float("nan")), B.ERR_INVALID_ARG), (dict(x=None), B.ERR_INVALID_ARG),
+    (dict(gamma=None), B.ERR_INVALID_ARG), (dict(beta=None), B.ERR_INVALID_ARG),
+    (dict(w=None), B.ERR_INVALID_ARG), (dict(mean=None), B.ERR_INVALID_ARG),
+    (dict(rstd=P + 4), B.ERR_INVALID_ARG), (dict(outs=None), B.ERR_INVALID_ARG),
+    (dict(outs=[P, P, None, P, P]), B.ERR_INVALID_ARG),
+    (dict(outs=[P, P, P, P, P + 8]), B.ERR_INVALID_ARG),
+    (dict(ws=None), B.ERR_WORKSPACE), (dict(wsb=100), B.ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("over,code", LNL_BAD)
+def test_ln_linear_fwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_ln_linear_fwd(*lnl_args(**over)) == code
