@@ -110,12 +110,31 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
  *   k must be 128; 1 <= n_out <= 8; every cols[i] a positive multiple of 4
  *   and ncols <= 1024; m >= 1; eps finite and >= 0.
  *   cols and outs are host arrays; tensor pointers are device memory,
- *   16-byte aligned.  Same workspace, stream and error rules as above. */
-int tri_ln_linear_fwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
-                                      const int64_t* cols, size_t* bytes);
+ *   16-byte aligned.  No workspace.  Same stream and error rules as above. */
 int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, float eps,
                       const void* x, const void* gamma, const void* beta, const void* w,
-                      void* const* outs, float* mean, float* rstd, void* workspace,
+                      void* const* outs, float* mean, float* rstd, void* stream);
+
+/* Bytes of device workspace tri_ln_linear_bwd needs for these sizes. */
+int tri_ln_linear_bwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
+                                      const int64_t* cols, size_t* bytes);
+
+/* Backward pass of the fused layer-norm + linear projection for
+ * L = sum(do2 * o2) (appendix table of fused operators: do1 = do2 W^T,
+ * dW = o1^T do2, dgamma = sum over rows of do1 * xhat, dbeta = sum over
+ * rows of do1, dx = rstd (do1 gamma - c1 xhat - c2) with c1, c2 the row
+ * means over the k features of xhat do1 gamma and of do1 gamma).  Takes the
+ * forward's x, gamma, beta, w and its saved mean and rstd, and douts: n_out
+ * tensors [m][cols[i]] holding do2 split like the forward's outputs.
+ * Writes dx [m][k] (dtype), dw [k][ncols], dgamma [k] and dbeta [k] (fp32,
+ * sums over rows taken in a fixed order: bitwise reproducible).
+ *   Same size rules as tri_ln_linear_fwd, and ncols <= 544 and
+ *   (m + 32) * max(k, cols[i]) * 2 < 2^31 (TRIATTN_ERR_UNSUPPORTED else).
+ *   Same pointer, workspace, stream and error rules as above. */
+int tri_ln_linear_bwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols,
+                      const void* x, const void* gamma, const void* beta, const void* w,
+                      const float* mean, const float* rstd, const void* const* douts, void* dx,
+                      float* dw, float* dgamma, float* dbeta, void* workspace,
                       size_t workspace_bytes, void* stream);
 
 /* Static, human-readable name of a status code ("unknown status" otherwise). */

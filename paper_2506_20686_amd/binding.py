@@ -54,14 +54,18 @@ def lib():
                                            ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_int64)]
         _i64p = ctypes.POINTER(_i64)
-        L.tri_ln_linear_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _int, _i64p,
-                                                        ctypes.POINTER(_sz)]
         L.tri_ln_linear_fwd.argtypes = [_int, _i64, _i64, _int, _i64p, _f, _vp, _vp, _vp, _vp,
-                                        ctypes.POINTER(_vp), _vp, _vp, _vp, _sz, _vp]
+                                        ctypes.POINTER(_vp), _vp, _vp, _vp]
+        L.tri_ln_linear_bwd_workspace_bytes.argtypes = [_int, _i64, _i64, _int, _i64p,
+                                                        ctypes.POINTER(_sz)]
+        L.tri_ln_linear_bwd.argtypes = [_int, _i64, _i64, _int, _i64p, _vp, _vp, _vp, _vp, _vp,
+                                        _vp, ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _vp, _sz,
+                                        _vp]
         for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
                      "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
                      "tri_attn_timing_reset", "tri_attn_timing_read",
-                     "tri_ln_linear_fwd_workspace_bytes", "tri_ln_linear_fwd"):
+                     "tri_ln_linear_fwd", "tri_ln_linear_bwd_workspace_bytes",
+                     "tri_ln_linear_bwd"):
             getattr(L, name).restype = _int
         _LIB = L
     return _LIB
@@ -107,22 +111,32 @@ def _cols_arr(cols):
     return (_i64 * len(cols))(*[int(c) for c in cols])
 
 
-def tri_ln_linear_fwd_workspace_bytes(dtype: int, m: int, k: int, cols) -> int:
-    out = _sz(0)
-    st = lib().tri_ln_linear_fwd_workspace_bytes(dtype, m, k, len(cols), _cols_arr(cols),
-                                                 ctypes.byref(out))
-    if st != OK:
-        raise TriAttnError(st, "tri_ln_linear_fwd_workspace_bytes")
-    return out.value
-
-
-def tri_ln_linear_fwd(dtype, m, k, cols, eps, x, gamma, beta, w, outs, mean, rstd, workspace,
-                      workspace_bytes, stream) -> int:
+def tri_ln_linear_fwd(dtype, m, k, cols, eps, x, gamma, beta, w, outs, mean, rstd,
+                      stream) -> int:
     """Raw call: tensor arguments are integer device addresses; cols and outs
     are Python sequences (passed as host arrays)."""
     outs_arr = (_vp * len(outs))(*outs)
     return lib().tri_ln_linear_fwd(dtype, m, k, len(cols), _cols_arr(cols), eps, x, gamma, beta,
-                                   w, outs_arr, mean, rstd, workspace, workspace_bytes, stream)
+                                   w, outs_arr, mean, rstd, stream)
+
+
+def tri_ln_linear_bwd_workspace_bytes(dtype: int, m: int, k: int, cols) -> int:
+    out = _sz(0)
+    st = lib().tri_ln_linear_bwd_workspace_bytes(dtype, m, k, len(cols), _cols_arr(cols),
+                                                 ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_ln_linear_bwd_workspace_bytes")
+    return out.value
+
+
+def tri_ln_linear_bwd(dtype, m, k, cols, x, gamma, beta, w, mean, rstd, douts, dx, dw, dgamma,
+                      dbeta, workspace, workspace_bytes, stream) -> int:
+    """Raw call: tensor arguments are integer device addresses; cols and douts
+    are Python sequences (passed as host arrays)."""
+    douts_arr = (_vp * len(douts))(*douts)
+    return lib().tri_ln_linear_bwd(dtype, m, k, len(cols), _cols_arr(cols), x, gamma, beta, w,
+                                   mean, rstd, douts_arr, dx, dw, dgamma, dbeta, workspace,
+                                   workspace_bytes, stream)
 
 
 def tri_attn_timing_enable(on: bool) -> None:
@@ -270,8 +284,7 @@ def triangle_attention(q, k, v, g, bias, mask=None, node: int = STARTING, scale=
 
 # ---- fused layer-norm + linear projection ---------------------------------------------
 
-def ln_linear_fwd(x, gamma, beta, w, cols, eps: float = 1e-5,
-                  workspace: Optional[torch.Tensor] = None):
+def ln_linear_fwd(x, gamma, beta, w, cols, eps: float = 1e-5):
     """o2 = layer_norm(x) * gamma + beta, then @ w, split column-wise into
     len(cols) tensors [m, cols[i]].  x [m, k] bf16.  Returns (outs, mean,
     rstd)."""
@@ -287,12 +300,42 @@ def ln_linear_fwd(x, gamma, beta, w, cols, eps: float = 1e-5,
     outs = [torch.empty((m, int(c)), dtype=torch.bfloat16, device=dev) for c in cols]
     mean = torch.empty(m, dtype=torch.float32, device=dev)
     rstd = torch.empty(m, dtype=torch.float32, device=dev)
-    need = tri_ln_linear_fwd_workspace_bytes(BF16, m, k, cols)
-    if workspace is None or workspace.numel() < need:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     st = tri_ln_linear_fwd(BF16, m, k, cols, float(eps), _ptr(x), _ptr(gamma), _ptr(beta),
                            _ptr(w), [o.data_ptr() for o in outs], _ptr(mean), _ptr(rstd),
-                           _ptr(workspace), workspace.numel(), _stream(dev))
+                           _stream(dev))
     if st != OK:
         raise TriAttnError(st, "tri_ln_linear_fwd")
     return outs, mean, rstd
+
+
+def ln_linear_bwd(x, gamma, beta, w, mean, rstd, douts, eps: float = 1e-5,
+                  workspace: Optional[torch.Tensor] = None):
+    """Gradients of sum(do2 * o2) for ln_linear_fwd: douts are do2 split like
+    the forward's outputs.  Returns (dx [m, k] bf16, dw [k, ncols] fp32,
+    dgamma [k] fp32, dbeta [k] fp32).  eps is unused (the saved rstd holds it)."""
+    m, k = x.shape
+    dev = x.device
+    cols = [int(d.shape[1]) for d in douts]
+    ncols = sum(cols)
+    _check("x", x, (m, k), torch.bfloat16, dev)
+    _check("gamma", gamma, (k,), torch.bfloat16, dev)
+    _check("beta", beta, (k,), torch.bfloat16, dev)
+    _check("w", w, (k, ncols), torch.bfloat16, dev)
+    _check("mean", mean, (m,), torch.float32, dev)
+    _check("rstd", rstd, (m,), torch.float32, dev)
+    for i, d in enumerate(douts):
+        _check(f"douts[{i}]", d, (m, cols[i]), torch.bfloat16, dev)
+    dx = torch.empty_like(x)
+    dw = torch.empty((k, ncols), dtype=torch.float32, device=dev)
+    dgamma = torch.empty(k, dtype=torch.float32, device=dev)
+    dbeta = torch.empty(k, dtype=torch.float32, device=dev)
+    need = tri_ln_linear_bwd_workspace_bytes(BF16, m, k, cols)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_ln_linear_bwd(BF16, m, k, cols, _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w),
+                           _ptr(mean), _ptr(rstd), [d.data_ptr() for d in douts], _ptr(dx),
+                           _ptr(dw), _ptr(dgamma), _ptr(dbeta), _ptr(workspace),
+                           workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_ln_linear_bwd")
+    return dx, dw, dgamma, dbeta

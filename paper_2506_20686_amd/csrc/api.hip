@@ -1,3 +1,4 @@
+#include <algorithm>
 // C ABI of the triangle-attention library: argument checks, workspace
 // layout and launch sequencing.  Every check runs before the first HIP call.
 #include <math.h>
@@ -227,24 +228,39 @@ int lnl_check(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, i
 
 size_t lnl_np(int64_t ncols) { return (size_t)((ncols + 31) / 32 * 32); }
 
+// Where each 32-column tile of o2 (or dO2) lives (see LnlTile).
+void lnl_tiles(int64_t m, int64_t ncols, int n_out, const int* start, triattn::bf16* const* ptrs,
+               triattn::LnlTile* tile) {
+  for (int t = 0; t < (int)((ncols + 31) / 32); ++t) {
+    const int col = 32 * t;
+    int i = 0;
+    while (i + 1 < n_out && col >= start[i + 1]) ++i;
+    triattn::LnlTile& e = tile[t];
+    e.base = ptrs[i];
+    e.off = col - start[i];
+    e.w = start[i + 1] - start[i];
+    e.fast = (e.off + 32 <= e.w && e.w % 8 == 0 && e.off % 8 == 0 &&
+              (uint64_t)(m + 32) * (uint64_t)e.w * 2u < ((uint64_t)1 << 32))
+                 ? 1
+                 : 0;
+  }
+}
+
+// Columns per column group of the forward: the fewest groups of at most
+// LNL_GROUP columns, balanced, in whole 32-column tiles.
+int lnl_group_width(int64_t ncols) {
+  const int64_t tiles = (int64_t)lnl_np(ncols) / 32;
+  const int64_t groups = (tiles * 32 + triattn::LNL_GROUP - 1) / triattn::LNL_GROUP;
+  return (int)((tiles + groups - 1) / groups * 32);
+}
+
 }  // namespace
 
 extern "C" {
 
-int tri_ln_linear_fwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
-                                      const int64_t* cols, size_t* bytes) {
-  int64_t ncols = 0;
-  const int st = lnl_check(dtype, m, k, n_out, cols, &ncols);
-  if (st != TRIATTN_OK) return st;
-  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
-  *bytes = round256(lnl_np(ncols) * triattn::LNL_K * sizeof(triattn::bf16));
-  return TRIATTN_OK;
-}
-
 int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols, float eps,
                       const void* x, const void* gamma, const void* beta, const void* w,
-                      void* const* outs, float* mean, float* rstd, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+                      void* const* outs, float* mean, float* rstd, void* stream) {
   int64_t ncols = 0;
   int st = lnl_check(dtype, m, k, n_out, cols, &ncols);
   if (st != TRIATTN_OK) return st;
@@ -254,14 +270,10 @@ int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t*
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
   for (int i = 0; i < n_out; ++i)
     if (outs[i] == nullptr || !aligned16(outs[i])) return TRIATTN_ERR_INVALID_ARG;
-  size_t need = 0;
-  tri_ln_linear_fwd_workspace_bytes(dtype, m, k, n_out, cols, &need);
-  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < need)
-    return TRIATTN_ERR_WORKSPACE;
   triattn::LnlArgs a{};
   a.m = m;
   a.ncols = (int)ncols;
-  a.np = (int)lnl_np(ncols);
+  a.gw = lnl_group_width(ncols);
   a.n_out = n_out;
   int64_t c = 0;
   for (int i = 0; i < n_out; ++i) {
@@ -276,9 +288,90 @@ int tri_ln_linear_fwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t*
   a.beta = (const triattn::bf16*)beta;
   a.mean = mean;
   a.rstd = rstd;
-  if (triattn::launch_lnl_fwd(a, (triattn::bf16*)workspace, (const triattn::bf16*)w,
-                              (hipStream_t)stream) != hipSuccess)
+  a.w = (const triattn::bf16*)w;
+  lnl_tiles(m, ncols, n_out, a.start, a.out, a.tile);
+  if (triattn::launch_lnl_fwd(a, (hipStream_t)stream) != hipSuccess)
     return TRIATTN_ERR_HIP;
+  return TRIATTN_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Extra limits of the backward: W stays resident in LDS (ncols <= the
+// column group) and every tensor's byte range fits a buffer resource.
+int lnl_bwd_check(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols,
+                  int64_t* ncols) {
+  const int st = lnl_check(dtype, m, k, n_out, cols, ncols);
+  if (st != TRIATTN_OK) return st;
+  if (*ncols > triattn::LNL_GROUP) return TRIATTN_ERR_UNSUPPORTED;
+  int64_t widest = triattn::LNL_K;
+  for (int i = 0; i < n_out; ++i) widest = std::max<int64_t>(widest, cols[i]);
+  if ((uint64_t)(m + 32) * (uint64_t)widest * 2u >= ((uint64_t)1 << 31))
+    return TRIATTN_ERR_UNSUPPORTED;
+  return TRIATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_ln_linear_bwd_workspace_bytes(int dtype, int64_t m, int64_t k, int n_out,
+                                      const int64_t* cols, size_t* bytes) {
+  int64_t ncols = 0;
+  const int st = lnl_bwd_check(dtype, m, k, n_out, cols, &ncols);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = round256(triattn::lnl_bwd_workspace(m, (int)lnl_np(ncols)));
+  return TRIATTN_OK;
+}
+
+int tri_ln_linear_bwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t* cols,
+                      const void* x, const void* gamma, const void* beta, const void* w,
+                      const float* mean, const float* rstd, const void* const* douts, void* dx,
+                      float* dw, float* dgamma, float* dbeta, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  int64_t ncols = 0;
+  int st = lnl_bwd_check(dtype, m, k, n_out, cols, &ncols);
+  if (st != TRIATTN_OK) return st;
+  if (douts == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {x, gamma, beta, w, mean, rstd, dx, dw, dgamma, dbeta};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  for (int i = 0; i < n_out; ++i)
+    if (douts[i] == nullptr || !aligned16(douts[i])) return TRIATTN_ERR_INVALID_ARG;
+  size_t need = 0;
+  tri_ln_linear_bwd_workspace_bytes(dtype, m, k, n_out, cols, &need);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < need)
+    return TRIATTN_ERR_WORKSPACE;
+  triattn::LnlBwdArgs a{};
+  a.m = m;
+  a.ncols = (int)ncols;
+  a.np = (int)lnl_np(ncols);
+  a.n_out = n_out;
+  int64_t c = 0;
+  for (int i = 0; i < n_out; ++i) {
+    a.start[i] = (int)c;
+    a.dout[i] = (const triattn::bf16*)douts[i];
+    c += cols[i];
+  }
+  for (int i = n_out; i <= triattn::LNL_MAX_OUT; ++i) a.start[i] = (int)ncols;
+  a.x = (const triattn::bf16*)x;
+  a.gamma = (const triattn::bf16*)gamma;
+  a.beta = (const triattn::bf16*)beta;
+  a.w = (const triattn::bf16*)w;
+  a.mean = mean;
+  a.rstd = rstd;
+  a.dx = (triattn::bf16*)dx;
+  a.dw = dw;
+  a.dgamma = dgamma;
+  a.dbeta = dbeta;
+  a.nwg = triattn::lnl_bwd_partials(m);
+  a.gpart = (float*)workspace;
+  a.gsum = a.gpart + (size_t)a.nwg * (triattn::LNL_K + 1) * a.np;
+  lnl_tiles(m, ncols, n_out, a.start, (triattn::bf16* const*)a.dout, a.tile);
+  if (triattn::launch_lnl_bwd(a, (hipStream_t)stream) != hipSuccess) return TRIATTN_ERR_HIP;
   return TRIATTN_OK;
 }
 

@@ -54,20 +54,62 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& w, co
 // ---- fused layer-norm + linear projection (lnl.hip) ---------------------------------
 constexpr int LNL_K = 128;       // features per row (the pair channel width)
 constexpr int LNL_MAX_OUT = 8;   // output tensors o2's columns are split into
+constexpr int LNL_MAX_TILES = 32;  // 32-column output tiles (N <= 1024)
+
+// Output columns one workgroup keeps resident in LDS as W^T (a launch covers
+// N in ceil(N / LNL_GROUP) column groups).
+constexpr int LNL_GROUP = 544;
+
+// Where 32-column output tile T goes.  fast: all 32 columns lie in one
+// output i, 16-byte aligned (w and off multiples of 8), and (m + 32) w 2
+// bytes fit a buffer resource; the tile is then stored with buffer stores
+// at base + ((row w + off + 8 c) 2) bytes, rows past m dropped by the
+// resource's range check.  Other tiles use the per-quad table.
+struct LnlTile {
+  bf16* base;  // out[i]
+  int off;     // first column of the tile inside output i
+  int w;       // width of output i
+  int fast;
+  int pad;
+};
 
 struct LnlArgs {
   int64_t m;                     // rows
   int ncols;                     // output columns N (sum of the outputs' widths)
-  int np;                        // N rounded up to a multiple of 32
+  int gw;                        // columns per workgroup group (multiple of 32)
   int n_out;                     // output tensors
   int start[LNL_MAX_OUT + 1];    // first column of each output; start[n_out] = N
   float eps;
   const bf16 *x, *gamma, *beta;  // x [m][K], gamma and beta [K]
-  const bf16* wt;                // W^T [np][K] (prepared in the workspace)
+  const bf16* w;                 // W [K][N]
   bf16* out[LNL_MAX_OUT];        // output i: [m][start[i + 1] - start[i]]
   float *mean, *rstd;            // [m], saved for the backward
+  LnlTile tile[LNL_MAX_TILES];
 };
 
-hipError_t launch_lnl_fwd(const LnlArgs& a, bf16* wt, const bf16* w, hipStream_t s);
+hipError_t launch_lnl_fwd(const LnlArgs& a, hipStream_t s);
+
+// Backward (N <= LNL_GROUP).  Row sums go through per-workgroup partial
+// slabs: gpart [nwg][K + 1][np] holds, per workgroup of the row-sum kernel,
+// G = xhat^T dO2 (rows 0..K-1) and s = column sums of dO2 (row K); gsum
+// [K + 1][np] their fixed-order totals.
+struct LnlBwdArgs {
+  int64_t m;
+  int ncols, np, n_out;
+  int start[LNL_MAX_OUT + 1];
+  const bf16 *x, *gamma, *beta, *w;  // forward inputs
+  const float *mean, *rstd;          // forward statistics
+  const bf16* dout[LNL_MAX_OUT];     // dO2 split like the forward's outputs
+  bf16* dx;                          // [m][K]
+  float *dw, *dgamma, *dbeta;        // [K][N], [K], [K]
+  float *gpart, *gsum;               // workspace
+  int nwg;                           // workgroups of the row-sum kernel
+  LnlTile tile[LNL_MAX_TILES];       // dO2 source of each 32-column tile
+};
+
+// Workgroups of the row-sum kernel and workspace bytes for m rows, np columns.
+int lnl_bwd_partials(int64_t m);
+size_t lnl_bwd_workspace(int64_t m, int np);
+hipError_t launch_lnl_bwd(const LnlBwdArgs& a, hipStream_t s);
 
 }  // namespace triattn

@@ -17,102 +17,693 @@
 //    each lane stores runs of four consecutive output columns of its row;
 //  - the backward's sums over rows (dW, dgamma, dbeta) go to per-block
 //    partial sums reduced in a fixed order instead of atomics.
+#include <algorithm>
+
+#include "dma.h"
 #include "kernels.h"
 #include "timing.h"
 
 namespace triattn {
 
 // ---- forward --------------------------------------------------------------------------
+//
+// Persistent workgroups of LNF_WAVES waves, one per CU.  W^T of the
+// workgroup's column group stays in LDS for the whole launch (read once per
+// workgroup); each wave walks 32-row units u = its global wave index + i *
+// (waves in the grid), prefetching the next unit's rows while the current
+// one is computed.
+//
+// LDS W^T: row n (an output column) is 256 bytes = 16 chunks of 8 features;
+// chunk c of row n sits at chunk slot c ^ (n % 16), so the A-fragment read
+// (32 consecutive rows, one chunk each) hits 8 distinct 16-byte bank groups
+// in every aligned run of 8 lanes.
+//
+// Output tiles (32 rows x 32 columns) pass through a 2 KB LDS tile per wave
+// so that each store instruction writes 16 rows x 64 contiguous bytes.
+// Tiles that lie inside one output (all but a narrow output such as the
+// bias logits) are stored with buffer stores whose range check drops the
+// rows past m, so their epilogue has no branches and the compiler can
+// interleave it with the next tile's MFMAs.
 
-// W [K][N] -> W^T [np][K] (rows n >= N are zero): the A operand of o2^T =
-// W^T o1^T reads 16 contiguous bytes of a W^T row per lane.
-__global__ __launch_bounds__(256) void lnl_wt_kernel(const bf16* w, int N, int np, bf16* wt) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)np * LNL_K) return;
-  const int n = (int)(idx / LNL_K), k = (int)(idx % LNL_K);
-  wt[idx] = n < N ? w[(int64_t)k * N + n] : (bf16)0.f;
+constexpr int LNF_WAVES = 8;
+constexpr int LNF_NT = LNL_K / 16;  // MFMA contraction steps over the features
+constexpr int LNF_TILES = LNL_GROUP / 32;
+
+// Output address of a run of 4 columns: p + row * w.  v8: the run and the
+// next 4 columns are one 16-byte aligned run of the same output.
+typedef __attribute__((address_space(1))) bf16 gbf16;  // global memory (not flat)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) u32x4 gu32x4;
+typedef __attribute__((address_space(1))) u32x2 gu32x2;
+struct LnlQuad {
+  gbf16* p;
+  int w;
+  int v8;
+};
+
+__device__ inline uint32_t lnf_wt_off(int n, int c) { return n * 256 + 16 * (c ^ (n & 15)); }
+
+// Byte offset of 16-byte chunk c (columns 8 c .. 8 c + 7) of row r of a
+// staged 32 x 32 bf16 tile (64-byte rows, chunks permuted by row pairs).
+__device__ inline uint32_t lnf_stage_off(int r, int c) { return r * 64 + 16 * (c ^ ((r >> 1) & 3)); }
+
+// One wave's 32 rows (lane <-> row m, half g holds features 16 t + 8 g .. + 7).
+// Rows past the end read the last row (their results are never stored), so
+// the loads are unconditional and the compiler can count them in its waits.
+__device__ inline void lnf_load_rows(const LnlArgs& a, int64_t m, int g, bf16x8 (&xr)[LNF_NT]) {
+  const bf16* p = a.x + (m < a.m ? m : a.m - 1) * LNL_K + 8 * g;
+#pragma unroll
+  for (int t = 0; t < LNF_NT; ++t) xr[t] = *(const bf16x8*)(p + 16 * t);
 }
 
-// One wave = 32 rows (lane <-> row, lane half g holds features 16 t + 8 g ..
-// + 7 for t = 0..7).  Workgroup = 4 waves = 128 rows.
-__global__ __launch_bounds__(256) void lnl_fwd_kernel(LnlArgs a) {
-  using M = Mma<bf16>;
+__device__ inline void lnf_load_a(bf16x8 (&af)[LNF_NT], const uint32_t (&aoff)[LNF_NT], int nt) {
+#pragma unroll
+  for (int t = 0; t < LNF_NT; ++t) af[t] = lds_load16<bf16x8>(aoff[t] + nt * 8192);
+}
+
+// One 32 x 32 output tile: o2^T[n][m] = sum_k W^T[n][k] o1[m][k].
+__device__ inline f32x16 lnf_tile(const bf16x8 (&af)[LNF_NT], const bf16x8 (&of)[LNF_NT]) {
+  f32x16 acc = {};
+#pragma unroll
+  for (int t = 0; t < LNF_NT; ++t) acc = Mma<bf16>::mma(af[t], of[t], acc);
+  return acc;
+}
+
+// Lane (row l32, half g) holds columns 8 j + 4 g + 0..3 of the tile in
+// acc[4 j ..]: write them to the wave's LDS tile, then read back chunk
+// lane % 4 of rows lane / 4 and lane / 4 + 16.
+__device__ inline void lnf_stage(const f32x16& acc, char* stage, int lane, u32x4 (&v)[2]) {
+  const int l32 = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bf16x4 x{(bf16)acc[4 * j], (bf16)acc[4 * j + 1], (bf16)acc[4 * j + 2],
+                   (bf16)acc[4 * j + 3]};
+    *(bf16x4*)(stage + lnf_stage_off(l32, j) + 8 * g) = x;
+  }
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr)
+    v[rr] = *(const u32x4*)(stage + lnf_stage_off((lane >> 2) + 16 * rr, lane & 3));
+}
+
+// Store a tile that lies inside one output (LnlTile::fast).
+__device__ inline void lnf_store_fast(const f32x16& acc, char* stage, const LnlTile& tl,
+                                      int lane, int64_t m0, int64_t m) {
+  u32x4 v[2];
+  lnf_stage(acc, stage, lane, v);
+  const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(tl.base, (short)0,
+                                                     (int)(uint32_t)(m * tl.w * 2), 0x00020000);
+  const uint32_t voff =
+      ((uint32_t)(m0 + (lane >> 2)) * (uint32_t)tl.w + (uint32_t)(tl.off + 8 * (lane & 3))) * 2u;
+  __builtin_amdgcn_raw_buffer_store_b128(v[0], r, voff, 0, 0);
+  __builtin_amdgcn_raw_buffer_store_b128(v[1], r, voff + 32u * (uint32_t)tl.w, 0, 0);
+}
+
+// Store any tile: each 16-byte chunk goes out as one 16-byte run or two
+// 8-byte runs per the quad table tq (the tile's 8 entries).
+__device__ inline void lnf_store_any(const f32x16& acc, char* stage, const LnlQuad* tq, int lane,
+                                     int64_t m0, int64_t mrows) {
+  u32x4 v[2];
+  lnf_stage(acc, stage, lane, v);
+  const int c = lane & 3;
+  const LnlQuad e0 = tq[2 * c], e1 = tq[2 * c + 1];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    const int64_t row = m0 + (lane >> 2) + 16 * rr;
+    if (row >= mrows || e0.p == nullptr) continue;
+    if (e0.v8) {
+      *(gu32x4*)(e0.p + row * e0.w) = v[rr];
+    } else {
+      *(gu32x2*)(e0.p + row * e0.w) = u32x2{v[rr][0], v[rr][1]};
+      if (e1.p != nullptr) *(gu32x2*)(e1.p + row * e1.w) = u32x2{v[rr][2], v[rr][3]};
+    }
+  }
+}
+
+__global__ __launch_bounds__(64 * LNF_WAVES) void lnl_fwd_kernel(LnlArgs a) {
+  __shared__ __align__(16) bf16 wt[LNL_GROUP * LNL_K];  // W^T of the group
+  __shared__ __align__(16) LnlQuad quad[LNL_GROUP / 4];
+  __shared__ __align__(16) bf16 gb[2][LNL_K];           // gamma, beta
+  __shared__ __align__(16) char stage[LNF_WAVES][32 * 64];
+  __shared__ int order[LNF_TILES];                        // fast tiles first
+  __shared__ int nfast_s;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = tid >> 6;
-  const int64_t m = (int64_t)blockIdx.x * 128 + wave * 32 + l32;
-  const bool mok = m < a.m;
-  constexpr int NT = LNL_K / 16;  // MFMA contraction steps over the features
+  const int c0 = blockIdx.y * a.gw;
+  const int gn = min(a.gw, a.ncols - c0);  // columns of this group
+  const int gnp = (gn + 31) & ~31;
+  const int nq = gnp / 4;
+  const int ntiles = gnp / 32;
 
-  bf16x8 xr[NT];
+  // W^T of the group (columns past the group are zero): all loads first
+  {
+    constexpr int NT = 64 * LNF_WAVES;
+    constexpr int FILL = (LNL_K * (LNL_GROUP / 4) + NT - 1) / NT;
+    bf16x4 wv[FILL];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
-    xr[t] = mok ? *(const bf16x8*)(a.x + m * LNL_K + 16 * t + 8 * g) : bf16x8{};
-  // row statistics: this lane's 64 features, then the other half (lane ^ 32)
-  float s = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) s += (float)xr[t][e];
-  const float mean = wave_xor32_sum(s) * (1.f / LNL_K);
-  float v = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float c = (float)xr[t][e] - mean;
-      v += c * c;
+    for (int i = 0; i < FILL; ++i) {
+      const int idx = tid + i * NT, k = idx / nq, n = 4 * (idx - k * nq);
+      wv[i] = (idx < LNL_K * nq && n < gn) ? *(const bf16x4*)(a.w + (int64_t)k * a.ncols + c0 + n)
+                                           : bf16x4{};
     }
-  const float var = wave_xor32_sum(v) * (1.f / LNL_K);
-  const float rstd = 1.f / sqrtf(var + a.eps);
-  if (mok && g == 0) {
-    a.mean[m] = mean;
-    a.rstd[m] = rstd;
+#pragma unroll
+    for (int i = 0; i < FILL; ++i) {
+      const int idx = tid + i * NT, k = idx / nq, n = 4 * (idx - k * nq);
+      if (idx < LNL_K * nq) {
+        char* base = (char*)wt + 2 * (k & 7);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) *(bf16*)(base + lnf_wt_off(n + e, k >> 3)) = wv[i][e];
+      }
+    }
   }
-  // o1 = xhat gamma + beta as the B operand (contraction over the features)
-  bf16x8 of[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const bf16x8 gm = *(const bf16x8*)(a.gamma + 16 * t + 8 * g);
-    const bf16x8 bt = *(const bf16x8*)(a.beta + 16 * t + 8 * g);
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      of[t][e] = (bf16)(((float)xr[t][e] - mean) * rstd * (float)gm[e] + (float)bt[e]);
-  }
-
-  // output tiles of 32 columns: o2^T tile = W^T rows x o1^T
-  for (int nt = 0; nt < a.np / 32; ++nt) {
-    const bf16* wrow = a.wt + (int64_t)(nt * 32 + l32) * LNL_K + 8 * g;
-    f32x16 acc = {};
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc = M::mma(*(const bf16x8*)(wrow + 16 * t), of[t], acc);
-    if (!mok) continue;
-    // lane (row m, half g) holds columns nt 32 + 8 j + 4 g + 0..3
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = nt * 32 + 8 * j + 4 * g;
-      if (col >= a.ncols) break;
+  // output address of every run of 4 columns of the group
+  for (int q = tid; q < nq; q += 64 * LNF_WAVES) {
+    LnlQuad e{nullptr, 0, 0};
+    if (4 * q < gn) {
+      const int col = c0 + 4 * q;
       int i = 0;
+      while (i + 1 < a.n_out && col >= a.start[i + 1]) ++i;
+      const int w = a.start[i + 1] - a.start[i], off = col - a.start[i];
+      e.p = (gbf16*)(a.out[i] + off);
+      e.w = w;
+      e.v8 = (w % 8 == 0 && off % 8 == 0) ? 1 : 0;
+    }
+    quad[q] = e;
+  }
+  if (tid < LNL_K) {
+    gb[0][tid] = a.gamma[tid];
+    gb[1][tid] = a.beta[tid];
+  }
+  if (tid == 0) {
+    int nf = 0;
+    for (int nt = 0; nt < ntiles; ++nt)
+      if (a.tile[c0 / 32 + nt].fast) order[nf++] = nt;
+    int k = nf;
+    for (int nt = 0; nt < ntiles; ++nt)
+      if (!a.tile[c0 / 32 + nt].fast) order[k++] = nt;
+    nfast_s = nf;
+  }
+  __syncthreads();
+
+  uint32_t aoff[LNF_NT];
 #pragma unroll
-      for (int u = 1; u < LNL_MAX_OUT; ++u) i += (u < a.n_out && col >= a.start[u]) ? 1 : 0;
-      const int w = a.start[i + 1] - a.start[i];
-      store4(a.out[i] + m * w + (col - a.start[i]),
-             f32x4{acc[4 * j], acc[4 * j + 1], acc[4 * j + 2], acc[4 * j + 3]});
+  for (int t = 0; t < LNF_NT; ++t) aoff[t] = lds_addr(wt) + lnf_wt_off(l32, 2 * t + g);
+  char* st = stage[wave];
+  const int nfast = nfast_s;
+  const bool stats_out = blockIdx.y == 0;
+  const int64_t units = (a.m + 31) / 32;
+  const int64_t stride = (int64_t)gridDim.x * LNF_WAVES;
+  int64_t u = (int64_t)blockIdx.x * LNF_WAVES + wave;
+  bf16x8 xr[LNF_NT];
+  lnf_load_rows(a, u * 32 + l32, g, xr);
+  // tile id (uniform) of position i of the order
+  auto tile_at = [&](int i) { return __builtin_amdgcn_readfirstlane(order[i]); };
+
+  for (; u < units; u += stride) {
+    // gamma and beta are re-read from LDS per unit rather than held in registers
+    asm volatile("" ::: "memory");
+    const int64_t m0 = u * 32, m = m0 + l32;
+    // row statistics: this lane's 64 features, then the other half (lane ^ 32);
+    // two passes over the registers (mean, then the centred sum of squares)
+    float xv[LNF_NT][8];
+    float s = 0.f;
+#pragma unroll
+    for (int t = 0; t < LNF_NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        xv[t][e] = (float)xr[t][e];
+        s += xv[t][e];
+      }
+    const float mean = wave_xor32_sum(s) * (1.f / LNL_K);
+    float v = 0.f;
+#pragma unroll
+    for (int t = 0; t < LNF_NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        xv[t][e] -= mean;
+        v = fmaf(xv[t][e], xv[t][e], v);
+      }
+    const float var = wave_xor32_sum(v) * (1.f / LNL_K);
+    const float rstd = 1.f / sqrtf(var + a.eps);
+    if (stats_out && m < a.m && g == 0) {
+      a.mean[m] = mean;
+      a.rstd[m] = rstd;
+    }
+    // o1 = xhat gamma + beta as the B operand (contraction over the features)
+    bf16x8 of[LNF_NT];
+#pragma unroll
+    for (int t = 0; t < LNF_NT; ++t) {
+      const bf16x8 gm = *(const bf16x8*)(&gb[0][16 * t + 8 * g]);
+      const bf16x8 bt = *(const bf16x8*)(&gb[1][16 * t + 8 * g]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) of[t][e] = (bf16)fmaf(xv[t][e] * rstd, (float)gm[e], (float)bt[e]);
+    }
+    lnf_load_rows(a, (u + stride) * 32 + l32, g, xr);  // next unit
+
+    // Tiles inside one output: the MFMAs of the next tile are issued before
+    // this one is stored (positions past the last are clamped; their results
+    // are unused), and two accumulators alternate so no tile is copied.
+    bf16x8 af[LNF_NT];
+    if (nfast > 0) {
+      const int last = nfast - 1;
+      int t0 = tile_at(0);
+      lnf_load_a(af, aoff, t0);
+      f32x16 acc0 = lnf_tile(af, of), acc1;
+      int t1 = tile_at(min(1, last));
+      lnf_load_a(af, aoff, t1);
+      for (int i = 0; i < nfast; i += 2) {
+        acc1 = lnf_tile(af, of);
+        const int t2 = tile_at(min(i + 2, last));
+        lnf_load_a(af, aoff, t2);
+        lnf_store_fast(acc0, st, a.tile[c0 / 32 + t0], lane, m0, a.m);
+        if (i + 1 >= nfast) break;
+        acc0 = lnf_tile(af, of);
+        const int t3 = tile_at(min(i + 3, last));
+        lnf_load_a(af, aoff, t3);
+        lnf_store_fast(acc1, st, a.tile[c0 / 32 + t1], lane, m0, a.m);
+        t0 = t2;
+        t1 = t3;
+      }
+    }
+    // the other tiles
+    for (int i = nfast; i < ntiles; ++i) {
+      const int t = tile_at(i);
+      lnf_load_a(af, aoff, t);
+      const f32x16 acc = lnf_tile(af, of);
+      lnf_store_any(acc, st, quad + t * 8, lane, m0, a.m);
     }
   }
 }
 
-hipError_t launch_lnl_fwd(const LnlArgs& a, bf16* wt, const bf16* w, hipStream_t s) {
-  {
-    KernelTimer t(K_LNL_PREP, s);
-    const int64_t nw = (int64_t)a.np * LNL_K;
-    hipLaunchKernelGGL(lnl_wt_kernel, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s, w,
-                       a.ncols, a.np, wt);
+hipError_t launch_lnl_fwd(const LnlArgs& a, hipStream_t s) {
+  const int groups = (a.ncols + a.gw - 1) / a.gw;
+  const int64_t units = (a.m + 31) / 32;
+  const int64_t per_group = std::max<int64_t>(1, 256 / groups);
+  const int nwg = (int)std::min<int64_t>(per_group, (units + LNF_WAVES - 1) / LNF_WAVES);
+  KernelTimer t(K_LNL_FWD, s);
+  hipLaunchKernelGGL(lnl_fwd_kernel, dim3((unsigned)nwg, (unsigned)groups), dim3(64 * LNF_WAVES),
+                     0, s, a);
+  return hipGetLastError();
+}
+
+// ---- backward -------------------------------------------------------------------------
+//
+// Per row (appendix table of fused operators):  do1 = dO2 W^T,
+//   wdy = do1 gamma,  c1 = sum_k xhat wdy / K,  c2 = sum_k wdy / K,
+//   dx = rstd (wdy - c1 xhat - c2).
+// The sums over rows are regrouped so that they all come from one pass over
+// dO2 and x:  G = xhat^T dO2 [K][N] and s = sum_m dO2 [N] give
+//   dW = o1^T dO2 = gamma G + beta s^T,  dgamma = sum_n W G,  dbeta = W s.
+// Kernels: lnl_bwd_dx (dx), lnl_bwd_g (G and s per workgroup, partial
+// slabs), lnl_reduce (the slabs summed in a fixed order), lnl_finish (dW,
+// dgamma, dbeta).
+
+// lnl_bwd_dx: persistent workgroups of LBX_WAVES waves, W resident in LDS as
+// rows k of 16-byte chunks of 8 columns (chunk c of row k at slot c ^ (k % 8),
+// 72 chunk slots per row), each wave walking 32-row units.  do1^T tiles
+// [32 k][32 m] = W rows x dO2 rows^T: the dO2 B fragments (lane <-> row m,
+// 8 consecutive columns) come straight from HBM, D steps ahead.
+constexpr int LBX_WAVES = 8;
+constexpr int LBX_PITCH = 72 * 16;
+constexpr int LBX_AHEAD = 4;  // dO2 fragments in flight per lane
+
+__device__ inline uint32_t lbx_w_off(int k, int c) { return k * LBX_PITCH + 16 * (c ^ (k & 7)); }
+
+// dO2 fragment of 16-column step s for row m: columns 16 s + 8 g .. + 7.
+__device__ inline bf16x8 lbx_load_b(const LnlBwdArgs& a, const LnlQuad* quad, int s, int g,
+                                    int64_t m) {
+  const LnlTile& tl = a.tile[s >> 1];
+  if (tl.fast) {
+    const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(tl.base, (short)0,
+                                                       (int)(uint32_t)(a.m * tl.w * 2), 0x00020000);
+    const uint32_t voff = ((uint32_t)m * (uint32_t)tl.w + (uint32_t)(tl.off + 16 * (s & 1) + 8 * g)) * 2u;
+    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
   }
-  LnlArgs b = a;
-  b.wt = wt;
+  const int q = 2 * (2 * s + g);
+  const LnlQuad e0 = quad[q], e1 = quad[q + 1];
+  const bool ok = m < a.m;
+  const u32x2 lo = (ok && e0.p) ? *(const gu32x2*)(e0.p + m * e0.w) : u32x2{0u, 0u};
+  const u32x2 hi = (ok && e1.p) ? *(const gu32x2*)(e1.p + m * e1.w) : u32x2{0u, 0u};
+  return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+}
+
+// Output address table of the dO2 slices (as the forward's, for reading).
+__device__ inline void lnl_quad_table(const int* start, int n_out, bf16* const* ptrs, int ncols,
+                                      int nq, LnlQuad* quad, int tid, int nthreads) {
+  for (int q = tid; q < nq; q += nthreads) {
+    LnlQuad e{nullptr, 0, 0};
+    const int col = 4 * q;
+    if (col < ncols) {
+      int i = 0;
+      while (i + 1 < n_out && col >= start[i + 1]) ++i;
+      const int w = start[i + 1] - start[i], off = col - start[i];
+      e.p = (gbf16*)(ptrs[i] + off);
+      e.w = w;
+      e.v8 = (w % 8 == 0 && off % 8 == 0) ? 1 : 0;
+    }
+    quad[q] = e;
+  }
+}
+
+__global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a) {
+  __shared__ __align__(16) char wk[LNL_K * LBX_PITCH];
+  __shared__ __align__(16) LnlQuad quad[LNL_GROUP / 4];
+  __shared__ __align__(16) float gam[LNL_K];
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int wave = tid >> 6;
+  const int nq = a.np / 4;
+  {  // W [K][N] into LDS (columns past N zero): all loads first
+    constexpr int NT = 64 * LBX_WAVES;
+    constexpr int FILL = (LNL_K * (LNL_GROUP / 4) + NT - 1) / NT;
+    u32x2 wv[FILL];
+#pragma unroll
+    for (int i = 0; i < FILL; ++i) {
+      const int idx = tid + i * NT, k = idx / nq, q = idx - k * nq;
+      wv[i] = (idx < LNL_K * nq && 4 * q < a.ncols)
+                  ? *(const u32x2*)(a.w + (int64_t)k * a.ncols + 4 * q)
+                  : u32x2{0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < FILL; ++i) {
+      const int idx = tid + i * NT, k = idx / nq, q = idx - k * nq;
+      if (idx < LNL_K * nq) *(u32x2*)(wk + lbx_w_off(k, q >> 1) + 8 * (q & 1)) = wv[i];
+    }
+  }
+  lnl_quad_table(a.start, a.n_out, (bf16* const*)a.dout, a.ncols, nq, quad, tid, 64 * LBX_WAVES);
+  if (tid < LNL_K) gam[tid] = (float)a.gamma[tid];
+  __syncthreads();
+
+  // A fragment of (k tile kt, step s): lane row k = 32 kt + l32, chunk
+  // 2 s + g = 8 (s / 4) + (2 (s % 4) + g)  ->  ao[s % 4] + kt * 32 rows + 128 (s / 4)
+  uint32_t ao[4];
+#pragma unroll
+  for (int s4 = 0; s4 < 4; ++s4) ao[s4] = lds_addr(wk) + lbx_w_off(l32, 2 * s4 + g);
+  const int nsteps = a.np / 16;
+  const int64_t units = (a.m + 31) / 32;
+  const int64_t stride = (int64_t)gridDim.x * LBX_WAVES;
+  for (int64_t u = (int64_t)blockIdx.x * LBX_WAVES + wave; u < units; u += stride) {
+    const int64_t m = u * 32 + l32;
+    const bool mok = m < a.m;
+    // this row's x at k = 32 kt + 8 j + 4 g + 0..3 and its statistics (for the epilogue)
+    u32x2 xq[16];
+#pragma unroll
+    for (int f = 0; f < 16; ++f)
+      xq[f] = mok ? *(const u32x2*)(a.x + m * LNL_K + 8 * f + 4 * g) : u32x2{0u, 0u};
+    const float mean = mok ? a.mean[m] : 0.f, rstd = mok ? a.rstd[m] : 0.f;
+
+    f32x16 acc[4] = {};
+    bf16x8 bq[LBX_AHEAD];
+#pragma unroll
+    for (int d = 0; d < LBX_AHEAD; ++d) bq[d] = d < nsteps ? lbx_load_b(a, quad, d, g, m) : bf16x8{};
+    for (int s0 = 0; s0 < nsteps; s0 += LBX_AHEAD) {
+#pragma unroll
+      for (int d = 0; d < LBX_AHEAD; ++d) {
+        const int s = s0 + d;
+        if (s < nsteps) {
+          const uint32_t ad = ao[d] + 128 * (s >> 2);
+          const bf16x8 b = bq[d];
+          if (s + LBX_AHEAD < nsteps) bq[d] = lbx_load_b(a, quad, s + LBX_AHEAD, g, m);
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+            acc[kt] = Mma<bf16>::mma(lds_load16<bf16x8>(ad + kt * 32 * LBX_PITCH), b, acc[kt]);
+        }
+      }
+    }
+    // lane (row m, half g) holds do1[m][32 kt + 8 j + 4 g + i] in acc[kt][4 j + i]
+    float c1 = 0.f, c2 = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x4 xv = __builtin_bit_cast(bf16x4, xq[4 * kt + j]);
+        const f32x4 gm = *(const f32x4*)(gam + 32 * kt + 8 * j + 4 * g);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float xh = ((float)xv[i] - mean) * rstd;
+          const float wdy = acc[kt][4 * j + i] * gm[i];
+          c1 = fmaf(xh, wdy, c1);
+          c2 += wdy;
+        }
+      }
+    c1 = wave_xor32_sum(c1) * (1.f / LNL_K);
+    c2 = wave_xor32_sum(c2) * (1.f / LNL_K);
+    if (mok) {
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const bf16x4 xv = __builtin_bit_cast(bf16x4, xq[4 * kt + j]);
+          const f32x4 gm = *(const f32x4*)(gam + 32 * kt + 8 * j + 4 * g);
+          f32x4 d;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float xh = ((float)xv[i] - mean) * rstd;
+            d[i] = rstd * (acc[kt][4 * j + i] * gm[i] - c1 * xh - c2);
+          }
+          store4(a.dx + m * LNL_K + 32 * kt + 8 * j + 4 * g, d);
+        }
+    }
+  }
+}
+
+// lnl_bwd_g: persistent workgroups of LBG_WAVES waves; each workgroup walks
+// 32-row units u = blockIdx + i * gridDim, staging the unit's x, mean, rstd
+// and dO2 rows in LDS with buffer-resource DMA one unit ahead (double
+// buffered; rows past m read as zeros).  Wave w accumulates the G tiles
+// (k tile w % 4, column tiles w / 4 + 2 i) over all its units in registers:
+// A = xhat^T (transposed x reads, normalised in registers), B = dO2
+// (transposed reads), contraction over the unit's 32 rows.  The waves of k
+// tile 0 also sum the B fragments into s.  At the end each workgroup writes
+// its slab of gpart.
+constexpr int LBG_WAVES = 8;
+constexpr int LBG_SLOT = 56 * 1024;  // staged bytes per unit (x 8 KB, mean, rstd, dO2, zeros)
+constexpr int LBG_ZERO = LBG_SLOT - 64;
+constexpr int LBG_MAXOPS = 64;
+constexpr int LBG_TPW = (LNL_GROUP / 32 + 1) / 2;  // column tiles per wave (at most)
+
+struct LbgOp {
+  const char* src;    // tensor base
+  uint32_t rowbytes;  // bytes per row of the tensor
+  uint32_t voff;      // byte offset of this 1 KB piece inside the unit's rows
+  uint32_t lds;       // destination offset inside a slot
+  uint32_t nbytes;    // bytes of the tensor (range of the buffer resource)
+};
+
+__global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a) {
+  __shared__ __align__(16) char stage[2 * LBG_SLOT];
+  __shared__ LbgOp ops[LBG_MAXOPS];
+  __shared__ uint32_t qoff[LNL_GROUP / 4];  // per 4 columns: offset in a slot of row 0
+  __shared__ uint32_t qpitch[LNL_GROUP / 4];
+  __shared__ int nops_s;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
+  const int wave = tid >> 6;
+  const int nq = a.np / 4, ntiles = a.np / 32;
+  const uint32_t mb = (uint32_t)a.m;  // rows fit 32 bits (checked by the caller)
+  if (tid == 0) {
+    int no = 0;
+    uint32_t lds = 0;
+    for (int j = 0; j < 8; ++j)
+      ops[no++] = LbgOp{(const char*)a.x, 2 * LNL_K, 1024u * j, lds + 1024u * j, mb * 2 * LNL_K};
+    lds += 8192;
+    ops[no++] = LbgOp{(const char*)a.mean, 4, 0, lds, mb * 4};
+    ops[no++] = LbgOp{(const char*)a.rstd, 4, 0, lds + 1024, mb * 4};
+    lds += 2048;
+    int region[LNL_MAX_OUT];
+    for (int i = 0; i < a.n_out; ++i) {
+      const uint32_t w = a.start[i + 1] - a.start[i], bytes = 64 * w, nop = (bytes + 1023) / 1024;
+      region[i] = lds;
+      for (uint32_t j = 0; j < nop; ++j)
+        ops[no++] = LbgOp{(const char*)a.dout[i], 2 * w, 1024u * j, lds + 1024u * j, mb * 2 * w};
+      lds += 1024 * nop;
+    }
+    for (int q = 0; q < nq; ++q) {
+      const int col = 4 * q;
+      if (col < a.ncols) {
+        int i = 0;
+        while (i + 1 < a.n_out && col >= a.start[i + 1]) ++i;
+        qoff[q] = region[i] + 2 * (col - a.start[i]);
+        qpitch[q] = 2 * (a.start[i + 1] - a.start[i]);
+      } else {
+        qoff[q] = LBG_ZERO;
+        qpitch[q] = 0;
+      }
+    }
+    nops_s = no;
+  }
+  if (tid < 32) *(uint32_t*)(stage + LBG_ZERO + 4 * (tid & 15) + ((tid >> 4) ? LBG_SLOT : 0)) = 0u;
+  __syncthreads();
+  const int nops = nops_s;
+
+  // this wave's tiles
+  const int kt = wave & 3, t0 = wave >> 2;
+  const int nt_w = t0 < ntiles ? (ntiles - t0 + 1) / 2 : 0;
+  // transposed-read addresses: lane supplies position pe (+ p0) and columns
+  // 16 (G % 2) + 4 j of its tile (TrAddr's pattern over row-major rows)
+  const int G = lane >> 4, jj = lane & 3, pe = ((lane & 15) >> 2) + 4 * (G >> 1);
+  const int cq = 4 * (G & 1) + jj;  // quad of the tile this lane supplies
+  const uint32_t sbase = lds_addr(stage);
+  const uint32_t xa = sbase + pe * 256 + 2 * (32 * kt + 4 * cq);
+  uint32_t ba[LBG_TPW], bp[LBG_TPW];
+#pragma unroll
+  for (int i = 0; i < LBG_TPW; ++i) {
+    const int T = t0 + 2 * i, q = T < ntiles ? 8 * T + cq : 0;
+    bp[i] = qpitch[q];
+    ba[i] = sbase + qoff[q] + pe * bp[i];
+  }
+  const uint32_t sa = sbase + 8192;  // mean (+ 1024: rstd)
+
+  f32x16 acc[LBG_TPW] = {};
+  float ssum[LBG_TPW] = {};
+  const int64_t units = (a.m + 31) / 32;
+  auto issue = [&](int64_t u, int slot) {
+    for (int o = wave; o < nops; o += LBG_WAVES) {
+      const LbgOp op = ops[o];
+      const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(op.src), (short)0,
+                                                         (int)op.nbytes, 0x00020000);
+      const uint32_t voff = (uint32_t)u * 32u * op.rowbytes + op.voff + 16u * lane;
+      dma16b(r, voff, stage + slot * LBG_SLOT + op.lds);
+    }
+  };
+  int64_t u = blockIdx.x;
+  if (u < units) issue(u, 0);
+  for (int it = 0; u < units; ++it, u += gridDim.x) {
+    const int slot = it & 1;
+    wait_vm<0>();
+    lds_barrier();
+    if (u + gridDim.x < units) issue(u + gridDim.x, slot ^ 1);
+    const uint32_t so = slot * LBG_SLOT;
+    // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
+    // channels 32 kt + l32, normalised with those positions' statistics
+    s16x4 xr[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xr[q] = ds_read_tr<0>(xa + so + 8 * q * 256);
+    tr_wait(xr);
+    bf16x8 af[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const bf16x8 xv = tr_frag(xr, h);
+      const f32x4 m0 = *(const f32x4*)(stage + (sa - sbase) + so + 4 * (16 * h + 4 * g));
+      const f32x4 m1 = *(const f32x4*)(stage + (sa - sbase) + so + 4 * (16 * h + 8 + 4 * g));
+      const f32x4 r0 = *(const f32x4*)(stage + (sa - sbase) + so + 1024 + 4 * (16 * h + 4 * g));
+      const f32x4 r1 =
+          *(const f32x4*)(stage + (sa - sbase) + so + 1024 + 4 * (16 * h + 8 + 4 * g));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        af[h][e] = (bf16)(((float)xv[e] - m0[e]) * r0[e]);
+        af[h][4 + e] = (bf16)(((float)xv[4 + e] - m1[e]) * r1[e]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LBG_TPW; ++i) {
+      if (i < nt_w) {
+        s16x4 br[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) br[q] = ds_read_tr<0>(ba[i] + so + 8 * q * bp[i]);
+        tr_wait(br);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const bf16x8 bf = tr_frag(br, h);
+          acc[i] = Mma<bf16>::mma(af[h], bf, acc[i]);
+          if (kt == 0)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ssum[i] += (float)bf[e];
+        }
+      }
+    }
+  }
+  // this workgroup's slab: G rows k = 32 kt + 8 j + 4 g + i, column 32 T + l32
+  float* slab = a.gpart + (int64_t)blockIdx.x * (LNL_K + 1) * a.np;
+  const int l32 = lane & 31;
+#pragma unroll
+  for (int i = 0; i < LBG_TPW; ++i) {
+    if (i < nt_w) {
+      const int n = 32 * (t0 + 2 * i) + l32;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) slab[(int64_t)(32 * kt + acc_row(v, g)) * a.np + n] = acc[i][v];
+      if (kt == 0) {
+        const float st = wave_xor32_sum(ssum[i]);
+        if (g == 0) slab[(int64_t)LNL_K * a.np + n] = st;
+      }
+    }
+  }
+}
+
+// gsum[r][n] = sum over workgroups p (in order p = c, c + 8, ..., then the 8
+// chains c = 0..7 in order) of gpart[p][r][n]; one workgroup per (row r,
+// 128 columns).
+__global__ __launch_bounds__(256) void lnl_reduce_kernel(LnlBwdArgs a) {
+  __shared__ f32x4 red[8][32];
+  const int r = blockIdx.y, t = threadIdx.x, n4 = t & 31, c = t >> 5;
+  const int n = blockIdx.x * 128 + 4 * n4;
+  f32x4 s = {};
+  if (n < a.np)
+    for (int p = c; p < a.nwg; p += 8)
+      s += *(const f32x4*)(a.gpart + ((int64_t)p * (LNL_K + 1) + r) * a.np + n);
+  red[c][n4] = s;
+  __syncthreads();
+  if (t < 32 && n < a.np) {
+    f32x4 tot = red[0][t];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) tot += red[i][t];
+    *(f32x4*)(a.gsum + (int64_t)r * a.np + n) = tot;
+  }
+}
+
+// dW[k][n] = gamma_k G[k][n] + beta_k s[n];  dgamma[k] = sum_n W[k][n] G[k][n];
+// dbeta[k] = sum_n W[k][n] s[n]  (per-thread partials, then a fixed tree).
+__global__ __launch_bounds__(256) void lnl_finish_kernel(LnlBwdArgs a) {
+  __shared__ float rg[256], rb[256];
+  const int k = blockIdx.x, t = threadIdx.x;
+  const float gk = (float)a.gamma[k], bk = (float)a.beta[k];
+  const float* G = a.gsum + (int64_t)k * a.np;
+  const float* S = a.gsum + (int64_t)LNL_K * a.np;
+  float pg = 0.f, pb = 0.f;
+  for (int n = t; n < a.ncols; n += 256) {
+    const float gv = G[n], sv = S[n], wv = (float)a.w[(int64_t)k * a.ncols + n];
+    a.dw[(int64_t)k * a.ncols + n] = fmaf(gk, gv, bk * sv);
+    pg = fmaf(wv, gv, pg);
+    pb = fmaf(wv, sv, pb);
+  }
+  rg[t] = pg;
+  rb[t] = pb;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (t < h) {
+      rg[t] += rg[t + h];
+      rb[t] += rb[t + h];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    a.dgamma[k] = rg[0];
+    a.dbeta[k] = rb[0];
+  }
+}
+
+int lnl_bwd_partials(int64_t m) { return (int)std::min<int64_t>(256, (m + 31) / 32); }
+
+size_t lnl_bwd_workspace(int64_t m, int np) {
+  const size_t slab = (size_t)(LNL_K + 1) * np * sizeof(float);
+  return (size_t)lnl_bwd_partials(m) * slab + slab;
+}
+
+hipError_t launch_lnl_bwd(const LnlBwdArgs& a, hipStream_t s) {
+  const int64_t units = (a.m + 31) / 32;
   {
-    KernelTimer t(K_LNL_FWD, s);
-    hipLaunchKernelGGL(lnl_fwd_kernel, dim3((unsigned)((a.m + 127) / 128)), dim3(256), 0, s, b);
+    KernelTimer t(K_LNL_BWD_DX, s);
+    const int nwg = (int)std::min<int64_t>(256, (units + LBX_WAVES - 1) / LBX_WAVES);
+    hipLaunchKernelGGL(lnl_bwd_dx_kernel, dim3(nwg), dim3(64 * LBX_WAVES), 0, s, a);
+  }
+  {
+    KernelTimer t(K_LNL_BWD_G, s);
+    hipLaunchKernelGGL(lnl_bwd_g_kernel, dim3(a.nwg), dim3(64 * LBG_WAVES), 0, s, a);
+  }
+  {
+    KernelTimer t(K_LNL_REDUCE, s);
+    hipLaunchKernelGGL(lnl_reduce_kernel, dim3((a.np + 127) / 128, LNL_K + 1), dim3(256), 0, s, a);
+  }
+  {
+    KernelTimer t(K_LNL_FINISH, s);
+    hipLaunchKernelGGL(lnl_finish_kernel, dim3(LNL_K), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

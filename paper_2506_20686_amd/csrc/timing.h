@@ -16,11 +16,11 @@ enum KernelId {
   K_DKDV,
   K_DB,
   K_DB_REDUCE,
-  K_LNL_PREP,
   K_LNL_FWD,
   K_LNL_BWD_DX,
-  K_LNL_BWD_DW,
+  K_LNL_BWD_G,
   K_LNL_REDUCE,
+  K_LNL_FINISH,
   K_COUNT
 };
 

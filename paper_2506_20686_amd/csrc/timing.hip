@@ -14,8 +14,8 @@ namespace {
 
 const char* const kNames[K_COUNT] = {"prep_bias",   "prep_kbits", "fwd",        "bwd_prep",
                                      "bwd_pad",     "dq",         "dkdv",       "db",
-                                     "db_reduce",   "lnl_prep",   "lnl_fwd",    "lnl_bwd_dx",
-                                     "lnl_bwd_dw",  "lnl_reduce"};
+                                     "db_reduce",   "lnl_fwd",    "lnl_bwd_dx",
+                                     "lnl_bwd_g",   "lnl_reduce", "lnl_finish"};
 
 struct Pending {
   int id;

@@ -148,20 +148,12 @@ COLS = [128, 128, 128, 128, 4]
 
 def lnl_args(**over):
     a = dict(dtype=B.BF16, m=1000, k=128, cols=COLS, eps=1e-5, x=P, gamma=P, beta=P, w=P,
-             outs=[P] * len(over.get("cols", COLS)), mean=P, rstd=P, ws=P, wsb=1 << 30,
-             stream=None)
+             outs=[P] * len(over.get("cols", COLS)), mean=P, rstd=P, stream=None)
     a.update(over)
     cols = (ctypes.c_int64 * len(a["cols"]))(*a["cols"])
     outs = None if a["outs"] is None else (ctypes.c_void_p * len(a["outs"]))(*a["outs"])
     return (a["dtype"], a["m"], a["k"], len(a["cols"]), cols, a["eps"], a["x"], a["gamma"],
-            a["beta"], a["w"], outs, a["mean"], a["rstd"], a["ws"], a["wsb"], a["stream"])
-
-
-def test_ln_linear_workspace_size(lib):
-    for cols in ([128], [4], COLS, [512, 512]):
-        got = B.tri_ln_linear_fwd_workspace_bytes(B.BF16, 5000, 128, cols)
-        np_ = (sum(cols) + 31) // 32 * 32
-        assert got >= np_ * 128 * 2
+            a["beta"], a["w"], outs, a["mean"], a["rstd"], a["stream"])
 
 
 LNL_BAD = [
@@ -176,10 +168,49 @@ LNL_BAD = [
     (dict(rstd=P + 4), B.ERR_INVALID_ARG), (dict(outs=None), B.ERR_INVALID_ARG),
     (dict(outs=[P, P, None, P, P]), B.ERR_INVALID_ARG),
     (dict(outs=[P, P, P, P, P + 8]), B.ERR_INVALID_ARG),
-    (dict(ws=None), B.ERR_WORKSPACE), (dict(wsb=100), B.ERR_WORKSPACE),
 ]
 
 
 @pytest.mark.parametrize("over,code", LNL_BAD)
 def test_ln_linear_fwd_rejects_before_any_hip_call(lib, over, code):
     assert lib.tri_ln_linear_fwd(*lnl_args(**over)) == code
+
+
+def lnl_bwd_args(**over):
+    cols = over.get("cols", COLS)
+    a = dict(dtype=B.BF16, m=1000, k=128, cols=cols, x=P, gamma=P, beta=P, w=P, mean=P, rstd=P,
+             douts=[P] * len(cols), dx=P, dw=P, dgamma=P, dbeta=P, ws=P, wsb=1 << 30,
+             stream=None)
+    a.update(over)
+    c = (ctypes.c_int64 * len(a["cols"]))(*a["cols"])
+    douts = None if a["douts"] is None else (ctypes.c_void_p * len(a["douts"]))(*a["douts"])
+    return (a["dtype"], a["m"], a["k"], len(a["cols"]), c, a["x"], a["gamma"], a["beta"],
+            a["w"], a["mean"], a["rstd"], douts, a["dx"], a["dw"], a["dgamma"], a["dbeta"],
+            a["ws"], a["wsb"], a["stream"])
+
+
+def test_ln_linear_bwd_workspace_size(lib):
+    for m, cols in ((1, [4]), (5000, COLS), (768 * 768, COLS), (77, [32, 64, 8, 96, 4])):
+        got = B.tri_ln_linear_bwd_workspace_bytes(B.BF16, m, 128, cols)
+        np_ = (sum(cols) + 31) // 32 * 32
+        parts = min(256, (m + 31) // 32)
+        assert got >= (parts + 1) * 129 * np_ * 4
+        assert got % 256 == 0
+
+
+LNL_BWD_BAD = [
+    (dict(dtype=B.F32), B.ERR_UNSUPPORTED), (dict(m=0), B.ERR_INVALID_ARG),
+    (dict(k=64), B.ERR_UNSUPPORTED), (dict(cols=[512, 64]), B.ERR_UNSUPPORTED),
+    (dict(cols=[128, 6]), B.ERR_UNSUPPORTED), (dict(m=1 << 30), B.ERR_UNSUPPORTED),
+    (dict(x=None), B.ERR_INVALID_ARG), (dict(mean=None), B.ERR_INVALID_ARG),
+    (dict(rstd=P + 4), B.ERR_INVALID_ARG), (dict(dx=None), B.ERR_INVALID_ARG),
+    (dict(dw=None), B.ERR_INVALID_ARG), (dict(dgamma=None), B.ERR_INVALID_ARG),
+    (dict(dbeta=P + 8), B.ERR_INVALID_ARG), (dict(douts=None), B.ERR_INVALID_ARG),
+    (dict(douts=[P, P, P, None, P]), B.ERR_INVALID_ARG),
+    (dict(ws=None), B.ERR_WORKSPACE), (dict(wsb=100), B.ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("over,code", LNL_BWD_BAD)
+def test_ln_linear_bwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_ln_linear_bwd(*lnl_bwd_args(**over)) == code

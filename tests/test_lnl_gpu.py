@@ -3,7 +3,12 @@ ABI) against the fp64 oracle, on the same seeded bf16 inputs.
 
 Tolerance: the bf16 bound used for the attention, |gpu - oracle| <= 2e-2 +
 1e-2 |oracle| elementwise plus a relative Frobenius error <= 1e-2; the fp32
-row statistics to 1e-5 relative.  Small problems are compared in full
+row statistics to 1e-5 relative.  The sums over rows (dW, dgamma, dbeta) add
+m terms whose bf16 factor xhat carries a relative rounding error up to 2^-9,
+so their error grows like 2^-9 times the l2 norm of the terms, which is the
+size of a typical entry: for them the absolute part of the bound is 2e-2
+times the RMS of the oracle's entries (about four times the largest error
+that rounding noise produces over 70k entries).  Small problems are compared in full
 (several 32-row tiles, a ragged tail); the attention-input shape at N = 768
 (589824 rows) is compared on sampled rows.
 """
@@ -20,12 +25,13 @@ DEV = "cuda:0"
 EPS = 1e-5
 
 
-def close(name, got, ref):
+def close(name, got, ref, row_sum=False):
     got = got.detach().double().cpu().numpy()
     assert got.shape == ref.shape, name
     assert np.all(np.isfinite(got)), f"{name}: non-finite"
     err = np.abs(got - ref)
-    worst = np.max(err / (2e-2 + 1e-2 * np.abs(ref)), initial=0)
+    atol = 2e-2 * (np.sqrt(np.mean(ref ** 2)) if row_sum else 1.0)
+    worst = np.max(err / (atol + 1e-2 * np.abs(ref)), initial=0)
     assert worst <= 1.0, f"{name}: allclose violated (worst err/bound {worst:.3f})"
     nrm = np.linalg.norm(ref)
     if nrm > 0:
@@ -75,3 +81,57 @@ def test_forward_is_bitwise_deterministic():
     for x, y in zip(a[0], b[0]):
         assert torch.equal(x, y)
     assert torch.equal(a[1], b[1]) and torch.equal(a[2], b[2])
+
+
+# ---- backward ---------------------------------------------------------------------------
+
+def run_bwd(t, douts=None):
+    d = {k: t[k].to(DEV) for k in ("x", "gamma", "beta", "w")}
+    _, mean, rstd = B.ln_linear_fwd(d["x"], d["gamma"], d["beta"], d["w"], t["cols"], EPS)
+    do2 = t["do2"] if douts is None else douts
+    parts = [p.contiguous().to(DEV) for p in torch.split(do2, list(t["cols"]), dim=1)]
+    out = B.ln_linear_bwd(d["x"], d["gamma"], d["beta"], d["w"], mean, rstd, parts)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("m,cols", [(1, (4,)), (37, (128, 4)), (300, W.LNL_COLS),
+                                    (5000, W.LNL_COLS), (129, (32, 64, 8, 96, 4, 4, 8, 12))])
+def test_backward_full(m, cols):
+    t = W.lnl_inputs(m, cols, seed=100 + m)
+    dx, dw, dg, db = run_bwd(t)
+    rdx, rdw, rdg, rdb = oracle.lnl_bwd(t["x"], t["gamma"], t["beta"], t["w"], t["do2"], EPS)
+    close("dx", dx, rdx)
+    close("dw", dw, rdw, row_sum=True)
+    close("dgamma", dg, rdg, row_sum=True)
+    close("dbeta", db, rdb, row_sum=True)
+
+
+def test_backward_attention_inputs_n768_sampled_rows():
+    # the full launch at m = 768^2 with dO2 nonzero on a sample of rows only:
+    # the sums over rows then cover exactly those rows, and dx is zero elsewhere
+    m = 768 * 768
+    t = W.lnl_inputs(m, W.LNL_COLS, seed=7)
+    rows = np.unique(np.concatenate([np.arange(0, 64), np.linspace(64, m - 65, 1900).astype(int),
+                                     np.arange(m - 64, m)]))
+    sel = torch.zeros(m, dtype=torch.bool)
+    sel[torch.from_numpy(rows)] = True
+    do2 = torch.where(sel[:, None], t["do2"], torch.zeros((), dtype=torch.bfloat16))
+    dx, dw, dg, db = run_bwd(t, douts=do2)
+    sub = {k: t[k][torch.from_numpy(rows)] for k in ("x",)}
+    rdx, rdw, rdg, rdb = oracle.lnl_bwd(sub["x"], t["gamma"], t["beta"], t["w"],
+                                        do2[torch.from_numpy(rows)], EPS)
+    close("dx (sampled rows)", dx[torch.from_numpy(rows)], rdx)
+    rest = dx[~sel.to(dx.device)]
+    assert torch.count_nonzero(rest).item() == 0, "dx must vanish where dO2 is zero"
+    close("dw", dw, rdw, row_sum=True)
+    close("dgamma", dg, rdg, row_sum=True)
+    close("dbeta", db, rdb, row_sum=True)
+
+
+def test_backward_is_bitwise_deterministic():
+    t = W.lnl_inputs(20000, W.LNL_COLS, seed=11)
+    a = run_bwd(t)
+    b = run_bwd(t)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
