@@ -16,6 +16,13 @@ library records on its launch stream during the same timed steps.
 
 The "cpu_baseline" leg times the fp64 oracle on the host cores on a bounded
 sample of the same workload (it is a reference point, not a target).
+
+--workload lnl_bf16_n768 instead measures the fused layer-norm + linear
+projection that produces the attention inputs (m = 768^2 rows of 128
+features -> Q, K, V, G [m][128] and the bias logits [m][4]): one step is its
+forward and backward, the metric is algorithmic HBM GB/s (every input read
+once, every output written once, per step time), and the roofline is HBM
+bandwidth.
 """
 from __future__ import annotations
 
@@ -48,7 +55,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=None, help="workload name (default: the N=768 one)")
+    ap.add_argument("--workload", default=None,
+                    help="workload name (default: the N=768 attention one; lnl_bf16_n768 runs "
+                         "the fused layer-norm + linear projection)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -70,18 +79,26 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_bytes": src.numel() * 4, "launches": 5}), flush=True)
 
 
-def kernel_source_hash():
-    """Hash of the kernel sources; a traffic figure measured on other sources is stale."""
+# Sources whose change can change a kernel family's memory traffic (its
+# kernels, the shared device headers, the host code that picks launch shapes).
+SOURCE_FAMILIES = {
+    "tri": ("fwd.hip", "bwd.hip", "api.hip", "common.h", "dma.h", "stage.h", "kernels.h"),
+    "lnl": ("lnl.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
+}
+
+
+def kernel_source_hash(family="tri"):
+    """Hash of a kernel family's sources; a traffic figure measured on other sources is
+    stale."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_20686_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in sorted(SOURCE_FAMILIES[family]):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(kernel, workload):
+def recorded_traffic(kernel, workload, family="tri"):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 --pmc summary, or
     None if there is none or it was taken on different kernel sources."""
     path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_traffic.md")
@@ -90,7 +107,7 @@ def recorded_traffic(kernel, workload):
     text = open(path).read()
     m = re.search(r"bytes_per_launch:\s*([0-9.eE+]+)", text)
     s = re.search(r"source_hash:\s*([0-9a-f]+)", text)
-    if not m or not s or s.group(1) != kernel_source_hash():
+    if not m or not s or s.group(1) != kernel_source_hash(family):
         return None
     return float(m.group(1))
 
@@ -129,6 +146,139 @@ def cpu_baseline(w, t, target_s):
                       f"dB (a row sum of the same dS) not included"}
 
 
+def lnl_kernel_bytes(m, cols, k=128):
+    """Algorithmic HBM bytes per launch of the fused projection's main kernels."""
+    n = int(sum(cols))
+    return {"lnl_fwd": m * k * 2 + m * n * 2 + m * 8,
+            "lnl_bwd_dx": 2 * m * k * 2 + m * n * 2 + m * 8,
+            "lnl_bwd_g": m * k * 2 + m * n * 2 + m * 8}
+
+
+def lnl_cpu_baseline(t, target_s):
+    """Time the fp64 oracle on a sample of R rows: forward, then the backward
+    of those rows (dx and their sums over rows).  Unit: algorithmic GB/s."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2506_20686_amd import workloads as W
+
+    m = t["x"].shape[0]
+    arr = {k: np.ascontiguousarray(t[k].double().numpy()) for k in ("gamma", "beta", "w")}
+
+    def run(rows):
+        sel = torch.as_tensor(rows)
+        xs = np.ascontiguousarray(t["x"][sel].double().numpy())
+        ds = np.ascontiguousarray(t["do2"][sel].double().numpy())
+        t0 = time.perf_counter()
+        oracle.lnl_fwd(xs, arr["gamma"], arr["beta"], arr["w"])
+        oracle.lnl_bwd(xs, arr["gamma"], arr["beta"], arr["w"], ds)
+        return time.perf_counter() - t0
+
+    trial_rows = 512
+    trial = run([int(i * m / trial_rows) for i in range(trial_rows)])
+    rows = max(trial_rows, min(m, int(trial_rows * target_s / max(trial, 1e-3))))
+    dt = run([int(i * m / rows) for i in range(rows)])
+    b = W.lnl_step_bytes(rows, t["cols"])
+    return {"value": (b["fwd"] + b["bwd"]) / dt / 1e9, "unit": "GB/s",
+            "cores": oracle.max_threads(), "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"{rows} of {m} rows (evenly spaced): forward and backward of those rows, "
+                      f"fp64, their sums over rows only; algorithmic bytes of {rows} rows"}
+
+
+def bench_lnl(args, name):
+    """Forward + backward of the fused layer-norm + linear projection."""
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    from paper_2506_20686_amd import workloads as W
+
+    spec = W.LNL_WORKLOADS[name]
+    m, cols = spec["m"], tuple(spec["cols"])
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    t = W.lnl_inputs(m, cols, seed=0)
+    x, gamma, beta, w = (t[k].to(dev) for k in ("x", "gamma", "beta", "w"))
+    douts = [p.contiguous().to(dev) for p in torch.split(t["do2"], list(cols), dim=1)]
+    ncols = sum(cols)
+    outs = [torch.empty((m, c), dtype=torch.bfloat16, device=dev) for c in cols]
+    mean = torch.empty(m, dtype=torch.float32, device=dev)
+    rstd = torch.empty(m, dtype=torch.float32, device=dev)
+    dx = torch.empty_like(x)
+    dw = torch.empty((128, ncols), dtype=torch.float32, device=dev)
+    dg = torch.empty(128, dtype=torch.float32, device=dev)
+    db = torch.empty(128, dtype=torch.float32, device=dev)
+    ws_bytes = B.tri_ln_linear_bwd_workspace_bytes(B.BF16, m, 128, cols)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda a: a.data_ptr()  # noqa: E731
+
+    def step():
+        st = B.tri_ln_linear_fwd(B.BF16, m, 128, cols, 1e-5, P(x), P(gamma), P(beta), P(w),
+                                 [P(o) for o in outs], P(mean), P(rstd), stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_ln_linear_fwd")
+        st = B.tri_ln_linear_bwd(B.BF16, m, 128, cols, P(x), P(gamma), P(beta), P(w), P(mean),
+                                 P(rstd), [P(d) for d in douts], P(dx), P(dw), P(dg), P(db),
+                                 P(ws), ws_bytes, stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_ln_linear_bwd")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    B.tri_attn_timing_reset()
+    B.tri_attn_timing_enable(True)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize(dev)
+    t1 = time.perf_counter()
+    B.tri_attn_timing_enable(False)
+    ktimes = B.kernel_times()
+    peak_bytes = torch.cuda.max_memory_allocated(dev)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    sb = W.lnl_step_bytes(m, cols)
+    step_bytes = sb["fwd"] + sb["bwd"]
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    kb = lnl_kernel_bytes(m, cols)
+    per_kernel = {k: {"avg_ms": round(v[0] / v[1], 5), "launches": v[1],
+                      "share": round(v[0] / max(1e-9, sum(x[0] for x in ktimes.values())), 4)}
+                  for k, v in ktimes.items() if v[1] > 0}
+    dom = max((k for k in per_kernel if k in kb), key=lambda k: ktimes[k][0])
+    avg_s = ktimes[dom][0] / ktimes[dom][1] * 1e-3
+    achieved = kb[dom] / avg_s / 1e9
+    out = {
+        "metric": "fused layer-norm + linear projection fwd+bwd, algorithmic HBM GB/s at m=768^2",
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals; the paper's pair representations are not available)",
+        "config": {"workload": name, "m": m, "k": 128, "cols": list(cols),
+                   "parallelism": "none (1 GPU)"},
+        "step_bytes": int(step_bytes),
+        "peak_hbm_bytes": int(peak_bytes),
+        "workspace_bytes": int(ws_bytes),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
+                     "traffic": recorded_traffic(dom, name, "lnl")},
+        "per_kernel": per_kernel,
+    }
+    out["cpu_baseline"] = lnl_cpu_baseline(t, args.cpu_seconds) if args.cpu_seconds > 0 else None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -154,6 +304,9 @@ def main():
         sys.exit(1)
 
     name = args.workload or W.HEADLINE
+    if name in W.LNL_WORKLOADS:
+        bench_lnl(args, name)
+        return
     w = W.WORKLOADS[name]
     dev = torch.device("cuda:0")
     dt = B.BF16 if w.dtype == torch.bfloat16 else B.F32

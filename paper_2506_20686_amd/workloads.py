@@ -137,3 +137,21 @@ def lnl_inputs(m: int, cols=LNL_COLS, seed: int = 0, k: int = LNL_K):
     w = draw((k, ncols), 1.0 / math.sqrt(k))
     do2 = draw((m, ncols))
     return dict(x=x, gamma=gamma, beta=beta, w=w, do2=do2, cols=tuple(cols))
+
+
+# The fused projection's benchmark shape: the attention inputs of the N = 768
+# pair representation (m = N^2 rows), and a small case for parity runs.
+LNL_WORKLOADS = {
+    "lnl_bf16_n768": dict(m=768 * 768, cols=LNL_COLS),
+    "lnl_bf16_n64": dict(m=64 * 64, cols=LNL_COLS),
+}
+
+
+def lnl_step_bytes(m: int, cols=LNL_COLS, k: int = LNL_K) -> dict:
+    """Algorithmic HBM bytes of one forward + backward of the fused projection
+    (each input read once, each output written once; bf16 tensors, fp32
+    statistics and weight gradients)."""
+    n = int(sum(cols))
+    fwd = m * k * 2 + m * n * 2 + m * 8 + k * n * 2 + 4 * k
+    bwd = m * k * 2 + m * n * 2 + m * 8 + m * k * 2 + k * n * (2 + 4) + 4 * k + 8 * k
+    return {"fwd": fwd, "bwd": bwd}
