@@ -152,6 +152,21 @@ struct TrAddr {
   // immediate offsets cover a whole block.
 };
 
+// 16-byte LDS read of DMA-staged data.  An ordinary load of an LDS array
+// that DMA writes makes the compiler wait for every outstanding vector load
+// first (it cannot tell which DMA filled what), so staged data is read with
+// inline assembly and waited for with lds_wait.
+__device__ inline f32x4 ds_read_b128_asm(uint32_t addr) {
+  f32x4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+template <int N>
+__device__ inline void lds_wait(f32x4 (&r)[N]) {
+  static_assert(N == 4, "four registers");
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
+}
+
 // Wait for all outstanding LDS reads, tied to the registers they fill so
 // that no use of them is scheduled before the wait.
 __device__ inline void tr_wait(s16x4 (&r)[4]) {

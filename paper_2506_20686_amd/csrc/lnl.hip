@@ -467,16 +467,17 @@ __global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a
 
 // lnl_bwd_g: persistent workgroups of LBG_WAVES waves; each workgroup walks
 // 32-row units u = blockIdx + i * gridDim, staging the unit's x, mean, rstd
-// and dO2 rows in LDS with buffer-resource DMA one unit ahead (double
-// buffered; rows past m read as zeros).  Wave w accumulates the G tiles
+// and dO2 rows in LDS with buffer-resource DMA (rows past m read as zeros)
+// into a ring of up to three slots, two units ahead.  A wave issues the same
+// pieces for every unit and nothing else, so it knows exactly how many of its
+// loads may still be in flight when a unit must have landed.  Wave w accumulates the G tiles
 // (k tile w % 4, column tiles w / 4 + 2 i) over all its units in registers:
 // A = xhat^T (transposed x reads, normalised in registers), B = dO2
-// (transposed reads), contraction over the unit's 32 rows.  The waves of k
-// tile 0 also sum the B fragments into s.  At the end each workgroup writes
+// (transposed reads), contraction over the unit's 32 rows.  One wave of each
+// column tile also sums its B fragments into s.  At the end each workgroup writes
 // its slab of gpart.
 constexpr int LBG_WAVES = 8;
-constexpr int LBG_SLOT = 56 * 1024;  // staged bytes per unit (x 8 KB, mean, rstd, dO2, zeros)
-constexpr int LBG_ZERO = LBG_SLOT - 64;
+constexpr int LBG_STAGE = 148 * 1024;  // ring bytes
 constexpr int LBG_MAXOPS = 64;
 constexpr int LBG_TPW = (LNL_GROUP / 32 + 1) / 2;  // column tiles per wave (at most)
 
@@ -488,12 +489,48 @@ struct LbgOp {
   uint32_t nbytes;    // bytes of the tensor (range of the buffer resource)
 };
 
+// Rows of 256 bytes (x, and dO2 outputs 128 columns wide) are staged with
+// their 16-byte chunks permuted: chunk c of row p sits at slot c ^ 4 (p % 4),
+// so the transposed reads of 4 consecutive rows hit four different 64-byte
+// bank windows.  The DMA writes a piece's lanes to consecutive LDS bytes, so
+// the lane that fills slot c' of row p loads chunk c' ^ 4 (p % 4).
+__device__ inline uint32_t lbg_swz_lane(int lane) {
+  const int r = lane >> 4;
+  return 256u * r + 16u * ((lane & 15) ^ (4 * (r & 3)));
+}
+__device__ inline uint32_t lbg_swz_off(int p, int col) {  // byte offset of (row p, column col)
+  return p * 256 + 16 * ((col >> 3) ^ (4 * (p & 3))) + 2 * (col & 7);
+}
+
+// s_waitcnt vmcnt(n) for a wave-uniform n in [0, 15].
+__device__ inline void wait_vm_n(int n) {
+  switch (n) {
+    case 0: wait_vm<0>(); break;
+    case 1: wait_vm<1>(); break;
+    case 2: wait_vm<2>(); break;
+    case 3: wait_vm<3>(); break;
+    case 4: wait_vm<4>(); break;
+    case 5: wait_vm<5>(); break;
+    case 6: wait_vm<6>(); break;
+    case 7: wait_vm<7>(); break;
+    case 8: wait_vm<8>(); break;
+    case 9: wait_vm<9>(); break;
+    case 10: wait_vm<10>(); break;
+    case 11: wait_vm<11>(); break;
+    case 12: wait_vm<12>(); break;
+    case 13: wait_vm<13>(); break;
+    case 14: wait_vm<14>(); break;
+    default: wait_vm<15>(); break;
+  }
+}
+
 __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a) {
-  __shared__ __align__(16) char stage[2 * LBG_SLOT];
+  __shared__ __align__(16) char stage[LBG_STAGE];
   __shared__ LbgOp ops[LBG_MAXOPS];
-  __shared__ uint32_t qoff[LNL_GROUP / 4];  // per 4 columns: offset in a slot of row 0
-  __shared__ uint32_t qpitch[LNL_GROUP / 4];
-  __shared__ int nops_s;
+  __shared__ uint32_t qreg[LNL_GROUP / 4];  // per 4 columns: staged region (offset in a slot)
+  __shared__ uint32_t qcol[LNL_GROUP / 4];  // first column inside the output
+  __shared__ uint32_t qpitch[LNL_GROUP / 4];  // row pitch in bytes (0: past N, read zeros)
+  __shared__ int nops_s, slot_s;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5;
   const int wave = tid >> 6;
   const int nq = a.np / 4, ntiles = a.np / 32;
@@ -515,23 +552,33 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
         ops[no++] = LbgOp{(const char*)a.dout[i], 2 * w, 1024u * j, lds + 1024u * j, mb * 2 * w};
       lds += 1024 * nop;
     }
+    // then 64 zero bytes; a slot is a multiple of 256 bytes
+    const uint32_t zero = lds;
     for (int q = 0; q < nq; ++q) {
       const int col = 4 * q;
       if (col < a.ncols) {
         int i = 0;
         while (i + 1 < a.n_out && col >= a.start[i + 1]) ++i;
-        qoff[q] = region[i] + 2 * (col - a.start[i]);
+        qreg[q] = region[i];
+        qcol[q] = col - a.start[i];
         qpitch[q] = 2 * (a.start[i + 1] - a.start[i]);
       } else {
-        qoff[q] = LBG_ZERO;
+        qreg[q] = zero;
+        qcol[q] = 0;
         qpitch[q] = 0;
       }
     }
     nops_s = no;
+    slot_s = (int)((zero + 64 + 255) & ~255u);
   }
-  if (tid < 32) *(uint32_t*)(stage + LBG_ZERO + 4 * (tid & 15) + ((tid >> 4) ? LBG_SLOT : 0)) = 0u;
   __syncthreads();
-  const int nops = nops_s;
+  const int nops = nops_s, sb = slot_s;
+  const int nslots = LBG_STAGE / sb >= 3 ? 3 : 2;
+  const int ahead = nslots - 1;                          // units in flight beyond the current
+  const int nw = nops > wave ? (nops - wave + LBG_WAVES - 1) / LBG_WAVES : 0;  // pieces per unit
+  const uint32_t zoff = (uint32_t)sb - 64;
+  if (tid < 16 * nslots) *(uint32_t*)(stage + (tid >> 4) * sb + zoff + 4 * (tid & 15)) = 0u;
+  __syncthreads();
 
   // this wave's tiles
   const int kt = wave & 3, t0 = wave >> 2;
@@ -541,37 +588,68 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
   const int G = lane >> 4, jj = lane & 3, pe = ((lane & 15) >> 2) + 4 * (G >> 1);
   const int cq = 4 * (G & 1) + jj;  // quad of the tile this lane supplies
   const uint32_t sbase = lds_addr(stage);
-  const uint32_t xa = sbase + pe * 256 + 2 * (32 * kt + 4 * cq);
+  const uint32_t xa = sbase + lbg_swz_off(pe, 32 * kt + 4 * cq);
   uint32_t ba[LBG_TPW], bp[LBG_TPW];
 #pragma unroll
   for (int i = 0; i < LBG_TPW; ++i) {
     const int T = t0 + 2 * i, q = T < ntiles ? 8 * T + cq : 0;
-    bp[i] = qpitch[q];
-    ba[i] = sbase + qoff[q] + pe * bp[i];
+    const uint32_t pitch = qpitch[q];
+    bp[i] = pitch;
+    ba[i] = sbase + qreg[q] +
+            (pitch == 256 ? lbg_swz_off(pe, qcol[q]) : pe * pitch + 2 * qcol[q]);
   }
+  // this wave's DMA pieces (the same for every unit)
+  const uint32_t lplain = 16u * lane, lswz = lbg_swz_lane(lane);
   const uint32_t sa = sbase + 8192;  // mean (+ 1024: rstd)
 
   f32x16 acc[LBG_TPW] = {};
   float ssum[LBG_TPW] = {};
+  const bf16x2 one2 = {(bf16)1.f, (bf16)1.f};
   const int64_t units = (a.m + 31) / 32;
+  // this wave's pieces of a unit (the same nw for every unit); the two
+  // statistics pieces need only the unit's 32 x 4 bytes
+  // (the table is read once per unit and its fields made wave-uniform, so the
+  // buffer resources live in scalar registers and each piece is one instruction)
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto issue = [&](int64_t u, int slot) {
-    for (int o = wave; o < nops; o += LBG_WAVES) {
-      const LbgOp op = ops[o];
-      const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(op.src), (short)0,
-                                                         (int)op.nbytes, 0x00020000);
-      const uint32_t voff = (uint32_t)u * 32u * op.rowbytes + op.voff + 16u * lane;
-      dma16b(r, voff, stage + slot * LBG_SLOT + op.lds);
+    if (u >= units) return;
+    LbgOp op[LBG_MAXOPS / LBG_WAVES];
+#pragma unroll
+    for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i)
+      if (i < nw) op[i] = ops[wave_u + LBG_WAVES * i];
+#pragma unroll
+    for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i) {
+      if (i >= nw) break;
+      // (readfirstlane returns int: widen through uint32_t, never sign-extend)
+      const uint64_t src =
+          (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)op[i].src) |
+          ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(
+               (uint32_t)((uintptr_t)op[i].src >> 32))
+           << 32);
+      const uint32_t rowbytes = __builtin_amdgcn_readfirstlane(op[i].rowbytes);
+      const uint32_t pvoff = __builtin_amdgcn_readfirstlane(op[i].voff);
+      const uint32_t plds = __builtin_amdgcn_readfirstlane(op[i].lds);
+      const uint32_t nbytes = __builtin_amdgcn_readfirstlane(op[i].nbytes);
+      const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)(uintptr_t)src, (short)0,
+                                                         (int)nbytes, 0x00020000);
+      const uint32_t voff =
+          (uint32_t)u * 32u * rowbytes + pvoff + (rowbytes == 256 ? lswz : lplain);
+      if (rowbytes != 4 || lane < 8) dma16b(r, voff, stage + slot * sb + plds);
     }
   };
   int64_t u = blockIdx.x;
-  if (u < units) issue(u, 0);
+  for (int i = 0; i < ahead; ++i) issue(u + (int64_t)i * gridDim.x, i);
   for (int it = 0; u < units; ++it, u += gridDim.x) {
-    const int slot = it & 1;
-    wait_vm<0>();
-    lds_barrier();
-    if (u + gridDim.x < units) issue(u + gridDim.x, slot ^ 1);
-    const uint32_t so = slot * LBG_SLOT;
-    // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
+    const int slot = it % nslots;
+    // this unit's pieces have landed once at most those of the units issued
+    // after it are in flight
+    int later = 0;
+    for (int i = 1; i < ahead; ++i) later += u + (int64_t)i * gridDim.x < units ? 1 : 0;
+    wait_vm_n(later * nw);
+    lds_barrier();  // for every wave; and the slot refilled next is free
+    issue(u + (int64_t)ahead * gridDim.x, (it + ahead) % nslots);
+    const uint32_t so = slot * sb;
+  // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
     // channels 32 kt + l32, normalised with those positions' statistics
     s16x4 xr[4];
 #pragma unroll
@@ -581,15 +659,18 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const bf16x8 xv = tr_frag(xr, h);
-      const f32x4 m0 = *(const f32x4*)(stage + (sa - sbase) + so + 4 * (16 * h + 4 * g));
-      const f32x4 m1 = *(const f32x4*)(stage + (sa - sbase) + so + 4 * (16 * h + 8 + 4 * g));
-      const f32x4 r0 = *(const f32x4*)(stage + (sa - sbase) + so + 1024 + 4 * (16 * h + 4 * g));
-      const f32x4 r1 =
-          *(const f32x4*)(stage + (sa - sbase) + so + 1024 + 4 * (16 * h + 8 + 4 * g));
+      // mean and rstd of the 8 positions (two runs of 4)
+      f32x4 st[4];
+      const uint32_t sp = sa + so + 4 * (16 * h + 4 * g);
+      st[0] = ds_read_b128_asm(sp);
+      st[1] = ds_read_b128_asm(sp + 32);
+      st[2] = ds_read_b128_asm(sp + 1024);
+      st[3] = ds_read_b128_asm(sp + 1024 + 32);
+      lds_wait(st);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        af[h][e] = (bf16)(((float)xv[e] - m0[e]) * r0[e]);
-        af[h][4 + e] = (bf16)(((float)xv[4 + e] - m1[e]) * r1[e]);
+        af[h][e] = (bf16)(((float)xv[e] - st[0][e]) * st[2][e]);
+        af[h][4 + e] = (bf16)(((float)xv[4 + e] - st[1][e]) * st[3][e]);
       }
     }
 #pragma unroll
@@ -603,13 +684,22 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
         for (int h = 0; h < 2; ++h) {
           const bf16x8 bf = tr_frag(br, h);
           acc[i] = Mma<bf16>::mma(af[h], bf, acc[i]);
-          if (kt == 0)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ssum[i] += (float)bf[e];
+          if (i % 4 == kt)  // column sums: each tile by one of its four waves
+          {
+            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 0, 1), one2,
+                                                      ssum[i], false);
+            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 2, 3), one2,
+                                                      ssum[i], false);
+            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 4, 5), one2,
+                                                      ssum[i], false);
+            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 6, 7), one2,
+                                                      ssum[i], false);
+          }
         }
       }
     }
   }
+  wait_vm<0>();  // the pieces issued past the last unit land before the wave ends
   // this workgroup's slab: G rows k = 32 kt + 8 j + 4 g + i, column 32 T + l32
   float* slab = a.gpart + (int64_t)blockIdx.x * (LNL_K + 1) * a.np;
   const int l32 = lane & 31;
@@ -619,7 +709,7 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
       const int n = 32 * (t0 + 2 * i) + l32;
 #pragma unroll
       for (int v = 0; v < 16; ++v) slab[(int64_t)(32 * kt + acc_row(v, g)) * a.np + n] = acc[i][v];
-      if (kt == 0) {
+      if (i % 4 == kt) {
         const float st = wave_xor32_sum(ssum[i]);
         if (g == 0) slab[(int64_t)LNL_K * a.np + n] = st;
       }
