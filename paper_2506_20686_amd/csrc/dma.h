@@ -152,19 +152,29 @@ struct TrAddr {
   // immediate offsets cover a whole block.
 };
 
-// 16-byte LDS read of DMA-staged data.  An ordinary load of an LDS array
-// that DMA writes makes the compiler wait for every outstanding vector load
-// first (it cannot tell which DMA filled what), so staged data is read with
-// inline assembly and waited for with lds_wait.
-__device__ inline f32x4 ds_read_b128_asm(uint32_t addr) {
-  f32x4 r;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
-  return r;
+// DMA-staged data is read with inline assembly: an ordinary load of an LDS
+// array that DMA writes makes the compiler wait for every outstanding vector
+// load first (it cannot tell which DMA filled what).
+// Four LDS reads and the wait for them in ONE asm statement.  A read issued
+// by one statement and waited for by a later one leaves the compiler free to
+// copy the destination register in between, before the data has arrived;
+// within one statement it cannot.  Early-clobber outputs keep the
+// destinations off the address registers.
+__device__ inline void tr_read4_wait(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
+                                     s16x4 (&r)[4]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %4\n\tds_read_b64_tr_b16 %1, %5\n\t"
+      "ds_read_b64_tr_b16 %2, %6\n\tds_read_b64_tr_b16 %3, %7\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+      : "v"(a0), "v"(a1), "v"(a2), "v"(a3));
 }
-template <int N>
-__device__ inline void lds_wait(f32x4 (&r)[N]) {
-  static_assert(N == 4, "four registers");
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]));
+__device__ inline void b128_read4_wait(uint32_t a0, uint32_t a1, uint32_t a2, uint32_t a3,
+                                       f32x4 (&r)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\t"
+      "ds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+      : "v"(a0), "v"(a1), "v"(a2), "v"(a3));
 }
 
 // Wait for all outstanding LDS reads, tied to the registers they fill so

@@ -613,10 +613,10 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto issue = [&](int64_t u, int slot) {
     if (u >= units) return;
-    LbgOp op[LBG_MAXOPS / LBG_WAVES];
+    LbgOp op[LBG_MAXOPS / LBG_WAVES];  // read unconditionally: one wait for all
 #pragma unroll
     for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i)
-      if (i < nw) op[i] = ops[wave_u + LBG_WAVES * i];
+      op[i] = ops[min(wave_u + LBG_WAVES * i, nops - 1)];
 #pragma unroll
     for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i) {
       if (i >= nw) break;
@@ -652,9 +652,7 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
   // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
     // channels 32 kt + l32, normalised with those positions' statistics
     s16x4 xr[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) xr[q] = ds_read_tr<0>(xa + so + 8 * q * 256);
-    tr_wait(xr);
+    tr_read4_wait(xa + so, xa + so + 2048, xa + so + 4096, xa + so + 6144, xr);
     bf16x8 af[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -662,11 +660,7 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
       // mean and rstd of the 8 positions (two runs of 4)
       f32x4 st[4];
       const uint32_t sp = sa + so + 4 * (16 * h + 4 * g);
-      st[0] = ds_read_b128_asm(sp);
-      st[1] = ds_read_b128_asm(sp + 32);
-      st[2] = ds_read_b128_asm(sp + 1024);
-      st[3] = ds_read_b128_asm(sp + 1024 + 32);
-      lds_wait(st);
+      b128_read4_wait(sp, sp + 32, sp + 1024, sp + 1024 + 32, st);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         af[h][e] = (bf16)(((float)xv[e] - st[0][e]) * st[2][e]);
@@ -677,9 +671,8 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
     for (int i = 0; i < LBG_TPW; ++i) {
       if (i < nt_w) {
         s16x4 br[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) br[q] = ds_read_tr<0>(ba[i] + so + 8 * q * bp[i]);
-        tr_wait(br);
+        const uint32_t b0 = ba[i] + so, bs = 8 * bp[i];
+        tr_read4_wait(b0, b0 + bs, b0 + 2 * bs, b0 + 3 * bs, br);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const bf16x8 bf = tr_frag(br, h);

@@ -96,7 +96,10 @@ def run_bwd(t, douts=None):
 
 
 @pytest.mark.parametrize("m,cols", [(1, (4,)), (37, (128, 4)), (300, W.LNL_COLS),
-                                    (5000, W.LNL_COLS), (129, (32, 64, 8, 96, 4, 4, 8, 12))])
+                                    (5000, W.LNL_COLS), (129, (32, 64, 8, 96, 4, 4, 8, 12)),
+                                    (64, (32,)), (64, (64,)), (96, (96,)), (33, (16, 16)),
+                                    (3000, (128, 64)), (40, (100, 20, 4)),
+                                    (70, (132, 132, 132, 132, 16))])
 def test_backward_full(m, cols):
     t = W.lnl_inputs(m, cols, seed=100 + m)
     dx, dw, dg, db = run_bwd(t)
