@@ -94,6 +94,48 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
                  size_t workspace_bytes, void* stream);
 
+/* Starting node over a contiguous range of rows: one GPU's share of the
+ * pair representation when it is split into contiguous shards along one
+ * sequence axis (Section IV-B, sequence parallelism).  Rows of the starting
+ * node are independent attention problems, so a range of `rows` rows
+ * (1 <= rows <= n) gives exactly those rows of the whole call's results.
+ * Tensors are local to the range, row 0 being the range's first row:
+ *   q, k, v, g, out, dout, dq, dk, dv, dg : [rows][n][h][d]  (dtype)
+ *   lse                                     : [rows][n][h]     (fp32)
+ *   mask                                    : [rows][n]        (uint8; NULL = all valid)
+ *   bias                                    : [n][n][h]        (dtype, the whole map)
+ *   dbias_partial                           : [n][n][h]        (fp32)
+ * dbias_partial is this range's term of the bias gradient, the sum over its
+ * rows, kept in fp32: the whole gradient is the sum of every range's term
+ * (in a fixed order for reproducible results), rounded once.  The ending
+ * node's shards are starting-node shards of the transposed map (ending =
+ * starting applied to T(q), T(k), T(v), T(g) with bias^T and mask^T, T
+ * swapping the two pair axes), which is where the re-shard between the two
+ * nodes puts them.  Size, pointer, workspace, stream and error rules as
+ * above; rows outside [1, n] is TRIATTN_ERR_INVALID_ARG. */
+int tri_attn_rows_fwd_workspace_bytes(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d,
+                                      size_t* bytes);
+
+/* Forward pass of rows [0, rows) of a range (same outputs as tri_attn_fwd
+ * for those rows). */
+int tri_attn_rows_fwd(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d, float scale,
+                      const void* q, const void* k, const void* v, const void* g,
+                      const void* bias, const uint8_t* mask, void* out, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace tri_attn_rows_bwd needs for these sizes. */
+int tri_attn_rows_bwd_workspace_bytes(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d,
+                                      size_t* bytes);
+
+/* Backward pass of a range: dq, dk, dv, dg of its rows (as tri_attn_bwd
+ * gives them) and its fp32 bias-gradient term dbias_partial. */
+int tri_attn_rows_bwd(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d, float scale,
+                      const void* q, const void* k, const void* v, const void* g,
+                      const void* bias, const uint8_t* mask, const void* out, const float* lse,
+                      const void* dout, void* dq, void* dk, void* dv, void* dg,
+                      float* dbias_partial, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
 /* Fused layer-norm + linear projection (Section IV, fused layer-norm &
  * linear projection; forward formulas in the appendix table of fused
  * operators): the step that produces the attention inputs from the pair

@@ -46,6 +46,12 @@ def lib():
         L.tri_attn_bwd_workspace_bytes.argtypes = L.tri_attn_fwd_workspace_bytes.argtypes
         L.tri_attn_fwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
         L.tri_attn_bwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz, _vp]
+        L.tri_attn_rows_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _i64, _i64,
+                                                        ctypes.POINTER(_sz)]
+        L.tri_attn_rows_bwd_workspace_bytes.argtypes = L.tri_attn_rows_fwd_workspace_bytes.argtypes
+        L.tri_attn_rows_fwd.argtypes = [_int, _i64, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
+        L.tri_attn_rows_bwd.argtypes = [_int, _i64, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz,
+                                                                                          _vp]
         L.tri_attn_status_string.argtypes = [_int]
         L.tri_attn_status_string.restype = ctypes.c_char_p
         L.tri_attn_timing_enable.argtypes = [_int]
@@ -65,7 +71,9 @@ def lib():
                      "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
                      "tri_attn_timing_reset", "tri_attn_timing_read",
                      "tri_ln_linear_fwd", "tri_ln_linear_bwd_workspace_bytes",
-                     "tri_ln_linear_bwd"):
+                     "tri_ln_linear_bwd", "tri_attn_rows_fwd_workspace_bytes",
+                     "tri_attn_rows_bwd_workspace_bytes", "tri_attn_rows_fwd",
+                     "tri_attn_rows_bwd"):
             getattr(L, name).restype = _int
         _LIB = L
     return _LIB
@@ -105,6 +113,37 @@ def tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, 
     """Raw call: every tensor argument is an integer device address (or None)."""
     return lib().tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
                               dout, dq, dk, dv, dg, dbias, workspace, workspace_bytes, stream)
+
+
+def tri_attn_rows_fwd_workspace_bytes(dtype: int, n: int, rows: int, h: int, d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_rows_fwd_workspace_bytes(dtype, n, rows, h, d, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_rows_fwd_workspace_bytes")
+    return out.value
+
+
+def tri_attn_rows_bwd_workspace_bytes(dtype: int, n: int, rows: int, h: int, d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_rows_bwd_workspace_bytes(dtype, n, rows, h, d, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_rows_bwd_workspace_bytes")
+    return out.value
+
+
+def tri_attn_rows_fwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, lse, workspace,
+                      workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_rows_fwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                                   workspace, workspace_bytes, stream)
+
+
+def tri_attn_rows_bwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, lse, dout, dq,
+                      dk, dv, dg, dbias_partial, workspace, workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_rows_bwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                                   dout, dq, dk, dv, dg, dbias_partial, workspace,
+                                   workspace_bytes, stream)
 
 
 def _cols_arr(cols):
@@ -259,6 +298,65 @@ def bwd(q, k, v, g, bias, out, lse, dout, mask=None, node: int = STARTING,
     if st != OK:
         raise TriAttnError(st, "tri_attn_bwd")
     return dq, dk, dv, dg, dbias
+
+
+def _rows_common(q, k, v, g, bias, mask):
+    if q.dim() != 4:
+        raise ValueError("q must be [rows, n, h, d]")
+    rows, n, h, d = q.shape
+    if q.dtype not in _DTYPES:
+        raise ValueError(f"unsupported dtype {q.dtype}")
+    dev = q.device
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g)):
+        _check(name, t, (rows, n, h, d), q.dtype, dev)
+    _check("bias", bias, (n, n, h), q.dtype, dev)
+    if mask is not None:
+        _check("mask", mask, (rows, n), torch.uint8, dev)
+    return rows, n, h, d, _DTYPES[q.dtype], dev
+
+
+def rows_fwd(q, k, v, g, bias, mask=None, scale: Optional[float] = None,
+             workspace: Optional[torch.Tensor] = None):
+    """Starting-node forward over a range of rows: q, k, v, g [rows, n, h, d]
+    (the range's rows), bias [n, n, h] (whole map), mask [rows, n].  Returns
+    (out [rows, n, h, d], lse [rows, n, h] fp32)."""
+    rows, n, h, d, dt, dev = _rows_common(q, k, v, g, bias, mask)
+    scale = default_scale(d) if scale is None else float(scale)
+    out = torch.empty_like(q)
+    lse = torch.empty((rows, n, h), dtype=torch.float32, device=dev)
+    need = tri_attn_rows_fwd_workspace_bytes(dt, n, rows, h, d)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_attn_rows_fwd(dt, n, rows, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                           _ptr(bias), _ptr(mask), _ptr(out), _ptr(lse), _ptr(workspace),
+                           workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_rows_fwd")
+    return out, lse
+
+
+def rows_bwd(q, k, v, g, bias, out, lse, dout, mask=None, scale: Optional[float] = None,
+             workspace: Optional[torch.Tensor] = None):
+    """Starting-node backward over a range of rows.  Returns (dq, dk, dv, dg
+    [rows, n, h, d], dbias_partial [n, n, h] fp32: the range's term of the
+    bias gradient)."""
+    rows, n, h, d, dt, dev = _rows_common(q, k, v, g, bias, mask)
+    _check("out", out, (rows, n, h, d), q.dtype, dev)
+    _check("dout", dout, (rows, n, h, d), q.dtype, dev)
+    _check("lse", lse, (rows, n, h), torch.float32, dev)
+    scale = default_scale(d) if scale is None else float(scale)
+    dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
+    dbp = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+    need = tri_attn_rows_bwd_workspace_bytes(dt, n, rows, h, d)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_attn_rows_bwd(dt, n, rows, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                           _ptr(bias), _ptr(mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq),
+                           _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbp), _ptr(workspace),
+                           workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_rows_bwd")
+    return dq, dk, dv, dg, dbp
 
 
 class TriangleAttention(torch.autograd.Function):

@@ -28,17 +28,17 @@ int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Row chunks of the bias-gradient reduction: about 2304 workgroups of
-// 128 queries x 128 keys (nine rounds of one per CU on 256 CUs), at most 16
-// partial slabs.
-int db_row_chunks(int64_t n, int64_t h) {
+// Row chunks of the bias-gradient reduction over nr rows: about 2304
+// workgroups of 128 queries x 128 keys (nine rounds of one per CU on 256
+// CUs), at most 16 partial slabs.
+int db_row_chunks(int64_t n, int64_t nr, int64_t h) {
   const int64_t tiles = h * ((n + 127) / 128) * ((n + 127) / 128);
   int64_t c = (2304 + tiles - 1) / tiles;
   if (c > 16) c = 16;
-  if (c > n) c = n;
+  if (c > nr) c = nr;
   if (c < 1) c = 1;
-  const int64_t rpc = (n + c - 1) / c;
-  return (int)((n + rpc - 1) / rpc);
+  const int64_t rpc = (nr + c - 1) / c;
+  return (int)((nr + rpc - 1) / rpc);
 }
 
 struct Layout {
@@ -46,12 +46,13 @@ struct Layout {
   int nrc;
 };
 
-// Workspace layout (offsets in bytes, each 256-aligned):
-//   forward : bt [H][np][np] f32, kbits [n][np/32] u32, rowfull [n] u32
-//   backward: bt, btT [H][np][np] f32, kbits, rowfull, lse2 and dsum [H][n][np] f32,
-//             dA [n][n][H][32] dtype (bf16: plus its low part, same size),
+// Workspace layout for nr rows of pair length n (offsets in bytes, each
+// 256-aligned):
+//   forward : bt [H][np][np] f32, kbits [nr][np/32] u32, rowfull [nr] u32
+//   backward: bt, btT [H][np][np] f32, kbits, rowfull, lse2 and dsum [H][nr][np] f32,
+//             dA [nr][n][H][32] dtype (bf16: plus its low part, same size),
 //             slabs [nrc][H][np][np] f32
-Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
+Layout plan(bool bwd, int dtype, int64_t n, int64_t nr, int64_t h) {
   const size_t np = (size_t)((n + 31) / 32 * 32);
   const size_t plane = (size_t)h * np * np * sizeof(float);
   Layout L{};
@@ -63,21 +64,21 @@ Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
     off += round256(plane);
   }
   L.kbits = off;
-  off += round256((size_t)n * (np / 32) * sizeof(uint32_t));
+  off += round256((size_t)nr * (np / 32) * sizeof(uint32_t));
   L.rowfull = off;
-  off += round256((size_t)n * sizeof(uint32_t));
+  off += round256((size_t)nr * sizeof(uint32_t));
   if (bwd) {
-    const size_t rows = (size_t)h * n * np * sizeof(float);
+    const size_t rows = (size_t)h * nr * np * sizeof(float);
     L.lse2 = off;
     off += round256(rows);
     L.dsum = off;
     off += round256(rows);
-    const size_t pair = (size_t)n * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4);
+    const size_t pair = (size_t)nr * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4);
     L.da = off;
     off += round256(pair);
     L.dalo = off;
     if (dtype == TRIATTN_BF16) off += round256(pair);
-    L.nrc = db_row_chunks(n, h);
+    L.nrc = db_row_chunks(n, nr, h);
     L.slabs = off;
     off += round256((size_t)L.nrc * plane);
   }
@@ -85,9 +86,12 @@ Layout plan(bool bwd, int dtype, int64_t n, int64_t h) {
   return L;
 }
 
-Geom geom(int node, int64_t n, int64_t h, float scale) {
+// nr = rows computed: n for a whole call, a row range's length otherwise
+// (starting node only; the range's tensors then hold nr rows).
+Geom geom(int node, int64_t n, int64_t nr, int64_t h, float scale) {
   Geom g;
   g.n = (int)n;
+  g.nr = (int)nr;
   g.H = (int)h;
   g.np = (int)((n + 31) / 32 * 32);
   g.nkt = g.np / 32;
@@ -123,7 +127,7 @@ template <typename T>
 int run_bwd(int node, const Geom& g, const Layout& L, const void* q, const void* k,
             const void* v, const void* gate, const void* bias, const uint8_t* mask,
             const void* out, const float* lse, const void* dout, void* dq, void* dk, void* dv,
-            void* dg, void* dbias, void* ws, hipStream_t s) {
+            void* dg, void* dbias, float* dbias_f32, void* ws, hipStream_t s) {
   const triattn::Prep p = prep_ptrs(L, ws, true);
   char* b = (char*)ws;
   const triattn::BwdWs w{(float*)(b + L.lse2), (float*)(b + L.dsum), (void*)(b + L.da),
@@ -133,7 +137,7 @@ int run_bwd(int node, const Geom& g, const Layout& L, const void* q, const void*
     return TRIATTN_ERR_HIP;
   if (triattn::launch_bwd<T>(g, node, p, w, (const T*)q, (const T*)k, (const T*)v,
                              (const T*)gate, (const T*)out, lse, (const T*)dout, (T*)dq, (T*)dk,
-                             (T*)dv, (T*)dg, (T*)dbias, s) != hipSuccess)
+                             (T*)dv, (T*)dg, (T*)dbias, dbias_f32, s) != hipSuccess)
     return TRIATTN_ERR_HIP;
   return TRIATTN_OK;
 }
@@ -147,7 +151,7 @@ int tri_attn_fwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int6
   const int st = check_shape(node, dtype, n, h, d);
   if (st != TRIATTN_OK) return st;
   if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
-  *bytes = plan(false, dtype, n, h).total;
+  *bytes = plan(false, dtype, n, n, h).total;
   return TRIATTN_OK;
 }
 
@@ -156,7 +160,7 @@ int tri_attn_bwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int6
   const int st = check_shape(node, dtype, n, h, d);
   if (st != TRIATTN_OK) return st;
   if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
-  *bytes = plan(true, dtype, n, h).total;
+  *bytes = plan(true, dtype, n, n, h).total;
   return TRIATTN_OK;
 }
 
@@ -170,10 +174,10 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const void* ptrs[] = {q, k, v, g, bias, out, lse};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(false, dtype, n, h);
+  const Layout L = plan(false, dtype, n, n, h);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale);
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return run_fwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, workspace, s);
@@ -191,16 +195,97 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(true, dtype, n, h);
+  const Layout L = plan(true, dtype, n, n, h);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale);
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return run_bwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
-                                  dv, dg, dbias, workspace, s);
+                                  dv, dg, dbias, nullptr, workspace, s);
   return run_bwd<float>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk, dv, dg,
-                        dbias, workspace, s);
+                        dbias, nullptr, workspace, s);
+}
+
+// ---- starting node over a range of rows -------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+int rows_check(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d) {
+  const int st = check_shape(TRIATTN_STARTING, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (rows < 1 || rows > n) return TRIATTN_ERR_INVALID_ARG;
+  return TRIATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_attn_rows_fwd_workspace_bytes(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d,
+                                      size_t* bytes) {
+  const int st = rows_check(dtype, n, rows, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = plan(false, dtype, n, rows, h).total;
+  return TRIATTN_OK;
+}
+
+int tri_attn_rows_bwd_workspace_bytes(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d,
+                                      size_t* bytes) {
+  const int st = rows_check(dtype, n, rows, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = plan(true, dtype, n, rows, h).total;
+  return TRIATTN_OK;
+}
+
+int tri_attn_rows_fwd(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d, float scale,
+                      const void* q, const void* k, const void* v, const void* g,
+                      const void* bias, const uint8_t* mask, void* out, float* lse,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int st = rows_check(dtype, n, rows, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(false, dtype, n, rows, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(TRIATTN_STARTING, n, rows, h, scale);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == TRIATTN_BF16)
+    return run_fwd<triattn::bf16>(TRIATTN_STARTING, geo, L, q, k, v, g, bias, mask, out, lse,
+                                  workspace, s);
+  return run_fwd<float>(TRIATTN_STARTING, geo, L, q, k, v, g, bias, mask, out, lse, workspace,
+                        s);
+}
+
+int tri_attn_rows_bwd(int dtype, int64_t n, int64_t rows, int64_t h, int64_t d, float scale,
+                      const void* q, const void* k, const void* v, const void* g,
+                      const void* bias, const uint8_t* mask, const void* out, const float* lse,
+                      const void* dout, void* dq, void* dk, void* dv, void* dg,
+                      float* dbias_partial, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  int st = rows_check(dtype, n, rows, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias_partial};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(true, dtype, n, rows, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(TRIATTN_STARTING, n, rows, h, scale);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == TRIATTN_BF16)
+    return run_bwd<triattn::bf16>(TRIATTN_STARTING, geo, L, q, k, v, g, bias, mask, out, lse,
+                                  dout, dq, dk, dv, dg, nullptr, dbias_partial, workspace, s);
+  return run_bwd<float>(TRIATTN_STARTING, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
+                        dv, dg, nullptr, dbias_partial, workspace, s);
 }
 
 // ---- fused layer-norm + linear projection ---------------------------------------------

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
                                                        T* dalo, float* lse2) {
   const int64_t tix = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t idx = tix >> 2;  // (a, b, h)
-  const int64_t total = (int64_t)G.n * G.n * G.H;
+  const int64_t total = (int64_t)G.nr * G.n * G.H;  // [nr][n][H] (ending node: nr = n)
   if (idx >= total) return;
   const int64_t base = idx * HEAD_DIM + 8 * (tix & 3);
 #pragma unroll
@@ -77,7 +77,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
     const int a = (int)(pair / G.n), b = (int)(pair % G.n);
     const int row = node == 0 ? a : b, qi = node == 0 ? b : a;
     const float l = lse[idx];
-    lse2[((int64_t)h * G.n + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
+    lse2[((int64_t)h * G.nr + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
   }
 }
 
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
 __global__ __launch_bounds__(256) void bwd_pad_kernel(Geom G, float* lse2, float* dsum) {
   const int pad = G.np - G.n;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)G.H * G.n * pad) return;
+  if (idx >= (int64_t)G.H * G.nr * pad) return;
   const int64_t hr = idx / pad;
   const int64_t at = hr * G.np + G.n + (int)(idx % pad);
   lse2[at] = pos_inf();
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int qb = w % a.nblk, rh = w / a.nblk;
-  const int r = rh % G.n, h = rh / G.n;
+  const int r = rh % G.nr, h = rh / G.nr;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int q0 = qb * BWD_BLK + wave * TILE;
   const bool active = q0 < G.n;
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
     row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
     row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
     if constexpr (kSplitDA<T>) row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
-    l2 = a.lse2[((int64_t)h * G.n + r) * G.np + q];
+    l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
     zero_frags<T>(qf);
     zero_frags<T>(daf);
@@ -239,7 +239,7 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   if (!active) return;
   const float dsum = wave_xor32_sum(dpart);
   if (!qok) return;
-  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = -dsum;  // stored negated
+  if (g == 0) a.dsum[((int64_t)h * G.nr + r) * G.np + q] = -dsum;  // stored negated
   const int64_t base = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -285,21 +285,21 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int nrg = (G.n + QD_ROWS - 1) / QD_ROWS;
+  const int nrg = (G.nr + QD_ROWS - 1) / QD_ROWS;
   const int qb = w % nqb, rg = (w / nqb) % nrg, h = w / (nqb * nrg);
   const int r0 = rg * QD_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qtl = wave % QD_QT, ri = wave / QD_QT;
-  const int last = G.n - 1;
+  const int last = G.nr - 1;  // last row
   const int r = min(r0 + ri, last);
-  const bool rok = r0 + ri < G.n;
+  const bool rok = r0 + ri < G.nr;
   const int q0 = qb * 32 * QD_QT + qtl * TILE;
   const int q = q0 + l32;
   const bool active = rok && q0 < G.n;
   const bool qok = q < G.n;
   const int nkt = G.nkt;
-  const int nrows = min(QD_ROWS, G.n - r0);  // rows of this group that exist
+  const int nrows = min(QD_ROWS, G.nr - r0);  // rows of this group that exist
   const float c1 = G.scale * LOG2E;
 
   __shared__ __align__(16) char smem[QD_SLOTS * QD_SLOT];
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
     row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
     row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
     row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
-    l2 = a.lse2[((int64_t)h * G.n + r) * G.np + q];
+    l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
     zero_frags<bf16>(qf);
     zero_frags<bf16>(daf);
@@ -329,7 +329,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   // u % 2 (keys 16 (u % 2) + lane / 4) of tile u / 2 of [K rows, V rows];
   // otherwise quarter v % 4 of bias tile v / 4, v = u - 4 QD_ROWS.  Lane
   // offsets are fixed; the source bases advance by one key tile per issue.
-  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const void* src[QD_OPS];
   const void* srcend[QD_OPS];
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   if (!active) return;
   const float dsum = wave_xor32_sum(dpart);
   if (!qok) return;
-  if (g == 0) a.dsum[((int64_t)h * G.n + r) * G.np + q] = -dsum;  // stored negated
+  if (g == 0) a.dsum[((int64_t)h * G.nr + r) * G.np + q] = -dsum;  // stored negated
   const int64_t gb = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -511,7 +511,7 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int kbk = w % a.nblk, rh = w / a.nblk;
-  const int r = rh % G.n, h = rh / G.n;
+  const int r = rh % G.nr, h = rh / G.nr;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int kt = kbk * BWD_WAVES + wave;  // this wave's key tile
   const bool active = kt < G.nkt;
@@ -544,8 +544,8 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   const float c1 = G.scale * LOG2E;
   f32x16 dkt = {}, dvt = {};
   const int ktc = active ? kt : 0;  // key tile of the key-major bias (0 for idle waves)
-  const float* l2row = a.lse2 + ((int64_t)h * G.n + r) * G.np;
-  const float* drow = a.dsum + ((int64_t)h * G.n + r) * G.np;
+  const float* l2row = a.lse2 + ((int64_t)h * G.nr + r) * G.np;
+  const float* drow = a.dsum + ((int64_t)h * G.nr + r) * G.np;
   const int nblk = (G.nkt + 1) >> 1;  // query blocks of 64
   const float kmask = kvalid ? 0.f : neg_inf();
   auto bias_tile = [&](int t) {
@@ -694,15 +694,15 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int nrg = (G.n + KD_ROWS - 1) / KD_ROWS;
+  const int nrg = (G.nr + KD_ROWS - 1) / KD_ROWS;
   const int kbk = w % a.nblk, rg = (w / a.nblk) % nrg, h = w / (a.nblk * nrg);
   const int r0 = rg * KD_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ri = wave >> 2;                 // row of this wave (0..3)
-  const int last = G.n - 1;
+  const int last = G.nr - 1;  // last row
   const int r = min(r0 + ri, last);
-  const bool rok = r0 + ri < G.n;
+  const bool rok = r0 + ri < G.nr;
   const int kt = kbk * 4 + (wave & 3);      // this wave's key tile
   const int nkt = G.nkt;
   const bool active = rok && kt < nkt;
@@ -736,7 +736,7 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   // positions 16 (w % 2) + lane / 4.  Op 1: the low part of dA of row
   // w / 2 (waves 0-7), or lse2 (waves 8-11) / -D (waves 12-15) of row w % 4,
   // 128 bytes (lanes 0..7).  Op 2: bias tile w / 4, quarter w % 4.
-  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
   const int p16 = 16 * (wave & 1) + (lane >> 2);
   const uint32_t pvoff = (uint32_t)(((int64_t)p16 * G.sPos + hb + 8 * ((lane & 3) ^ swz(p16))) * 2);
   const int64_t tstep = (int64_t)TILE * G.sPos;  // elements per query tile
@@ -749,7 +749,7 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   const bool lo_op = wave < KD_HALF;
   const int lidx = wave - KD_HALF;                 // lse2 rows, then -D rows
   const float* pl = (lidx < KD_ROWS ? a.lse2 : a.dsum) +
-                    ((int64_t)h * G.n + min(r0 + lidx % KD_ROWS, last)) * G.np;
+                    ((int64_t)h * G.nr + min(r0 + lidx % KD_ROWS, last)) * G.np;
   const float* const plend = pl + G.np;
   char* const dst1 = lo_op ? smem + KD_LO + orow * KD_BLK + 1024 * (wave & 1)
                            : smem + KD_L2 + 128 * lidx;
@@ -951,7 +951,7 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   auto row_bits = [&](int r, int half) -> uint64_t {
     return block_bits(a.kbits + (int64_t)r * G.nkt, G.nkt, (kt0 >> 1) + half);
   };
-  const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
+  const int r0 = rc * a.rpc, r1 = min(G.nr, r0 + a.rpc);
 
   // thread -> (half of the 128 positions, piece index within the half)
   const int half = tid >> 8, pt = tid & 255;
@@ -966,7 +966,7 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
     qp.load(a.q + rowbase, G.sPos, qstart + SPAN * half, last, pt);
     dap.load(a.da + rowbase, G.sPos, qstart + SPAN * half, last, pt);
     if constexpr (kSplitDA<T>) dlp.load(a.dalo + rowbase, G.sPos, qstart + SPAN * half, last, pt);
-    const int64_t at = ((int64_t)h * G.n + r) * G.np + sq;
+    const int64_t at = ((int64_t)h * G.nr + r) * G.np + sq;
     sv = tid < DB_ROWS ? a.lse2[at] : a.dsum[at];
   };
   auto store_row = [&](int r) {
@@ -1101,9 +1101,9 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   // 16 (w % 8) + lane / 4.  Op 1: Q (waves 0-7) or dA (waves 8-15) of the
   // 128 queries.  Op 2: the low part of dA (waves 0-7), lse2 (waves 8-11)
   // or -D (waves 12-15), 128 bytes per wave (lanes 0..7).
-  const int r0 = rc * a.rpc, r1 = min(G.n, r0 + a.rpc);
+  const int r0 = rc * a.rpc, r1 = min(G.nr, r0 + a.rpc);
   const int nr = max(r1 - r0, 0);
-  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
   const int hb = h * HEAD_DIM;
   const int pp = 16 * (wave & 7) + (lane >> 2);  // position (key or query) of this lane
   const int pc = (lane & 3) ^ swz(pp);
@@ -1115,7 +1115,7 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
       (uint32_t)(((int64_t)(qstart + pp) * G.sPos + hb + 8 * pc) * 2);
   // op 2: dA low (waves 0-7, same lane offsets as op 1) or lse2 / -D rows
   const bool lo_op = wave < 8;
-  const float* lrow = (wave < 12 ? a.lse2 : a.dsum) + (int64_t)h * G.n * G.np;
+  const float* lrow = (wave < 12 ? a.lse2 : a.dsum) + (int64_t)h * G.nr * G.np;
   const uint32_t voff2 =
       lo_op ? voff1 : (uint32_t)((qstart + 32 * (wave & 3) + 4 * lane) * 4);
   char* const dst0 = smem + (wave < 8 ? DBD_OK : DBD_OV) + 1024 * (wave & 7);
@@ -1126,11 +1126,11 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
     // rows past the chunk copy nothing (empty resources) but keep the wait
     // counts uniform
     const bool real = r < r1;
-    const int64_t rb = (int64_t)min(r, G.n - 1) * G.sRow;
+    const int64_t rb = (int64_t)min(r, G.nr - 1) * G.sRow;
     const bf16* p0 = src0 + rb;
     const bf16* p1 = src1 + rb;
     const bf16* p2 = a.dalo + rb;
-    const float* pl = lrow + (int64_t)min(r, G.n - 1) * G.np;
+    const float* pl = lrow + (int64_t)min(r, G.nr - 1) * G.np;
     dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff0,
            dst0 + slot * DBD_SLOT);
     dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff1,
@@ -1256,30 +1256,31 @@ __global__ __launch_bounds__(256) void db_reduce_kernel(Geom G, int node, int nr
 template <typename T>
 hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, const T* q,
                       const T* k, const T* v, const T* gate, const T* out, const float* lse,
-                      const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, hipStream_t s) {
+                      const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, float* dbias_f32,
+                      hipStream_t s) {
   T* da = (T*)ws.da;
   T* dalo = (T*)ws.dalo;
-  const int64_t npair = (int64_t)g.n * g.n * g.H;
+  const int64_t npair = (int64_t)g.nr * g.n * g.H;
   {
     KernelTimer t(K_BWD_PREP, s);
     hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((4 * npair + 255) / 256)), dim3(256),
                        0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
   }
   if (g.np > g.n) {
-    const int64_t npad = (int64_t)g.H * g.n * (g.np - g.n);
+    const int64_t npad = (int64_t)g.H * g.nr * (g.np - g.n);
     KernelTimer t(K_BWD_PAD, s);
     hipLaunchKernelGGL(bwd_pad_kernel, dim3((unsigned)((npad + 255) / 256)), dim3(256), 0, s, g,
                        ws.lse2, ws.dsum);
   }
   BwdArgs<T> a{g, p.bt, p.btT, p.kbits, p.rowfull, q, k, v, da, dalo, ws.lse2, ws.dsum, dq, dk, dv, ws.slabs,
-               (g.n + BWD_BLK - 1) / BWD_BLK, ws.nrc, (g.n + ws.nrc - 1) / ws.nrc};
-  const int64_t nrow = (int64_t)a.nblk * g.n * g.H;
+               (g.n + BWD_BLK - 1) / BWD_BLK, ws.nrc, (g.nr + ws.nrc - 1) / ws.nrc};
+  const int64_t nrow = (int64_t)a.nblk * g.nr * g.H;
   {
     // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
     if constexpr (std::is_same<T, bf16>::value) {
       const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
-      const int64_t nwg = (int64_t)nqb * ((g.n + QD_ROWS - 1) / QD_ROWS) * g.H;
+      const int64_t nwg = (int64_t)nqb * ((g.nr + QD_ROWS - 1) / QD_ROWS) * g.H;
       hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(64 * QD_WAVES), 0, s, a, nqb);
     } else {
       hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
@@ -1288,7 +1289,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     KernelTimer t(K_DKDV, s);
     if constexpr (std::is_same<T, bf16>::value) {
-      const int64_t nwg = (int64_t)a.nblk * ((g.n + KD_ROWS - 1) / KD_ROWS) * g.H;
+      const int64_t nwg = (int64_t)a.nblk * ((g.nr + KD_ROWS - 1) / KD_ROWS) * g.H;
       hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(64 * KD_WAVES), 0, s, a);
     } else {
       hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
@@ -1307,8 +1308,12 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     const int64_t nred = (int64_t)g.H * g.n * ((g.n + 3) / 4);
     KernelTimer t(K_DB_REDUCE, s);
-    hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0, s,
-                       g, node, ws.nrc, ws.slabs, dbias);
+    if (dbias_f32)
+      hipLaunchKernelGGL(db_reduce_kernel<float>, dim3((unsigned)((nred + 255) / 256)), dim3(256),
+                         0, s, g, node, ws.nrc, ws.slabs, dbias_f32);
+    else
+      hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0,
+                         s, g, node, ws.nrc, ws.slabs, dbias);
   }
   return hipGetLastError();
 }
@@ -1316,10 +1321,10 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
 template hipError_t launch_bwd<bf16>(const Geom&, int, const Prep&, const BwdWs&, const bf16*,
                                      const bf16*, const bf16*, const bf16*, const bf16*,
                                      const float*, const bf16*, bf16*, bf16*, bf16*, bf16*,
-                                     bf16*, hipStream_t);
+                                     bf16*, float*, hipStream_t);
 template hipError_t launch_bwd<float>(const Geom&, int, const Prep&, const BwdWs&, const float*,
                                       const float*, const float*, const float*, const float*,
                                       const float*, const float*, float*, float*, float*, float*,
-                                      float*, hipStream_t);
+                                      float*, float*, hipStream_t);
 
 }  // namespace triattn

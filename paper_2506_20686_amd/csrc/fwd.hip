@@ -89,7 +89,7 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
   }
   {
     KernelTimer t(K_PREP_KBITS, s);
-    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.n), dim3(256), 0, s, g, node, mask,
+    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.nr), dim3(256), 0, s, g, node, mask,
                        p.kbits, p.rowfull);
   }
   return hipGetLastError();
@@ -132,9 +132,9 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int qb = w % a.nqb, rh = w / a.nqb;
-  const int nrp = (G.n + FWD_ROWS - 1) / FWD_ROWS;
+  const int nrp = (G.nr + FWD_ROWS - 1) / FWD_ROWS;
   const int r0 = (rh % nrp) * FWD_ROWS, h = rh / nrp;
-  const bool row1 = FWD_ROWS > 1 && r0 + 1 < G.n;  // the second row exists
+  const bool row1 = FWD_ROWS > 1 && r0 + 1 < G.nr;  // the second row exists
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int q0 = qb * FWD_QBLK + wave * TILE;  // first query of this wave
   const bool active = q0 < G.n;
@@ -145,14 +145,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   __shared__ __align__(16) T ks[2 * FWD_ROWS * ROW_TILE];
   __shared__ __align__(16) T vt[2 * FWD_ROWS * TRANS_TILE];
 
-  const int last = G.n - 1;
+  const int last = G.n - 1;  // last key position
   int64_t rowbase[FWD_ROWS];
   typename M::frag qf[FWD_ROWS][M::KCH];
   const uint32_t* kb[FWD_ROWS];
   SoftmaxState st[FWD_ROWS];
 #pragma unroll
   for (int i = 0; i < FWD_ROWS; ++i) {
-    const int r = min(r0 + i, last);
+    const int r = min(r0 + i, G.nr - 1);
     rowbase[i] = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
     kb[i] = a.kbits + (int64_t)r * G.nkt;
     if (qok)
@@ -375,17 +375,17 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   using F = bf16x8;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int nrg = (G.n + FO_ROWS - 1) / FO_ROWS;
+  const int nrg = (G.nr + FO_ROWS - 1) / FO_ROWS;
   const int qb = w % a.nqb, rg = (w / a.nqb) % nrg, h = w / (a.nqb * nrg);
   const int r0 = rg * FO_ROWS;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qh = wave & 1, ri = wave >> 1;
   const int row = r0 + ri;  // this wave's row
-  const bool rok = row < G.n;
-  const int nkt = G.nkt, last = G.n - 1;
+  const bool rok = row < G.nr;
+  const int nkt = G.nkt, last = G.nr - 1;  // last row
   const float c1 = G.scale * LOG2E;
-  const int nrows = min(FO_ROWS, G.n - r0);  // rows of this group that exist
+  const int nrows = min(FO_ROWS, G.nr - r0);  // rows of this group that exist
 
   __shared__ __align__(16) char smem[FO_SLOTS * FO_SLOT];
 
@@ -421,7 +421,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   // counts uniform.
   const int dblk = wave;  // K0..K3, V0..V3
   const int dp = lane >> 2;
-  const int64_t tensor = (int64_t)G.n * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
   const bf16* dsrc = dblk < 4 ? a.k : a.v;
   const bf16* dptr = dsrc + (int64_t)min(r0 + (dblk & 3), last) * G.sRow + hb;
   const bf16* const dend = dsrc + tensor;
@@ -622,11 +622,11 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, p.rowfull, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   if constexpr (std::is_same<T, bf16>::value) {
-    const int64_t nwg = (int64_t)a.nqb * ((g.n + FO_ROWS - 1) / FO_ROWS) * g.H;
+    const int64_t nwg = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a);
   } else {
-    const int64_t nwg = (int64_t)a.nqb * ((g.n + FWD_ROWS - 1) / FWD_ROWS) * g.H;
+    const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL(fwd_kernel<T>, dim3((unsigned)nwg), dim3(256), 0, s, a);
   }

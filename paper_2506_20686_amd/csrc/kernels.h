@@ -13,11 +13,12 @@ namespace triattn {
 // ending node row = b and position = a, so the ending node is the same
 // kernel with the two strides swapped; no transpose copy is made.
 struct Geom {
-  int n;     // tokens per pair axis
+  int n;     // tokens per pair axis (queries and keys of a row)
+  int nr;    // rows this call computes (n, or a row range's length)
   int H;     // heads
   int np;    // n rounded up to a multiple of 32
   int nkt;   // np / 32 key tiles
-  int64_t sRow, sPos;  // element strides of [n][n][H][32] tensors
+  int64_t sRow, sPos;  // element strides of [nr][n][H][32] tensors
   int64_t lRow, lPos;  // element strides of [n][n][H] tensors (lse)
   float scale;         // softmax scale on Q K^T
 };
@@ -27,14 +28,14 @@ struct Prep {
   float* bt;       // [H][np/32][np/32][1024] bias(q, k) / scale in accumulator order,
                    //   lanes <-> queries (zero padded)
   float* btT;      // the same with lanes <-> keys (backward only; may be null)
-  uint32_t* kbits; // [n][nkt]     bit e of word t: key 32 t + e is valid for that row
-  uint32_t* rowfull;  // [n]     1 iff every key < n is valid for that row, else 0
+  uint32_t* kbits; // [nr][nkt]    bit e of word t: key 32 t + e is valid for that row
+  uint32_t* rowfull;  // [nr]    1 iff every key < n is valid for that row, else 0
 };
 
 struct BwdWs {
-  float* lse2;   // [H][n][np]  lse * log2(e); +inf where the query has no valid key
-  float* dsum;   // [H][n][np]  -D, D = rowsum(dO * O) (stored negated: it enters as -D)
-  void* da;      // [n][n][H][32] dtype: dA = dO * sigmoid(G), laid out like dO
+  float* lse2;   // [H][nr][np]  lse * log2(e); +inf where the query has no valid key
+  float* dsum;   // [H][nr][np]  -D, D = rowsum(dO * O) (stored negated: it enters as -D)
+  void* da;      // [nr][n][H][32] dtype: dA = dO * sigmoid(G), laid out like dO
   void* dalo;    // bf16 only: dA - bf16(dA) rounded to bf16 (null for fp32)
   float* slabs;  // [nrc][H][np][np] per-row-chunk partial bias gradients
   int nrc;       // row chunks of the bias-gradient reduction
@@ -46,10 +47,13 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
 template <typename T>
 hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, const T* v,
                       const T* gate, T* out, float* lse, hipStream_t s);
+// dbias_f32, when not null, receives the bias gradient in fp32 (a row range's
+// partial sum, to be added to other ranges' before rounding) and dbias is unused.
 template <typename T>
 hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& w, const T* q,
                       const T* k, const T* v, const T* gate, const T* out, const float* lse,
-                      const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, hipStream_t s);
+                      const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, float* dbias_f32,
+                      hipStream_t s);
 
 // ---- fused layer-norm + linear projection (lnl.hip) ---------------------------------
 constexpr int LNL_K = 128;       // features per row (the pair channel width)

@@ -61,6 +61,39 @@ WORKLOADS = {
 HEADLINE = "tri_bf16_n768"
 
 
+@dataclasses.dataclass(frozen=True)
+class RowsWorkload:
+    """One GPU's share of a row-sharded starting node: rows [r0, r0 + rows)
+    of the named whole-map workload (G = n / rows GPUs)."""
+    name: str
+    base: str
+    r0: int
+    rows: int
+
+    @property
+    def flops_fwd_bwd(self) -> float:
+        w = WORKLOADS[self.base]
+        return 14.0 * self.rows * w.n ** 2 * w.h * w.d
+
+
+ROWS_WORKLOADS = {
+    # N = 768 split over 8 GPUs: the fourth GPU's 96 rows
+    "tri_rows_bf16_n768_r96": RowsWorkload("tri_rows_bf16_n768_r96", "tri_bf16_n768", 288, 96),
+}
+
+
+def rows_inputs(rw: RowsWorkload):
+    """The shard's inputs: q, k, v, g, dout, mask [rows, ...] (contiguous
+    slices of the whole map's starting-node inputs), the whole bias, plus the
+    whole map's inputs under "whole"."""
+    t = workload_inputs(WORKLOADS[rw.base], STARTING)
+    sl = slice(rw.r0, rw.r0 + rw.rows)
+    s = {k: t[k][sl].contiguous() for k in ("q", "k", "v", "g", "dout", "mask")}
+    s["bias"] = t["bias"]
+    s["whole"] = t
+    return s
+
+
 def key_mask(n: int, n_pad: int, node: int) -> torch.Tensor:
     """[n, n] uint8 mask that excludes the last n_pad tokens as keys."""
     m = (torch.arange(n) < n - n_pad).to(torch.uint8)

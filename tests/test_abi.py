@@ -214,3 +214,80 @@ LNL_BWD_BAD = [
 @pytest.mark.parametrize("over,code", LNL_BWD_BAD)
 def test_ln_linear_bwd_rejects_before_any_hip_call(lib, over, code):
     assert lib.tri_ln_linear_bwd(*lnl_bwd_args(**over)) == code
+
+
+# ---- starting node over a range of rows -----------------------------------------------
+
+@pytest.mark.parametrize("dtype", [B.F32, B.BF16])
+def test_rows_workspace_sizes(lib, dtype):
+    for n, h in ((1, 1), (37, 1), (768, 4), (1536, 4)):
+        whole = [ws_bytes(f, B.STARTING, dtype, n, h, 32)[1]
+                 for f in (lib.tri_attn_fwd_workspace_bytes, lib.tri_attn_bwd_workspace_bytes)]
+        prev = [0, 0]
+        for rows in sorted({1, max(1, n // 8), max(1, n // 2), n}):
+            got = []
+            for f in (lib.tri_attn_rows_fwd_workspace_bytes, lib.tri_attn_rows_bwd_workspace_bytes):
+                st, b = ws_bytes(f, dtype, n, rows, h, 32)
+                assert st == B.OK
+                got.append(b)
+            # the whole range needs what the whole call needs; fewer rows never need more
+            assert all(g >= p for g, p in zip(got, prev))
+            if rows == n:
+                assert got == whole
+            prev = got
+
+
+def test_rows_workspace_size_errors(lib):
+    for f in (lib.tri_attn_rows_fwd_workspace_bytes, lib.tri_attn_rows_bwd_workspace_bytes):
+        assert ws_bytes(f, B.BF16, 16, 0, 2, 32)[0] == B.ERR_INVALID_ARG
+        assert ws_bytes(f, B.BF16, 16, 17, 2, 32)[0] == B.ERR_INVALID_ARG
+        assert ws_bytes(f, B.BF16, 16, -1, 2, 32)[0] == B.ERR_INVALID_ARG
+        assert ws_bytes(f, 7, 16, 4, 2, 32)[0] == B.ERR_INVALID_ARG
+        assert ws_bytes(f, B.BF16, 16, 4, 2, 64)[0] == B.ERR_UNSUPPORTED
+        assert f(B.BF16, 16, 4, 2, 32, None) == B.ERR_INVALID_ARG
+
+
+def rows_fwd_args(**over):
+    a = dict(dtype=B.BF16, n=16, rows=4, h=2, d=32, scale=0.17, q=P, k=P, v=P, g=P, bias=P,
+             mask=None, out=P, lse=P, ws=P, wsb=1 << 30, stream=None)
+    a.update(over)
+    return (a["dtype"], a["n"], a["rows"], a["h"], a["d"], a["scale"], a["q"], a["k"], a["v"],
+            a["g"], a["bias"], a["mask"], a["out"], a["lse"], a["ws"], a["wsb"], a["stream"])
+
+
+def rows_bwd_args(**over):
+    a = dict(dtype=B.BF16, n=16, rows=4, h=2, d=32, scale=0.17, q=P, k=P, v=P, g=P, bias=P,
+             mask=None, out=P, lse=P, dout=P, dq=P, dk=P, dv=P, dg=P, dbias=P, ws=P,
+             wsb=1 << 30, stream=None)
+    a.update(over)
+    return (a["dtype"], a["n"], a["rows"], a["h"], a["d"], a["scale"], a["q"], a["k"], a["v"],
+            a["g"], a["bias"], a["mask"], a["out"], a["lse"], a["dout"], a["dq"], a["dk"],
+            a["dv"], a["dg"], a["dbias"], a["ws"], a["wsb"], a["stream"])
+
+
+ROWS_BAD = [(o, c) for o, c in FWD_BAD if "node" not in o] + [
+    (dict(rows=0), B.ERR_INVALID_ARG), (dict(rows=17), B.ERR_INVALID_ARG),
+    (dict(rows=-3), B.ERR_INVALID_ARG),
+]
+
+
+@pytest.mark.parametrize("over,code", ROWS_BAD)
+def test_rows_fwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_rows_fwd(*rows_fwd_args(**over)) == code
+
+
+@pytest.mark.parametrize("over,code", ROWS_BAD + [(o, c) for o, c in BWD_BAD
+                                                   if o not in [x for x, _ in FWD_BAD]])
+def test_rows_bwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_rows_bwd(*rows_bwd_args(**over)) == code
+
+
+def test_rows_undersized_workspace(lib):
+    for rows in (1, 5, 16):
+        for f, call, mk in ((lib.tri_attn_rows_fwd_workspace_bytes, lib.tri_attn_rows_fwd,
+                             rows_fwd_args),
+                            (lib.tri_attn_rows_bwd_workspace_bytes, lib.tri_attn_rows_bwd,
+                             rows_bwd_args)):
+            st, need = ws_bytes(f, B.BF16, 16, rows, 2, 32)
+            assert st == B.OK
+            assert call(*mk(rows=rows, wsb=need - 1)) == B.ERR_WORKSPACE
