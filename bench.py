@@ -23,6 +23,10 @@ features -> Q, K, V, G [m][128] and the bias logits [m][4]): one step is its
 forward and backward, the metric is algorithmic HBM GB/s (every input read
 once, every output written once, per step time), and the roofline is HBM
 bandwidth.
+
+--workload tri_rows_bf16_n768_r96 measures one GPU's share of the row-sharded
+starting node (Section IV-B): rows 288..383 of the N = 768 map through the
+row-range entry points, forward and backward, nominal 14 R N^2 H d flop.
 """
 from __future__ import annotations
 
@@ -57,7 +61,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=None,
                     help="workload name (default: the N=768 attention one; lnl_bf16_n768 runs "
-                         "the fused layer-norm + linear projection)")
+                         "the fused layer-norm + linear projection; tri_rows_bf16_n768_r96 "
+                         "one GPU's 96-row shard of the starting node)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -112,10 +117,11 @@ def recorded_traffic(kernel, workload, family="tri"):
     return float(m.group(1))
 
 
-def cpu_baseline(w, t, target_s):
+def cpu_baseline(w, t, target_s, row_range=None):
     """Time the fp64 oracle (as it stands) on rows of the starting node: the
     forward and the per-row gradients (dQ, dK, dV, dG) of R rows, nominal
-    14 N^2 H d flop per row.  R is sized from a trial of one row per thread."""
+    14 N^2 H d flop per row.  R is sized from a trial of one row per thread;
+    row_range = (r0, rows) draws them from that range only."""
     import numpy as np
 
     import oracle
@@ -133,16 +139,18 @@ def cpu_baseline(w, t, target_s):
 
     # the oracle spreads rows over its threads: size the sample from a trial
     # with one row per thread
-    nt = max(1, min(w.n, oracle.max_threads()))
-    trial = run(list(range(nt)))
-    rows = max(nt, min(w.n, int(nt * target_s / max(trial, 1e-3)) // nt * nt))
-    sel = [int(i * w.n / rows) for i in range(rows)]
+    r0, span = (0, w.n) if row_range is None else row_range
+    nt = max(1, min(span, oracle.max_threads()))
+    trial = run(list(range(r0, r0 + nt)))
+    rows = max(nt, min(span, int(nt * target_s / max(trial, 1e-3)) // nt * nt))
+    sel = [r0 + int(i * span / rows) for i in range(rows)]
     dt = run(sel)
     flop = 14.0 * w.n ** 2 * w.h * w.d * rows
+    where = f"{w.n} rows" if row_range is None else f"rows {r0}..{r0 + span - 1} of {w.n}"
     return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(),
             "kind": "oracle", "seconds": round(dt, 3),
             "sample": f"starting node of {w.name}: forward + per-row gradients (dQ, dK, dV, dG) "
-                      f"of {rows} of {w.n} rows, fp64, nominal 14*N^2*H*d flop per row; "
+                      f"of {rows} of {where}, fp64, nominal 14*N^2*H*d flop per row; "
                       f"dB (a row sum of the same dS) not included"}
 
 
@@ -279,6 +287,106 @@ def bench_lnl(args, name):
     print(json.dumps(out), flush=True)
 
 
+def bench_rows(args, name):
+    """One GPU's share of the row-sharded starting node: forward + backward of
+    `rows` rows of the whole map through tri_attn_rows_{fwd,bwd}, shard-local
+    tensors, the whole bias, an fp32 bias-gradient term.  Nominal 14 R N^2 H d
+    flop per step; MFMA roofline of the dominant kernel."""
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    from paper_2506_20686_amd import workloads as W
+
+    rw = W.ROWS_WORKLOADS[name]
+    w = W.WORKLOADS[rw.base]
+    dev = torch.device("cuda:0")
+    dt = B.BF16
+    n, h, d, R = w.n, w.h, w.d, rw.rows
+    scale = 1.0 / math.sqrt(d)
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    s = W.rows_inputs(rw)
+    x = {k: s[k].to(dev) for k in ("q", "k", "v", "g", "bias", "dout", "mask")}
+    x["out"] = torch.empty_like(x["q"])
+    x["lse"] = torch.empty((R, n, h), dtype=torch.float32, device=dev)
+    for gname in ("dq", "dk", "dv", "dg"):
+        x[gname] = torch.empty_like(x["q"])
+    x["dbp"] = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+    ws_bytes = max(B.tri_attn_rows_fwd_workspace_bytes(dt, n, R, h, d),
+                   B.tri_attn_rows_bwd_workspace_bytes(dt, n, R, h, d))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda a: a.data_ptr()  # noqa: E731
+
+    def step():
+        st = B.tri_attn_rows_fwd(dt, n, R, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                 P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
+                                 P(ws), ws_bytes, stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_attn_rows_fwd")
+        st = B.tri_attn_rows_bwd(dt, n, R, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                 P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
+                                 P(x["dout"]), P(x["dq"]), P(x["dk"]), P(x["dv"]), P(x["dg"]),
+                                 P(x["dbp"]), P(ws), ws_bytes, stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_attn_rows_bwd")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    B.tri_attn_timing_reset()
+    B.tri_attn_timing_enable(True)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize(dev)
+    t1 = time.perf_counter()
+    B.tri_attn_timing_enable(False)
+    ktimes = B.kernel_times()
+    peak_bytes = torch.cuda.max_memory_allocated(dev)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    tflops = rw.flops_fwd_bwd / (ms * 1e-3) / 1e12
+    peak = MFMA_BF16_PEAK_TFLOPS
+    per_kernel = {k: {"avg_ms": round(v[0] / v[1], 5), "launches": v[1],
+                      "share": round(v[0] / max(1e-9, sum(y[0] for y in ktimes.values())), 4)}
+                  for k, v in ktimes.items() if v[1] > 0}
+    dom = max((k for k in per_kernel if k in KERNEL_FLOP_PER_LOGIT_D),
+              key=lambda k: ktimes[k][0])
+    avg_s = ktimes[dom][0] / ktimes[dom][1] * 1e-3
+    achieved = KERNEL_FLOP_PER_LOGIT_D[dom] * d * R * n * n * h / avg_s / 1e12
+    out = {
+        "metric": f"triangle-attn fwd+bwd TFLOP/s on one GPU's {R}-row shard of the N={n} "
+                  "starting node",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals, rows of the N=768 attention workload's inputs)",
+        "config": {"workload": name, "n": n, "rows": R, "first_row": rw.r0, "heads": h,
+                   "head_dim": d, "nodes": ["starting"], "mask": "all keys valid",
+                   "parallelism": f"one of {n // R} row shards (1 GPU)"},
+        "pct_of_peak": round(100.0 * tflops / peak, 3),
+        "peak_hbm_bytes": int(peak_bytes),
+        "workspace_bytes": int(ws_bytes),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 3),
+                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 5),
+                     "traffic": recorded_traffic(dom, name)},
+        "per_kernel": per_kernel,
+    }
+    out["cpu_baseline"] = (cpu_baseline(w, s["whole"], args.cpu_seconds, (rw.r0, R))
+                           if args.cpu_seconds > 0 else None)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -306,6 +414,9 @@ def main():
     name = args.workload or W.HEADLINE
     if name in W.LNL_WORKLOADS:
         bench_lnl(args, name)
+        return
+    if name in W.ROWS_WORKLOADS:
+        bench_rows(args, name)
         return
     w = W.WORKLOADS[name]
     dev = torch.device("cuda:0")

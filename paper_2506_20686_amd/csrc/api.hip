@@ -28,17 +28,27 @@ int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Row chunks of the bias-gradient reduction over nr rows: about 2304
-// workgroups of 128 queries x 128 keys (nine rounds of one per CU on 256
-// CUs), at most 16 partial slabs.
+// Row chunks of the bias-gradient reduction over nr rows (at most 16 partial
+// slabs).  Each workgroup of the bias-gradient kernel takes 128 queries x 128
+// keys of one head over one chunk of rows and fills a CU on its own, so the
+// kernel runs in rounds of 256 workgroups.  The cost model, in units of one
+// row's work: per round the chunk's rows plus about 3.3 for the workgroup's
+// fixed work (bias tile, pipeline fill, slab store), plus about 1 per slab
+// for the reduction that reads the slabs back.
 int db_row_chunks(int64_t n, int64_t nr, int64_t h) {
   const int64_t tiles = h * ((n + 127) / 128) * ((n + 127) / 128);
-  int64_t c = (2304 + tiles - 1) / tiles;
-  if (c > 16) c = 16;
-  if (c > nr) c = nr;
-  if (c < 1) c = 1;
-  const int64_t rpc = (nr + c - 1) / c;
-  return (int)((nr + rpc - 1) / rpc);
+  int best = 1;
+  double best_cost = 1e300;
+  for (int64_t c = 1; c <= 16 && c <= nr; ++c) {
+    const int64_t rpc = (nr + c - 1) / c, chunks = (nr + rpc - 1) / rpc;
+    const int64_t rounds = (tiles * chunks + 255) / 256;
+    const double cost = (double)rounds * ((double)rpc + 3.3) + (double)chunks;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = (int)chunks;
+    }
+  }
+  return best;
 }
 
 struct Layout {
