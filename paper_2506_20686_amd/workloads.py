@@ -188,3 +188,41 @@ def lnl_step_bytes(m: int, cols=LNL_COLS, k: int = LNL_K) -> dict:
     fwd = m * k * 2 + m * n * 2 + m * 8 + k * n * 2 + 4 * k
     bwd = m * k * 2 + m * n * 2 + m * 8 + m * k * 2 + k * n * (2 + 4) + 4 * k + 8 * k
     return {"fwd": fwd, "bwd": bwd}
+
+
+# ---- transition layer ------------------------------------------------------------------
+
+# The pair transition of an AF3 pair stack: c_z = 128 features, SwiGLU hidden
+# width F = 4 c_z = 512 (W1 [128][1024], W2 [512][128]).
+TRN_C = 128
+TRN_F = 512
+
+
+def trn_inputs(m: int, seed: int = 0, c: int = TRN_C, f: int = TRN_F):
+    """x [m, c] ~ N(0.3, 1.5^2); gamma ~ 1 + 0.2 N(0, 1); beta ~ 0.2 N(0, 1);
+    W1 [c, 2f] ~ N(0, 1/c); W2 [f, c] ~ N(0, 1/f); dout [m, c] ~ N(0, 1);
+    drawn in that order from one CPU generator, rounded to bf16."""
+    gen = torch.Generator("cpu").manual_seed(seed)
+
+    def draw(shape, std=1.0, mean=0.0):
+        return (torch.randn(*shape, generator=gen) * std + mean).to(torch.bfloat16)
+
+    x = draw((m, c), 1.5, 0.3)
+    gamma = draw((c,), 0.2, 1.0)
+    beta = draw((c,), 0.2)
+    w1 = draw((c, 2 * f), 1.0 / math.sqrt(c))
+    w2 = draw((f, c), 1.0 / math.sqrt(f))
+    dout = draw((m, c))
+    return dict(x=x, gamma=gamma, beta=beta, w1=w1, w2=w2, dout=dout)
+
+
+# The benchmark shape: the pair representation of the N = 768 map.
+TRN_WORKLOADS = {"trn_bf16_n768": 768 * 768, "trn_bf16_n64": 64 * 64}
+
+
+def trn_step_flops(m: int, c: int = TRN_C, f: int = TRN_F) -> float:
+    """Algorithmic flop of one forward + backward: forward o1 W1 (2 m c 2f) and
+    u W2 (2 m f c); backward du (2 m c f), dW2 (2 m f c), dW1 (2 m c 2f) and
+    do1 (2 m 2f c): 18 m c f in all (the backward's recomputation of o1 W1 is
+    not counted)."""
+    return 18.0 * m * c * f
