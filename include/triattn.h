@@ -179,6 +179,48 @@ int tri_ln_linear_bwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t*
                       float* dw, float* dgamma, float* dbeta, void* workspace,
                       size_t workspace_bytes, void* stream);
 
+/* Fused transition layer (Section IV: fused layer-norm & linear projection,
+ * fused SwiGLU, fused transition layer; forward and backward in the
+ * appendix listing of the transition layer).  For every row x of x [m][c]:
+ *   o1 = (x - mean) * rstd * gamma + beta,  rstd = 1 / sqrt(var + eps),
+ *        mean and var (biased) over the row's c features;
+ *   [a | b] = o1 W1,  W1 [c][2f]: a = columns 0..f-1, b = columns f..2f-1;
+ *   u = a * sigmoid(a) * b                    (SwiGLU)
+ *   out = u W2,  W2 [f][c].
+ * out [m][c] (dtype) and mean, rstd [m] (fp32, saved for the backward).
+ * Neither [a | b] nor u is written to memory.
+ *   dtype: TRIATTN_BF16 only (x, gamma [c], beta [c], W1, W2, out; fp32
+ *          statistics and accumulation), TRIATTN_ERR_UNSUPPORTED else.
+ *   c must be 128; f a multiple of 128, at most 2048; 1 <= m <= 2^31;
+ *   eps finite and >= 0.  Pointers are device memory, 16-byte aligned.
+ *   The workspace (size from the matching call) holds the weights in the
+ *   order the kernels read them.  Same stream and error rules as above. */
+int tri_transition_fwd_workspace_bytes(int dtype, int64_t m, int64_t c, int64_t f,
+                                       size_t* bytes);
+int tri_transition_fwd(int dtype, int64_t m, int64_t c, int64_t f, float eps, const void* x,
+                       const void* gamma, const void* beta, const void* w1, const void* w2,
+                       void* out, float* mean, float* rstd, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* Backward of the transition layer for L = sum(dout * out): takes the
+ * forward's x, gamma, beta, W1, W2, its saved mean and rstd, and dout
+ * [m][c]; recomputes [a | b] and writes dx [m][c] (dtype) and dW1 [c][2f],
+ * dW2 [f][c], dgamma [c], dbeta [c] (fp32 sums over rows taken in a fixed
+ * order: bitwise reproducible).  With du = dout W2^T:
+ *   da = du * b * sigmoid(a) * (1 + a (1 - sigmoid(a))),  db = du * a * sigmoid(a),
+ *   dW2 = u^T dout,  dW1 = o1^T [da | db],  do1 = [da | db] W1^T,
+ *   dgamma = sum over rows of do1 * xhat,  dbeta = sum over rows of do1,
+ *   dx = rstd (do1 gamma - c1 xhat - c2), c1 and c2 the row means of
+ *   xhat do1 gamma and of do1 gamma.
+ * Same size, pointer, workspace, stream and error rules as the forward. */
+int tri_transition_bwd_workspace_bytes(int dtype, int64_t m, int64_t c, int64_t f,
+                                       size_t* bytes);
+int tri_transition_bwd(int dtype, int64_t m, int64_t c, int64_t f, const void* x,
+                       const void* gamma, const void* beta, const void* w1, const void* w2,
+                       const float* mean, const float* rstd, const void* dout, void* dx,
+                       float* dw1, float* dw2, float* dgamma, float* dbeta, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code ("unknown status" otherwise). */
 const char* tri_attn_status_string(int status);
 

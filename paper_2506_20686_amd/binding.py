@@ -67,6 +67,15 @@ def lib():
         L.tri_ln_linear_bwd.argtypes = [_int, _i64, _i64, _int, _i64p, _vp, _vp, _vp, _vp, _vp,
                                         _vp, ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _vp, _sz,
                                         _vp]
+        L.tri_transition_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _i64,
+                                                         ctypes.POINTER(_sz)]
+        L.tri_transition_bwd_workspace_bytes.argtypes = \
+            L.tri_transition_fwd_workspace_bytes.argtypes
+        L.tri_transition_fwd.argtypes = [_int, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
+        L.tri_transition_bwd.argtypes = [_int, _i64, _i64, _i64] + [_vp] * 14 + [_sz, _vp]
+        for name in ("tri_transition_fwd_workspace_bytes", "tri_transition_bwd_workspace_bytes",
+                     "tri_transition_fwd", "tri_transition_bwd"):
+            getattr(L, name).restype = _int
         for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
                      "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
                      "tri_attn_timing_reset", "tri_attn_timing_read",
@@ -176,6 +185,37 @@ def tri_ln_linear_bwd(dtype, m, k, cols, x, gamma, beta, w, mean, rstd, douts, d
     return lib().tri_ln_linear_bwd(dtype, m, k, len(cols), _cols_arr(cols), x, gamma, beta, w,
                                    mean, rstd, douts_arr, dx, dw, dgamma, dbeta, workspace,
                                    workspace_bytes, stream)
+
+
+def tri_transition_fwd_workspace_bytes(dtype: int, m: int, c: int, f: int) -> int:
+    out = _sz(0)
+    st = lib().tri_transition_fwd_workspace_bytes(dtype, m, c, f, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_transition_fwd_workspace_bytes")
+    return out.value
+
+
+def tri_transition_bwd_workspace_bytes(dtype: int, m: int, c: int, f: int) -> int:
+    out = _sz(0)
+    st = lib().tri_transition_bwd_workspace_bytes(dtype, m, c, f, ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_transition_bwd_workspace_bytes")
+    return out.value
+
+
+def tri_transition_fwd(dtype, m, c, f, eps, x, gamma, beta, w1, w2, out, mean, rstd, workspace,
+                       workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_transition_fwd(dtype, m, c, f, eps, x, gamma, beta, w1, w2, out, mean,
+                                    rstd, workspace, workspace_bytes, stream)
+
+
+def tri_transition_bwd(dtype, m, c, f, x, gamma, beta, w1, w2, mean, rstd, dout, dx, dw1, dw2,
+                       dgamma, dbeta, workspace, workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_transition_bwd(dtype, m, c, f, x, gamma, beta, w1, w2, mean, rstd, dout,
+                                    dx, dw1, dw2, dgamma, dbeta, workspace, workspace_bytes,
+                                    stream)
 
 
 def tri_attn_timing_enable(on: bool) -> None:
@@ -437,3 +477,63 @@ def ln_linear_bwd(x, gamma, beta, w, mean, rstd, douts, eps: float = 1e-5,
     if st != OK:
         raise TriAttnError(st, "tri_ln_linear_bwd")
     return dx, dw, dgamma, dbeta
+
+
+# ---- fused transition layer -------------------------------------------------------------
+
+def _trn_common(x, gamma, beta, w1, w2):
+    if x.dim() != 2:
+        raise ValueError("x must be [m, c]")
+    m, c = x.shape
+    f = w2.shape[0]
+    dev = x.device
+    _check("x", x, (m, c), torch.bfloat16, dev)
+    _check("gamma", gamma, (c,), torch.bfloat16, dev)
+    _check("beta", beta, (c,), torch.bfloat16, dev)
+    _check("w1", w1, (c, 2 * f), torch.bfloat16, dev)
+    _check("w2", w2, (f, c), torch.bfloat16, dev)
+    return m, c, f, dev
+
+
+def transition_fwd(x, gamma, beta, w1, w2, eps: float = 1e-5,
+                   workspace: Optional[torch.Tensor] = None):
+    """out = (silu(a) * b) @ w2 with [a | b] = layer_norm(x) * gamma + beta
+    @ w1.  x [m, c] bf16, w1 [c, 2f], w2 [f, c].  Returns (out, mean, rstd)."""
+    m, c, f, dev = _trn_common(x, gamma, beta, w1, w2)
+    out = torch.empty_like(x)
+    mean = torch.empty(m, dtype=torch.float32, device=dev)
+    rstd = torch.empty(m, dtype=torch.float32, device=dev)
+    need = tri_transition_fwd_workspace_bytes(BF16, m, c, f)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_transition_fwd(BF16, m, c, f, float(eps), _ptr(x), _ptr(gamma), _ptr(beta),
+                            _ptr(w1), _ptr(w2), _ptr(out), _ptr(mean), _ptr(rstd),
+                            _ptr(workspace), workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_transition_fwd")
+    return out, mean, rstd
+
+
+def transition_bwd(x, gamma, beta, w1, w2, mean, rstd, dout,
+                   workspace: Optional[torch.Tensor] = None):
+    """Gradients of sum(dout * out) for transition_fwd.  Returns (dx [m, c]
+    bf16, dw1 [c, 2f], dw2 [f, c], dgamma [c], dbeta [c], all fp32 but dx)."""
+    m, c, f, dev = _trn_common(x, gamma, beta, w1, w2)
+    _check("mean", mean, (m,), torch.float32, dev)
+    _check("rstd", rstd, (m,), torch.float32, dev)
+    _check("dout", dout, (m, c), torch.bfloat16, dev)
+    dx = torch.empty_like(x)
+    dw1 = torch.empty((c, 2 * f), dtype=torch.float32, device=dev)
+    dw2 = torch.empty((f, c), dtype=torch.float32, device=dev)
+    dgamma = torch.empty(c, dtype=torch.float32, device=dev)
+    dbeta = torch.empty(c, dtype=torch.float32, device=dev)
+    need = tri_transition_bwd_workspace_bytes(BF16, m, c, f)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = tri_transition_bwd(BF16, m, c, f, _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w1),
+                            _ptr(w2), _ptr(mean), _ptr(rstd), _ptr(dout), _ptr(dx), _ptr(dw1),
+                            _ptr(dw2), _ptr(dgamma), _ptr(dbeta), _ptr(workspace),
+                            workspace.numel(), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_transition_bwd")
+    return dx, dw1, dw2, dgamma, dbeta

@@ -470,6 +470,134 @@ int tri_ln_linear_bwd(int dtype, int64_t m, int64_t k, int n_out, const int64_t*
   return TRIATTN_OK;
 }
 
+// ---- fused transition layer ---------------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+constexpr int64_t TRN_MAX_F = 2048;
+
+int trn_check(int dtype, int64_t m, int64_t c, int64_t f) {
+  if (dtype != TRIATTN_F32 && dtype != TRIATTN_BF16) return TRIATTN_ERR_INVALID_ARG;
+  if (m < 1 || m > ((int64_t)1 << 31) || c < 1 || f < 1) return TRIATTN_ERR_INVALID_ARG;
+  if (dtype != TRIATTN_BF16 || c != triattn::TRN_C || f % triattn::TRN_GROUP != 0 ||
+      f > TRN_MAX_F)
+    return TRIATTN_ERR_UNSUPPORTED;
+  return TRIATTN_OK;
+}
+
+struct TrnLayout {
+  size_t img, part, gsum, total;
+  int nparts;
+};
+
+TrnLayout trn_plan(bool bwd, int64_t m, int64_t f) {
+  TrnLayout L{};
+  const size_t nch = (size_t)(f / triattn::TRN_FC);
+  L.img = 0;
+  size_t off = round256(nch * (bwd ? triattn::TRN_BWD_IMG : triattn::TRN_FWD_IMG));
+  if (bwd) {
+    L.nparts = triattn::trn_bwd_parts(m, (int)f);
+    L.part = off;
+    off += round256((size_t)L.nparts * (size_t)triattn::trn_part_floats((int)f) * sizeof(float));
+    L.gsum = off;
+    off += round256(((size_t)triattn::TRN_C * 2 * f + 2 * f) * sizeof(float));
+  }
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_transition_fwd_workspace_bytes(int dtype, int64_t m, int64_t c, int64_t f,
+                                       size_t* bytes) {
+  const int st = trn_check(dtype, m, c, f);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = trn_plan(false, m, f).total;
+  return TRIATTN_OK;
+}
+
+int tri_transition_bwd_workspace_bytes(int dtype, int64_t m, int64_t c, int64_t f,
+                                       size_t* bytes) {
+  const int st = trn_check(dtype, m, c, f);
+  if (st != TRIATTN_OK) return st;
+  if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = trn_plan(true, m, f).total;
+  return TRIATTN_OK;
+}
+
+int tri_transition_fwd(int dtype, int64_t m, int64_t c, int64_t f, float eps, const void* x,
+                       const void* gamma, const void* beta, const void* w1, const void* w2,
+                       void* out, float* mean, float* rstd, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = trn_check(dtype, m, c, f);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(eps) && eps >= 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {x, gamma, beta, w1, w2, out, mean, rstd};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const TrnLayout L = trn_plan(false, m, f);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  triattn::TrnFwdArgs a{};
+  a.m = m;
+  a.f = (int)f;
+  a.eps = eps;
+  a.x = (const triattn::bf16*)x;
+  a.gamma = (const triattn::bf16*)gamma;
+  a.beta = (const triattn::bf16*)beta;
+  a.w1 = (const triattn::bf16*)w1;
+  a.w2 = (const triattn::bf16*)w2;
+  a.img = (char*)workspace + L.img;
+  a.out = (triattn::bf16*)out;
+  a.mean = mean;
+  a.rstd = rstd;
+  return triattn::launch_trn_fwd(a, (hipStream_t)stream) == hipSuccess ? TRIATTN_OK
+                                                                        : TRIATTN_ERR_HIP;
+}
+
+int tri_transition_bwd(int dtype, int64_t m, int64_t c, int64_t f, const void* x,
+                       const void* gamma, const void* beta, const void* w1, const void* w2,
+                       const float* mean, const float* rstd, const void* dout, void* dx,
+                       float* dw1, float* dw2, float* dgamma, float* dbeta, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int st = trn_check(dtype, m, c, f);
+  if (st != TRIATTN_OK) return st;
+  const void* ptrs[] = {x, gamma, beta, w1, w2, mean, rstd, dout, dx, dw1, dw2, dgamma, dbeta};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const TrnLayout L = trn_plan(true, m, f);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  triattn::TrnBwdArgs a{};
+  a.m = m;
+  a.f = (int)f;
+  a.x = (const triattn::bf16*)x;
+  a.gamma = (const triattn::bf16*)gamma;
+  a.beta = (const triattn::bf16*)beta;
+  a.w1 = (const triattn::bf16*)w1;
+  a.w2 = (const triattn::bf16*)w2;
+  a.mean = mean;
+  a.rstd = rstd;
+  a.dout = (const triattn::bf16*)dout;
+  a.dx = (triattn::bf16*)dx;
+  a.dw1 = dw1;
+  a.dw2 = dw2;
+  a.dgamma = dgamma;
+  a.dbeta = dbeta;
+  char* b = (char*)workspace;
+  a.img = b + L.img;
+  a.part = (float*)(b + L.part);
+  a.gsum = (float*)(b + L.gsum);
+  a.nparts = L.nparts;
+  return triattn::launch_trn_bwd(a, (hipStream_t)stream) == hipSuccess ? TRIATTN_OK
+                                                                        : TRIATTN_ERR_HIP;
+}
+
 const char* tri_attn_status_string(int status) {
   switch (status) {
     case TRIATTN_OK: return "ok";

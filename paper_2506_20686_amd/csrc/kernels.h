@@ -116,4 +116,42 @@ int lnl_bwd_partials(int64_t m);
 size_t lnl_bwd_workspace(int64_t m, int np);
 hipError_t launch_lnl_bwd(const LnlBwdArgs& a, hipStream_t s);
 
+// ---- fused transition layer (trn.hip) -----------------------------------------------
+constexpr int TRN_C = 128;         // features per row (the pair channel width)
+constexpr int TRN_FC = 32;         // hidden columns per weight chunk
+constexpr int TRN_FWD_IMG = 24576; // bytes of one chunk's forward weight image
+constexpr int TRN_BWD_IMG = 40960; // bytes of one chunk's backward weight image
+constexpr int TRN_GROUP = 128;     // hidden columns per workgroup of the weight-gradient kernel
+
+struct TrnFwdArgs {
+  int64_t m;                     // rows
+  int f;                         // hidden width F (a multiple of TRN_GROUP)
+  float eps;
+  const bf16 *x, *gamma, *beta;  // x [m][C], gamma and beta [C]
+  const bf16 *w1, *w2;           // W1 [C][2F], W2 [F][C]
+  char* img;                     // workspace: F / 32 forward chunk images
+  bf16* out;                     // [m][C]
+  float *mean, *rstd;            // [m], saved for the backward
+};
+
+struct TrnBwdArgs {
+  int64_t m;
+  int f;
+  const bf16 *x, *gamma, *beta, *w1, *w2;
+  const float *mean, *rstd;      // forward statistics
+  const bf16* dout;              // [m][C]
+  bf16* dx;                      // [m][C]
+  float *dw1, *dw2, *dgamma, *dbeta;  // [C][2F], [F][C], [C], [C]
+  char* img;                     // workspace: F / 32 backward chunk images
+  float* part;                   // workspace: nparts partial sums (see trn_part_floats)
+  float* gsum;                   // workspace: G [C][2F] and s [2F] totals
+  int nparts;                    // row partitions of the weight-gradient kernel
+};
+
+// Floats of one partial-sum block: G [C][2F], s [2F], dW2 [F][C].
+__host__ __device__ inline int64_t trn_part_floats(int f) { return (int64_t)TRN_C * 2 * f + 2 * f + (int64_t)f * TRN_C; }
+int trn_bwd_parts(int64_t m, int f);
+hipError_t launch_trn_fwd(const TrnFwdArgs& a, hipStream_t s);
+hipError_t launch_trn_bwd(const TrnBwdArgs& a, hipStream_t s);
+
 }  // namespace triattn

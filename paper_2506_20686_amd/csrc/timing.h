@@ -21,6 +21,12 @@ enum KernelId {
   K_LNL_BWD_G,
   K_LNL_REDUCE,
   K_LNL_FINISH,
+  K_TRN_PACK,
+  K_TRN_FWD,
+  K_TRN_BWD_DX,
+  K_TRN_BWD_W,
+  K_TRN_REDUCE,
+  K_TRN_FINISH,
   K_COUNT
 };
 

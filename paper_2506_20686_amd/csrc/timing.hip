@@ -15,7 +15,9 @@ namespace {
 const char* const kNames[K_COUNT] = {"prep_bias",   "prep_kbits", "fwd",        "bwd_prep",
                                      "bwd_pad",     "dq",         "dkdv",       "db",
                                      "db_reduce",   "lnl_fwd",    "lnl_bwd_dx",
-                                     "lnl_bwd_g",   "lnl_reduce", "lnl_finish"};
+                                     "lnl_bwd_g",   "lnl_reduce", "lnl_finish",
+                                     "trn_pack",    "trn_fwd",    "trn_bwd_dx",
+                                     "trn_bwd_w",   "trn_reduce", "trn_finish"};
 
 struct Pending {
   int id;

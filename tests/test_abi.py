@@ -24,7 +24,7 @@ def lib():
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(tri_(?:attn|ln_linear)_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(tri_(?:attn|ln_linear|transition)_\w+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol(lib):
@@ -291,3 +291,78 @@ def test_rows_undersized_workspace(lib):
             st, need = ws_bytes(f, B.BF16, 16, rows, 2, 32)
             assert st == B.OK
             assert call(*mk(rows=rows, wsb=need - 1)) == B.ERR_WORKSPACE
+
+
+# ---- fused transition layer -----------------------------------------------------------
+
+def test_transition_workspace_sizes(lib):
+    for m, f in ((1, 128), (1000, 512), (768 * 768, 512), (4096, 2048)):
+        st, fw = ws_bytes(lib.tri_transition_fwd_workspace_bytes, B.BF16, m, 128, f)
+        assert st == B.OK and fw >= (f // 32) * 24576
+        st, bw = ws_bytes(lib.tri_transition_bwd_workspace_bytes, B.BF16, m, 128, f)
+        # weight images, at least one partial-sum block and the totals
+        assert st == B.OK and bw >= (f // 32) * 40960 + (128 * 2 * f * 2 + 4 * f + f * 128) * 4
+        # the workspace does not grow with m beyond the partial-sum blocks
+        assert bw < (f // 32) * 40960 + 257 * (128 * 2 * f + 2 * f + f * 128) * 4 + (1 << 20)
+    f = lib.tri_transition_fwd_workspace_bytes
+    assert ws_bytes(f, B.BF16, 0, 128, 512)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, B.BF16, 10, 128, 0)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, 9, 10, 128, 512)[0] == B.ERR_INVALID_ARG
+    assert ws_bytes(f, B.F32, 10, 128, 512)[0] == B.ERR_UNSUPPORTED
+    assert ws_bytes(f, B.BF16, 10, 64, 512)[0] == B.ERR_UNSUPPORTED
+    assert ws_bytes(f, B.BF16, 10, 128, 500)[0] == B.ERR_UNSUPPORTED
+    assert ws_bytes(f, B.BF16, 10, 128, 4096)[0] == B.ERR_UNSUPPORTED
+    assert f(B.BF16, 10, 128, 512, None) == B.ERR_INVALID_ARG
+
+
+def trn_fwd_args(**over):
+    a = dict(dtype=B.BF16, m=64, c=128, f=512, eps=1e-5, x=P, gamma=P, beta=P, w1=P, w2=P, out=P,
+             mean=P, rstd=P, ws=P, wsb=1 << 30, stream=None)
+    a.update(over)
+    return tuple(a[k] for k in ("dtype", "m", "c", "f", "eps", "x", "gamma", "beta", "w1", "w2",
+                                "out", "mean", "rstd", "ws", "wsb", "stream"))
+
+
+def trn_bwd_args(**over):
+    a = dict(dtype=B.BF16, m=64, c=128, f=512, x=P, gamma=P, beta=P, w1=P, w2=P, mean=P, rstd=P,
+             dout=P, dx=P, dw1=P, dw2=P, dgamma=P, dbeta=P, ws=P, wsb=1 << 30, stream=None)
+    a.update(over)
+    return tuple(a[k] for k in ("dtype", "m", "c", "f", "x", "gamma", "beta", "w1", "w2", "mean",
+                                "rstd", "dout", "dx", "dw1", "dw2", "dgamma", "dbeta", "ws", "wsb",
+                                "stream"))
+
+
+TRN_COMMON_BAD = [
+    (dict(dtype=5), B.ERR_INVALID_ARG), (dict(m=0), B.ERR_INVALID_ARG),
+    (dict(f=0), B.ERR_INVALID_ARG), (dict(dtype=B.F32), B.ERR_UNSUPPORTED),
+    (dict(c=96), B.ERR_UNSUPPORTED), (dict(f=200), B.ERR_UNSUPPORTED),
+    (dict(x=None), B.ERR_INVALID_ARG), (dict(w1=P + 8), B.ERR_INVALID_ARG),
+    (dict(gamma=None), B.ERR_INVALID_ARG), (dict(w2=None), B.ERR_INVALID_ARG),
+    (dict(mean=None), B.ERR_INVALID_ARG), (dict(rstd=P + 4), B.ERR_INVALID_ARG),
+    (dict(ws=None), B.ERR_WORKSPACE), (dict(wsb=100), B.ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("over,code", TRN_COMMON_BAD + [
+    (dict(eps=-1.0), B.ERR_INVALID_ARG), (dict(eps=float("nan")), B.ERR_INVALID_ARG),
+    (dict(out=None), B.ERR_INVALID_ARG)])
+def test_transition_fwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_transition_fwd(*trn_fwd_args(**over)) == code
+
+
+@pytest.mark.parametrize("over,code", TRN_COMMON_BAD + [
+    (dict(dout=None), B.ERR_INVALID_ARG), (dict(dx=None), B.ERR_INVALID_ARG),
+    (dict(dw1=None), B.ERR_INVALID_ARG), (dict(dw2=P + 2), B.ERR_INVALID_ARG),
+    (dict(dgamma=None), B.ERR_INVALID_ARG), (dict(dbeta=None), B.ERR_INVALID_ARG)])
+def test_transition_bwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_transition_bwd(*trn_bwd_args(**over)) == code
+
+
+def test_transition_undersized_workspace(lib):
+    for fn, call, mk in ((lib.tri_transition_fwd_workspace_bytes, lib.tri_transition_fwd,
+                          trn_fwd_args),
+                         (lib.tri_transition_bwd_workspace_bytes, lib.tri_transition_bwd,
+                          trn_bwd_args)):
+        st, need = ws_bytes(fn, B.BF16, 64, 128, 512)
+        assert st == B.OK
+        assert call(*mk(wsb=need - 1)) == B.ERR_WORKSPACE
