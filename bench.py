@@ -27,6 +27,10 @@ bandwidth.
 --workload tri_rows_bf16_n768_r96 measures one GPU's share of the row-sharded
 starting node (Section IV-B): rows 288..383 of the N = 768 map through the
 row-range entry points, forward and backward, nominal 14 R N^2 H d flop.
+
+--workload trn_bf16_n768 measures the fused transition layer (layer norm,
+W1 [128][1024], SwiGLU, W2 [512][128]) on the N = 768 pair representation
+(m = 768^2 rows): forward and backward, algorithmic 18 m c F flop per step.
 """
 from __future__ import annotations
 
@@ -62,7 +66,8 @@ def parse():
     ap.add_argument("--workload", default=None,
                     help="workload name (default: the N=768 attention one; lnl_bf16_n768 runs "
                          "the fused layer-norm + linear projection; tri_rows_bf16_n768_r96 "
-                         "one GPU's 96-row shard of the starting node)")
+                         "one GPU's 96-row shard of the starting node; trn_bf16_n768 the fused "
+                         "transition layer)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -89,6 +94,7 @@ def copy_calibration(nbytes):
 SOURCE_FAMILIES = {
     "tri": ("fwd.hip", "bwd.hip", "api.hip", "common.h", "dma.h", "stage.h", "kernels.h"),
     "lnl": ("lnl.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
+    "trn": ("trn.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
 }
 
 
@@ -287,6 +293,142 @@ def bench_lnl(args, name):
     print(json.dumps(out), flush=True)
 
 
+def trn_kernel_flops(m, c=128, f=512):
+    """MFMA flop per launch of the transition layer's main kernels: the
+    products each performs (the backward kernels recompute [a | b] = o1 W1
+    and du = dout W2^T, which counts here but not in the step's 18 m c f)."""
+    return {"trn_fwd": 6.0 * m * c * f,           # o1 W1 (2 m c 2f), u W2 (2 m f c)
+            "trn_bwd_dx": 10.0 * m * c * f,       # du, o1 W1, dh W1^T
+            "trn_bwd_w": 12.0 * m * c * f}        # o1 W1, du, xhat^T dh, u^T dout
+
+
+def trn_cpu_baseline(t, target_s):
+    """Time the fp64 oracle on a sample of R rows: forward, then the backward
+    of those rows with their sums over rows.  Unit: algorithmic TFLOP/s (18 c
+    f flop per row)."""
+    import numpy as np
+
+    from oracle import transition as OT
+    from paper_2506_20686_amd import workloads as W
+
+    m = t["x"].shape[0]
+    w = {k: np.ascontiguousarray(t[k].double().numpy()) for k in ("gamma", "beta", "w1", "w2")}
+
+    def run(rows):
+        sel = np.asarray(rows)
+        xs = np.ascontiguousarray(t["x"].double().numpy()[sel])
+        ds = np.ascontiguousarray(t["dout"].double().numpy()[sel])
+        t0 = time.perf_counter()
+        OT.trn_fwd(xs, w["gamma"], w["beta"], w["w1"], w["w2"])
+        OT.trn_bwd(xs, w["gamma"], w["beta"], w["w1"], w["w2"], ds)
+        return time.perf_counter() - t0
+
+    trial_rows = 4096
+    trial = run([int(i * m / trial_rows) for i in range(trial_rows)])
+    rows = max(trial_rows, min(m, int(trial_rows * target_s / max(trial, 1e-3))))
+    dt = run([int(i * m / rows) for i in range(rows)])
+    flop = W.trn_step_flops(rows)
+    threads = os.environ.get("OMP_NUM_THREADS") or str(os.cpu_count())
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle", "seconds": round(dt, 3),
+            "sample": f"{rows} of {m} rows (evenly spaced): forward and backward of those rows "
+                      f"with their sums over rows, fp64 numpy (BLAS threads: {threads}); "
+                      f"algorithmic 18*c*f flop per row"}
+
+
+def bench_trn(args, name):
+    """Forward + backward of the fused transition layer."""
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    from paper_2506_20686_amd import workloads as W
+
+    m, c, f = W.TRN_WORKLOADS[name], W.TRN_C, W.TRN_F
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    torch.zeros(1, device=dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    t = W.trn_inputs(m, seed=0)
+    x, gamma, beta, w1, w2, dout = (t[k].to(dev) for k in ("x", "gamma", "beta", "w1", "w2",
+                                                             "dout"))
+    out = torch.empty_like(x)
+    mean = torch.empty(m, dtype=torch.float32, device=dev)
+    rstd = torch.empty(m, dtype=torch.float32, device=dev)
+    dx = torch.empty_like(x)
+    dw1 = torch.empty((c, 2 * f), dtype=torch.float32, device=dev)
+    dw2 = torch.empty((f, c), dtype=torch.float32, device=dev)
+    dg = torch.empty(c, dtype=torch.float32, device=dev)
+    db = torch.empty(c, dtype=torch.float32, device=dev)
+    ws_bytes = max(B.tri_transition_fwd_workspace_bytes(B.BF16, m, c, f),
+                   B.tri_transition_bwd_workspace_bytes(B.BF16, m, c, f))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda a: a.data_ptr()  # noqa: E731
+
+    def step():
+        st = B.tri_transition_fwd(B.BF16, m, c, f, 1e-5, P(x), P(gamma), P(beta), P(w1), P(w2),
+                                  P(out), P(mean), P(rstd), P(ws), ws_bytes, stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_transition_fwd")
+        st = B.tri_transition_bwd(B.BF16, m, c, f, P(x), P(gamma), P(beta), P(w1), P(w2),
+                                  P(mean), P(rstd), P(dout), P(dx), P(dw1), P(dw2), P(dg), P(db),
+                                  P(ws), ws_bytes, stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_transition_bwd")
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+    B.tri_attn_timing_reset()
+    B.tri_attn_timing_enable(True)
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize(dev)
+    t1 = time.perf_counter()
+    B.tri_attn_timing_enable(False)
+    ktimes = B.kernel_times()
+    peak_bytes = torch.cuda.max_memory_allocated(dev)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    tflops = W.trn_step_flops(m) / (ms * 1e-3) / 1e12
+    kf = trn_kernel_flops(m, c, f)
+    per_kernel = {k: {"avg_ms": round(v[0] / v[1], 5), "launches": v[1],
+                      "share": round(v[0] / max(1e-9, sum(y[0] for y in ktimes.values())), 4)}
+                  for k, v in ktimes.items() if v[1] > 0}
+    dom = max((k for k in per_kernel if k in kf), key=lambda k: ktimes[k][0])
+    avg_s = ktimes[dom][0] / ktimes[dom][1] * 1e-3
+    achieved = kf[dom] / avg_s / 1e12
+    peak = MFMA_BF16_PEAK_TFLOPS
+    out_line = {
+        "metric": "fused transition layer (layer norm, W1, SwiGLU, W2) fwd+bwd TFLOP/s at "
+                  "m=768^2, c=128, F=512",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals; the paper's pair representations are not available)",
+        "config": {"workload": name, "m": m, "c": c, "f": f, "parallelism": "none (1 GPU)"},
+        "pct_of_peak": round(100.0 * tflops / peak, 3),
+        "peak_hbm_bytes": int(peak_bytes),
+        "workspace_bytes": int(ws_bytes),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 3),
+                     "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 5),
+                     "traffic": recorded_traffic(dom, name, "trn")},
+        "per_kernel": per_kernel,
+    }
+    out_line["cpu_baseline"] = (trn_cpu_baseline(t, args.cpu_seconds) if args.cpu_seconds > 0
+                                else None)
+    print(json.dumps(out_line), flush=True)
+
+
 def bench_rows(args, name):
     """One GPU's share of the row-sharded starting node: forward + backward of
     `rows` rows of the whole map through tri_attn_rows_{fwd,bwd}, shard-local
@@ -417,6 +559,9 @@ def main():
         return
     if name in W.ROWS_WORKLOADS:
         bench_rows(args, name)
+        return
+    if name in W.TRN_WORKLOADS:
+        bench_trn(args, name)
         return
     w = W.WORKLOADS[name]
     dev = torch.device("cuda:0")

@@ -365,9 +365,9 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_dx_kernel(TrnBwdArgs a
 //
 // Workgroup (part p, column group cg): rows of part p, hidden columns
 // cg * 128 .. + 127.  Wave w owns hidden columns f0 = cg * 128 + 16 w .. + 15
-// and keeps W1's a and b columns and W2's rows for them in registers.  Per
-// block of 32 rows (x, dout and the statistics staged in LDS, shared by the
-// waves):
+// and keeps W1's a and b columns and W2's rows for them in LDS (fragment
+// order).  Per block of 32 rows (o1, xhat and dout staged in LDS by all
+// threads, shared by the waves):
 //   hC  [32 rows x 32 cols]  = o1 . W1[:, a cols | b cols]      (lane <-> column)
 //   duC [32 rows x 32 cols]  = dout . W2^T[:, f cols, twice]     (both halves)
 //   the a lane and the b lane of a column swap values, so each has a, b, du:
@@ -377,7 +377,11 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_dx_kernel(TrnBwdArgs a
 // The x and dout tiles are stored as four 32-column blocks of 64-byte rows
 // (blk_off), so their transposed reads are the attention kernels' ones.
 
-constexpr int W_SLOT = 2 * 8192 + 256;  // x tile, dout tile, mean[32], rstd[32]
+// One ring slot: o1 (bf16), xhat (bf16) and dout tiles of 32 rows, each as
+// four 32-column blocks of 64-byte rows (blk_off).  The staging threads
+// normalise once per block for all waves.
+constexpr int W_SLOT = 3 * 8192;
+constexpr int W_XH = 8192, W_DO = 16384;
 
 __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a, int64_t rpp) {
   __shared__ __align__(16) char ring[2][W_SLOT];
@@ -410,34 +414,41 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
     wf1[wave][s][lane] = w1f;
     if (is_a) wf2[wave][s][16 * g + l32] = *(const bf16x8*)(a.w2 + (int64_t)fl * TRN_C + 16 * s + 8 * g);
   }
+  __syncthreads();  // gamma, beta
 
-  // staging: thread tid copies 16 bytes of x and of dout (row tid / 16,
-  // chunk tid % 16) and threads < 32 / 64 the statistics
+  // staging: thread tid takes 8 features (chunk tid % 16) of row tid / 16:
+  // x, dout and the row's statistics; it writes o1 and xhat in bf16 and dout
   const int sr = tid >> 4, sc = tid & 15;
   const uint32_t soff = (sc >> 2) * 2048 + blk_off(sr, sc & 3);
-  auto stage_load = [&](int ib, f32x4& xv, f32x4& dv, float& sv) {
+  struct Staged {
+    bf16x8 x, d;
+    float mean, rstd;
+  };
+  auto stage_load = [&](int ib, Staged& v) {
     const int64_t row = r0 + 32 * (int64_t)ib + sr;
     const bool ok = row < r1;
     const int64_t rc = ok ? row : r0;
-    xv = *(const f32x4*)(a.x + rc * TRN_C + 8 * sc);
-    dv = ok ? *(const f32x4*)(a.dout + rc * TRN_C + 8 * sc) : f32x4{};  // no contribution
-    sv = 0.f;
-    if (tid < 64) {
-      const int64_t rs = r0 + 32 * (int64_t)ib + (tid & 31);
-      const int64_t rsc = rs < r1 ? rs : r0;
-      sv = tid < 32 ? a.mean[rsc] : a.rstd[rsc];
+    v.x = *(const bf16x8*)(a.x + rc * TRN_C + 8 * sc);
+    v.d = ok ? *(const bf16x8*)(a.dout + rc * TRN_C + 8 * sc) : bf16x8{};  // no contribution
+    v.mean = a.mean[rc];
+    v.rstd = a.rstd[rc];
+  };
+  auto stage_store = [&](char* slot, const Staged& v) {
+    bf16x8 o1, xh;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float h = ((float)v.x[e] - v.mean) * v.rstd;
+      xh[e] = (bf16)h;
+      o1[e] = (bf16)fmaf(h, gb[0][8 * sc + e], gb[1][8 * sc + e]);
     }
+    *(bf16x8*)(slot + soff) = o1;
+    *(bf16x8*)(slot + W_XH + soff) = xh;
+    *(bf16x8*)(slot + W_DO + soff) = v.d;
   };
-  auto stage_store = [&](char* slot, const f32x4& xv, const f32x4& dv, float sv) {
-    *(f32x4*)(slot + soff) = xv;
-    *(f32x4*)(slot + 8192 + soff) = dv;
-    if (tid < 64) ((float*)(slot + 16384))[tid] = sv;
-  };
-  f32x4 xv, dv;
-  float sv;
+  Staged sv;
   if (nb > 0) {
-    stage_load(0, xv, dv, sv);
-    stage_store(ring[0], xv, dv, sv);
+    stage_load(0, sv);
+    stage_store(ring[0], sv);
   }
   __syncthreads();
 
@@ -453,24 +464,14 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
   for (int ib = 0; ib < nb; ++ib) {
     const char* cur = ring[ib & 1];
     const bool more = ib + 1 < nb;
-    if (more) stage_load(ib + 1, xv, dv, sv);
-    const float* smean = (const float*)(cur + 16384);
-    const float* srstd = smean + 32;
+    if (more) stage_load(ib + 1, sv);
     // o1 and dout as A operands (lane <-> row l32, features 16 s + 8 g ..)
-    const float mu = smean[l32], rs = srstd[l32];
     f32x16 hC = {}, duC = {};
 #pragma unroll
     for (int s = 0; s < TRN_NT; ++s) {
       const uint32_t o = (s >> 1) * 2048 + blk_off(l32, 2 * (s & 1) + g);
-      const bf16x8 xr = *(const bf16x8*)(cur + o);
-      bf16x8 o1;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int k = 16 * s + 8 * g + e;
-        o1[e] = (bf16)fmaf(((float)xr[e] - mu) * rs, gb[0][k], gb[1][k]);
-      }
-      hC = Mma<bf16>::mma(o1, wf1[wave][s][lane], hC);
-      duC = Mma<bf16>::mma(*(const bf16x8*)(cur + 8192 + o), wf2[wave][s][16 * g + (l32 & 15)],
+      hC = Mma<bf16>::mma(*(const bf16x8*)(cur + o), wf1[wave][s][lane], hC);
+      duC = Mma<bf16>::mma(*(const bf16x8*)(cur + W_DO + o), wf2[wave][s][16 * g + (l32 & 15)],
                            duC);
     }
     // swap with the partner lane (a <-> b of the same hidden column)
@@ -491,27 +492,14 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
       bf16x8 bf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) bf[e] = (bf16)dh[8 * s + e];
-      float m8[8], r8[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int r = acc_k(s, g, e);
-        m8[e] = smean[r];
-        r8[e] = srstd[r];
-      }
 #pragma unroll
       for (int t = 0; t < 4; t += 2) {
-        const uint32_t b0 = lds_addr(cur + t * 2048), b1 = b0 + 2048;
+        const uint32_t b0 = lds_addr(cur + W_XH + t * 2048), b1 = b0 + 2048;
         s16x4 rr[4];
         tr_read4_wait(b0 + tr.off(16 * s), b0 + tr.off(16 * s + 8), b1 + tr.off(16 * s),
                       b1 + tr.off(16 * s + 8), rr);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const bf16x8 xt = tr_frag(rr, h);
-          bf16x8 af;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) af[e] = (bf16)(((float)xt[e] - m8[e]) * r8[e]);
-          G[t + h] = Mma<bf16>::mma(af, bf, G[t + h]);
-        }
+        for (int h = 0; h < 2; ++h) G[t + h] = Mma<bf16>::mma(tr_frag(rr, h), bf, G[t + h]);
       }
     }
     // dW2 += u^T dout: A = u (lane <-> hidden column, group q takes rows
@@ -522,7 +510,7 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
 #pragma unroll
     for (int ot = 0; ot < 8; ot += 2) {
       // tiles ot and ot + 1 are the two 16-column halves of one 32-column block
-      const uint32_t tb = lds_addr(cur + 8192 + (ot >> 1) * 2048);
+      const uint32_t tb = lds_addr(cur + W_DO + (ot >> 1) * 2048);
       const int half = 8 * (qj & 1);
       const uint32_t c0 = 2 * 0 + (qj >> 1), c1 = 2 * 1 + (qj >> 1);
       s16x4 rr[4];
@@ -531,7 +519,7 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
       W2a[ot] = mma16(ua, tr_frag(rr, 0), W2a[ot]);
       W2a[ot + 1] = mma16(ua, tr_frag(rr, 1), W2a[ot + 1]);
     }
-    if (more) stage_store(ring[(ib + 1) & 1], xv, dv, sv);
+    if (more) stage_store(ring[(ib + 1) & 1], sv);
     __syncthreads();
   }
 
