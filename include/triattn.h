@@ -94,6 +94,28 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
                  size_t workspace_bytes, void* stream);
 
+/* A batch of `batch` independent pair maps (each sample with its own bias
+ * and mask): tensors gain a leading batch axis,
+ *   q, k, v, g, out, dout, dq, dk, dv, dg : [batch][n][n][h][d]
+ *   bias, dbias, lse                        : [batch][n][n][h]
+ *   mask                                    : [batch][n][n]  (NULL = all valid)
+ * and sample b gives exactly what tri_attn_fwd / tri_attn_bwd give for its
+ * slices.  The samples run one after another on `stream` and share the
+ * workspace, whose size is the unbatched one (tri_attn_fwd_workspace_bytes /
+ * tri_attn_bwd_workspace_bytes for n, h, d).  The base pointers follow the
+ * unbatched rules; 1 <= batch <= 2^20.  The per-sample slices of bias,
+ * dbias, lse and mask need only element alignment. */
+int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
+                         float scale, const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, void* out, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream);
+int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
+                         float scale, const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, const void* out,
+                         const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                         void* dg, void* dbias, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
 /* Starting node over a contiguous range of rows: one GPU's share of the
  * pair representation when it is split into contiguous shards along one
  * sequence axis (Section IV-B, sequence parallelism).  Rows of the starting

@@ -52,6 +52,12 @@ def lib():
         L.tri_attn_rows_fwd.argtypes = [_int, _i64, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
         L.tri_attn_rows_bwd.argtypes = [_int, _i64, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz,
                                                                                           _vp]
+        L.tri_attn_fwd_batched.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _f] + [_vp] * 9 + \
+            [_sz, _vp]
+        L.tri_attn_bwd_batched.argtypes = [_int, _int, _i64, _i64, _i64, _i64, _f] + [_vp] * 15 + \
+            [_sz, _vp]
+        L.tri_attn_fwd_batched.restype = _int
+        L.tri_attn_bwd_batched.restype = _int
         L.tri_attn_status_string.argtypes = [_int]
         L.tri_attn_status_string.restype = ctypes.c_char_p
         L.tri_attn_timing_enable.argtypes = [_int]
@@ -153,6 +159,21 @@ def tri_attn_rows_bwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, 
     return lib().tri_attn_rows_bwd(dtype, n, rows, h, d, scale, q, k, v, g, bias, mask, out, lse,
                                    dout, dq, dk, dv, dg, dbias_partial, workspace,
                                    workspace_bytes, stream)
+
+
+def tri_attn_fwd_batched(node, dtype, batch, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                         workspace, workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_fwd_batched(node, dtype, batch, n, h, d, scale, q, k, v, g, bias, mask,
+                                      out, lse, workspace, workspace_bytes, stream)
+
+
+def tri_attn_bwd_batched(node, dtype, batch, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                         dout, dq, dk, dv, dg, dbias, workspace, workspace_bytes, stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_bwd_batched(node, dtype, batch, n, h, d, scale, q, k, v, g, bias, mask,
+                                      out, lse, dout, dq, dk, dv, dg, dbias, workspace,
+                                      workspace_bytes, stream)
 
 
 def _cols_arr(cols):
@@ -272,20 +293,23 @@ def _check(name, t, shape, dtype, device):
 
 
 def _common(q, k, v, g, bias, mask):
-    if q.dim() != 4:
-        raise ValueError("q must be [n, n, h, d]")
-    n, n2, h, d = q.shape
+    """Shapes of a single map ([n, n, h, d]) or a batch ([b, n, n, h, d]);
+    returns (lead, n, h, d, dtype code, device) with lead = () or (b,)."""
+    if q.dim() not in (4, 5):
+        raise ValueError("q must be [n, n, h, d] or [b, n, n, h, d]")
+    lead = tuple(q.shape[:-4])
+    n, n2, h, d = q.shape[-4:]
     if n != n2:
         raise ValueError("q must be square in its two pair axes")
     if q.dtype not in _DTYPES:
         raise ValueError(f"unsupported dtype {q.dtype}")
     dev = q.device
     for name, t in (("q", q), ("k", k), ("v", v), ("g", g)):
-        _check(name, t, (n, n, h, d), q.dtype, dev)
-    _check("bias", bias, (n, n, h), q.dtype, dev)
+        _check(name, t, lead + (n, n, h, d), q.dtype, dev)
+    _check("bias", bias, lead + (n, n, h), q.dtype, dev)
     if mask is not None:
-        _check("mask", mask, (n, n), torch.uint8, dev)
-    return n, h, d, _DTYPES[q.dtype], dev
+        _check("mask", mask, lead + (n, n), torch.uint8, dev)
+    return lead, n, h, d, _DTYPES[q.dtype], dev
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -302,41 +326,49 @@ def default_scale(d: int) -> float:
 
 def fwd(q, k, v, g, bias, mask=None, node: int = STARTING, scale: Optional[float] = None,
         workspace: Optional[torch.Tensor] = None):
-    """Triangle attention forward.  Returns (out [n,n,h,d], lse [n,n,h] fp32)."""
-    n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
+    """Triangle attention forward.  Returns (out [n,n,h,d], lse [n,n,h] fp32);
+    with a leading batch axis on every tensor, the batched call."""
+    lead, n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
     scale = default_scale(d) if scale is None else float(scale)
     out = torch.empty_like(q)
-    lse = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+    lse = torch.empty(lead + (n, n, h), dtype=torch.float32, device=dev)
     need = tri_attn_fwd_workspace_bytes(node, dt, n, h, d)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    st = tri_attn_fwd(node, dt, n, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias),
-                      _ptr(mask), _ptr(out), _ptr(lse), _ptr(workspace), workspace.numel(),
-                      _stream(dev))
+    args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
+            _ptr(lse), _ptr(workspace), workspace.numel(), _stream(dev))
+    if lead:
+        st = tri_attn_fwd_batched(node, dt, lead[0], n, h, d, *args)
+    else:
+        st = tri_attn_fwd(node, dt, n, h, d, *args)
     if st != OK:
-        raise TriAttnError(st, "tri_attn_fwd")
+        raise TriAttnError(st, "tri_attn_fwd_batched" if lead else "tri_attn_fwd")
     return out, lse
 
 
 def bwd(q, k, v, g, bias, out, lse, dout, mask=None, node: int = STARTING,
         scale: Optional[float] = None, workspace: Optional[torch.Tensor] = None):
-    """Triangle attention backward.  Returns (dq, dk, dv, dg, dbias)."""
-    n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
-    _check("out", out, (n, n, h, d), q.dtype, dev)
-    _check("dout", dout, (n, n, h, d), q.dtype, dev)
-    _check("lse", lse, (n, n, h), torch.float32, dev)
+    """Triangle attention backward.  Returns (dq, dk, dv, dg, dbias); batched
+    when the tensors have a leading batch axis."""
+    lead, n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
+    _check("out", out, lead + (n, n, h, d), q.dtype, dev)
+    _check("dout", dout, lead + (n, n, h, d), q.dtype, dev)
+    _check("lse", lse, lead + (n, n, h), torch.float32, dev)
     scale = default_scale(d) if scale is None else float(scale)
     dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
     dbias = torch.empty_like(bias)
     need = tri_attn_bwd_workspace_bytes(node, dt, n, h, d)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    st = tri_attn_bwd(node, dt, n, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias),
-                      _ptr(mask), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
-                      _ptr(dv), _ptr(dg), _ptr(dbias), _ptr(workspace), workspace.numel(),
-                      _stream(dev))
+    args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
+            _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbias),
+            _ptr(workspace), workspace.numel(), _stream(dev))
+    if lead:
+        st = tri_attn_bwd_batched(node, dt, lead[0], n, h, d, *args)
+    else:
+        st = tri_attn_bwd(node, dt, n, h, d, *args)
     if st != OK:
-        raise TriAttnError(st, "tri_attn_bwd")
+        raise TriAttnError(st, "tri_attn_bwd_batched" if lead else "tri_attn_bwd")
     return dq, dk, dv, dg, dbias
 
 

@@ -217,6 +217,101 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                         dbias, nullptr, workspace, s);
 }
 
+// ---- a batch of pair maps -----------------------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+constexpr int64_t MAX_BATCH = (int64_t)1 << 20;
+
+// Per-sample element counts and the checks shared by the batched calls.
+struct BatchStrides {
+  int64_t pair, bias, lse, mask;  // elements per sample
+  size_t el;                      // bytes per dtype element
+};
+
+BatchStrides batch_strides(int dtype, int64_t n, int64_t h, int64_t d) {
+  return BatchStrides{n * n * h * d, n * n * h, n * n * h, n * n,
+                      (size_t)(dtype == TRIATTN_BF16 ? 2 : 4)};
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
+                         float scale, const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, void* out, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (batch < 1 || batch > MAX_BATCH) return TRIATTN_ERR_INVALID_ARG;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(false, dtype, n, n, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(node, n, n, h, scale);
+  const BatchStrides S = batch_strides(dtype, n, h, d);
+  hipStream_t s = (hipStream_t)stream;
+  for (int64_t b = 0; b < batch; ++b) {
+    const size_t op = (size_t)(b * S.pair) * S.el, ob = (size_t)(b * S.bias) * S.el;
+    const uint8_t* mb = mask ? mask + b * S.mask : nullptr;
+    float* lb = lse + b * S.lse;
+    const int r =
+        dtype == TRIATTN_BF16
+            ? run_fwd<triattn::bf16>(node, geo, L, (const char*)q + op, (const char*)k + op,
+                                     (const char*)v + op, (const char*)g + op,
+                                     (const char*)bias + ob, mb, (char*)out + op, lb, workspace, s)
+            : run_fwd<float>(node, geo, L, (const char*)q + op, (const char*)k + op,
+                             (const char*)v + op, (const char*)g + op, (const char*)bias + ob, mb,
+                             (char*)out + op, lb, workspace, s);
+    if (r != TRIATTN_OK) return r;
+  }
+  return TRIATTN_OK;
+}
+
+int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
+                         float scale, const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, const void* out,
+                         const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                         void* dg, void* dbias, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  int st = check_shape(node, dtype, n, h, d);
+  if (st != TRIATTN_OK) return st;
+  if (batch < 1 || batch > MAX_BATCH) return TRIATTN_ERR_INVALID_ARG;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Layout L = plan(true, dtype, n, n, h);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+    return TRIATTN_ERR_WORKSPACE;
+  const Geom geo = geom(node, n, n, h, scale);
+  const BatchStrides S = batch_strides(dtype, n, h, d);
+  hipStream_t s = (hipStream_t)stream;
+  for (int64_t b = 0; b < batch; ++b) {
+    const size_t op = (size_t)(b * S.pair) * S.el, ob = (size_t)(b * S.bias) * S.el;
+    const uint8_t* mb = mask ? mask + b * S.mask : nullptr;
+    const float* lb = lse + b * S.lse;
+    auto P = [&](const void* p) { return (const char*)p + op; };
+    auto W = [&](void* p) { return (char*)p + op; };
+    const int r =
+        dtype == TRIATTN_BF16
+            ? run_bwd<triattn::bf16>(node, geo, L, P(q), P(k), P(v), P(g),
+                                     (const char*)bias + ob, mb, P(out), lb, P(dout), W(dq), W(dk),
+                                     W(dv), W(dg), (char*)dbias + ob, nullptr, workspace, s)
+            : run_bwd<float>(node, geo, L, P(q), P(k), P(v), P(g), (const char*)bias + ob, mb,
+                             P(out), lb, P(dout), W(dq), W(dk), W(dv), W(dg), (char*)dbias + ob,
+                             nullptr, workspace, s);
+    if (r != TRIATTN_OK) return r;
+  }
+  return TRIATTN_OK;
+}
+
 // ---- starting node over a range of rows -------------------------------------------------
 
 }  // extern "C"

@@ -366,3 +366,41 @@ def test_transition_undersized_workspace(lib):
         st, need = ws_bytes(fn, B.BF16, 64, 128, 512)
         assert st == B.OK
         assert call(*mk(wsb=need - 1)) == B.ERR_WORKSPACE
+
+
+# ---- batched attention -------------------------------------------------------------------
+
+def batched_fwd_args(**over):
+    a = dict(batch=3)
+    a.update({k: v for k, v in over.items() if k == "batch"})
+    base = fwd_args(**{k: v for k, v in over.items() if k != "batch"})
+    return base[:2] + (a["batch"],) + base[2:]
+
+
+def batched_bwd_args(**over):
+    a = dict(batch=3)
+    a.update({k: v for k, v in over.items() if k == "batch"})
+    base = bwd_args(**{k: v for k, v in over.items() if k != "batch"})
+    return base[:2] + (a["batch"],) + base[2:]
+
+
+@pytest.mark.parametrize("over,code", FWD_BAD + [(dict(batch=0), B.ERR_INVALID_ARG),
+                                                 (dict(batch=-2), B.ERR_INVALID_ARG),
+                                                 (dict(batch=(1 << 20) + 1), B.ERR_INVALID_ARG)])
+def test_batched_fwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_fwd_batched(*batched_fwd_args(**over)) == code
+
+
+@pytest.mark.parametrize("over,code", BWD_BAD + [(dict(batch=0), B.ERR_INVALID_ARG)])
+def test_batched_bwd_rejects_before_any_hip_call(lib, over, code):
+    assert lib.tri_attn_bwd_batched(*batched_bwd_args(**over)) == code
+
+
+def test_batched_workspace_is_the_unbatched_one(lib):
+    for node in (0, 1):
+        st, need = ws_bytes(lib.tri_attn_bwd_workspace_bytes, node, B.BF16, 16, 2, 32)
+        assert lib.tri_attn_bwd_batched(*batched_bwd_args(node=node, wsb=need - 1)) == \
+            B.ERR_WORKSPACE
+        st, need = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, 16, 2, 32)
+        assert lib.tri_attn_fwd_batched(*batched_fwd_args(node=node, wsb=need - 1)) == \
+            B.ERR_WORKSPACE
