@@ -18,11 +18,12 @@ constexpr int64_t MAX_H = 64;
 
 size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d) {
+// d = 32 natively; the whole-map calls also take d = 16 (padded to 32).
+int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d, bool allow16 = false) {
   if (node != TRIATTN_STARTING && node != TRIATTN_ENDING) return TRIATTN_ERR_INVALID_ARG;
   if (dtype != TRIATTN_F32 && dtype != TRIATTN_BF16) return TRIATTN_ERR_INVALID_ARG;
   if (n < 1 || n > MAX_N || h < 1 || h > MAX_H || d < 1) return TRIATTN_ERR_INVALID_ARG;
-  if (d != triattn::HEAD_DIM) return TRIATTN_ERR_UNSUPPORTED;
+  if (d != triattn::HEAD_DIM && !(allow16 && d == 16)) return TRIATTN_ERR_UNSUPPORTED;
   return TRIATTN_OK;
 }
 
@@ -152,25 +153,86 @@ int run_bwd(int node, const Geom& g, const Layout& L, const void* q, const void*
   return TRIATTN_OK;
 }
 
+// Workspace of a whole-map call: the d = 32 layout, then (d = 16) the
+// padded copies [n][n][h][32] of q, k, v, g and out (forward) or of q, k, v,
+// g, out, dout, dq, dk, dv, dg (backward).
+struct Whole {
+  Layout L;
+  size_t pad0, pad_bytes, total;
+};
+
+Whole whole_plan(bool bwd, int dtype, int64_t n, int64_t h, int64_t d) {
+  Whole w{plan(bwd, dtype, n, n, h), 0, 0, 0};
+  w.pad0 = w.L.total;
+  const int npad = d == 16 ? (bwd ? 10 : 5) : 0;
+  w.pad_bytes = round256((size_t)n * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4));
+  w.total = w.pad0 + (size_t)npad * w.pad_bytes;
+  return w;
+}
+
+template <typename T>
+int fwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, const void* k,
+            const void* v, const void* gate, const void* bias, const uint8_t* mask, void* out,
+            float* lse, void* ws, hipStream_t s) {
+  if (d == triattn::HEAD_DIM)
+    return run_fwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, ws, s);
+  const int64_t rows = (int64_t)g.n * g.n * g.H;
+  char* p[5];
+  for (int i = 0; i < 5; ++i) p[i] = (char*)ws + W.pad0 + i * W.pad_bytes;
+  const void* in[4] = {q, k, v, gate};
+  for (int i = 0; i < 4; ++i)
+    if (triattn::launch_pad16(in[i], p[i], rows, sizeof(T), s) != hipSuccess)
+      return TRIATTN_ERR_HIP;
+  const int r = run_fwd<T>(node, g, W.L, p[0], p[1], p[2], p[3], bias, mask, p[4], lse, ws, s);
+  if (r != TRIATTN_OK) return r;
+  return triattn::launch_unpad16(p[4], out, rows, sizeof(T), s) == hipSuccess ? TRIATTN_OK
+                                                                               : TRIATTN_ERR_HIP;
+}
+
+template <typename T>
+int bwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, const void* k,
+            const void* v, const void* gate, const void* bias, const uint8_t* mask,
+            const void* out, const float* lse, const void* dout, void* dq, void* dk, void* dv,
+            void* dg, void* dbias, void* ws, hipStream_t s) {
+  if (d == triattn::HEAD_DIM)
+    return run_bwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, dout, dq, dk, dv, dg,
+                      dbias, nullptr, ws, s);
+  const int64_t rows = (int64_t)g.n * g.n * g.H;
+  char* p[10];
+  for (int i = 0; i < 10; ++i) p[i] = (char*)ws + W.pad0 + i * W.pad_bytes;
+  const void* in[6] = {q, k, v, gate, out, dout};
+  for (int i = 0; i < 6; ++i)
+    if (triattn::launch_pad16(in[i], p[i], rows, sizeof(T), s) != hipSuccess)
+      return TRIATTN_ERR_HIP;
+  const int r = run_bwd<T>(node, g, W.L, p[0], p[1], p[2], p[3], bias, mask, p[4], lse, p[5],
+                           p[6], p[7], p[8], p[9], dbias, nullptr, ws, s);
+  if (r != TRIATTN_OK) return r;
+  void* outs[4] = {dq, dk, dv, dg};
+  for (int i = 0; i < 4; ++i)
+    if (triattn::launch_unpad16(p[6 + i], outs[i], rows, sizeof(T), s) != hipSuccess)
+      return TRIATTN_ERR_HIP;
+  return TRIATTN_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
 int tri_attn_fwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
                                  size_t* bytes) {
-  const int st = check_shape(node, dtype, n, h, d);
+  const int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
-  *bytes = plan(false, dtype, n, n, h).total;
+  *bytes = whole_plan(false, dtype, n, h, d).total;
   return TRIATTN_OK;
 }
 
 int tri_attn_bwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,
                                  size_t* bytes) {
-  const int st = check_shape(node, dtype, n, h, d);
+  const int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
-  *bytes = plan(true, dtype, n, n, h).total;
+  *bytes = whole_plan(true, dtype, n, h, d).total;
   return TRIATTN_OK;
 }
 
@@ -178,20 +240,21 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  const void* q, const void* k, const void* v, const void* g, const void* bias,
                  const uint8_t* mask, void* out, float* lse, void* workspace,
                  size_t workspace_bytes, void* stream) {
-  int st = check_shape(node, dtype, n, h, d);
+  int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
   const void* ptrs[] = {q, k, v, g, bias, out, lse};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(false, dtype, n, n, h);
-  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+  const Whole W = whole_plan(false, dtype, n, h, d);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
   const Geom geo = geom(node, n, n, h, scale);
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
-    return run_fwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, workspace, s);
-  return run_fwd<float>(node, geo, L, q, k, v, g, bias, mask, out, lse, workspace, s);
+    return fwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, workspace,
+                                  s);
+  return fwd_one<float>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, workspace, s);
 }
 
 int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
@@ -199,22 +262,22 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  const uint8_t* mask, const void* out, const float* lse, const void* dout,
                  void* dq, void* dk, void* dv, void* dg, void* dbias, void* workspace,
                  size_t workspace_bytes, void* stream) {
-  int st = check_shape(node, dtype, n, h, d);
+  int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
   const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(true, dtype, n, n, h);
-  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+  const Whole W = whole_plan(true, dtype, n, h, d);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
   const Geom geo = geom(node, n, n, h, scale);
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
-    return run_bwd<triattn::bf16>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
-                                  dv, dg, dbias, nullptr, workspace, s);
-  return run_bwd<float>(node, geo, L, q, k, v, g, bias, mask, out, lse, dout, dq, dk, dv, dg,
-                        dbias, nullptr, workspace, s);
+    return bwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, dout, dq,
+                                  dk, dv, dg, dbias, workspace, s);
+  return bwd_one<float>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, dout, dq, dk, dv, dg,
+                        dbias, workspace, s);
 }
 
 // ---- a batch of pair maps -----------------------------------------------------------------
@@ -244,15 +307,15 @@ int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
                          float scale, const void* q, const void* k, const void* v, const void* g,
                          const void* bias, const uint8_t* mask, void* out, float* lse,
                          void* workspace, size_t workspace_bytes, void* stream) {
-  int st = check_shape(node, dtype, n, h, d);
+  int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (batch < 1 || batch > MAX_BATCH) return TRIATTN_ERR_INVALID_ARG;
   if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
   const void* ptrs[] = {q, k, v, g, bias, out, lse};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(false, dtype, n, n, h);
-  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+  const Whole W = whole_plan(false, dtype, n, h, d);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
   const Geom geo = geom(node, n, n, h, scale);
   const BatchStrides S = batch_strides(dtype, n, h, d);
@@ -263,10 +326,10 @@ int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
     float* lb = lse + b * S.lse;
     const int r =
         dtype == TRIATTN_BF16
-            ? run_fwd<triattn::bf16>(node, geo, L, (const char*)q + op, (const char*)k + op,
+            ? fwd_one<triattn::bf16>(node, geo, W, d, (const char*)q + op, (const char*)k + op,
                                      (const char*)v + op, (const char*)g + op,
                                      (const char*)bias + ob, mb, (char*)out + op, lb, workspace, s)
-            : run_fwd<float>(node, geo, L, (const char*)q + op, (const char*)k + op,
+            : fwd_one<float>(node, geo, W, d, (const char*)q + op, (const char*)k + op,
                              (const char*)v + op, (const char*)g + op, (const char*)bias + ob, mb,
                              (char*)out + op, lb, workspace, s);
     if (r != TRIATTN_OK) return r;
@@ -280,15 +343,15 @@ int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
                          const float* lse, const void* dout, void* dq, void* dk, void* dv,
                          void* dg, void* dbias, void* workspace, size_t workspace_bytes,
                          void* stream) {
-  int st = check_shape(node, dtype, n, h, d);
+  int st = check_shape(node, dtype, n, h, d, true);
   if (st != TRIATTN_OK) return st;
   if (batch < 1 || batch > MAX_BATCH) return TRIATTN_ERR_INVALID_ARG;
   if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
   const void* ptrs[] = {q, k, v, g, bias, out, lse, dout, dq, dk, dv, dg, dbias};
   for (const void* p : ptrs)
     if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
-  const Layout L = plan(true, dtype, n, n, h);
-  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < L.total)
+  const Whole W = whole_plan(true, dtype, n, h, d);
+  if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
   const Geom geo = geom(node, n, n, h, scale);
   const BatchStrides S = batch_strides(dtype, n, h, d);
@@ -298,15 +361,15 @@ int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
     const uint8_t* mb = mask ? mask + b * S.mask : nullptr;
     const float* lb = lse + b * S.lse;
     auto P = [&](const void* p) { return (const char*)p + op; };
-    auto W = [&](void* p) { return (char*)p + op; };
+    auto Q = [&](void* p) { return (char*)p + op; };
     const int r =
         dtype == TRIATTN_BF16
-            ? run_bwd<triattn::bf16>(node, geo, L, P(q), P(k), P(v), P(g),
-                                     (const char*)bias + ob, mb, P(out), lb, P(dout), W(dq), W(dk),
-                                     W(dv), W(dg), (char*)dbias + ob, nullptr, workspace, s)
-            : run_bwd<float>(node, geo, L, P(q), P(k), P(v), P(g), (const char*)bias + ob, mb,
-                             P(out), lb, P(dout), W(dq), W(dk), W(dv), W(dg), (char*)dbias + ob,
-                             nullptr, workspace, s);
+            ? bwd_one<triattn::bf16>(node, geo, W, d, P(q), P(k), P(v), P(g),
+                                     (const char*)bias + ob, mb, P(out), lb, P(dout), Q(dq), Q(dk),
+                                     Q(dv), Q(dg), (char*)dbias + ob, workspace, s)
+            : bwd_one<float>(node, geo, W, d, P(q), P(k), P(v), P(g), (const char*)bias + ob, mb,
+                             P(out), lb, P(dout), Q(dq), Q(dk), Q(dv), Q(dg), (char*)dbias + ob,
+                             workspace, s);
     if (r != TRIATTN_OK) return r;
   }
   return TRIATTN_OK;

@@ -55,6 +55,12 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& w, co
                       const T* dout, T* dq, T* dk, T* dv, T* dg, T* dbias, float* dbias_f32,
                       hipStream_t s);
 
+// d = 16 through the d = 32 kernels (pad.hip): rows of 16 channels copied
+// into rows of 32 with zeros, and back.
+hipError_t launch_pad16(const void* src, void* dst, int64_t rows, int elem_bytes, hipStream_t s);
+hipError_t launch_unpad16(const void* src, void* dst, int64_t rows, int elem_bytes,
+                          hipStream_t s);
+
 // ---- fused layer-norm + linear projection (lnl.hip) ---------------------------------
 constexpr int LNL_K = 128;       // features per row (the pair channel width)
 constexpr int LNL_MAX_OUT = 8;   // output tensors o2's columns are split into

@@ -27,6 +27,7 @@ enum KernelId {
   K_TRN_BWD_W,
   K_TRN_REDUCE,
   K_TRN_FINISH,
+  K_PAD,
   K_COUNT
 };
 

@@ -17,7 +17,8 @@ const char* const kNames[K_COUNT] = {"prep_bias",   "prep_kbits", "fwd",        
                                      "db_reduce",   "lnl_fwd",    "lnl_bwd_dx",
                                      "lnl_bwd_g",   "lnl_reduce", "lnl_finish",
                                      "trn_pack",    "trn_fwd",    "trn_bwd_dx",
-                                     "trn_bwd_w",   "trn_reduce", "trn_finish"};
+                                     "trn_bwd_w",   "trn_reduce", "trn_finish",
+                                     "pad16"};
 
 struct Pending {
   int id;

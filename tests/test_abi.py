@@ -101,7 +101,7 @@ def bwd_args(**over):
 FWD_BAD = [
     (dict(node=5), B.ERR_INVALID_ARG), (dict(dtype=-1), B.ERR_INVALID_ARG),
     (dict(n=0), B.ERR_INVALID_ARG), (dict(h=0), B.ERR_INVALID_ARG),
-    (dict(d=16), B.ERR_UNSUPPORTED), (dict(scale=0.0), B.ERR_INVALID_ARG),
+    (dict(d=64), B.ERR_UNSUPPORTED), (dict(d=24), B.ERR_UNSUPPORTED), (dict(scale=0.0), B.ERR_INVALID_ARG),
     (dict(scale=-1.0), B.ERR_INVALID_ARG), (dict(scale=float("nan")), B.ERR_INVALID_ARG),
     (dict(scale=float("inf")), B.ERR_INVALID_ARG),
     (dict(q=None), B.ERR_INVALID_ARG), (dict(k=None), B.ERR_INVALID_ARG),
@@ -266,6 +266,7 @@ def rows_bwd_args(**over):
 
 
 ROWS_BAD = [(o, c) for o, c in FWD_BAD if "node" not in o] + [
+    (dict(d=16), B.ERR_UNSUPPORTED),  # row ranges take d = 32 only
     (dict(rows=0), B.ERR_INVALID_ARG), (dict(rows=17), B.ERR_INVALID_ARG),
     (dict(rows=-3), B.ERR_INVALID_ARG),
 ]
@@ -404,3 +405,18 @@ def test_batched_workspace_is_the_unbatched_one(lib):
         st, need = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, 16, 2, 32)
         assert lib.tri_attn_fwd_batched(*batched_fwd_args(node=node, wsb=need - 1)) == \
             B.ERR_WORKSPACE
+
+
+def test_d16_workspace_adds_padded_copies(lib):
+    """d = 16 runs the d = 32 kernels on zero-padded copies kept in the
+    workspace: 5 (forward) and 10 (backward) tensors of [n][n][h][32]."""
+    for dtype, el in ((B.BF16, 2), (B.F32, 4)):
+        for node in (0, 1):
+            n, h = 40, 3
+            pad = -(-n * n * h * 32 * el // 256) * 256
+            for fn, k in ((lib.tri_attn_fwd_workspace_bytes, 5),
+                          (lib.tri_attn_bwd_workspace_bytes, 10)):
+                st, b32 = ws_bytes(fn, node, dtype, n, h, 32)
+                st16, b16 = ws_bytes(fn, node, dtype, n, h, 16)
+                assert st == st16 == B.OK
+                assert b16 == b32 + k * pad

@@ -1,0 +1,80 @@
+"""GPU parity of triangle attention with head dimension d = 16 against the
+fp64 oracle (d = 16), with the tolerances of the d = 32 tests.  d = 16 runs
+the d = 32 kernels on copies whose channels 16..31 are zero; the results
+must equal, bitwise, those of a d = 32 call on such padded inputs."""
+import pytest
+import torch
+
+import oracle
+from paper_2506_20686_amd import binding as B
+from paper_2506_20686_amd import workloads as W
+
+from test_parity_gpu import DEV, close
+
+pytestmark = pytest.mark.gpu
+
+
+def inputs16(n, h, dtype, seed, masked=True):
+    t, gen = W.make_inputs(n, h, 16, dtype, seed=seed)
+    t["mask"] = W.random_mask(n, 0.8, gen) if masked else None
+    return t
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+@pytest.mark.parametrize("n,h", [(1, 1), (37, 2), (100, 4)])
+def test_d16_matches_oracle(dtype, node, n, h):
+    t = inputs16(n, h, dtype, seed=700 + n + node)
+    d = {k: (v.to(DEV) if v is not None else None) for k, v in t.items()}
+    out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], node)
+    grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d["mask"], node)
+    torch.cuda.synchronize()
+    assert out.shape == (n, n, h, 16)
+    ro, rl = oracle.fwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["mask"])
+    rg = oracle.bwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["dout"], t["mask"])
+    close("out", out, ro, dtype)
+    close("lse", lse, rl, dtype)
+    for name, a, r in zip(("dq", "dk", "dv", "dg", "dbias"), grads, rg):
+        close(name, a, r, dtype)
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_d16_equals_padded_d32_bitwise(node):
+    n, h = 64, 2
+    t = inputs16(n, h, torch.bfloat16, seed=31 + node)
+    d = {k: v.to(DEV) for k, v in t.items()}
+
+    def pad(x):
+        return torch.nn.functional.pad(x, (0, 16)).contiguous()
+
+    scale = 0.25  # 1 / sqrt(16), passed to both calls
+    out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], node, scale)
+    grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d["mask"],
+                  node, scale)
+    p = {k: pad(d[k]) for k in ("q", "k", "v", "g", "dout")}
+    o2, l2 = B.fwd(p["q"], p["k"], p["v"], p["g"], d["bias"], d["mask"], node, scale)
+    g2 = B.bwd(p["q"], p["k"], p["v"], p["g"], d["bias"], o2, l2, p["dout"], d["mask"], node,
+               scale)
+    assert torch.equal(out, o2[..., :16]) and torch.equal(lse, l2)
+    for a, b in zip(grads[:4], g2[:4]):
+        assert torch.equal(a, b[..., :16])
+    assert torch.equal(grads[4], g2[4])
+
+
+def test_d16_batched():
+    b, n, h = 2, 50, 2
+    parts = [inputs16(n, h, torch.bfloat16, seed=40 + i) for i in range(b)]
+    t = {k: torch.stack([p[k] for p in parts]) for k in parts[0]}
+    d = {k: v.to(DEV) for k, v in t.items()}
+    out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], B.ENDING)
+    grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d["mask"],
+                  B.ENDING)
+    torch.cuda.synchronize()
+    for i in range(b):
+        ro, rl = oracle.fwd(B.ENDING, t["q"][i], t["k"][i], t["v"][i], t["g"][i], t["bias"][i],
+                            t["mask"][i])
+        rg = oracle.bwd(B.ENDING, t["q"][i], t["k"][i], t["v"][i], t["g"][i], t["bias"][i],
+                        t["dout"][i], t["mask"][i])
+        close(f"out[{i}]", out[i], ro, torch.bfloat16)
+        for name, a, r in zip(("dq", "dk", "dv", "dg", "dbias"), grads, rg):
+            close(f"{name}[{i}]", a[i], r, torch.bfloat16)
