@@ -579,7 +579,7 @@ def main():
         host[node] = t
         x = {k: t[k].to(dev) for k in ("q", "k", "v", "g", "bias", "dout", "mask")}
         x["out"] = torch.empty_like(x["q"])
-        x["lse"] = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+        x["lse"] = torch.empty(x["bias"].shape, dtype=torch.float32, device=dev)
         for gname in ("dq", "dk", "dv", "dg"):
             x[gname] = torch.empty_like(x["q"])
         x["dbias"] = torch.empty_like(x["bias"])
@@ -590,17 +590,24 @@ def main():
     stream = torch.cuda.current_stream(dev).cuda_stream
     P = lambda a: a.data_ptr()  # noqa: E731
 
+    if w.batch > 1:
+        fwd_call = lambda node, *a: B.tri_attn_fwd_batched(node, dt, w.batch, *a)  # noqa: E731
+        bwd_call = lambda node, *a: B.tri_attn_bwd_batched(node, dt, w.batch, *a)  # noqa: E731
+    else:
+        fwd_call = lambda node, *a: B.tri_attn_fwd(node, dt, *a)  # noqa: E731
+        bwd_call = lambda node, *a: B.tri_attn_bwd(node, dt, *a)  # noqa: E731
+
     def step():
         for node, x in per_node:
-            st = B.tri_attn_fwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
-                                P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
-                                P(ws), ws_bytes, stream)
+            st = fwd_call(node, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]), P(x["g"]),
+                          P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]), P(ws), ws_bytes,
+                          stream)
             if st != B.OK:
                 raise B.TriAttnError(st, "tri_attn_fwd")
-            st = B.tri_attn_bwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
-                                P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]),
-                                P(x["dout"]), P(x["dq"]), P(x["dk"]), P(x["dv"]), P(x["dg"]),
-                                P(x["dbias"]), P(ws), ws_bytes, stream)
+            st = bwd_call(node, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]), P(x["g"]),
+                          P(x["bias"]), P(x["mask"]), P(x["out"]), P(x["lse"]), P(x["dout"]),
+                          P(x["dq"]), P(x["dk"]), P(x["dv"]), P(x["dg"]), P(x["dbias"]), P(ws),
+                          ws_bytes, stream)
             if st != B.OK:
                 raise B.TriAttnError(st, "tri_attn_bwd")
 
@@ -635,7 +642,9 @@ def main():
     traffic = recorded_traffic(dom, name)
 
     out = {
-        "metric": "triangle-attn fwd+bwd TFLOP/s (% of bf16 MFMA peak) at N=768; peak HBM bytes",
+        "metric": ("triangle-attn fwd+bwd TFLOP/s (% of bf16 MFMA peak) at N=768; peak HBM bytes"
+                   if name == W.HEADLINE else
+                   f"triangle-attn fwd+bwd TFLOP/s (nominal 14 N^3 H d per sample) on {name}"),
         "value": round(tflops, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -648,7 +657,7 @@ def main():
         "dtype": "bf16" if dt == B.BF16 else "f32",
         "data": "synthetic (seeded normals; the paper's PDB-derived pair representations are "
                 "not available)",
-        "config": {"workload": name, "n": n, "heads": h, "head_dim": d,
+        "config": {"workload": name, "batch": w.batch, "n": n, "heads": h, "head_dim": d,
                    "nodes": [W.NODE_NAMES[x] for x in w.nodes], "mask": "all keys valid"
                    if w.pad_frac == 0 and w.rand_pad_frac == 0 else "key padding",
                    "bias_std": round(w.bias_std, 4), "parallelism": "none (1 GPU)"},
@@ -662,7 +671,10 @@ def main():
         "per_kernel": per_kernel,
     }
     if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(w, host[w.nodes[0]], args.cpu_seconds)
+        h0 = host[w.nodes[0]]
+        if w.batch > 1:  # sample 0
+            h0 = {k: (v[0] if hasattr(v, "dim") else v) for k, v in h0.items()}
+        out["cpu_baseline"] = cpu_baseline(w, h0, args.cpu_seconds)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

@@ -38,12 +38,13 @@ class Workload:
     pad_frac: float = 0.0        # fixed key padding: floor(pad_frac * n) tokens
     rand_pad_frac: float = 0.0   # random key padding: Uniform{0..floor(rand_pad_frac * n)}
     seed: int = 0
+    batch: int = 1               # independent pair maps (sample i drawn with seed + i)
 
     @property
     def flops_fwd_bwd(self) -> float:
         """Nominal fwd+bwd flop: 4 N^3 H d forward (Q K^T, P V) plus
-        10 N^3 H d backward (S recompute, dV, dP, dK, dQ)."""
-        return 14.0 * self.n ** 3 * self.h * self.d
+        10 N^3 H d backward (S recompute, dV, dP, dK, dQ), per sample."""
+        return 14.0 * self.batch * self.n ** 3 * self.h * self.d
 
 
 # Triangle-attention shapes of AF3 pair stacks: H = 4 heads of d = 32.
@@ -57,6 +58,11 @@ WORKLOADS = {
                               bias_std=math.sqrt(2.0)),
     "tri_start_bf16_n1536_pad5": Workload("tri_start_bf16_n1536_pad5", 1536, 4, 32, torch.bfloat16,
                                           (STARTING,), pad_frac=0.05),
+    # a batch of four N = 384 maps (per-sample bias and mask) and heads of 16 channels
+    "tri_bf16_b4_n384": Workload("tri_bf16_b4_n384", 384, 4, 32, torch.bfloat16, (STARTING, ENDING),
+                                 bias_std=math.sqrt(2.0), batch=4),
+    "tri_bf16_n768_d16": Workload("tri_bf16_n768_d16", 768, 4, 16, torch.bfloat16,
+                                  (STARTING, ENDING), bias_std=math.sqrt(2.0)),
 }
 HEADLINE = "tri_bf16_n768"
 
@@ -132,8 +138,17 @@ def make_inputs(n: int, h: int, d: int, dtype: torch.dtype, seed: int = 0,
 
 def workload_inputs(w: Workload, node: Optional[int] = None):
     """Inputs of a named workload for one node variant: a dict with q, k, v,
-    g, bias, dout, mask (uint8 [n,n]) and n_pad."""
+    g, bias, dout, mask (uint8 [n,n]) and n_pad; with batch > 1 every tensor
+    has a leading batch axis (sample i from seed + i, the same key padding)."""
     node = w.nodes[0] if node is None else node
+    if w.batch > 1:
+        parts = [workload_inputs(dataclasses.replace(w, batch=1, seed=w.seed + i), node)
+                 for i in range(w.batch)]
+        t = {k: torch.stack([p[k] for p in parts]) for k in ("q", "k", "v", "g", "bias", "dout",
+                                                             "mask")}
+        t["n_pad"] = parts[0]["n_pad"]
+        t["node"] = node
+        return t
     t, gen = make_inputs(w.n, w.h, w.d, w.dtype, w.seed, w.bias_std)
     n_pad = int(math.floor(w.pad_frac * w.n))
     if w.rand_pad_frac > 0:
