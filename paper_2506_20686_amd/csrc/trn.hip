@@ -206,18 +206,21 @@ __device__ inline void store_row(bf16* base, int64_t row, int g, const f32x16 (&
 // ---- forward -------------------------------------------------------------------------
 //
 // Persistent workgroups of 8 waves (one per CU); a workgroup takes blocks of
-// 256 rows (32 per wave) and, per block, streams the F / 32 chunk images.
+// 256 rows (32 per wave) and, per block, streams the F / 32 chunk images,
+// two chunks per ring slot (one barrier per 64 hidden columns).
+
+constexpr int FWD_CPS = 2;  // chunk images per ring slot
 
 __global__ __launch_bounds__(TRN_THREADS, 1) void trn_fwd_kernel(TrnFwdArgs a) {
-  __shared__ __align__(16) char ring[2][TRN_FWD_IMG];
+  __shared__ __align__(16) char ring[2][FWD_CPS * TRN_FWD_IMG];
   __shared__ __align__(16) float gb[2][TRN_C];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = tid >> 6;
   const int64_t nblk = (a.m + TRN_ROWS - 1) / TRN_ROWS;
   if ((int64_t)blockIdx.x >= nblk) return;  // whole workgroup, before any barrier
-  const int nch = a.f / TRN_FC;
-  const int64_t nsteps = (nblk - blockIdx.x + gridDim.x - 1) / gridDim.x * nch;
-  constexpr int PER = TRN_FWD_IMG / 16 / TRN_THREADS;
+  const int nst = a.f / TRN_FC / FWD_CPS;  // ring stages per block (F is a multiple of 128)
+  const int64_t nsteps = (nblk - blockIdx.x + gridDim.x - 1) / gridDim.x * nst;
+  constexpr int PER = FWD_CPS * TRN_FWD_IMG / 16 / TRN_THREADS;
   Stage<PER> st;
   st.load(a.img, tid);
   if (tid < TRN_C) {
@@ -247,23 +250,28 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_fwd_kernel(TrnFwdArgs a) {
       a.rstd[row] = rstd;
     }
     f32x16 acc[4] = {};
-    for (int j = 0; j < nch; ++j, ++step) {
-      const char* cur = ring[step & 1];
+    for (int j = 0; j < nst; ++j, ++step) {
+      const char* slot = ring[step & 1];
       const bool more = step + 1 < nsteps;
-      if (more) st.load(a.img + (int64_t)(j + 1 == nch ? 0 : j + 1) * TRN_FWD_IMG, tid);
-      const f32x16 ha = h_tile(cur, a1, of);
-      const f32x16 hb = h_tile(cur + OFF_A1B, a1, of);
-      bf16x8 uf[2];
+      if (more)
+        st.load(a.img + (int64_t)(j + 1 == nst ? 0 : j + 1) * FWD_CPS * TRN_FWD_IMG, tid);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float x = ha[v];
-        uf[v >> 3][v & 7] = (bf16)(x * sigm(x) * hb[v]);
+      for (int c = 0; c < FWD_CPS; ++c) {
+        const char* cur = slot + c * TRN_FWD_IMG;
+        const f32x16 ha = h_tile(cur, a1, of);
+        const f32x16 hb = h_tile(cur + OFF_A1B, a1, of);
+        bf16x8 uf[2];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float x = ha[v];
+          uf[v >> 3][v & 7] = (bf16)(x * sigm(x) * hb[v]);
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int s = 0; s < 2; ++s)
+            acc[t] = Mma<bf16>::mma(*(const bf16x8*)(cur + a2[t][s]), uf[s], acc[t]);
       }
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-          acc[t] = Mma<bf16>::mma(*(const bf16x8*)(cur + a2[t][s]), uf[s], acc[t]);
       if (more) st.store(ring[(step + 1) & 1], tid);
       __syncthreads();
     }
@@ -474,14 +482,20 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
       duC = Mma<bf16>::mma(*(const bf16x8*)(cur + W_DO + o), wf2[wave][s][16 * g + (l32 & 15)],
                            duC);
     }
-    // swap with the partner lane (a <-> b of the same hidden column)
+    // a and b of the same hidden column sit in lanes l and l ^ 16 (rows of
+    // 16 lanes: a in the even rows, b in the odd ones).  v_permlane16_swap
+    // of h with itself leaves the even-row value (a) in its first result and
+    // the odd-row value (b) in its second, in every lane.  Both lanes then
+    // compute u; the a lane keeps da, the b lane db (selects, no branches).
     f32x16 dh, u;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const float other = __shfl_xor(hC[v], 16);
-      const float av = is_a ? hC[v] : other, bv = is_a ? other : hC[v];
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(hC[v]),
+                                                      __float_as_uint(hC[v]), false, false);
+      const float av = __uint_as_float(r[0]), bv = __uint_as_float(r[1]);
       const float sg = sigm(av), silu = av * sg;
-      dh[v] = is_a ? duC[v] * bv * sg * (1.f + av * (1.f - sg)) : duC[v] * silu;
+      const float fa = bv * fmaf(silu, 1.f - sg, sg);  // b sigmoid(a) (1 + a (1 - sigmoid(a)))
+      dh[v] = duC[v] * (is_a ? fa : silu);
       u[v] = silu * bv;
       ssum += dh[v];
     }
