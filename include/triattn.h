@@ -35,7 +35,8 @@
  *   - d must be 32; the whole-map and batched calls also take d = 16, which
  *     they run through the d = 32 kernels on zero-padded copies held in the
  *     workspace (zero channels add exact zeros: the results are those of
- *     d = 16).  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
+ *     d = 16), and d = 64, which runs register-staged kernels built for 64
+ *     channels.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
  *     positive (1/sqrt(d) is the usual choice).
  *   - The library never allocates or frees memory and never synchronises:
  *     work is enqueued on `stream` (a hipStream_t; NULL is the default stream)
@@ -61,7 +62,7 @@ extern "C" {
 typedef enum {
   TRIATTN_OK = 0,
   TRIATTN_ERR_INVALID_ARG = 1, /* null pointer, bad enum, size or scale out of range */
-  TRIATTN_ERR_UNSUPPORTED = 2, /* a value the library does not implement (e.g. d = 64) */
+  TRIATTN_ERR_UNSUPPORTED = 2, /* a value the library does not implement (e.g. d = 128) */
   TRIATTN_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
   TRIATTN_ERR_HIP = 4          /* a HIP launch reported an error */
 } triattn_status;

@@ -18,14 +18,19 @@ constexpr int64_t MAX_H = 64;
 
 size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// d = 32 natively; the whole-map calls also take d = 16 (padded to 32).
-int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d, bool allow16 = false) {
+// d = 32 everywhere; the whole-map and batched calls also take d = 16
+// (padded to 32) and d = 64 (the register-staged kernels).
+int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d, bool whole = false) {
   if (node != TRIATTN_STARTING && node != TRIATTN_ENDING) return TRIATTN_ERR_INVALID_ARG;
   if (dtype != TRIATTN_F32 && dtype != TRIATTN_BF16) return TRIATTN_ERR_INVALID_ARG;
   if (n < 1 || n > MAX_N || h < 1 || h > MAX_H || d < 1) return TRIATTN_ERR_INVALID_ARG;
-  if (d != triattn::HEAD_DIM && !(allow16 && d == 16)) return TRIATTN_ERR_UNSUPPORTED;
+  if (d != triattn::HEAD_DIM && !(whole && (d == 16 || d == 64))) return TRIATTN_ERR_UNSUPPORTED;
   return TRIATTN_OK;
 }
+
+// Channels per head the kernels run with: 64 for d = 64, else 32 (d = 16 is
+// padded to 32).
+int64_t kernel_d(int64_t d) { return d == 64 ? 64 : triattn::HEAD_DIM; }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -63,7 +68,7 @@ struct Layout {
 //   backward: bt, btT [H][np][np] f32, kbits, rowfull, lse2 and dsum [H][nr][np] f32,
 //             dA [nr][n][H][32] dtype (bf16: plus its low part, same size),
 //             slabs [nrc][H][np][np] f32
-Layout plan(bool bwd, int dtype, int64_t n, int64_t nr, int64_t h) {
+Layout plan(bool bwd, int dtype, int64_t n, int64_t nr, int64_t h, int64_t kd = 32) {
   const size_t np = (size_t)((n + 31) / 32 * 32);
   const size_t plane = (size_t)h * np * np * sizeof(float);
   Layout L{};
@@ -84,7 +89,7 @@ Layout plan(bool bwd, int dtype, int64_t n, int64_t nr, int64_t h) {
     off += round256(rows);
     L.dsum = off;
     off += round256(rows);
-    const size_t pair = (size_t)nr * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4);
+    const size_t pair = (size_t)nr * n * h * kd * (dtype == TRIATTN_BF16 ? 2 : 4);
     L.da = off;
     off += round256(pair);
     L.dalo = off;
@@ -99,14 +104,15 @@ Layout plan(bool bwd, int dtype, int64_t n, int64_t nr, int64_t h) {
 
 // nr = rows computed: n for a whole call, a row range's length otherwise
 // (starting node only; the range's tensors then hold nr rows).
-Geom geom(int node, int64_t n, int64_t nr, int64_t h, float scale) {
+Geom geom(int node, int64_t n, int64_t nr, int64_t h, float scale, int64_t kd = 32) {
   Geom g;
   g.n = (int)n;
   g.nr = (int)nr;
   g.H = (int)h;
   g.np = (int)((n + 31) / 32 * 32);
   g.nkt = g.np / 32;
-  const int64_t pos = h * triattn::HEAD_DIM, row = n * pos;
+  g.d = (int)kd;
+  const int64_t pos = h * kd, row = n * pos;
   g.sRow = node == TRIATTN_STARTING ? row : pos;
   g.sPos = node == TRIATTN_STARTING ? pos : row;
   g.lRow = node == TRIATTN_STARTING ? n * h : h;
@@ -162,7 +168,7 @@ struct Whole {
 };
 
 Whole whole_plan(bool bwd, int dtype, int64_t n, int64_t h, int64_t d) {
-  Whole w{plan(bwd, dtype, n, n, h), 0, 0, 0};
+  Whole w{plan(bwd, dtype, n, n, h, kernel_d(d)), 0, 0, 0};
   w.pad0 = w.L.total;
   const int npad = d == 16 ? (bwd ? 10 : 5) : 0;
   w.pad_bytes = round256((size_t)n * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4));
@@ -174,7 +180,7 @@ template <typename T>
 int fwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, const void* k,
             const void* v, const void* gate, const void* bias, const uint8_t* mask, void* out,
             float* lse, void* ws, hipStream_t s) {
-  if (d == triattn::HEAD_DIM)
+  if (d != 16)
     return run_fwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, ws, s);
   const int64_t rows = (int64_t)g.n * g.n * g.H;
   char* p[5];
@@ -194,7 +200,7 @@ int bwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, c
             const void* v, const void* gate, const void* bias, const uint8_t* mask,
             const void* out, const float* lse, const void* dout, void* dq, void* dk, void* dv,
             void* dg, void* dbias, void* ws, hipStream_t s) {
-  if (d == triattn::HEAD_DIM)
+  if (d != 16)
     return run_bwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, dout, dq, dk, dv, dg,
                       dbias, nullptr, ws, s);
   const int64_t rows = (int64_t)g.n * g.n * g.H;
@@ -249,7 +255,7 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const Whole W = whole_plan(false, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return fwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, workspace,
@@ -271,7 +277,7 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const Whole W = whole_plan(true, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return bwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, dout, dq,
@@ -317,7 +323,7 @@ int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Whole W = whole_plan(false, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
   for (int64_t b = 0; b < batch; ++b) {
@@ -353,7 +359,7 @@ int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Whole W = whole_plan(true, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale);
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
   for (int64_t b = 0; b < batch; ++b) {

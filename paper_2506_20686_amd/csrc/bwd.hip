@@ -38,10 +38,10 @@ constexpr bool kSplitDA = std::is_same<T, bf16>::value;
 
 // ---- elementwise preparation -------------------------------------------------------
 
-// Four threads per (pair, head): thread t handles channels 8 (t % 4) .. +7,
-// so every load and store is 16 contiguous bytes and a wave covers 16 whole
-// (pair, head) rows.
-template <typename T>
+// Four threads per (pair, head): thread t handles channels 32 c + 8 (t % 4)
+// .. +7 for c < D / 32, so every load and store is 16 contiguous bytes and a
+// wave covers 16 whole (pair, head) rows.
+template <typename T, int D = HEAD_DIM>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T* out,
                                                        const float* lse, const T* gate,
                                                        const T* dout, T* dg, T* da,
@@ -50,9 +50,10 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
   const int64_t idx = tix >> 2;  // (a, b, h)
   const int64_t total = (int64_t)G.nr * G.n * G.H;  // [nr][n][H] (ending node: nr = n)
   if (idx >= total) return;
-  const int64_t base = idx * HEAD_DIM + 8 * (tix & 3);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int jj = 0; jj < 2 * (D / 32); ++jj) {
+    const int j = jj & 1;
+    const int64_t base = idx * D + 32 * (jj >> 1) + 8 * (tix & 3);
     const f32x4 go = load4(dout + base + 4 * j), oo = load4(out + base + 4 * j);
     const f32x4 gg = load4(gate + base + 4 * j);
     f32x4 dgv, dav;
@@ -117,9 +118,12 @@ struct BwdArgs {
 // Per (row, head, 128 queries): stream the row's keys in blocks of 64 (K, K^T
 // and V staged in LDS, double-buffered).  dQ = scale (X - D Y) with
 // X = sum_k P dP K, Y = sum_k P K and D = sum_k P dP, all from one pass.
-template <typename T>
+template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
+  using TL = Tiles<D>;
+  constexpr int KCH = kch<T, D>();
+  constexpr int NO = D / 32;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int qb = w % a.nblk, rh = w / a.nblk;
@@ -130,28 +134,28 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   const int q = q0 + l32;  // lane <-> query
   const bool qok = q < G.n;
 
-  __shared__ __align__(16) T ks[2 * ROW_TILE];    // K   [key][channel]
-  __shared__ __align__(16) T kT[2 * TRANS_TILE];  // K^T [channel][key]
-  __shared__ __align__(16) T vs[2 * ROW_TILE];    // V   [key][channel]
+  __shared__ __align__(16) T ks[2 * TL::ROWT];    // K   [key][channel]
+  __shared__ __align__(16) T kT[2 * TL::TRANS];  // K^T [channel][key]
+  __shared__ __align__(16) T vs[2 * TL::ROWT];    // V   [key][channel]
 
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * D;
   const T* kr = a.k + rowbase;
   const T* vr = a.v + rowbase;
   const int last = G.n - 1;
-  typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+  typename M::frag qf[KCH], daf[KCH], dalf[KCH];
   float l2 = pos_inf();
-  zero_frags<T>(dalf);
+  zero_frags(dalf);
   if (qok) {
     row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
     row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
     if constexpr (kSplitDA<T>) row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
     l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
-    zero_frags<T>(qf);
-    zero_frags<T>(daf);
+    zero_frags(qf);
+    zero_frags(daf);
   }
   const float c1 = G.scale * LOG2E;
-  f32x16 xt = {}, yt = {};
+  f32x16 xt[NO] = {}, yt[NO] = {};
   float dpart = 0.f;
   const uint32_t* kb = a.kbits + (int64_t)r * G.nkt;
   const int nblk = (G.nkt + 1) >> 1;
@@ -163,22 +167,22 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   auto sub_tile = [&](const T* ksb, const T* kTb, const T* vsb, const f32x16& bias, uint32_t bits,
                       int u) {
     // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
-    typename M::frag af[M::KCH];
-    row_frags(ksb + (32 * u + l32) * LDS_ROW, g, af);
+    typename M::frag af[KCH];
+    row_frags(ksb + (32 * u + l32) * TL::ROW, g, af);
     f32x16 s = M::mma(af[0], qf[0], bias);
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], qf[t], s);
+    for (int t = 1; t < KCH; ++t) s = M::mma(af[t], qf[t], s);
     if (bits != 0xffffffffu) mask_rows(s, bits, g);
 #pragma unroll
     for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2));
     // dP^T = V dA^T, then P dP and its running sum D
-    row_frags(vsb + (32 * u + l32) * LDS_ROW, g, af);
+    row_frags(vsb + (32 * u + l32) * TL::ROW, g, af);
     f32x16 dp = M::mma(af[0], daf[0], f32x16{});
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], daf[t], dp);
+    for (int t = 1; t < KCH; ++t) dp = M::mma(af[t], daf[t], dp);
     if constexpr (kSplitDA<T>) {
 #pragma unroll
-      for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
+      for (int t = 0; t < KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
@@ -186,18 +190,21 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
       dpart += dp[v];
     }
     // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the keys)
-    typename M::frag pf[M::PCH], xf[M::PCH];
-    quad_frags(kTb + l32 * LDS_TROW + 32 * u, g, xf);
+    typename M::frag pf[M::PCH], sf[M::PCH], xf[M::PCH];
     acc_frags(dp, pf);
+    acc_frags(s, sf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) xt = M::mma(xf[t], pf[t], xt);
-    acc_frags(s, pf);
+    for (int c = 0; c < NO; ++c) {
+      quad_frags(kTb + (32 * c + l32) * LDS_TROW + 32 * u, g, xf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) yt = M::mma(xf[t], pf[t], yt);
+      for (int t = 0; t < M::PCH; ++t) xt[c] = M::mma(xf[t], pf[t], xt[c]);
+#pragma unroll
+      for (int t = 0; t < M::PCH; ++t) yt[c] = M::mma(xf[t], sf[t], yt[c]);
+    }
   };
 
-  PairPiece<T> kp;
-  RowPiece<T> vp;
+  PairPiece<T, D> kp;
+  RowPiece<T, D> vp;
   uint64_t bb = block_bits(kb, G.nkt, 0);
   kp.load(kr, G.sPos, 0, last, tid);
   vp.load(vr, G.sPos, 0, last, tid);
@@ -216,17 +223,17 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
     n1 = bias_tile(2 * bn + 1);
     const int buf = b & 1;
     if (active) {
-      const T* ksb = ks + buf * ROW_TILE;
-      const T* kTb = kT + buf * TRANS_TILE;
-      const T* vsb = vs + buf * ROW_TILE;
+      const T* ksb = ks + buf * TL::ROWT;
+      const T* kTb = kT + buf * TL::TRANS;
+      const T* vsb = vs + buf * TL::ROWT;
       if ((uint32_t)bb) sub_tile(ksb, kTb, vsb, c0, (uint32_t)bb, 0);
       if ((uint32_t)(bb >> 32)) sub_tile(ksb, kTb, vsb, c1, (uint32_t)(bb >> 32), 1);
     }
     if (b + 1 < nblk) {
       kp.validate(tid, bbn);
-      kp.store_rows(ks + (buf ^ 1) * ROW_TILE, tid);
-      kp.store_trans(kT + (buf ^ 1) * TRANS_TILE, tid);
-      vp.store(vs + (buf ^ 1) * ROW_TILE, tid, bbn);
+      kp.store_rows(ks + (buf ^ 1) * TL::ROWT, tid);
+      kp.store_trans(kT + (buf ^ 1) * TL::TRANS, tid);
+      vp.store(vs + (buf ^ 1) * TL::ROWT, tid, bbn);
     }
     __syncthreads();
     bb = bbn;
@@ -242,12 +249,15 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
   if (g == 0) a.dsum[((int64_t)h * G.nr + r) * G.np + q] = -dsum;  // stored negated
   const int64_t base = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    f32x4 x;
+  for (int c = 0; c < NO; ++c)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
-    store4(a.dq + base + 8 * j + 4 * g, x);
-  }
+    for (int j = 0; j < 4; ++j) {
+      f32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        x[e] = (xt[c][4 * j + e] - dsum * yt[c][4 * j + e]) * G.scale;
+      store4(a.dq + base + 32 * c + 8 * j + 4 * g, x);
+    }
 }
 
 // bf16 dQ (and D) with asynchronous LDS staging (see dma.h).  One workgroup
@@ -315,9 +325,9 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
     row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
     l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
-    zero_frags<bf16>(qf);
-    zero_frags<bf16>(daf);
-    zero_frags<bf16>(dalf);
+    zero_frags(qf);
+    zero_frags(daf);
+    zero_frags(dalf);
   }
   bool rows_full = true;
   for (int i = 0; i < nrows; ++i) rows_full = rows_full && const_load(a.rowfull + r0 + i) != 0u;
@@ -505,9 +515,12 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
 // Per (row, head, 128 keys; wave <-> 32 keys, lane <-> key): stream the row's
 // queries in blocks of 64 (Q, Q^T, dA, dA^T, the low part of dA, lse2 and -D
 // staged in LDS, double-buffered).  The paper's first backward stage.
-template <typename T>
+template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
+  using TL = Tiles<D>;
+  constexpr int KCH = kch<T, D>();
+  constexpr int NO = D / 32;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int kbk = w % a.nblk, rh = w / a.nblk;
@@ -520,29 +533,29 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   const bool kvalid = (bits >> l32) & 1u;
   const bool work = bits != 0u;  // some key of this wave is valid for the row
 
-  __shared__ __align__(16) T qs[2 * ROW_TILE];      // Q    [query][channel]
-  __shared__ __align__(16) T qT[2 * TRANS_TILE];    // Q^T  [channel][query]
-  __shared__ __align__(16) T das[2 * ROW_TILE];     // dA
-  __shared__ __align__(16) T daT[2 * TRANS_TILE];   // dA^T
-  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * ROW_TILE : 1];  // low part of dA
+  __shared__ __align__(16) T qs[2 * TL::ROWT];      // Q    [query][channel]
+  __shared__ __align__(16) T qT[2 * TL::TRANS];    // Q^T  [channel][query]
+  __shared__ __align__(16) T das[2 * TL::ROWT];     // dA
+  __shared__ __align__(16) T daT[2 * TL::TRANS];   // dA^T
+  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * TL::ROWT : 1];  // low part of dA
   __shared__ __align__(16) float l2s[2 * SPAN];     // lse2 of the block's queries
   __shared__ __align__(16) float nds[2 * SPAN];     // -D of the block's queries
 
-  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+  const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * D;
   const T* qr = a.q + rowbase;
   const T* dar = a.da + rowbase;
   const T* dalr = kSplitDA<T> ? a.dalo + rowbase : nullptr;
   const int last = G.n - 1;
-  typename M::frag kf[M::KCH], vf[M::KCH];
+  typename M::frag kf[KCH], vf[KCH];
   if (kvalid) {
     row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
     row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
   } else {
-    zero_frags<T>(kf);
-    zero_frags<T>(vf);
+    zero_frags(kf);
+    zero_frags(vf);
   }
   const float c1 = G.scale * LOG2E;
-  f32x16 dkt = {}, dvt = {};
+  f32x16 dkt[NO] = {}, dvt[NO] = {};
   const int ktc = active ? kt : 0;  // key tile of the key-major bias (0 for idle waves)
   const float* l2row = a.lse2 + ((int64_t)h * G.nr + r) * G.np;
   const float* drow = a.dsum + ((int64_t)h * G.nr + r) * G.np;
@@ -555,8 +568,8 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
     return x;
   };
 
-  PairPiece<T> qp, dap;
-  RowPiece<T> dlp;
+  PairPiece<T, D> qp, dap;
+  RowPiece<T, D> dlp;
   float sv = 0.f;  // thread < 64: lse2 of query tid; 64 <= thread < 128: -D of query tid-64
   const int sq = tid & 63;
   auto load_block = [&](int b) {
@@ -570,11 +583,11 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
     const uint64_t vb = range_bits64(b * SPAN, G.n);
     qp.validate(tid, vb);
     dap.validate(tid, vb);
-    qp.store_rows(qs + bf * ROW_TILE, tid);
-    qp.store_trans(qT + bf * TRANS_TILE, tid);
-    dap.store_rows(das + bf * ROW_TILE, tid);
-    dap.store_trans(daT + bf * TRANS_TILE, tid);
-    if constexpr (kSplitDA<T>) dlp.store(dals + bf * ROW_TILE, tid, vb);
+    qp.store_rows(qs + bf * TL::ROWT, tid);
+    qp.store_trans(qT + bf * TL::TRANS, tid);
+    dap.store_rows(das + bf * TL::ROWT, tid);
+    dap.store_trans(daT + bf * TL::TRANS, tid);
+    if constexpr (kSplitDA<T>) dlp.store(dals + bf * TL::ROWT, tid, vb);
     const bool in = b * SPAN + sq < G.np;  // queries n..np-1 carry +inf / 0 already
     if (tid < SPAN)
       l2s[bf * SPAN + sq] = in ? sv : pos_inf();
@@ -582,39 +595,45 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
       nds[bf * SPAN + sq] = in ? sv : 0.f;
   };
   auto sub_tile = [&](int bf, const f32x16& bias, int u) {
-    const T* qsb = qs + bf * ROW_TILE;
+    const T* qsb = qs + bf * TL::ROWT;
     // S = bias + Q K^T (lane <-> key, registers <-> queries)
-    typename M::frag af[M::KCH];
-    row_frags(qsb + (32 * u + l32) * LDS_ROW, g, af);
+    typename M::frag af[KCH];
+    row_frags(qsb + (32 * u + l32) * TL::ROW, g, af);
     f32x16 s = M::mma(af[0], kf[0], bias);
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], kf[t], s);
+    for (int t = 1; t < KCH; ++t) s = M::mma(af[t], kf[t], s);
     // P = exp2(S scale log2 e - lse2[query])
     const f32x16 l2 = load_quads(l2s + bf * SPAN + 32 * u + 4 * g);
 #pragma unroll
     for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -l2[v]));
     // dP - D = dA V^T - D, then dS = P (dP - D)
-    row_frags(das + bf * ROW_TILE + (32 * u + l32) * LDS_ROW, g, af);
+    row_frags(das + bf * TL::ROWT + (32 * u + l32) * TL::ROW, g, af);
     f32x16 dp = M::mma(af[0], vf[0], load_quads(nds + bf * SPAN + 32 * u + 4 * g));
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], vf[t], dp);
+    for (int t = 1; t < KCH; ++t) dp = M::mma(af[t], vf[t], dp);
     if constexpr (kSplitDA<T>) {
-      row_frags(dals + bf * ROW_TILE + (32 * u + l32) * LDS_ROW, g, af);
+      row_frags(dals + bf * TL::ROWT + (32 * u + l32) * TL::ROW, g, af);
 #pragma unroll
-      for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], vf[t], dp);
+      for (int t = 0; t < KCH; ++t) dp = M::mma(af[t], vf[t], dp);
     }
 #pragma unroll
     for (int v = 0; v < 16; ++v) dp[v] *= s[v];
     // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the block's queries)
     typename M::frag pf[M::PCH], xf[M::PCH];
     acc_frags(s, pf);
-    quad_frags(daT + bf * TRANS_TILE + l32 * LDS_TROW + 32 * u, g, xf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) dvt = M::mma(xf[t], pf[t], dvt);
+    for (int c = 0; c < NO; ++c) {
+      quad_frags(daT + bf * TL::TRANS + (32 * c + l32) * LDS_TROW + 32 * u, g, xf);
+#pragma unroll
+      for (int t = 0; t < M::PCH; ++t) dvt[c] = M::mma(xf[t], pf[t], dvt[c]);
+    }
     acc_frags(dp, pf);
-    quad_frags(qT + bf * TRANS_TILE + l32 * LDS_TROW + 32 * u, g, xf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) dkt = M::mma(xf[t], pf[t], dkt);
+    for (int c = 0; c < NO; ++c) {
+      quad_frags(qT + bf * TL::TRANS + (32 * c + l32) * LDS_TROW + 32 * u, g, xf);
+#pragma unroll
+      for (int t = 0; t < M::PCH; ++t) dkt[c] = M::mma(xf[t], pf[t], dkt[c]);
+    }
   };
 
   load_block(0);
@@ -642,17 +661,19 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
   if (!active || key >= G.n) return;
   const int64_t base = rowbase + (int64_t)key * G.sPos;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c0 = 8 * j + 4 * g;
-    f32x4 x, y;
+  for (int c = 0; c < NO; ++c)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = dvt[4 * j + e];
-      y[e] = dkt[4 * j + e] * G.scale;
+    for (int j = 0; j < 4; ++j) {
+      const int c0 = 32 * c + 8 * j + 4 * g;
+      f32x4 x, y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = dvt[c][4 * j + e];
+        y[e] = dkt[c][4 * j + e] * G.scale;
+      }
+      store4(a.dv + base + c0, x);
+      store4(a.dk + base + c0, y);
     }
-    store4(a.dv + base + c0, x);
-    store4(a.dk + base + c0, y);
-  }
 }
 
 // bf16 dK, dV with asynchronous LDS staging (see dma.h).  One workgroup =
@@ -723,8 +744,8 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
     row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
   } else {
-    zero_frags<bf16>(kf);
-    zero_frags<bf16>(vf);
+    zero_frags(kf);
+    zero_frags(vf);
   }
   // the fragments are plain register loads: let them complete before any
   // DMA is issued (with both kinds outstanding the compiler would wait for
@@ -913,9 +934,11 @@ constexpr int DB_ROWS = 2 * SPAN;  // keys (and queries) per workgroup block
 // its low part), lse2 and -D of the 128 queries are loaded with coalesced
 // 16-byte pieces (issued before the previous row's compute) and staged in
 // LDS.  The bias tiles stay in registers for all rows.
-template <typename T>
+template <typename T, int D>
 __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   using M = Mma<T>;
+  using TL = Tiles<D>;
+  constexpr int KCH = kch<T, D>();
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int kbk = w % a.nblk;
@@ -929,11 +952,11 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   const bool active = q0 < G.n;
   const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) T ks[2 * ROW_TILE];   // K  [key][channel] of the 128 keys
-  __shared__ __align__(16) T vs[2 * ROW_TILE];   // V
-  __shared__ __align__(16) T qs[2 * ROW_TILE];   // Q  [query][channel] of the 128 queries
-  __shared__ __align__(16) T das[2 * ROW_TILE];  // dA
-  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * ROW_TILE : 1];
+  __shared__ __align__(16) T ks[2 * TL::ROWT];   // K  [key][channel] of the 128 keys
+  __shared__ __align__(16) T vs[2 * TL::ROWT];   // V
+  __shared__ __align__(16) T qs[2 * TL::ROWT];   // Q  [query][channel] of the 128 queries
+  __shared__ __align__(16) T das[2 * TL::ROWT];  // dA
+  __shared__ __align__(16) T dals[kSplitDA<T> ? 2 * TL::ROWT : 1];
   __shared__ __align__(16) float l2s[DB_ROWS];   // lse2 of the queries (+inf: none valid)
   __shared__ __align__(16) float nds[DB_ROWS];   // -D
 
@@ -956,11 +979,11 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   // thread -> (half of the 128 positions, piece index within the half)
   const int half = tid >> 8, pt = tid & 255;
   const uint64_t qvalid = range_bits64(qstart + SPAN * half, G.n);
-  RowPiece<T> kp, vp, qp, dap, dlp;
+  RowPiece<T, D> kp, vp, qp, dap, dlp;
   float sv = 0.f;  // thread < 128: lse2 of query tid; 128 <= thread < 256: -D of query tid-128
   const int sq = min(qstart + (tid & 127), G.np - 1);
   auto load_row = [&](int r) {
-    const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+    const int64_t rowbase = (int64_t)r * G.sRow + (int64_t)h * D;
     kp.load(a.k + rowbase, G.sPos, kstart + SPAN * half, last, pt);
     vp.load(a.v + rowbase, G.sPos, kstart + SPAN * half, last, pt);
     qp.load(a.q + rowbase, G.sPos, qstart + SPAN * half, last, pt);
@@ -971,11 +994,11 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
   };
   auto store_row = [&](int r) {
     const uint64_t kv = row_bits(r, half);
-    kp.store(ks + half * ROW_TILE, pt, kv);
-    vp.store(vs + half * ROW_TILE, pt, kv);
-    qp.store(qs + half * ROW_TILE, pt, qvalid);
-    dap.store(das + half * ROW_TILE, pt, qvalid);
-    if constexpr (kSplitDA<T>) dlp.store(dals + half * ROW_TILE, pt, qvalid);
+    kp.store(ks + half * TL::ROWT, pt, kv);
+    vp.store(vs + half * TL::ROWT, pt, kv);
+    qp.store(qs + half * TL::ROWT, pt, qvalid);
+    dap.store(das + half * TL::ROWT, pt, qvalid);
+    if constexpr (kSplitDA<T>) dlp.store(dals + half * TL::ROWT, pt, qvalid);
     const bool in = qstart + (tid & 127) < G.n;
     if (tid < DB_ROWS)
       l2s[tid] = in ? sv : pos_inf();
@@ -993,29 +1016,29 @@ __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
     load_row(min(r + 1, r1 - 1));         // the last row reloads itself, unused
     const float l2 = l2s[qw + l32];
     if (active && bb != 0ull && !__all(l2 == pos_inf())) {
-      typename M::frag qf[M::KCH], daf[M::KCH], dalf[M::KCH];
-      row_frags(qs + (qw + l32) * LDS_ROW, g, qf);
-      row_frags(das + (qw + l32) * LDS_ROW, g, daf);
-      if constexpr (kSplitDA<T>) row_frags(dals + (qw + l32) * LDS_ROW, g, dalf);
+      typename M::frag qf[KCH], daf[KCH], dalf[KCH];
+      row_frags(qs + (qw + l32) * TL::ROW, g, qf);
+      row_frags(das + (qw + l32) * TL::ROW, g, daf);
+      if constexpr (kSplitDA<T>) row_frags(dals + (qw + l32) * TL::ROW, g, dalf);
       const f32x16 ndv = splat16(nds[qw + l32]);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const uint32_t bits = (uint32_t)(bb >> (32 * u));
         if (bits == 0u) continue;
-        const int off = (SPAN * kh + 32 * u + l32) * LDS_ROW;
-        typename M::frag af[M::KCH];
+        const int off = (SPAN * kh + 32 * u + l32) * TL::ROW;
+        typename M::frag af[KCH];
         row_frags(ks + off, g, af);
         f32x16 s = M::mma(af[0], qf[0], binit[u]);
 #pragma unroll
-        for (int t = 1; t < M::KCH; ++t) s = M::mma(af[t], qf[t], s);
+        for (int t = 1; t < KCH; ++t) s = M::mma(af[t], qf[t], s);
         if (bits != 0xffffffffu) mask_rows(s, bits, g);
         row_frags(vs + off, g, af);
         f32x16 dp = M::mma(af[0], daf[0], ndv);
 #pragma unroll
-        for (int t = 1; t < M::KCH; ++t) dp = M::mma(af[t], daf[t], dp);
+        for (int t = 1; t < KCH; ++t) dp = M::mma(af[t], daf[t], dp);
         if constexpr (kSplitDA<T>) {
 #pragma unroll
-          for (int t = 0; t < M::KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
+          for (int t = 0; t < KCH; ++t) dp = M::mma(af[t], dalf[t], dp);
         }
 #pragma unroll
         for (int v = 0; v < 16; ++v)
@@ -1261,10 +1284,15 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   T* da = (T*)ws.da;
   T* dalo = (T*)ws.dalo;
   const int64_t npair = (int64_t)g.nr * g.n * g.H;
+  const bool d64 = g.d == 64;  // register-staged kernels with 64 channels per head
   {
     KernelTimer t(K_BWD_PREP, s);
-    hipLaunchKernelGGL(bwd_prep_kernel<T>, dim3((unsigned)((4 * npair + 255) / 256)), dim3(256),
-                       0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+    if (d64)
+      hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), dim3((unsigned)((4 * npair + 255) / 256)),
+                         dim3(256), 0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+    else
+      hipLaunchKernelGGL((bwd_prep_kernel<T, 32>), dim3((unsigned)((4 * npair + 255) / 256)),
+                         dim3(256), 0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
   }
   if (g.np > g.n) {
     const int64_t npad = (int64_t)g.H * g.nr * (g.np - g.n);
@@ -1278,32 +1306,39 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
-    if constexpr (std::is_same<T, bf16>::value) {
+    if (d64) {
+      hipLaunchKernelGGL((dq_kernel<T, 64>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+    } else if constexpr (std::is_same<T, bf16>::value) {
       const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
       const int64_t nwg = (int64_t)nqb * ((g.nr + QD_ROWS - 1) / QD_ROWS) * g.H;
       hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(64 * QD_WAVES), 0, s, a, nqb);
     } else {
-      hipLaunchKernelGGL(dq_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dq_kernel<T, 32>), dim3((unsigned)nrow), dim3(256), 0, s, a);
     }
   }
   {
     KernelTimer t(K_DKDV, s);
-    if constexpr (std::is_same<T, bf16>::value) {
+    if (d64) {
+      hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+    } else if constexpr (std::is_same<T, bf16>::value) {
       const int64_t nwg = (int64_t)a.nblk * ((g.nr + KD_ROWS - 1) / KD_ROWS) * g.H;
       hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(64 * KD_WAVES), 0, s, a);
     } else {
-      hipLaunchKernelGGL(dkdv_kernel<T>, dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dkdv_kernel<T, 32>), dim3((unsigned)nrow), dim3(256), 0, s, a);
     }
   }
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
-    if constexpr (std::is_same<T, bf16>::value) {
+    if (d64) {
+      hipLaunchKernelGGL((db_kernel<T, 64>), dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+    } else if constexpr (std::is_same<T, bf16>::value) {
       const int nkb = (g.n + DBD_K - 1) / DBD_K;
       const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
       hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg), dim3(64 * DBD_WAVES), 0, s, a, nkb);
-    } else
-      hipLaunchKernelGGL(db_kernel<T>, dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((db_kernel<T, 32>), dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+    }
   }
   {
     const int64_t nred = (int64_t)g.H * g.n * ((g.n + 3) / 4);

@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace triattn {
 
 typedef __bf16 bf16;
@@ -66,25 +68,34 @@ struct Mma<float> {
   }
 };
 
-// Operand fragments of one 32-channel row (row-major [.][32] data, the row
-// being this lane's A row or B column).  Slot assignment: bf16 chunk t holds
-// channels 16 t + 8 g .. +7; fp32 chunk t holds channel 16 g + t.
-__device__ inline void row_frags(const bf16* p, int g, bf16x8 (&f)[Mma<bf16>::KCH]) {
-#pragma unroll
-  for (int t = 0; t < Mma<bf16>::KCH; ++t) f[t] = *(const bf16x8*)(p + 16 * t + 8 * g);
+// MFMA steps over the channels of a D-channel row.
+template <typename T, int D>
+constexpr int kch() {
+  return std::is_same<T, bf16>::value ? D / 16 : D / 2;
 }
-__device__ inline void row_frags(const float* p, int g, float (&f)[Mma<float>::KCH]) {
+
+// Operand fragments of one row of N MFMA steps (row-major [.][D] data, the
+// row being this lane's A row or B column).  Slot assignment: bf16 chunk t
+// holds channels 16 t + 8 g .. +7 (N = D / 16); fp32 chunk t holds channel
+// N g + t (N = D / 2).
+template <int N>
+__device__ inline void row_frags(const bf16* p, int g, bf16x8 (&f)[N]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f32x4 x = *(const f32x4*)(p + 16 * g + 4 * i);
+  for (int t = 0; t < N; ++t) f[t] = *(const bf16x8*)(p + 16 * t + 8 * g);
+}
+template <int N>
+__device__ inline void row_frags(const float* p, int g, float (&f)[N]) {
+#pragma unroll
+  for (int i = 0; i < N / 4; ++i) {
+    f32x4 x = *(const f32x4*)(p + N * g + 4 * i);
 #pragma unroll
     for (int e = 0; e < 4; ++e) f[4 * i + e] = x[e];
   }
 }
-template <typename T>
-__device__ inline void zero_frags(typename Mma<T>::frag (&f)[Mma<T>::KCH]) {
+template <typename F, int N>
+__device__ inline void zero_frags(F (&f)[N]) {
 #pragma unroll
-  for (int t = 0; t < Mma<T>::KCH; ++t) f[t] = typename Mma<T>::frag{};
+  for (int t = 0; t < N; ++t) f[t] = F{};
 }
 
 // Fragments of a transposed tile row p[0..31] whose index is the contraction

@@ -120,15 +120,21 @@ struct FwdArgs {
 // Online-softmax state of one (row, 32 queries) pair of a wave.  The row
 // sums of P accumulate on the MFMA: register 0 of the lanes of half 0 of
 // `l` holds sum_k P for the lane's query (see ones_row0).
+template <int D>
 struct SoftmaxState {
   float m;
   f32x16 l;
-  f32x16 o;  // O^T accumulator: registers <-> channels, lane <-> query
+  f32x16 o[D / 32];  // O^T accumulators (32 channels each): registers <-> channels, lane <-> query
 };
 
-template <typename T>
+// Forward with register-staged operand blocks (stage.h), for D = 32 or 64
+// channels per head.
+template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   using M = Mma<T>;
+  using TL = Tiles<D>;
+  constexpr int KCH = kch<T, D>();
+  constexpr int NO = D / 32;
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int qb = w % a.nqb, rh = w / a.nqb;
@@ -142,26 +148,27 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   const bool qok = q < G.n;
 
   // K block [key][channel] and V^T block [channel][key] of both rows, 2 buffers
-  __shared__ __align__(16) T ks[2 * FWD_ROWS * ROW_TILE];
-  __shared__ __align__(16) T vt[2 * FWD_ROWS * TRANS_TILE];
+  __shared__ __align__(16) T ks[2 * FWD_ROWS * TL::ROWT];
+  __shared__ __align__(16) T vt[2 * FWD_ROWS * TL::TRANS];
 
   const int last = G.n - 1;  // last key position
   int64_t rowbase[FWD_ROWS];
-  typename M::frag qf[FWD_ROWS][M::KCH];
+  typename M::frag qf[FWD_ROWS][KCH];
   const uint32_t* kb[FWD_ROWS];
-  SoftmaxState st[FWD_ROWS];
+  SoftmaxState<D> st[FWD_ROWS];
 #pragma unroll
   for (int i = 0; i < FWD_ROWS; ++i) {
     const int r = min(r0 + i, G.nr - 1);
-    rowbase[i] = (int64_t)r * G.sRow + (int64_t)h * HEAD_DIM;
+    rowbase[i] = (int64_t)r * G.sRow + (int64_t)h * D;
     kb[i] = a.kbits + (int64_t)r * G.nkt;
     if (qok)
       row_frags(a.q + rowbase[i] + (int64_t)q * G.sPos, g, qf[i]);
     else
-      zero_frags<T>(qf[i]);
+      zero_frags(qf[i]);
     st[i].m = neg_inf();
     st[i].l = f32x16{};
-    st[i].o = f32x16{};
+#pragma unroll
+    for (int c = 0; c < NO; ++c) st[i].o[c] = f32x16{};
   }
 
   const float c1 = G.scale * LOG2E;
@@ -179,23 +186,25 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   const typename M::frag ones = ones_row0<typename M::frag>(l32);
 
   // raise the running max to include mx (log2 units) and rescale the state
-  auto rescale = [&](SoftmaxState& S, float mx) {
+  auto rescale = [&](SoftmaxState<D>& S, float mx) {
     const float mnew = fmaxf(S.m, mx);
     const float alpha = __builtin_amdgcn_exp2f(S.m - mnew);
     S.l[0] *= alpha;  // rows 1..31 of l stay zero
 #pragma unroll
-    for (int v = 0; v < 16; ++v) S.o[v] *= alpha;
+    for (int c = 0; c < NO; ++c)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) S.o[c][v] *= alpha;
     S.m = mnew;
   };
 
   // one 32-key sub-tile of one row: logits, online softmax (base 2, stale max), P V
-  auto sub_tile = [&](SoftmaxState& S, const typename M::frag(&qfr)[M::KCH], const T* ksb,
+  auto sub_tile = [&](SoftmaxState<D>& S, const typename M::frag(&qfr)[KCH], const T* ksb,
                       const T* vtb, const f32x16& bias, uint32_t bits, int u) {
-    typename M::frag kf[M::KCH];
-    row_frags(ksb + (32 * u + l32) * LDS_ROW, g, kf);
+    typename M::frag kf[KCH];
+    row_frags(ksb + (32 * u + l32) * TL::ROW, g, kf);
     f32x16 s = M::mma(kf[0], qfr[0], bias);  // s^T = bias + K Q^T
 #pragma unroll
-    for (int t = 1; t < M::KCH; ++t) s = M::mma(kf[t], qfr[t], s);
+    for (int t = 1; t < KCH; ++t) s = M::mma(kf[t], qfr[t], s);
     if (bits != 0xffffffffu) mask_rows(s, bits, g);
     const float mx = wave_xor32_max(max16(s)) * c1;
     if (__any(mx > S.m + STALE_MAX_SLACK)) rescale(S, mx);
@@ -203,12 +212,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
     for (int v = 0; v < 16; ++v) s[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[v], c1, -S.m));
     typename M::frag pf[M::PCH], vf[M::PCH];
     acc_frags(s, pf);
-    quad_frags(vtb + l32 * LDS_TROW + 32 * u, g, vf);
 #pragma unroll
-    for (int t = 0; t < M::PCH; ++t) {
-      S.o = M::mma(vf[t], pf[t], S.o);  // O^T += V^T P^T
-      S.l = M::mma(ones, pf[t], S.l);   // row sums of P
+    for (int c = 0; c < NO; ++c) {
+      quad_frags(vtb + (32 * c + l32) * LDS_TROW + 32 * u, g, vf);
+#pragma unroll
+      for (int t = 0; t < M::PCH; ++t) S.o[c] = M::mma(vf[t], pf[t], S.o[c]);  // O^T += V^T P^T
     }
+#pragma unroll
+    for (int t = 0; t < M::PCH; ++t) S.l = M::mma(ones, pf[t], S.l);  // row sums of P
   };
 
   // A full 64-key block (every key valid in both rows): one straight-line
@@ -219,14 +230,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
     f32x16 s[FWD_ROWS][2];
 #pragma unroll
     for (int i = 0; i < FWD_ROWS; ++i) {
-      const T* ksb = ks + (buf * FWD_ROWS + i) * ROW_TILE;
+      const T* ksb = ks + (buf * FWD_ROWS + i) * TL::ROWT;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        typename M::frag kf[M::KCH];
-        row_frags(ksb + (32 * u + l32) * LDS_ROW, g, kf);
+        typename M::frag kf[KCH];
+        row_frags(ksb + (32 * u + l32) * TL::ROW, g, kf);
         s[i][u] = M::mma(kf[0], qf[i][0], u ? c1b : c0);
 #pragma unroll
-        for (int t = 1; t < M::KCH; ++t) s[i][u] = M::mma(kf[t], qf[i][t], s[i][u]);
+        for (int t = 1; t < KCH; ++t) s[i][u] = M::mma(kf[t], qf[i][t], s[i][u]);
       }
     }
     float mx[FWD_ROWS];
@@ -237,8 +248,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
       if (__any(mx[i] > st[i].m + STALE_MAX_SLACK)) rescale(st[i], mx[i]);
 #pragma unroll
     for (int i = 0; i < FWD_ROWS; ++i) {
-      SoftmaxState& S = st[i];
-      const T* vtb = vt + (buf * FWD_ROWS + i) * TRANS_TILE;
+      SoftmaxState<D>& S = st[i];
+      const T* vtb = vt + (buf * FWD_ROWS + i) * TL::TRANS;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
 #pragma unroll
@@ -246,12 +257,14 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
           s[i][u][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i][u][v], c1, -S.m));
         typename M::frag pf[M::PCH], vf[M::PCH];
         acc_frags(s[i][u], pf);
-        quad_frags(vtb + l32 * LDS_TROW + 32 * u, g, vf);
 #pragma unroll
-        for (int t = 0; t < M::PCH; ++t) {
-          S.o = M::mma(vf[t], pf[t], S.o);
-          S.l = M::mma(ones, pf[t], S.l);
+        for (int c = 0; c < NO; ++c) {
+          quad_frags(vtb + (32 * c + l32) * LDS_TROW + 32 * u, g, vf);
+#pragma unroll
+          for (int t = 0; t < M::PCH; ++t) S.o[c] = M::mma(vf[t], pf[t], S.o[c]);
         }
+#pragma unroll
+        for (int t = 0; t < M::PCH; ++t) S.l = M::mma(ones, pf[t], S.l);
       }
     }
   };
@@ -259,8 +272,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
   // staging: each row's block is 256 K pieces and 256 V pieces (64 positions
   // x 32 channels); thread tid moves FWD_ROWS consecutive pieces of row srow
   constexpr int TPR = 256 / FWD_ROWS;  // threads per staged row
-  RowPiece<T> kp[FWD_ROWS];
-  PairPiece<T> vp[FWD_ROWS];
+  RowPiece<T, D> kp[FWD_ROWS];
+  PairPiece<T, D> vp[FWD_ROWS];
   const int srow = tid / TPR;
   const int sp0 = FWD_ROWS * (tid % TPR);
   const T* skr = a.k + rowbase[srow];
@@ -273,8 +286,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
     }
   };
   auto stage_store = [&](int buf, const uint64_t(&bb)[FWD_ROWS]) {
-    T* kd = ks + (buf * FWD_ROWS + srow) * ROW_TILE;
-    T* vd = vt + (buf * FWD_ROWS + srow) * TRANS_TILE;
+    T* kd = ks + (buf * FWD_ROWS + srow) * TL::ROWT;
+    T* vd = vt + (buf * FWD_ROWS + srow) * TL::TRANS;
     const uint64_t v = bb[srow];
 #pragma unroll
     for (int i = 0; i < FWD_ROWS; ++i) {
@@ -305,8 +318,8 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
     } else if (active) {
 #pragma unroll
       for (int i = 0; i < FWD_ROWS; ++i) {
-        const T* ksb = ks + (buf * FWD_ROWS + i) * ROW_TILE;
-        const T* vtb = vt + (buf * FWD_ROWS + i) * TRANS_TILE;
+        const T* ksb = ks + (buf * FWD_ROWS + i) * TL::ROWT;
+        const T* vtb = vt + (buf * FWD_ROWS + i) * TL::TRANS;
         if ((uint32_t)bb[i]) sub_tile(st[i], qf[i], ksb, vtb, c0, (uint32_t)bb[i], 0);
         if ((uint32_t)(bb[i] >> 32))
           sub_tile(st[i], qf[i], ksb, vtb, c1b, (uint32_t)(bb[i] >> 32), 1);
@@ -328,19 +341,22 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
 #pragma unroll
   for (int i = 0; i < FWD_ROWS; ++i) {
     if (i == 1 && !row1) break;
-    const SoftmaxState& S = st[i];
+    const SoftmaxState<D>& S = st[i];
     const float lt = wave_xor32_sum(S.l[0]);  // half 1 holds zeros in register 0
     const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
     const int64_t base = rowbase[i] + (int64_t)q * G.sPos;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c0 = 8 * j + 4 * g;
-      const f32x4 gv = load4(a.gate + base + c0);
-      f32x4 ov;
+    for (int c = 0; c < NO; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) ov[e] = S.o[4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
-      store4(a.out + base + c0, ov);
-    }
+      for (int j = 0; j < 4; ++j) {
+        const int c0 = 32 * c + 8 * j + 4 * g;
+        const f32x4 gv = load4(a.gate + base + c0);
+        f32x4 ov;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          ov[e] = S.o[c][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+        store4(a.out + base + c0, ov);
+      }
     if (g == 0)
       a.lse[(int64_t)(r0 + i) * G.lRow + (int64_t)q * G.lPos + h] =
           lt > 0.f ? (S.m + log2f(lt)) * LN2 : neg_inf();
@@ -403,7 +419,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     if (act[i] && qv[i] < G.n)
       row_frags(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
     else
-      zero_frags<bf16>(qf[i]);
+      zero_frags(qf[i]);
   }
   const bool active = act[0];  // tile 1 active implies tile 0 active
   bool rows_full = true;
@@ -621,14 +637,17 @@ template <typename T>
 hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, const T* v,
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, p.rowfull, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
-  if constexpr (std::is_same<T, bf16>::value) {
-    const int64_t nwg = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
+  const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
+  if (g.d == 64) {
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwg), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg), dim3(256), 0, s, a);
+  } else if constexpr (std::is_same<T, bf16>::value) {
+    const int64_t nwd = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
+    KernelTimer t(K_FWD, s);
+    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwd), dim3(512), 0, s, a);
   } else {
-    const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL(fwd_kernel<T>, dim3((unsigned)nwg), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<T, 32>), dim3((unsigned)nwg), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

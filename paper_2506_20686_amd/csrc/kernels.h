@@ -18,7 +18,8 @@ struct Geom {
   int H;     // heads
   int np;    // n rounded up to a multiple of 32
   int nkt;   // np / 32 key tiles
-  int64_t sRow, sPos;  // element strides of [nr][n][H][32] tensors
+  int d;     // channels per head: 32, or 64 (register-staged kernels only)
+  int64_t sRow, sPos;  // element strides of [nr][n][H][d] tensors
   int64_t lRow, lPos;  // element strides of [n][n][H] tensors (lse)
   float scale;         // softmax scale on Q K^T
 };

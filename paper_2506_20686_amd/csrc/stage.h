@@ -14,14 +14,24 @@
 
 namespace triattn {
 
-constexpr int SPAN = 64;               // positions per staged block
-constexpr int LDS_ROW = HEAD_DIM + 8;  // row-major tile [position][channel]: 80-byte rows (bf16)
+constexpr int SPAN = 64;  // positions per staged block
 // Transposed tile [channel][position].  The row stride is an odd multiple of
 // 8 bytes (136 bytes for bf16, 272 for fp32), so the quad reads of 32
 // consecutive rows fall on 32 different bank pairs.
 constexpr int LDS_TROW = SPAN + 4;
-constexpr int ROW_TILE = SPAN * LDS_ROW;
-constexpr int TRANS_TILE = HEAD_DIM * LDS_TROW;
+
+// Tile shapes for D channels per position: row-major [position][channel]
+// with D + 8 elements per row (80-byte rows for bf16 at D = 32), and the
+// transposed [channel][position] tile.
+template <int D>
+struct Tiles {
+  static constexpr int ROW = D + 8;
+  static constexpr int ROWT = SPAN * ROW;
+  static constexpr int TRANS = D * LDS_TROW;
+};
+constexpr int LDS_ROW = Tiles<HEAD_DIM>::ROW;
+constexpr int ROW_TILE = Tiles<HEAD_DIM>::ROWT;
+constexpr int TRANS_TILE = Tiles<HEAD_DIM>::TRANS;
 
 template <typename T>
 struct Vec;
@@ -36,85 +46,117 @@ struct Vec<float> {
 
 __device__ inline bool bit64(uint64_t b, int i) { return (b >> i) & 1ull; }
 
-// One position x 8 channels: thread t holds position t / 4, channels
-// 8 (t % 4) .. +7.  Feeds a row-major tile.
-template <typename T>
+// One position x 8 channels per 32-channel group: thread t holds position
+// t / 4, channels 32 i + 8 (t % 4) .. +7 for i < D / 32.  Feeds a row-major
+// tile.
+template <typename T, int D = HEAD_DIM>
 struct RowPiece;
 
-template <>
-struct RowPiece<bf16> {
-  bf16x8 x;
+template <int D>
+struct RowPiece<bf16, D> {
+  bf16x8 x[D / 32];
   __device__ inline void load(const bf16* src, int64_t sPos, int start, int last, int t) {
     const int p = start + SPAN - 1 <= last ? start + (t >> 2) : min(start + (t >> 2), last);
-    x = *(const bf16x8*)(src + (int64_t)p * sPos + 8 * (t & 3));
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) x[i] = *(const bf16x8*)(src + (int64_t)p * sPos + 32 * i + 8 * (t & 3));
   }
   __device__ inline void store(bf16* tile, int t, uint64_t valid) const {
-    const bf16x8 v = (valid == ~0ull || bit64(valid, t >> 2)) ? x : bf16x8{};
-    *(bf16x8*)(tile + (t >> 2) * LDS_ROW + 8 * (t & 3)) = v;
+    const bool ok = valid == ~0ull || bit64(valid, t >> 2);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+      *(bf16x8*)(tile + (t >> 2) * Tiles<D>::ROW + 32 * i + 8 * (t & 3)) = ok ? x[i] : bf16x8{};
   }
 };
 
-template <>
-struct RowPiece<float> {
-  f32x4 lo, hi;
+template <int D>
+struct RowPiece<float, D> {
+  f32x4 lo[D / 32], hi[D / 32];
   __device__ inline void load(const float* src, int64_t sPos, int start, int last, int t) {
     const int p = min(start + (t >> 2), last);
-    const float* s = src + (int64_t)p * sPos + 8 * (t & 3);
-    lo = *(const f32x4*)s;
-    hi = *(const f32x4*)(s + 4);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+      const float* s = src + (int64_t)p * sPos + 32 * i + 8 * (t & 3);
+      lo[i] = *(const f32x4*)s;
+      hi[i] = *(const f32x4*)(s + 4);
+    }
   }
   __device__ inline void store(float* tile, int t, uint64_t valid) const {
     const bool ok = valid == ~0ull || bit64(valid, t >> 2);
-    float* d = tile + (t >> 2) * LDS_ROW + 8 * (t & 3);
-    *(f32x4*)d = ok ? lo : f32x4{};
-    *(f32x4*)(d + 4) = ok ? hi : f32x4{};
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+      float* d = tile + (t >> 2) * Tiles<D>::ROW + 32 * i + 8 * (t & 3);
+      *(f32x4*)d = ok ? lo[i] : f32x4{};
+      *(f32x4*)(d + 4) = ok ? hi[i] : f32x4{};
+    }
   }
 };
 
-// Two positions x 4 channels: thread t holds positions p, p + 1 with
-// p = 2 (t / 8) and channels 4 (t % 8) .. +3.  Feeds a row-major tile, a
-// transposed tile, or both.  Call validate() before storing.
-template <typename T>
+// Two positions x 4 channels per 32-channel group: thread t holds positions
+// p, p + 1 with p = 2 (t / 8) and channels 32 i + 4 (t % 8) .. +3 for
+// i < D / 32.  Feeds a row-major tile, a transposed tile, or both.  Call
+// validate() before storing.
+template <typename T, int D = HEAD_DIM>
 struct PairPiece {
   using V4 = typename Vec<T>::v4;
-  V4 x0, x1;
+  V4 x0[D / 32], x1[D / 32];
   __device__ inline void load(const T* src, int64_t sPos, int start, int last, int t) {
     const int p = start + 2 * (t >> 3), c0 = 4 * (t & 7);
-    x0 = *(const V4*)(src + (int64_t)min(p, last) * sPos + c0);
-    x1 = *(const V4*)(src + (int64_t)min(p + 1, last) * sPos + c0);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+      x0[i] = *(const V4*)(src + (int64_t)min(p, last) * sPos + 32 * i + c0);
+      x1[i] = *(const V4*)(src + (int64_t)min(p + 1, last) * sPos + 32 * i + c0);
+    }
   }
   __device__ inline void validate(int t, uint64_t valid) {
     if (valid == ~0ull) return;  // the common full block: no selects
     const int p = 2 * (t >> 3);
-    if (!bit64(valid, p)) x0 = V4{};
-    if (!bit64(valid, p + 1)) x1 = V4{};
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+      if (!bit64(valid, p)) x0[i] = V4{};
+      if (!bit64(valid, p + 1)) x1[i] = V4{};
+    }
   }
   __device__ inline void store_rows(T* tile, int t) const {
     const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
-    *(V4*)(tile + p * LDS_ROW + c0) = x0;
-    *(V4*)(tile + (p + 1) * LDS_ROW + c0) = x1;
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) {
+      *(V4*)(tile + p * Tiles<D>::ROW + 32 * i + c0) = x0[i];
+      *(V4*)(tile + (p + 1) * Tiles<D>::ROW + 32 * i + c0) = x1[i];
+    }
   }
-  __device__ inline void store_trans(T* tileT, int t) const;
+  __device__ inline void store_trans(T* tileT, int t) const {
+    const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) store_trans4(tileT + (32 * i + c0) * LDS_TROW + p, x0[i], x1[i]);
+  }
+  // channel j of the two positions -> row j of the transposed tile
+  __device__ static inline void store_trans4(T* d, const V4& a, const V4& b);
 };
 
 // Interleave the two positions' bf16 channels into 32-bit words with integer
 // ops (channel j of positions p and p + 1 form one word).
 template <>
-__device__ inline void PairPiece<bf16>::store_trans(bf16* tileT, int t) const {
-  const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
+__device__ inline void PairPiece<bf16, 32>::store_trans4(bf16* d, const bf16x4& x0, const bf16x4& x1) {
   const u32x2 a = __builtin_bit_cast(u32x2, x0), b = __builtin_bit_cast(u32x2, x1);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const uint32_t x = a[j >> 1], y = b[j >> 1];
     const uint32_t w = (j & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
-    *(uint32_t*)(tileT + (c0 + j) * LDS_TROW + p) = w;
+    *(uint32_t*)(d + j * LDS_TROW) = w;
   }
 }
 template <>
-__device__ inline void PairPiece<float>::store_trans(float* tileT, int t) const {
-  const int p = 2 * (t >> 3), c0 = 4 * (t & 7);
+__device__ inline void PairPiece<bf16, 64>::store_trans4(bf16* d, const bf16x4& x0, const bf16x4& x1) {
+  PairPiece<bf16, 32>::store_trans4(d, x0, x1);
+}
+template <>
+__device__ inline void PairPiece<float, 32>::store_trans4(float* d, const f32x4& x0, const f32x4& x1) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) *(f32x2*)(tileT + (c0 + j) * LDS_TROW + p) = f32x2{x0[j], x1[j]};
+  for (int j = 0; j < 4; ++j) *(f32x2*)(d + j * LDS_TROW) = f32x2{x0[j], x1[j]};
+}
+template <>
+__device__ inline void PairPiece<float, 64>::store_trans4(float* d, const f32x4& x0, const f32x4& x1) {
+  PairPiece<float, 32>::store_trans4(d, x0, x1);
 }
 
 // Bits of positions start .. start+63 that lie inside [0, n).

@@ -71,7 +71,7 @@ def test_workspace_size_errors(lib):
     assert ws_bytes(f, 0, B.BF16, 0, 1, 32)[0] == B.ERR_INVALID_ARG
     assert ws_bytes(f, 0, B.BF16, 8, 0, 32)[0] == B.ERR_INVALID_ARG
     assert ws_bytes(f, 0, B.BF16, 9000, 1, 32)[0] == B.ERR_INVALID_ARG
-    assert ws_bytes(f, 0, B.BF16, 8, 1, 64)[0] == B.ERR_UNSUPPORTED
+    assert ws_bytes(f, 0, B.BF16, 8, 1, 128)[0] == B.ERR_UNSUPPORTED
     assert f(0, B.BF16, 8, 1, 32, None) == B.ERR_INVALID_ARG
 
 
@@ -101,7 +101,7 @@ def bwd_args(**over):
 FWD_BAD = [
     (dict(node=5), B.ERR_INVALID_ARG), (dict(dtype=-1), B.ERR_INVALID_ARG),
     (dict(n=0), B.ERR_INVALID_ARG), (dict(h=0), B.ERR_INVALID_ARG),
-    (dict(d=64), B.ERR_UNSUPPORTED), (dict(d=24), B.ERR_UNSUPPORTED), (dict(scale=0.0), B.ERR_INVALID_ARG),
+    (dict(d=128), B.ERR_UNSUPPORTED), (dict(d=24), B.ERR_UNSUPPORTED), (dict(scale=0.0), B.ERR_INVALID_ARG),
     (dict(scale=-1.0), B.ERR_INVALID_ARG), (dict(scale=float("nan")), B.ERR_INVALID_ARG),
     (dict(scale=float("inf")), B.ERR_INVALID_ARG),
     (dict(q=None), B.ERR_INVALID_ARG), (dict(k=None), B.ERR_INVALID_ARG),
@@ -266,7 +266,7 @@ def rows_bwd_args(**over):
 
 
 ROWS_BAD = [(o, c) for o, c in FWD_BAD if "node" not in o] + [
-    (dict(d=16), B.ERR_UNSUPPORTED),  # row ranges take d = 32 only
+    (dict(d=16), B.ERR_UNSUPPORTED), (dict(d=64), B.ERR_UNSUPPORTED),  # row ranges: d = 32
     (dict(rows=0), B.ERR_INVALID_ARG), (dict(rows=17), B.ERR_INVALID_ARG),
     (dict(rows=-3), B.ERR_INVALID_ARG),
 ]
@@ -420,3 +420,19 @@ def test_d16_workspace_adds_padded_copies(lib):
                 st16, b16 = ws_bytes(fn, node, dtype, n, h, 16)
                 assert st == st16 == B.OK
                 assert b16 == b32 + k * pad
+
+
+def test_d64_workspace_scales_the_pair_buffers(lib):
+    """d = 64 runs the register-staged kernels with 64 channels: the dA
+    buffers (and the bf16 low part) double, nothing else changes."""
+    for dtype, el, parts in ((B.BF16, 2, 2), (B.F32, 4, 1)):
+        n, h = 40, 3
+        pair = -(-n * n * h * 32 * el // 256) * 256
+        pair64 = -(-n * n * h * 64 * el // 256) * 256
+        st, b32 = ws_bytes(lib.tri_attn_bwd_workspace_bytes, 0, dtype, n, h, 32)
+        st64, b64 = ws_bytes(lib.tri_attn_bwd_workspace_bytes, 0, dtype, n, h, 64)
+        assert st == st64 == B.OK
+        assert b64 == b32 + parts * (pair64 - pair)
+        st, f32_ = ws_bytes(lib.tri_attn_fwd_workspace_bytes, 0, dtype, n, h, 32)
+        st, f64_ = ws_bytes(lib.tri_attn_fwd_workspace_bytes, 0, dtype, n, h, 64)
+        assert f32_ == f64_
