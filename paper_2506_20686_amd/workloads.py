@@ -63,6 +63,8 @@ WORKLOADS = {
                                  bias_std=math.sqrt(2.0), batch=4),
     "tri_bf16_n768_d16": Workload("tri_bf16_n768_d16", 768, 4, 16, torch.bfloat16,
                                   (STARTING, ENDING), bias_std=math.sqrt(2.0)),
+    "tri_bf16_n768_d64": Workload("tri_bf16_n768_d64", 768, 4, 64, torch.bfloat16,
+                                  (STARTING, ENDING), bias_std=math.sqrt(2.0)),
 }
 HEADLINE = "tri_bf16_n768"
 
