@@ -533,8 +533,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the row-sharded "
-              "design is described in DESIGN.md); run it with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (one GPU's share "
+              "of a row-sharded run is --workload tri_rows_bf16_n768_r96); run it with --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.copy_bytes > 0:
