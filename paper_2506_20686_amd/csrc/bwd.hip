@@ -677,12 +677,13 @@ __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
 }
 
 // bf16 dK, dV with asynchronous LDS staging (see dma.h).  One workgroup =
-// 16 waves = 128 keys x 4 rows of one head: wave w owns key tile w % 4 of
-// the block (lane <-> key) in row r0 + w / 4.  Queries stream in tiles of
-// 32; per tile, Q, dA and its low part of the 4 rows, their lse2 and -D,
-// and the key-major bias tiles of the 128 keys (shared by the rows), 41 KB,
-// are copied HBM -> LDS by DMA into a three-slot ring, two tiles ahead.
-// One workgroup per CU runs four waves per SIMD.  Q^T and dA^T fragments
+// 4 KD_ROWS waves = 128 keys x KD_ROWS rows of one head: wave w owns key
+// tile w % 4 of the block (lane <-> key) in row r0 + w / 4.  Queries stream
+// in tiles of 32; per tile, Q, dA and its low part of the rows, their lse2
+// and -D, and the key-major bias tiles of the 128 keys (shared by the rows;
+// 16 KB of the 29 KB per tile at KD_ROWS = 2) are copied HBM -> LDS by DMA
+// into a ring of KD_SLOTS slots (57 KB of LDS at 2 rows and 2 slots).  Two
+// workgroups share a CU at four waves per SIMD.  Q^T and dA^T fragments
 // come from the transposing LDS read of the same row-major tiles.  The
 // DMAs go through buffer resources advanced in scalar registers, and the
 // loop is unrolled by the ring length, so no vector instruction is spent on
@@ -708,7 +709,7 @@ constexpr int KD_TS = KD_ROWS * KD_BLK;                // 8 KB: one slot of a ti
 constexpr int KD_Q = 0, KD_DA = KD_SLOTS * KD_TS, KD_LO = 2 * KD_SLOTS * KD_TS;
 constexpr int KD_BIAS = 3 * KD_SLOTS * KD_TS, KD_BS = 4 * 4096;
 constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
-constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 123 KB
+constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 57 KB at 2 rows, 2 slots
 
 __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a) {
   using M = Mma<bf16>;

@@ -127,6 +127,13 @@ def test_degenerate_masks(node):
     full_check(t, node, torch.bfloat16)
 
 
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_maximum_heads(node):
+    """h = 64, the largest head count the library takes."""
+    t = inputs(33, 64, torch.bfloat16, seed=640 + node, mask_kind="random")
+    full_check(t, node, torch.bfloat16)
+
+
 def test_non_default_scale():
     t = inputs(48, 2, torch.float32, seed=5, mask_kind="random")
     full_check(t, B.ENDING, torch.float32, scale=0.9)
