@@ -388,8 +388,13 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_dx_kernel(TrnBwdArgs a
 // One ring slot: o1 (bf16), xhat (bf16) and dout tiles of 32 rows, each as
 // four 32-column blocks of 64-byte rows (blk_off).  The staging threads
 // normalise once per block for all waves.
-constexpr int W_SLOT = 3 * 8192;
-constexpr int W_XH = 8192, W_DO = 16384;
+// Blocks sit W_BLK bytes apart (2 KB + 64): the staging stores of one wave
+// touch the four blocks of a row at once, and the extra 64 bytes put them on
+// different banks.  Every read stays inside one block.
+constexpr int W_BLK = 2048 + 64;
+constexpr int W_TILE = 4 * W_BLK;
+constexpr int W_SLOT = 3 * W_TILE;
+constexpr int W_XH = W_TILE, W_DO = 2 * W_TILE;
 
 __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a, int64_t rpp) {
   __shared__ __align__(16) char ring[2][W_SLOT];
@@ -427,7 +432,7 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
   // staging: thread tid takes 8 features (chunk tid % 16) of row tid / 16:
   // x, dout and the row's statistics; it writes o1 and xhat in bf16 and dout
   const int sr = tid >> 4, sc = tid & 15;
-  const uint32_t soff = (sc >> 2) * 2048 + blk_off(sr, sc & 3);
+  const uint32_t soff = (sc >> 2) * W_BLK + blk_off(sr, sc & 3);
   struct Staged {
     bf16x8 x, d;
     float mean, rstd;
@@ -468,7 +473,11 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
   // 16 (q % 2) + 4 (q / 2) + {0..3} and + 8 + {0..3}; supplying lane 4 e + j
   // of the group addresses row +e, columns 4 j .. + 3 of the 16-column tile
   const int qi = lane & 15, qe = qi >> 2, qj = qi & 3;
+  // the odd groups read their second quad of rows first: rows r and r + 16
+  // share banks, rows r + 24 and r do not (blk_off's permutation), so the two
+  // groups of each half-wave never read the same banks together
   const int qrow = 16 * (q & 1) + 4 * (q >> 1) + qe;
+  const int qfirst = qrow + 8 * (q & 1), qsecond = qrow + 8 * (1 - (q & 1));
   for (int ib = 0; ib < nb; ++ib) {
     const char* cur = ring[ib & 1];
     const bool more = ib + 1 < nb;
@@ -477,7 +486,7 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
     f32x16 hC = {}, duC = {};
 #pragma unroll
     for (int s = 0; s < TRN_NT; ++s) {
-      const uint32_t o = (s >> 1) * 2048 + blk_off(l32, 2 * (s & 1) + g);
+      const uint32_t o = (s >> 1) * W_BLK + blk_off(l32, 2 * (s & 1) + g);
       hC = Mma<bf16>::mma(*(const bf16x8*)(cur + o), wf1[wave][s][lane], hC);
       duC = Mma<bf16>::mma(*(const bf16x8*)(cur + W_DO + o), wf2[wave][s][16 * g + (l32 & 15)],
                            duC);
@@ -508,7 +517,7 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
       for (int e = 0; e < 8; ++e) bf[e] = (bf16)dh[8 * s + e];
 #pragma unroll
       for (int t = 0; t < 4; t += 2) {
-        const uint32_t b0 = lds_addr(cur + W_XH + t * 2048), b1 = b0 + 2048;
+        const uint32_t b0 = lds_addr(cur + W_XH + t * W_BLK), b1 = b0 + W_BLK;
         s16x4 rr[4];
         tr_read4_wait(b0 + tr.off(16 * s), b0 + tr.off(16 * s + 8), b1 + tr.off(16 * s),
                       b1 + tr.off(16 * s + 8), rr);
@@ -516,20 +525,21 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
         for (int h = 0; h < 2; ++h) G[t + h] = Mma<bf16>::mma(tr_frag(rr, h), bf, G[t + h]);
       }
     }
-    // dW2 += u^T dout: A = u (lane <-> hidden column, group q takes rows
-    // of registers 8 (q % 2) ..), B = dout^T reads
+    // dW2 += u^T dout: A = u (lane <-> hidden column; group q takes the rows
+    // of registers 8 (q % 2) .. + 7, the odd groups their upper quad first),
+    // B = dout^T reads of the same rows in the same order
     bf16x8 ua;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ua[e] = (bf16)((q & 1) ? u[8 + e] : u[e]);
+    for (int e = 0; e < 8; ++e) ua[e] = (bf16)((q & 1) ? u[e < 4 ? 12 + e : 4 + e] : u[e]);
 #pragma unroll
     for (int ot = 0; ot < 8; ot += 2) {
       // tiles ot and ot + 1 are the two 16-column halves of one 32-column block
-      const uint32_t tb = lds_addr(cur + W_DO + (ot >> 1) * 2048);
+      const uint32_t tb = lds_addr(cur + W_DO + (ot >> 1) * W_BLK);
       const int half = 8 * (qj & 1);
       const uint32_t c0 = 2 * 0 + (qj >> 1), c1 = 2 * 1 + (qj >> 1);
       s16x4 rr[4];
-      tr_read4_wait(tb + blk_off(qrow, c0) + half, tb + blk_off(qrow + 8, c0) + half,
-                    tb + blk_off(qrow, c1) + half, tb + blk_off(qrow + 8, c1) + half, rr);
+      tr_read4_wait(tb + blk_off(qfirst, c0) + half, tb + blk_off(qsecond, c0) + half,
+                    tb + blk_off(qfirst, c1) + half, tb + blk_off(qsecond, c1) + half, rr);
       W2a[ot] = mma16(ua, tr_frag(rr, 0), W2a[ot]);
       W2a[ot + 1] = mma16(ua, tr_frag(rr, 1), W2a[ot + 1]);
     }
