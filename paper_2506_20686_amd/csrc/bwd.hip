@@ -40,16 +40,19 @@ constexpr bool kSplitDA = std::is_same<T, bf16>::value;
 
 // Four threads per (pair, head): thread t handles channels 32 c + 8 (t % 4)
 // .. +7 for c < D / 32, so every load and store is 16 contiguous bytes and a
-// wave covers 16 whole (pair, head) rows.
+// wave covers 16 whole (pair, head) rows.  Grid: x over the (b, h) entries
+// of one pair row a = blockIdx.y (all index arithmetic in 32 bits but the
+// row offset).
 template <typename T, int D = HEAD_DIM>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T* out,
                                                        const float* lse, const T* gate,
                                                        const T* dout, T* dg, T* da,
                                                        T* dalo, float* lse2) {
-  const int64_t tix = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t idx = tix >> 2;  // (a, b, h)
-  const int64_t total = (int64_t)G.nr * G.n * G.H;  // [nr][n][H] (ending node: nr = n)
-  if (idx >= total) return;
+  const uint32_t tix = blockIdx.x * 256u + threadIdx.x;
+  const uint32_t in_row = tix >> 2;  // b * H + h
+  if (in_row >= (uint32_t)(G.n * G.H)) return;
+  const int pa = blockIdx.y;
+  const int64_t idx = (int64_t)pa * (G.n * G.H) + in_row;  // (a, b, h)
 #pragma unroll
   for (int jj = 0; jj < 2 * (D / 32); ++jj) {
     const int j = jj & 1;
@@ -59,7 +62,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
     f32x4 dgv, dav;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const float sg = 1.f / (1.f + __expf(-gg[e]));
+      const float sg = fast_rcp(1.f + __expf(-gg[e]));  // as the forward's gate
       dgv[e] = go[e] * oo[e] * (1.f - sg);
       dav[e] = go[e] * sg;
     }
@@ -73,10 +76,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
     }
   }
   if ((tix & 3) == 0) {
-    const int h = (int)(idx % G.H);
-    const int64_t pair = idx / G.H;
-    const int a = (int)(pair / G.n), b = (int)(pair % G.n);
-    const int row = node == 0 ? a : b, qi = node == 0 ? b : a;
+    const int b = (int)(in_row / (uint32_t)G.H), h = (int)(in_row - (uint32_t)b * G.H);
+    const int row = node == 0 ? pa : b, qi = node == 0 ? b : pa;
     const float l = lse[idx];
     lse2[((int64_t)h * G.nr + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
   }
@@ -1284,16 +1285,16 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
                       hipStream_t s) {
   T* da = (T*)ws.da;
   T* dalo = (T*)ws.dalo;
-  const int64_t npair = (int64_t)g.nr * g.n * g.H;
   const bool d64 = g.d == 64;  // register-staged kernels with 64 channels per head
   {
     KernelTimer t(K_BWD_PREP, s);
+    const dim3 grid((unsigned)((4 * g.n * g.H + 255) / 256), (unsigned)g.nr);
     if (d64)
-      hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), dim3((unsigned)((4 * npair + 255) / 256)),
-                         dim3(256), 0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+      hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), grid, dim3(256), 0, s, g, node, out, lse, gate,
+                         dout, dg, da, dalo, ws.lse2);
     else
-      hipLaunchKernelGGL((bwd_prep_kernel<T, 32>), dim3((unsigned)((4 * npair + 255) / 256)),
-                         dim3(256), 0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
+      hipLaunchKernelGGL((bwd_prep_kernel<T, 32>), grid, dim3(256), 0, s, g, node, out, lse, gate,
+                         dout, dg, da, dalo, ws.lse2);
   }
   if (g.np > g.n) {
     const int64_t npad = (int64_t)g.H * g.nr * (g.np - g.n);
