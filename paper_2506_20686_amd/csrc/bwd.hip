@@ -39,46 +39,81 @@ constexpr bool kSplitDA = std::is_same<T, bf16>::value;
 // ---- elementwise preparation -------------------------------------------------------
 
 // Four threads per (pair, head): thread t handles channels 32 c + 8 (t % 4)
-// .. +7 for c < D / 32, so every load and store is 16 contiguous bytes and a
-// wave covers 16 whole (pair, head) rows.  Grid: x over the (b, h) entries
-// of one pair row a = blockIdx.y (all index arithmetic in 32 bits but the
-// row offset).
+// .. +7 for c < D / 32, so every load and store is 16 contiguous bytes (bf16)
+// and a wave covers 16 whole (pair, head) rows.  All of a thread's loads are
+// issued before its first store (the compiler may not move loads past stores
+// to memory that could alias them).  Grid: x over the (b, h) entries of one
+// pair row a = blockIdx.y (all index arithmetic in 32 bits but the row
+// offset).
+template <typename T>
+struct Vec8 {
+  float x[8];
+};
+__device__ inline Vec8<bf16> load8(const bf16* p) {
+  const bf16x8 v = *(const bf16x8*)p;
+  Vec8<bf16> r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r.x[e] = (float)v[e];
+  return r;
+}
+__device__ inline Vec8<float> load8(const float* p) {
+  const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+  Vec8<float> r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    r.x[e] = a[e];
+    r.x[4 + e] = b[e];
+  }
+  return r;
+}
+__device__ inline void store8(bf16* p, const float (&x)[8]) {
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (bf16)x[e];
+  *(bf16x8*)p = v;
+}
+__device__ inline void store8(float* p, const float (&x)[8]) {
+  *(f32x4*)p = f32x4{x[0], x[1], x[2], x[3]};
+  *(f32x4*)(p + 4) = f32x4{x[4], x[5], x[6], x[7]};
+}
+
 template <typename T, int D = HEAD_DIM>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T* out,
                                                        const float* lse, const T* gate,
                                                        const T* dout, T* dg, T* da,
                                                        T* dalo, float* lse2) {
+  constexpr int NC = D / 32;  // 8-channel chunks per thread
   const uint32_t tix = blockIdx.x * 256u + threadIdx.x;
   const uint32_t in_row = tix >> 2;  // b * H + h
   if (in_row >= (uint32_t)(G.n * G.H)) return;
   const int pa = blockIdx.y;
   const int64_t idx = (int64_t)pa * (G.n * G.H) + in_row;  // (a, b, h)
+  const int64_t base = idx * D + 8 * (tix & 3);
+  Vec8<T> go[NC], oo[NC], gg[NC];
 #pragma unroll
-  for (int jj = 0; jj < 2 * (D / 32); ++jj) {
-    const int j = jj & 1;
-    const int64_t base = idx * D + 32 * (jj >> 1) + 8 * (tix & 3);
-    const f32x4 go = load4(dout + base + 4 * j), oo = load4(out + base + 4 * j);
-    const f32x4 gg = load4(gate + base + 4 * j);
-    f32x4 dgv, dav;
+  for (int c = 0; c < NC; ++c) {
+    go[c] = load8(dout + base + 32 * c);
+    oo[c] = load8(out + base + 32 * c);
+    gg[c] = load8(gate + base + 32 * c);
+  }
+  const float l = (tix & 3) == 0 ? lse[idx] : 0.f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float sg = fast_rcp(1.f + __expf(-gg[e]));  // as the forward's gate
-      dgv[e] = go[e] * oo[e] * (1.f - sg);
-      dav[e] = go[e] * sg;
+  for (int c = 0; c < NC; ++c) {
+    float dgv[8], dav[8], lo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float sg = fast_rcp(1.f + __expf(-gg[c].x[e]));  // as the forward's gate
+      dgv[e] = go[c].x[e] * oo[c].x[e] * (1.f - sg);
+      dav[e] = go[c].x[e] * sg;
+      lo[e] = dav[e] - (float)(bf16)dav[e];
     }
-    store4(dg + base + 4 * j, dgv);
-    store4(da + base + 4 * j, dav);
-    if constexpr (kSplitDA<T>) {
-      f32x4 lo;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) lo[e] = dav[e] - (float)(bf16)dav[e];
-      store4(dalo + base + 4 * j, lo);
-    }
+    store8(dg + base + 32 * c, dgv);
+    store8(da + base + 32 * c, dav);
+    if constexpr (kSplitDA<T>) store8(dalo + base + 32 * c, lo);
   }
   if ((tix & 3) == 0) {
     const int b = (int)(in_row / (uint32_t)G.H), h = (int)(in_row - (uint32_t)b * G.H);
     const int row = node == 0 ? pa : b, qi = node == 0 ? b : pa;
-    const float l = lse[idx];
     lse2[((int64_t)h * G.nr + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
   }
 }
