@@ -345,16 +345,20 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
     const float lt = wave_xor32_sum(S.l[0]);  // half 1 holds zeros in register 0
     const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
     const int64_t base = rowbase[i] + (int64_t)q * G.sPos;
+    f32x4 gv[NO][4];  // every gate load before the first store
+#pragma unroll
+    for (int c = 0; c < NO; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gv[c][j] = load4(a.gate + base + 32 * c + 8 * j + 4 * g);
 #pragma unroll
     for (int c = 0; c < NO; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int c0 = 32 * c + 8 * j + 4 * g;
-        const f32x4 gv = load4(a.gate + base + c0);
         f32x4 ov;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          ov[e] = S.o[c][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+          ov[e] = S.o[c][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[c][j][e]));
         store4(a.out + base + c0, ov);
       }
     if (g == 0)
@@ -610,6 +614,16 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
 
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active) return;
+  // every gate load is issued before the first store (a store to memory that
+  // could alias a later load keeps the compiler from moving the load up)
+  f32x4 gv[FO_QT][4];
+#pragma unroll
+  for (int i = 0; i < FO_QT; ++i) {
+    const bool ok = act[i] && qv[i] < G.n;
+    const int64_t gbase = myrow + (int64_t)(ok ? qv[i] : 0) * G.sPos;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gv[i][j] = load4(a.gate + gbase + 8 * j + 4 * g);
+  }
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
     const float lt = wave_xor32_sum(ls0[i] + ls1[i]);  // the lane halves hold 16 keys each
@@ -619,11 +633,10 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c0 = 8 * j + 4 * g;
-      const f32x4 gv = load4(a.gate + gbase + c0);
       f32x4 ov;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        ov[e] = o[i][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[e]));
+        ov[e] = o[i][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[i][j][e]));
       store4(a.out + gbase + c0, ov);
     }
     if (g == 0)
