@@ -367,9 +367,8 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   }
   bool rows_full = true;
   for (int i = 0; i < nrows; ++i) rows_full = rows_full && const_load(a.rowfull + r0 + i) != 0u;
-  // plain register loads: let them complete before any DMA is issued (with
-  // both kinds outstanding the compiler would wait for every DMA at each use)
-  wait_vm<0>();
+  // the plain register loads above stay in flight with the first DMAs: the
+  // first step's full wait (vmcnt 0) precedes every use of their registers
 
   // ---- DMA lanes.  Unit u = QD_OPS w + j of wave w: u < 4 QD_ROWS: half
   // u % 2 (keys 16 (u % 2) + lane / 4) of tile u / 2 of [K rows, V rows];
@@ -784,10 +783,8 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     zero_frags(kf);
     zero_frags(vf);
   }
-  // the fragments are plain register loads: let them complete before any
-  // DMA is issued (with both kinds outstanding the compiler would wait for
-  // every DMA at each use)
-  wait_vm<0>();
+  // the plain register loads above stay in flight with the first DMAs: the
+  // first step's full wait (vmcnt 0) precedes every use of their registers
 
   // ---- DMA lanes (lane offsets fixed, bases advanced per tile in scalar
   // registers).  Op 0: Q (waves 0-7) or dA (waves 8-15) of row (w % 8) / 2,

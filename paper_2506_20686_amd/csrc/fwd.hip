@@ -51,8 +51,11 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const 
     return node == 0 ? ((int64_t)qi * n + ki) * G.H + h : ((int64_t)ki * n + qi) * G.H + h;
   };
   const bool in = x < n && y < n;
-  bt[idx] = in ? (float)bias[at(x, y)] / G.scale : 0.f;
-  if (btT) btT[idx] = in ? (float)bias[at(y, x)] / G.scale : 0.f;
+  // both loads before either store
+  const float b0 = in ? (float)bias[at(x, y)] : 0.f;
+  const float b1 = in && btT ? (float)bias[at(y, x)] : 0.f;
+  bt[idx] = b0 / G.scale;
+  if (btT) btT[idx] = b1 / G.scale;
 }
 
 // kbits[row][t]: bit e set iff key 32 t + e < n and mask(row, key) != 0.
@@ -428,9 +431,8 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const bool active = act[0];  // tile 1 active implies tile 0 active
   bool rows_full = true;
   for (int i = 0; i < nrows; ++i) rows_full = rows_full && const_load(a.rowfull + r0 + i) != 0u;
-  // plain register loads: let them complete before any DMA is issued (with
-  // both kinds outstanding the compiler would wait for every DMA at each use)
-  wait_vm<0>();
+  // the plain register loads above stay in flight with the first DMAs: the
+  // first step's full wait (vmcnt 0) precedes every use of their registers
 
   // ---- DMA lanes.  Ops 0, 1: K or V tile of one row (wave w: K of row w
   // for w < 4, V of row w - 4 otherwise), keys 16 op + lane / 4.  Ops 2, 3:
