@@ -70,6 +70,11 @@ def parse():
                          "transition layer)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--configs", type=int, default=1,
+                    help="with the default workload: also time every workload configuration "
+                         "(N = 32 fp32 ... N = 1536, each node variant) and report its fwd and "
+                         "bwd time, TFLOP/s and peak HBM bytes in the same JSON line "
+                         "(0 skips it, as the profiling runs do)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -529,6 +534,101 @@ def bench_rows(args, name):
     print(json.dumps(out), flush=True)
 
 
+# The workload configurations reported beside the headline (one entry per
+# node variant): the small fp32 case, the padded N = 256 and N = 384 cases,
+# N = 768 and the N = 1536 memory stress.
+CONFIG_SWEEP = ("tri_start_fp32_n32", "tri_start_bf16_n256_pad10", "tri_end_bf16_n384_randpad15",
+                "tri_bf16_n768", "tri_start_bf16_n1536_pad5")
+
+
+def sweep_configs(steps):
+    """Forward and backward time, nominal and valid-key TFLOP/s and peak HBM
+    bytes of one fwd+bwd for every workload configuration and node variant.
+    Peak bytes are torch's max_memory_allocated over one fwd+bwd: `peak_hbm_bytes`
+    with the inputs and outputs resident, `extra_hbm_bytes` above them (the
+    workspace, i.e. what the method itself needs besides its operands)."""
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    from paper_2506_20686_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    P = lambda a: a.data_ptr()  # noqa: E731
+    res = []
+    for name in CONFIG_SWEEP:
+        w = W.WORKLOADS[name]
+        dt = B.BF16 if w.dtype == torch.bfloat16 else B.F32
+        n, h, d = w.n, w.h, w.d
+        scale = 1.0 / math.sqrt(d)
+        for node in w.nodes:
+            t = W.workload_inputs(w, node)
+            valid_keys = int(t["mask"].to(torch.int64).sum().item())  # over all rows
+            x = {k: t[k].to(dev) for k in ("q", "k", "v", "g", "bias", "dout", "mask")}
+            del t
+            x["out"] = torch.empty_like(x["q"])
+            x["lse"] = torch.empty(x["bias"].shape, dtype=torch.float32, device=dev)
+            for gname in ("dq", "dk", "dv", "dg"):
+                x[gname] = torch.empty_like(x["q"])
+            x["dbias"] = torch.empty_like(x["bias"])
+            torch.cuda.synchronize(dev)
+            resident = torch.cuda.memory_allocated(dev)
+            torch.cuda.reset_peak_memory_stats(dev)
+            ws_bytes = max(B.tri_attn_fwd_workspace_bytes(node, dt, n, h, d),
+                           B.tri_attn_bwd_workspace_bytes(node, dt, n, h, d))
+            ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
+            def fwd():
+                st = B.tri_attn_fwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                    P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]),
+                                    P(x["lse"]), P(ws), ws_bytes, stream)
+                if st != B.OK:
+                    raise B.TriAttnError(st, "tri_attn_fwd")
+
+            def bwd():
+                st = B.tri_attn_bwd(node, dt, n, h, d, scale, P(x["q"]), P(x["k"]), P(x["v"]),
+                                    P(x["g"]), P(x["bias"]), P(x["mask"]), P(x["out"]),
+                                    P(x["lse"]), P(x["dout"]), P(x["dq"]), P(x["dk"]),
+                                    P(x["dv"]), P(x["dg"]), P(x["dbias"]), P(ws), ws_bytes,
+                                    stream)
+                if st != B.OK:
+                    raise B.TriAttnError(st, "tri_attn_bwd")
+
+            fwd()
+            bwd()
+            torch.cuda.synchronize(dev)
+            peak = torch.cuda.max_memory_allocated(dev)
+            k = max(1, steps if n <= 768 else steps // 4)
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            tf = tb = 0.0
+            for _ in range(k):
+                ev[0].record()
+                fwd()
+                ev[1].record()
+                bwd()
+                ev[2].record()
+                ev[2].synchronize()
+                tf += ev[0].elapsed_time(ev[1])
+                tb += ev[1].elapsed_time(ev[2])
+            tf, tb = tf / k, tb / k
+            nominal = w.flops_fwd_bwd
+            effective = 14.0 * n * valid_keys * h * d  # logits of valid keys only
+            pk = MFMA_BF16_PEAK_TFLOPS if dt == B.BF16 else MFMA_FP32_PEAK_TFLOPS
+            res.append({
+                "workload": name, "node": W.NODE_NAMES[node], "n": n, "heads": h, "head_dim": d,
+                "dtype": "bf16" if dt == B.BF16 else "f32", "steps": k,
+                "fwd_ms": round(tf, 4), "bwd_ms": round(tb, 4),
+                "tflops": round(nominal / ((tf + tb) * 1e-3) / 1e12, 3),
+                "tflops_valid_keys": round(effective / ((tf + tb) * 1e-3) / 1e12, 3),
+                "pct_of_peak": round(100.0 * nominal / ((tf + tb) * 1e-3) / 1e12 / pk, 3),
+                "peak_hbm_bytes": int(peak), "extra_hbm_bytes": int(peak - resident),
+                "naive_logits_bytes": int(n ** 3 * h * (2 if dt == B.BF16 else 4)),
+            })
+            del x, ws
+            torch.cuda.empty_cache()
+    return res
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -671,6 +771,10 @@ def main():
                      "traffic": traffic},
         "per_kernel": per_kernel,
     }
+    if name == W.HEADLINE and args.configs:
+        del per_node, ws, x
+        torch.cuda.empty_cache()
+        out["configs"] = sweep_configs(args.steps)
     if args.cpu_seconds > 0:
         h0 = host[w.nodes[0]]
         if w.batch > 1:  # sample 0
