@@ -740,7 +740,7 @@ constexpr int KD_OPS = 2 + KD_BOPS;                    // DMA ops per thread per
 // offsets stay small enough for the immediate field of LDS instructions):
 // Q, dA and dA low [slot][row] tiles, bias [slot][key tile] (4 KB each),
 // lse2 / -D [slot][2][row][32].
-constexpr int KD_TS = KD_ROWS * KD_BLK;                // 8 KB: one slot of a tile region
+constexpr int KD_TS = KD_ROWS * KD_BLK;                // 4 KB at 2 rows: one slot of a tile region
 constexpr int KD_Q = 0, KD_DA = KD_SLOTS * KD_TS, KD_LO = 2 * KD_SLOTS * KD_TS;
 constexpr int KD_BIAS = 3 * KD_SLOTS * KD_TS, KD_BS = 4 * 4096;
 constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
