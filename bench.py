@@ -685,8 +685,13 @@ def main():
             x[gname] = torch.empty_like(x["q"])
         x["dbias"] = torch.empty_like(x["bias"])
         per_node.append((node, x))
-    ws_bytes = max(max(B.tri_attn_fwd_workspace_bytes(nd, dt, n, h, d),
-                       B.tri_attn_bwd_workspace_bytes(nd, dt, n, h, d)) for nd in w.nodes)
+    if w.batch > 1:  # one copy per sample: one launch per kernel for the whole batch
+        ws_bytes = max(max(B.tri_attn_fwd_batched_workspace_bytes(nd, dt, w.batch, n, h, d),
+                           B.tri_attn_bwd_batched_workspace_bytes(nd, dt, w.batch, n, h, d))
+                       for nd in w.nodes)
+    else:
+        ws_bytes = max(max(B.tri_attn_fwd_workspace_bytes(nd, dt, n, h, d),
+                           B.tri_attn_bwd_workspace_bytes(nd, dt, n, h, d)) for nd in w.nodes)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
     P = lambda a: a.data_ptr()  # noqa: E731

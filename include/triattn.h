@@ -104,11 +104,20 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
  *   bias, dbias, lse                        : [batch][n][n][h]
  *   mask                                    : [batch][n][n]  (NULL = all valid)
  * and sample b gives exactly what tri_attn_fwd / tri_attn_bwd give for its
- * slices.  The samples run one after another on `stream` and share the
- * workspace, whose size is the unbatched one (tri_attn_fwd_workspace_bytes /
- * tri_attn_bwd_workspace_bytes for n, h, d).  The base pointers follow the
- * unbatched rules; 1 <= batch <= 2^20.  The per-sample slices of bias,
- * dbias, lse and mask need only element alignment. */
+ * slices, bitwise.  With a workspace of the size the *_batched_workspace_bytes
+ * calls report (one copy of the unbatched workspace per sample), every kernel
+ * is launched once for the whole batch (the sample is the grid's third
+ * index), which keeps the GPU full when one sample's grid is small.  With the
+ * unbatched workspace size (tri_attn_fwd_workspace_bytes /
+ * tri_attn_bwd_workspace_bytes for n, h, d) the samples run one after another
+ * on `stream` and share it.  d = 16 always runs sample by sample, and so do
+ * batches above 65535.  The base pointers follow the unbatched rules;
+ * 1 <= batch <= 2^20.  The per-sample slices of bias, dbias, lse and mask need
+ * only element alignment. */
+int tri_attn_fwd_batched_workspace_bytes(int node, int dtype, int64_t batch, int64_t n,
+                                         int64_t h, int64_t d, size_t* bytes);
+int tri_attn_bwd_batched_workspace_bytes(int node, int dtype, int64_t batch, int64_t n,
+                                         int64_t h, int64_t d, size_t* bytes);
 int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
                          float scale, const void* q, const void* k, const void* v, const void* g,
                          const void* bias, const uint8_t* mask, void* out, float* lse,

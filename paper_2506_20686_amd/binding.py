@@ -58,6 +58,12 @@ def lib():
             [_sz, _vp]
         L.tri_attn_fwd_batched.restype = _int
         L.tri_attn_bwd_batched.restype = _int
+        L.tri_attn_fwd_batched_workspace_bytes.argtypes = [_int, _int, _i64, _i64, _i64, _i64,
+                                                           ctypes.POINTER(_sz)]
+        L.tri_attn_bwd_batched_workspace_bytes.argtypes = \
+            L.tri_attn_fwd_batched_workspace_bytes.argtypes
+        L.tri_attn_fwd_batched_workspace_bytes.restype = _int
+        L.tri_attn_bwd_batched_workspace_bytes.restype = _int
         L.tri_attn_status_string.argtypes = [_int]
         L.tri_attn_status_string.restype = ctypes.c_char_p
         L.tri_attn_timing_enable.argtypes = [_int]
@@ -105,6 +111,26 @@ def tri_attn_fwd_workspace_bytes(node: int, dtype: int, n: int, h: int, d: int) 
     st = lib().tri_attn_fwd_workspace_bytes(node, dtype, n, h, d, ctypes.byref(out))
     if st != OK:
         raise TriAttnError(st, "tri_attn_fwd_workspace_bytes")
+    return out.value
+
+
+def tri_attn_fwd_batched_workspace_bytes(node: int, dtype: int, batch: int, n: int, h: int,
+                                         d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_fwd_batched_workspace_bytes(node, dtype, batch, n, h, d,
+                                                    ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_fwd_batched_workspace_bytes")
+    return out.value
+
+
+def tri_attn_bwd_batched_workspace_bytes(node: int, dtype: int, batch: int, n: int, h: int,
+                                         d: int) -> int:
+    out = _sz(0)
+    st = lib().tri_attn_bwd_batched_workspace_bytes(node, dtype, batch, n, h, d,
+                                                    ctypes.byref(out))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_bwd_batched_workspace_bytes")
     return out.value
 
 
@@ -332,8 +358,11 @@ def fwd(q, k, v, g, bias, mask=None, node: int = STARTING, scale: Optional[float
     scale = default_scale(d) if scale is None else float(scale)
     out = torch.empty_like(q)
     lse = torch.empty(lead + (n, n, h), dtype=torch.float32, device=dev)
-    need = tri_attn_fwd_workspace_bytes(node, dt, n, h, d)
-    if workspace is None or workspace.numel() < need:
+    # a batch gets one copy of the workspace per sample (one launch per kernel
+    # for the whole batch); a smaller workspace passed in runs it sample by sample
+    one = tri_attn_fwd_workspace_bytes(node, dt, n, h, d)
+    need = tri_attn_fwd_batched_workspace_bytes(node, dt, lead[0], n, h, d) if lead else one
+    if workspace is None or workspace.numel() < one:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
             _ptr(lse), _ptr(workspace), workspace.numel(), _stream(dev))
@@ -357,8 +386,9 @@ def bwd(q, k, v, g, bias, out, lse, dout, mask=None, node: int = STARTING,
     scale = default_scale(d) if scale is None else float(scale)
     dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
     dbias = torch.empty_like(bias)
-    need = tri_attn_bwd_workspace_bytes(node, dt, n, h, d)
-    if workspace is None or workspace.numel() < need:
+    one = tri_attn_bwd_workspace_bytes(node, dt, n, h, d)
+    need = tri_attn_bwd_batched_workspace_bytes(node, dt, lead[0], n, h, d) if lead else one
+    if workspace is None or workspace.numel() < one:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
             _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dg), _ptr(dbias),

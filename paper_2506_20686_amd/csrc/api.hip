@@ -118,6 +118,8 @@ Geom geom(int node, int64_t n, int64_t nr, int64_t h, float scale, int64_t kd = 
   g.lRow = node == TRIATTN_STARTING ? n * h : h;
   g.lPos = node == TRIATTN_STARTING ? h : n * h;
   g.scale = scale;
+  g.batch = 1;
+  g.bPair = g.bBias = g.bMask = g.bWs = 0;
   return g;
 }
 
@@ -305,9 +307,48 @@ BatchStrides batch_strides(int dtype, int64_t n, int64_t h, int64_t d) {
                       (size_t)(dtype == TRIATTN_BF16 ? 2 : 4)};
 }
 
+// Batched calls run all samples in one launch per kernel (the sample is the
+// grid's z index, each sample with its own copy of the workspace) when the
+// workspace holds `batch` copies; otherwise, and for d = 16 (which goes
+// through per-sample zero-padded copies), sample by sample.
+constexpr int64_t MAX_GRID_BATCH = 65535;  // grid z extent
+bool one_grid(int64_t batch, int64_t d) { return batch > 1 && batch <= MAX_GRID_BATCH && d != 16; }
+size_t batched_bytes(bool bwd, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d) {
+  const size_t one = whole_plan(bwd, dtype, n, h, d).total;
+  return one_grid(batch, d) ? (size_t)batch * one : one;
+}
+// The geometry of a one-launch batch: per-sample strides of the tensors and
+// of the workspace.
+Geom batched_geom(Geom g, int64_t batch, const BatchStrides& S, bool mask, size_t ws_one) {
+  g.batch = (int)batch;
+  g.bPair = S.pair;
+  g.bBias = S.bias;
+  g.bMask = mask ? S.mask : 0;
+  g.bWs = (int64_t)ws_one;
+  return g;
+}
+
 }  // namespace
 
 extern "C" {
+
+int tri_attn_fwd_batched_workspace_bytes(int node, int dtype, int64_t batch, int64_t n,
+                                         int64_t h, int64_t d, size_t* bytes) {
+  const int st = check_shape(node, dtype, n, h, d, true);
+  if (st != TRIATTN_OK) return st;
+  if (batch < 1 || batch > MAX_BATCH || bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = batched_bytes(false, dtype, batch, n, h, d);
+  return TRIATTN_OK;
+}
+
+int tri_attn_bwd_batched_workspace_bytes(int node, int dtype, int64_t batch, int64_t n,
+                                         int64_t h, int64_t d, size_t* bytes) {
+  const int st = check_shape(node, dtype, n, h, d, true);
+  if (st != TRIATTN_OK) return st;
+  if (batch < 1 || batch > MAX_BATCH || bytes == nullptr) return TRIATTN_ERR_INVALID_ARG;
+  *bytes = batched_bytes(true, dtype, batch, n, h, d);
+  return TRIATTN_OK;
+}
 
 int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d,
                          float scale, const void* q, const void* k, const void* v, const void* g,
@@ -326,6 +367,13 @@ int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
+  if (one_grid(batch, d) && workspace_bytes / (size_t)batch >= W.total) {
+    const Geom gb = batched_geom(geo, batch, S, mask != nullptr, W.total);
+    return dtype == TRIATTN_BF16
+               ? fwd_one<triattn::bf16>(node, gb, W, d, q, k, v, g, bias, mask, out, lse,
+                                        workspace, s)
+               : fwd_one<float>(node, gb, W, d, q, k, v, g, bias, mask, out, lse, workspace, s);
+  }
   for (int64_t b = 0; b < batch; ++b) {
     const size_t op = (size_t)(b * S.pair) * S.el, ob = (size_t)(b * S.bias) * S.el;
     const uint8_t* mb = mask ? mask + b * S.mask : nullptr;
@@ -362,6 +410,14 @@ int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
+  if (one_grid(batch, d) && workspace_bytes / (size_t)batch >= W.total) {
+    const Geom gb = batched_geom(geo, batch, S, mask != nullptr, W.total);
+    return dtype == TRIATTN_BF16
+               ? bwd_one<triattn::bf16>(node, gb, W, d, q, k, v, g, bias, mask, out, lse, dout,
+                                        dq, dk, dv, dg, dbias, workspace, s)
+               : bwd_one<float>(node, gb, W, d, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
+                                dv, dg, dbias, workspace, s);
+  }
   for (int64_t b = 0; b < batch; ++b) {
     const size_t op = (size_t)(b * S.pair) * S.el, ob = (size_t)(b * S.bias) * S.el;
     const uint8_t* mb = mask ? mask + b * S.mask : nullptr;

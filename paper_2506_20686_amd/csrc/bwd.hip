@@ -82,6 +82,14 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
                                                        const float* lse, const T* gate,
                                                        const T* dout, T* dg, T* da,
                                                        T* dalo, float* lse2) {
+  out = at_sample(out, G.bPair);
+  gate = at_sample(gate, G.bPair);
+  dout = at_sample(dout, G.bPair);
+  dg = at_sample(dg, G.bPair);
+  lse = at_sample(lse, G.bBias);
+  da = ws_at_sample(da, G.bWs);
+  dalo = ws_at_sample(dalo, G.bWs);
+  lse2 = ws_at_sample(lse2, G.bWs);
   constexpr int NC = D / 32;  // 8-channel chunks per thread
   const uint32_t tix = blockIdx.x * 256u + threadIdx.x;
   const uint32_t in_row = tix >> 2;  // b * H + h
@@ -120,6 +128,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
 
 // Queries n .. np-1 of every row: no valid key (+inf) and D = 0.
 __global__ __launch_bounds__(256) void bwd_pad_kernel(Geom G, float* lse2, float* dsum) {
+  lse2 = ws_at_sample(lse2, G.bWs);
+  dsum = ws_at_sample(dsum, G.bWs);
   const int pad = G.np - G.n;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)G.H * G.nr * pad) return;
@@ -149,6 +159,28 @@ struct BwdArgs {
   int rpc;   // rows per chunk (db)
 };
 
+// This block's sample of a batched launch: every tensor and workspace piece
+// moved by the sample's strides (no change for sample 0).
+template <typename T>
+__device__ inline void to_sample(BwdArgs<T>& a) {
+  const Geom& G = a.g;
+  a.bt = ws_at_sample(a.bt, G.bWs);
+  a.btT = ws_at_sample(a.btT, G.bWs);
+  a.kbits = ws_at_sample(a.kbits, G.bWs);
+  a.rowfull = ws_at_sample(a.rowfull, G.bWs);
+  a.da = ws_at_sample(a.da, G.bWs);
+  a.dalo = ws_at_sample(a.dalo, G.bWs);
+  a.lse2 = ws_at_sample(a.lse2, G.bWs);
+  a.dsum = ws_at_sample(a.dsum, G.bWs);
+  a.slabs = ws_at_sample(a.slabs, G.bWs);
+  a.q = at_sample(a.q, G.bPair);
+  a.k = at_sample(a.k, G.bPair);
+  a.v = at_sample(a.v, G.bPair);
+  a.dq = at_sample(a.dq, G.bPair);
+  a.dk = at_sample(a.dk, G.bPair);
+  a.dv = at_sample(a.dv, G.bPair);
+}
+
 // ---- dQ (and D) ----------------------------------------------------------------------
 
 // Per (row, head, 128 queries): stream the row's keys in blocks of 64 (K, K^T
@@ -156,6 +188,7 @@ struct BwdArgs {
 // X = sum_k P dP K, Y = sum_k P K and D = sum_k P dP, all from one pass.
 template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
+  to_sample(a);
   using M = Mma<T>;
   using TL = Tiles<D>;
   constexpr int KCH = kch<T, D>();
@@ -327,6 +360,7 @@ static_assert(QD_UNITS % QD_WAVES == 0, "DMA units must split evenly over the wa
 static_assert(QD_SLOTS * QD_SLOT <= 65536, "slot offsets must fit the LDS immediate");
 
 __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4, 4))) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
+  to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -552,6 +586,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
 // staged in LDS, double-buffered).  The paper's first backward stage.
 template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void dkdv_kernel(BwdArgs<T> a) {
+  to_sample(a);
   using M = Mma<T>;
   using TL = Tiles<D>;
   constexpr int KCH = kch<T, D>();
@@ -747,6 +782,7 @@ constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
 constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 57 KB at 2 rows, 2 slots
 
 __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a) {
+  to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -970,6 +1006,7 @@ constexpr int DB_ROWS = 2 * SPAN;  // keys (and queries) per workgroup block
 // LDS.  The bias tiles stay in registers for all rows.
 template <typename T, int D>
 __global__ __launch_bounds__(512, 1) void db_kernel(BwdArgs<T> a) {
+  to_sample(a);
   using M = Mma<T>;
   using TL = Tiles<D>;
   constexpr int KCH = kch<T, D>();
@@ -1121,6 +1158,7 @@ constexpr int DBD_SLOTS = 3;
 constexpr int DBD_OPS = 3;                    // DMA ops per thread per row
 
 __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
+  to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -1292,6 +1330,8 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
 template <typename T>
 __global__ __launch_bounds__(256) void db_reduce_kernel(Geom G, int node, int nrc,
                                                         const float* slabs, T* dbias) {
+  slabs = ws_at_sample(slabs, G.bWs);
+  dbias = at_sample(dbias, G.bBias);
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (h, q, k / 4), k fastest
   const int64_t n = G.n, nk4 = (n + 3) / 4;
   if (idx >= (int64_t)G.H * n * nk4) return;
@@ -1320,7 +1360,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   const bool d64 = g.d == 64;  // register-staged kernels with 64 channels per head
   {
     KernelTimer t(K_BWD_PREP, s);
-    const dim3 grid((unsigned)((4 * g.n * g.H + 255) / 256), (unsigned)g.nr);
+    const dim3 grid((unsigned)((4 * g.n * g.H + 255) / 256), (unsigned)g.nr, (unsigned)g.batch);
     if (d64)
       hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), grid, dim3(256), 0, s, g, node, out, lse, gate,
                          dout, dg, da, dalo, ws.lse2);
@@ -1331,7 +1371,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   if (g.np > g.n) {
     const int64_t npad = (int64_t)g.H * g.nr * (g.np - g.n);
     KernelTimer t(K_BWD_PAD, s);
-    hipLaunchKernelGGL(bwd_pad_kernel, dim3((unsigned)((npad + 255) / 256)), dim3(256), 0, s, g,
+    hipLaunchKernelGGL(bwd_pad_kernel, dim3((unsigned)((npad + 255) / 256), 1, (unsigned)g.batch), dim3(256), 0, s, g,
                        ws.lse2, ws.dsum);
   }
   BwdArgs<T> a{g, p.bt, p.btT, p.kbits, p.rowfull, q, k, v, da, dalo, ws.lse2, ws.dsum, dq, dk, dv, ws.slabs,
@@ -1341,47 +1381,47 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
     if (d64) {
-      hipLaunchKernelGGL((dq_kernel<T, 64>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dq_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
       const int64_t nwg = (int64_t)nqb * ((g.nr + QD_ROWS - 1) / QD_ROWS) * g.H;
-      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg), dim3(64 * QD_WAVES), 0, s, a, nqb);
+      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
     } else {
-      hipLaunchKernelGGL((dq_kernel<T, 32>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dq_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
   }
   {
     KernelTimer t(K_DKDV, s);
     if (d64) {
-      hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int64_t nwg = (int64_t)a.nblk * ((g.nr + KD_ROWS - 1) / KD_ROWS) * g.H;
-      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg), dim3(64 * KD_WAVES), 0, s, a);
+      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
     } else {
-      hipLaunchKernelGGL((dkdv_kernel<T, 32>), dim3((unsigned)nrow), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((dkdv_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
   }
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
     if (d64) {
-      hipLaunchKernelGGL((db_kernel<T, 64>), dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+      hipLaunchKernelGGL((db_kernel<T, 64>), dim3((unsigned)ndb, 1, (unsigned)g.batch), dim3(64 * DB_WAVES), 0, s, a);
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int nkb = (g.n + DBD_K - 1) / DBD_K;
       const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
-      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg), dim3(64 * DBD_WAVES), 0, s, a, nkb);
+      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
     } else {
-      hipLaunchKernelGGL((db_kernel<T, 32>), dim3((unsigned)ndb), dim3(64 * DB_WAVES), 0, s, a);
+      hipLaunchKernelGGL((db_kernel<T, 32>), dim3((unsigned)ndb, 1, (unsigned)g.batch), dim3(64 * DB_WAVES), 0, s, a);
     }
   }
   {
     const int64_t nred = (int64_t)g.H * g.n * ((g.n + 3) / 4);
     KernelTimer t(K_DB_REDUCE, s);
     if (dbias_f32)
-      hipLaunchKernelGGL(db_reduce_kernel<float>, dim3((unsigned)((nred + 255) / 256)), dim3(256),
+      hipLaunchKernelGGL(db_reduce_kernel<float>, dim3((unsigned)((nred + 255) / 256), 1, (unsigned)g.batch), dim3(256),
                          0, s, g, node, ws.nrc, ws.slabs, dbias_f32);
     else
-      hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256)), dim3(256), 0,
+      hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256), 1, (unsigned)g.batch), dim3(256), 0,
                          s, g, node, ws.nrc, ws.slabs, dbias);
   }
   return hipGetLastError();

@@ -38,6 +38,9 @@ namespace triattn {
 template <typename T>
 __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const T* bias,
                                                         float* bt, float* btT) {
+  bias = at_sample(bias, G.bBias);
+  bt = ws_at_sample(bt, G.bWs);
+  btT = ws_at_sample(btT, G.bWs);
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t np = G.np, total = (int64_t)G.H * np * np;
   if (idx >= total) return;
@@ -64,6 +67,9 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const 
 // node reads mask[row][key], the ending node mask[key][row].
 __global__ __launch_bounds__(256) void prep_kbits_kernel(Geom G, int node, const uint8_t* mask,
                                                          uint32_t* kbits, uint32_t* rowfull) {
+  mask = at_sample(mask, G.bMask);
+  kbits = ws_at_sample(kbits, G.bWs);
+  rowfull = ws_at_sample(rowfull, G.bWs);
   const int row = blockIdx.x, t = threadIdx.x, n = G.n;
   uint32_t bits = 0, want = 0;
   if (t < G.nkt) {
@@ -87,12 +93,12 @@ hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* ma
   const int64_t nb = ((int64_t)g.H * g.np * g.np + 255) / 256;
   {
     KernelTimer t(K_PREP_BIAS, s);
-    hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb), dim3(256), 0, s, g, node, bias,
+    hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb, 1, (unsigned)g.batch), dim3(256), 0, s, g, node, bias,
                        p.bt, p.btT);
   }
   {
     KernelTimer t(K_PREP_KBITS, s);
-    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.nr), dim3(256), 0, s, g, node, mask,
+    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.nr, 1, (unsigned)g.batch), dim3(256), 0, s, g, node, mask,
                        p.kbits, p.rowfull);
   }
   return hipGetLastError();
@@ -120,6 +126,22 @@ struct FwdArgs {
   int nqb;  // query blocks per row
 };
 
+// This block's sample of a batched launch: every tensor and workspace piece
+// moved by the sample's strides (no change for sample 0).
+template <typename T>
+__device__ inline void to_sample(FwdArgs<T>& a) {
+  const Geom& G = a.g;
+  a.bt = ws_at_sample(a.bt, G.bWs);
+  a.kbits = ws_at_sample(a.kbits, G.bWs);
+  a.rowfull = ws_at_sample(a.rowfull, G.bWs);
+  a.q = at_sample(a.q, G.bPair);
+  a.k = at_sample(a.k, G.bPair);
+  a.v = at_sample(a.v, G.bPair);
+  a.gate = at_sample(a.gate, G.bPair);
+  a.out = at_sample(a.out, G.bPair);
+  a.lse = at_sample(a.lse, G.bBias);
+}
+
 // Online-softmax state of one (row, 32 queries) pair of a wave.  The row
 // sums of P accumulate on the MFMA: register 0 of the lanes of half 0 of
 // `l` holds sum_k P for the lane's query (see ones_row0).
@@ -134,6 +156,7 @@ struct SoftmaxState {
 // channels per head.
 template <typename T, int D>
 __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
+  to_sample(a);
   using M = Mma<T>;
   using TL = Tiles<D>;
   constexpr int KCH = kch<T, D>();
@@ -394,6 +417,7 @@ constexpr int FO_SLOTS = 2;
 
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void fwd_dma_kernel(FwdArgs<bf16> a) {
+  to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
   const Geom& G = a.g;
@@ -655,14 +679,14 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
   const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
   if (g.d == 64) {
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
   } else if constexpr (std::is_same<T, bf16>::value) {
     const int64_t nwd = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwd), dim3(512), 0, s, a);
+    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
   } else {
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL((fwd_kernel<T, 32>), dim3((unsigned)nwg), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fwd_kernel<T, 32>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

@@ -22,7 +22,31 @@ struct Geom {
   int64_t sRow, sPos;  // element strides of [nr][n][H][d] tensors
   int64_t lRow, lPos;  // element strides of [n][n][H] tensors (lse)
   float scale;         // softmax scale on Q K^T
+  // Batched launches (bf16, 32 channels): sample s = blockIdx.z of a grid
+  // with `batch` layers finds its tensors `s` strides past the first sample's
+  // and its own workspace `s * bWs` bytes past the first.  batch = 1 and zero
+  // strides otherwise.
+  int batch;
+  int64_t bPair;  // elements of one sample's [n][n][H][d] tensor
+  int64_t bBias;  // elements of one sample's [n][n][H] tensor (bias, dbias, lse)
+  int64_t bMask;  // bytes of one sample's [n][n] mask
+  int64_t bWs;    // bytes of one sample's workspace
 };
+
+// This block's sample of a batched launch (0 otherwise).
+__device__ inline int64_t sample_id() { return (int64_t)blockIdx.z; }
+template <typename P>
+__device__ inline P* at_sample(P* p, int64_t stride) {
+  return p ? p + sample_id() * stride : p;
+}
+template <typename P>
+__device__ inline P* ws_at_sample(P* p, int64_t bytes) {
+  return p ? (P*)((char*)p + sample_id() * bytes) : p;
+}
+template <typename P>
+__device__ inline const P* ws_at_sample(const P* p, int64_t bytes) {
+  return p ? (const P*)((const char*)p + sample_id() * bytes) : p;
+}
 
 // Workspace pieces (device pointers), see api.hip for sizes.
 struct Prep {

@@ -407,6 +407,30 @@ def test_batched_workspace_is_the_unbatched_one(lib):
             B.ERR_WORKSPACE
 
 
+def test_batched_workspace_sizes(lib):
+    """One launch per kernel for a batch needs one unbatched workspace per
+    sample; d = 16 (per-sample padded copies) and a batch of one need the
+    unbatched size; the size calls reject what the batched calls reject."""
+    fns = ((lib.tri_attn_fwd_batched_workspace_bytes, lib.tri_attn_fwd_workspace_bytes),
+           (lib.tri_attn_bwd_batched_workspace_bytes, lib.tri_attn_bwd_workspace_bytes))
+    for fb, f1 in fns:
+        for dtype in (B.BF16, B.F32):
+            for node in (0, 1):
+                for d in (16, 32, 64):
+                    st, one = ws_bytes(f1, node, dtype, 37, 3, d)
+                    assert st == B.OK
+                    for batch, k in ((1, 1), (4, 1 if d == 16 else 4),
+                                     (65535, 1 if d == 16 else 65535), (65536, 1)):
+                        out = ctypes.c_size_t(0)
+                        assert fb(node, dtype, batch, 37, 3, d, ctypes.byref(out)) == B.OK
+                        assert out.value == k * one, (node, dtype, d, batch)
+        out = ctypes.c_size_t(0)
+        assert fb(0, B.BF16, 0, 37, 3, 32, ctypes.byref(out)) == B.ERR_INVALID_ARG
+        assert fb(0, B.BF16, (1 << 20) + 1, 37, 3, 32, ctypes.byref(out)) == B.ERR_INVALID_ARG
+        assert fb(0, B.BF16, 2, 37, 3, 32, None) == B.ERR_INVALID_ARG
+        assert fb(0, B.BF16, 2, 37, 3, 48, ctypes.byref(out)) != B.OK
+
+
 def test_d16_workspace_adds_padded_copies(lib):
     """d = 16 runs the d = 32 kernels on zero-padded copies kept in the
     workspace: 5 (forward) and 10 (backward) tensors of [n][n][h][32]."""

@@ -1,7 +1,9 @@
 """GPU parity of the batched triangle attention (a leading batch axis, a
 bias and a mask per sample) against the fp64 oracle run per sample, with the
-tolerances of the unbatched tests; and bitwise equality of each sample with
-the unbatched call on its slices."""
+tolerances of the unbatched tests; bitwise equality of each sample with the
+unbatched call on its slices; and bitwise equality of the one-launch batch
+(a workspace per sample) with the sample-by-sample run (one shared
+workspace)."""
 import pytest
 import torch
 
@@ -67,3 +69,52 @@ def test_batched_equals_unbatched_bitwise(node):
         assert torch.equal(o1, out[i]) and torch.equal(l1, lse[i])
         for a, r in zip(g1, grads):
             assert torch.equal(a, r[i])
+
+
+def run_batched(d, node, ws_kind):
+    """fwd + bwd of a batch with the one-launch workspace ("grid") or the
+    unbatched one ("seq")."""
+    bsz, n, h, dd = d["q"].shape[0], d["q"].shape[1], d["q"].shape[3], d["q"].shape[4]
+    dt = B.BF16 if d["q"].dtype == torch.bfloat16 else B.F32
+    sizes = {"fwd": (B.tri_attn_fwd_batched_workspace_bytes, B.tri_attn_fwd_workspace_bytes),
+             "bwd": (B.tri_attn_bwd_batched_workspace_bytes, B.tri_attn_bwd_workspace_bytes)}
+    ws = {}
+    for kind, (fb, f1) in sizes.items():
+        nbytes = fb(node, dt, bsz, n, h, dd) if ws_kind == "grid" else f1(node, dt, n, h, dd)
+        ws[kind] = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d.get("mask"), node,
+                     workspace=ws["fwd"])
+    grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d.get("mask"),
+                  node, workspace=ws["bwd"])
+    torch.cuda.synchronize()
+    return (out, lse) + tuple(grads)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+@pytest.mark.parametrize("head_dim", [32, 64])
+def test_one_launch_batch_equals_sample_by_sample(dtype, node, head_dim):
+    b, n, h = 3, 67, 2
+    parts = []
+    for i in range(b):
+        t, gen = W.make_inputs(n, h, head_dim, dtype, seed=1300 + 7 * i + node)
+        t["mask"] = W.random_mask(n, 0.85, gen) if i != 1 else W.pair_mask(n, 9)
+        parts.append(t)
+    d = {k: torch.stack([p[k] for p in parts]).to(DEV) for k in parts[0]}
+    grid = run_batched(d, node, "grid")
+    seq = run_batched(d, node, "seq")
+    for name, a, r in zip(("out", "lse", "dq", "dk", "dv", "dg", "dbias"), grid, seq):
+        assert torch.equal(a, r), name
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_one_launch_batch_benchmark_shape(node):
+    """Four N = 384 maps (the batched benchmark shape), no mask: the one-launch
+    batch equals the sample-by-sample run bitwise."""
+    b, n, h = 4, 384, 4
+    parts = [W.make_inputs(n, h, 32, torch.bfloat16, seed=1700 + i)[0] for i in range(b)]
+    d = {k: torch.stack([p[k] for p in parts]).to(DEV) for k in parts[0] if k != "mask"}
+    grid = run_batched(d, node, "grid")
+    seq = run_batched(d, node, "seq")
+    for name, a, r in zip(("out", "lse", "dq", "dk", "dv", "dg", "dbias"), grid, seq):
+        assert torch.equal(a, r), name
