@@ -346,6 +346,16 @@ def _stream(dev):
     return torch.cuda.current_stream(dev).cuda_stream
 
 
+# The torch wrappers give a batch one workspace copy per sample (one launch per
+# kernel for the whole batch) up to this size, and the unbatched workspace
+# (sample by sample) beyond it.
+BATCH_WORKSPACE_LIMIT = 4 << 30
+
+
+def _batch_workspace(batched: int, one: int) -> int:
+    return batched if batched <= max(one, BATCH_WORKSPACE_LIMIT) else one
+
+
 def default_scale(d: int) -> float:
     return 1.0 / math.sqrt(d)
 
@@ -361,7 +371,8 @@ def fwd(q, k, v, g, bias, mask=None, node: int = STARTING, scale: Optional[float
     # a batch gets one copy of the workspace per sample (one launch per kernel
     # for the whole batch); a smaller workspace passed in runs it sample by sample
     one = tri_attn_fwd_workspace_bytes(node, dt, n, h, d)
-    need = tri_attn_fwd_batched_workspace_bytes(node, dt, lead[0], n, h, d) if lead else one
+    need = _batch_workspace(tri_attn_fwd_batched_workspace_bytes(node, dt, lead[0], n, h, d),
+                            one) if lead else one
     if workspace is None or workspace.numel() < one:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
@@ -387,7 +398,8 @@ def bwd(q, k, v, g, bias, out, lse, dout, mask=None, node: int = STARTING,
     dq, dk, dv, dg = (torch.empty_like(q) for _ in range(4))
     dbias = torch.empty_like(bias)
     one = tri_attn_bwd_workspace_bytes(node, dt, n, h, d)
-    need = tri_attn_bwd_batched_workspace_bytes(node, dt, lead[0], n, h, d) if lead else one
+    need = _batch_workspace(tri_attn_bwd_batched_workspace_bytes(node, dt, lead[0], n, h, d),
+                            one) if lead else one
     if workspace is None or workspace.numel() < one:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     args = (scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(bias), _ptr(mask), _ptr(out),
