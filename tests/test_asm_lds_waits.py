@@ -4,7 +4,7 @@ Some staged reads are issued by one inline-asm statement and waited for by a
 later one (s_waitcnt lgkmcnt), so that the wait can overlap other work.  The
 compiler does not know the read is still in flight and may not touch its
 destination registers in between: a copy or use before the wait would read
-stale data.  This test compiles the attention sources to gfx950 assembly and
+stale data.  This test compiles the kernel sources to gfx950 assembly and
 checks, for every inline-asm LDS read, that no instruction reads or writes its
 destination registers before an s_waitcnt lgkmcnt that retires it.  A planted
 hazard in a synthetic listing checks the scanner itself.
