@@ -112,6 +112,18 @@ def test_ragged_shapes(dtype, node, n, h, mask_kind):
 
 
 @pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+@pytest.mark.parametrize("n", [63, 65, 127, 128, 129, 191, 255, 257])
+def test_block_boundaries(node, n):
+    """n just below, at and above the 64- and 128-wide blocks of the bf16
+    kernels (query blocks of the forward and dQ, key blocks of dK/dV, the
+    128 x 128 bias-gradient blocks); random masks for odd n, none for even n
+    (the kernels' all-keys-valid loops)."""
+    t = inputs(n, 2, torch.bfloat16, seed=2000 + n + node,
+               mask_kind="random" if n % 2 else "none")
+    full_check(t, node, torch.bfloat16)
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
 def test_degenerate_masks(node):
     n, h = 40, 2
     t = inputs(n, h, torch.bfloat16, seed=77, mask_kind="none")
