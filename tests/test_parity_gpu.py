@@ -194,15 +194,35 @@ def test_backward_is_bitwise_deterministic(name, node):
         assert torch.equal(a, b)
 
 
-def test_ending_equals_transposed_starting_on_gpu():
-    t = inputs(70, 2, torch.bfloat16, seed=9, mask_kind="random")
+def _ending_vs_transposed_starting(t):
+    """The ending node reads every pair tensor with its two pair axes swapped
+    (Section IV-A: triangle attention around the ending node is the starting
+    node on the transposed pair map).  The kernels follow the same arithmetic
+    in the same order either way, so the ending node on the inputs and the
+    starting node on contiguous transposed copies agree bit for bit, in the
+    forward and in every gradient."""
     d = to_dev(t)
     T = lambda x: x.transpose(0, 1).contiguous()  # noqa: E731
+    dt = {k: T(d[k]) for k in ("q", "k", "v", "g", "bias", "mask", "dout")}
     oe, le = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], B.ENDING)
-    os_, ls = B.fwd(T(d["q"]), T(d["k"]), T(d["v"]), T(d["g"]), T(d["bias"]), T(d["mask"]),
-                    B.STARTING)
-    # same arithmetic in the same order on the same values: bitwise equal
+    os_, ls = B.fwd(dt["q"], dt["k"], dt["v"], dt["g"], dt["bias"], dt["mask"], B.STARTING)
     assert torch.equal(oe, T(os_)) and torch.equal(le, T(ls))
+    ge = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], oe, le, d["dout"], d["mask"], B.ENDING)
+    gs = B.bwd(dt["q"], dt["k"], dt["v"], dt["g"], dt["bias"], os_, ls, dt["dout"], dt["mask"],
+               B.STARTING)
+    for name, a, b in zip(("dq", "dk", "dv", "dg", "dbias"), ge, gs):
+        assert torch.equal(a, T(b)), name
+
+
+def test_ending_equals_transposed_starting_on_gpu():
+    _ending_vs_transposed_starting(inputs(70, 2, torch.bfloat16, seed=9, mask_kind="random"))
+
+
+def test_ending_equals_transposed_starting_headline_size():
+    # the N = 768, H = 4, d = 32 bf16 workload at full size, in the launch
+    # configuration the benchmark times
+    w = W.WORKLOADS[W.HEADLINE]
+    _ending_vs_transposed_starting(W.workload_inputs(w, B.ENDING))
 
 
 def test_peak_memory_is_quadratic():
