@@ -123,61 +123,3 @@ def trn_bwd(x, gamma, beta, w1, w2, dout, eps=1e-5, rows=None, sums=True):
             sel = want[r]
             dx[r[sel]] = d[sel]
     return dx, dw1, dw2, dgamma, dbeta
-
-
-def trn_sum_scales(x, gamma, beta, w1, w2, dout, eps=1e-5):
-    """Error scales of the four sums over rows of trn_bwd (dW1, dW2, dgamma,
-    dbeta) for an implementation that rounds its matrix operands to bf16 and
-    forms the sums regrouped: dW1 = gamma G + beta s^T, dgamma = sum_c W1 o
-    G, dbeta = W1 s with G = xhat^T dh and s = column sums of dh (o1 = xhat
-    gamma + beta substituted), and dW2 = u^T dout.  Returns two tuples (S, R)
-    of four arrays each.
-
-    S: rounding errors of the terms of G, s and dW2 add up like the l2 norms
-    over rows of those terms, carried into the regrouped results by |gamma|,
-    |beta| and |W1|:
-      dW1[k][c] : |gamma_k| sqrt(sum_r xhat^2 dh^2) + |beta_k| sqrt(sum_r dh^2)
-      dW2[f][k] : sqrt(sum_r u^2 dout^2)
-      dgamma[k] : sqrt(sum_c W1[k][c]^2 sum_r xhat^2 dh^2)
-      dbeta[k]  : sqrt(sum_c W1[k][c]^2 sum_r dh^2)
-    R: the same norms with dh and u replaced by the first-order change that
-    the rounding of o1 to bf16 (relative 2^-9 per feature, independent) makes
-    in them through a and b: da_err = 2^-9 sqrt(sum_k (o1_k W1[k][a col])^2),
-    likewise for b, propagated by the derivatives of da, db and u in a and b.
-    This term dominates where a factor of a term nearly vanishes (b close to
-    0), which a sum over few rows does not average out."""
-    x, gamma, beta, w1, w2, dout = (_f64(t) for t in (x, gamma, beta, w1, w2, dout))
-    m, c = x.shape
-    f = w2.shape[0]
-    gq, sq, s2 = np.zeros((c, 2 * f)), np.zeros(2 * f), np.zeros((f, c))
-    gr, sr, r2 = np.zeros((c, 2 * f)), np.zeros(2 * f), np.zeros((f, c))
-    w1sq = w1 ** 2
-    for r in _blocks(m, None):
-        xhat, o1, _, _ = _ln(x[r], gamma, beta, eps)
-        h = o1 @ w1
-        a, b = h[:, :f], h[:, f:]
-        dlt = 2.0 ** -9 * np.sqrt((o1 ** 2) @ w1sq)
-        ea, eb = dlt[:, :f], dlt[:, f:]
-        sg = _sigmoid(a)
-        phi = sg * (1.0 + a * (1.0 - sg))               # d silu / da
-        dphi = sg * (1.0 - sg) * (2.0 + a * (1.0 - 2.0 * sg))
-        do = dout[r]
-        du = do @ w2.T
-        dh = np.concatenate([du * b * phi, du * a * sg], axis=1)
-        edh = np.concatenate([np.abs(du) * (np.abs(phi) * eb + np.abs(b * dphi) * ea),
-                              np.abs(du * phi) * ea], axis=1)
-        eu = np.abs(phi * b) * ea + np.abs(a * sg) * eb
-        gq += (xhat ** 2).T @ (dh ** 2)
-        sq += (dh ** 2).sum(axis=0)
-        s2 += ((a * sg * b) ** 2).T @ (do ** 2)
-        gr += (xhat ** 2).T @ (edh ** 2)
-        sr += (edh ** 2).sum(axis=0)
-        r2 += (eu ** 2).T @ (do ** 2)
-
-    def regroup(g2, s_2):
-        dw1 = np.abs(gamma)[:, None] * np.sqrt(g2) + np.abs(beta)[:, None] * np.sqrt(s_2)[None, :]
-        return dw1, np.sqrt((w1sq * g2).sum(axis=1)), np.sqrt(w1sq @ s_2)
-
-    S1, Sg, Sb = regroup(gq, sq)
-    R1, Rg, Rb = regroup(gr, sr)
-    return (S1, np.sqrt(s2), Sg, Sb), (R1, np.sqrt(r2), Rg, Rb)

@@ -385,23 +385,27 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_dx_kernel(TrnBwdArgs a
 // The x and dout tiles are stored as four 32-column blocks of 64-byte rows
 // (blk_off), so their transposed reads are the attention kernels' ones.
 
-// One ring slot: o1 (bf16), xhat (bf16) and dout tiles of 32 rows, each as
-// four 32-column blocks of 64-byte rows (blk_off).  The staging threads
-// normalise once per block for all waves.
+// One ring slot: o1 (bf16), xhat (bf16), dout and the low part of o1
+// (o1 - bf16(o1), rounded to bf16) tiles of 32 rows, each as four 32-column
+// blocks of 64-byte rows (blk_off).  The staging threads normalise once per
+// block for all waves.  a and b are recomputed from o1 as the pair hi + lo:
+// rounding o1 to one bf16 moves a and b by up to 2^-9 of the l2 norm of
+// their terms, which is large against a or b where the terms cancel, and a
+// sum over a few rows does not average that out.
 // Blocks sit W_BLK bytes apart (2 KB + 64): the staging stores of one wave
 // touch the four blocks of a row at once, and the extra 64 bytes put them on
 // different banks.  Every read stays inside one block.
 constexpr int W_BLK = 2048 + 64;
 constexpr int W_TILE = 4 * W_BLK;
-constexpr int W_SLOT = 3 * W_TILE;
-constexpr int W_XH = W_TILE, W_DO = 2 * W_TILE;
+constexpr int W_SLOT = 4 * W_TILE;
+constexpr int W_XH = W_TILE, W_DO = 2 * W_TILE, W_OL = 3 * W_TILE;
 
 __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a, int64_t rpp) {
   __shared__ __align__(16) char ring[2][W_SLOT];
   __shared__ __align__(16) float gb[2][TRN_C];
-  // each wave's B operands W1[k][hcol] and W2[fl][k], fragment-major (the
-  // W2 fragments of lanes 16..31 of each half repeat lanes 0..15)
-  __shared__ __align__(16) bf16x8 wf1[TRN_WAVES][TRN_NT][64];
+  // each wave's B operands W2[fl][k], fragment-major (the W2 fragments of
+  // lanes 16..31 of each half repeat lanes 0..15); those of W1 stay in
+  // registers
   __shared__ __align__(16) bf16x8 wf2[TRN_WAVES][TRN_NT][32];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
   const int wave = tid >> 6, q = lane >> 4;
@@ -417,14 +421,13 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
     gb[0][tid] = (float)a.gamma[tid];
     gb[1][tid] = (float)a.beta[tid];
   }
-  // the wave's B operands W1[k][hcol] and W2[fl][k], k = 16 s + 8 g + e,
-  // kept in LDS for the whole launch
+  // the wave's B operands W1[k][hcol] (registers) and W2[fl][k] (LDS),
+  // k = 16 s + 8 g + e, kept for the whole launch
+  bf16x8 w1r[TRN_NT];
 #pragma unroll
   for (int s = 0; s < TRN_NT; ++s) {
-    bf16x8 w1f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) w1f[e] = a.w1[(int64_t)(16 * s + 8 * g + e) * 2 * f + hcol];
-    wf1[wave][s][lane] = w1f;
+    for (int e = 0; e < 8; ++e) w1r[s][e] = a.w1[(int64_t)(16 * s + 8 * g + e) * 2 * f + hcol];
     if (is_a) wf2[wave][s][16 * g + l32] = *(const bf16x8*)(a.w2 + (int64_t)fl * TRN_C + 16 * s + 8 * g);
   }
   __syncthreads();  // gamma, beta
@@ -447,16 +450,19 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
     v.rstd = a.rstd[rc];
   };
   auto stage_store = [&](char* slot, const Staged& v) {
-    bf16x8 o1, xh;
+    bf16x8 o1, ol, xh;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float h = ((float)v.x[e] - v.mean) * v.rstd;
       xh[e] = (bf16)h;
-      o1[e] = (bf16)fmaf(h, gb[0][8 * sc + e], gb[1][8 * sc + e]);
+      const float o = fmaf(h, gb[0][8 * sc + e], gb[1][8 * sc + e]);
+      o1[e] = (bf16)o;
+      ol[e] = (bf16)(o - (float)o1[e]);
     }
     *(bf16x8*)(slot + soff) = o1;
     *(bf16x8*)(slot + W_XH + soff) = xh;
     *(bf16x8*)(slot + W_DO + soff) = v.d;
+    *(bf16x8*)(slot + W_OL + soff) = ol;
   };
   Staged sv;
   if (nb > 0) {
@@ -487,7 +493,8 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
 #pragma unroll
     for (int s = 0; s < TRN_NT; ++s) {
       const uint32_t o = (s >> 1) * W_BLK + blk_off(l32, 2 * (s & 1) + g);
-      hC = Mma<bf16>::mma(*(const bf16x8*)(cur + o), wf1[wave][s][lane], hC);
+      hC = Mma<bf16>::mma(*(const bf16x8*)(cur + o), w1r[s], hC);
+      hC = Mma<bf16>::mma(*(const bf16x8*)(cur + W_OL + o), w1r[s], hC);
       duC = Mma<bf16>::mma(*(const bf16x8*)(cur + W_DO + o), wf2[wave][s][16 * g + (l32 & 15)],
                            duC);
     }
@@ -509,12 +516,17 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
       ssum += dh[v];
     }
     // G += xhat^T dh: A = xhat^T (lane <-> feature 32 t + l32, rows in
-    // accumulator order), B = dh from the registers
+    // accumulator order), B = dh from the registers as the pair hi + lo of
+    // bf16 numbers (with both xhat and dh rounded once, a sum over a few rows
+    // whose dh columns differ in size sits near the bf16 bound)
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      bf16x8 bf;
+      bf16x8 bf, bl;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) bf[e] = (bf16)dh[8 * s + e];
+      for (int e = 0; e < 8; ++e) {
+        bf[e] = (bf16)dh[8 * s + e];
+        bl[e] = (bf16)(dh[8 * s + e] - (float)bf[e]);
+      }
 #pragma unroll
       for (int t = 0; t < 4; t += 2) {
         const uint32_t b0 = lds_addr(cur + W_XH + t * W_BLK), b1 = b0 + W_BLK;
@@ -522,7 +534,10 @@ __global__ __launch_bounds__(TRN_THREADS, 1) void trn_bwd_w_kernel(TrnBwdArgs a,
         tr_read4_wait(b0 + tr.off(16 * s), b0 + tr.off(16 * s + 8), b1 + tr.off(16 * s),
                       b1 + tr.off(16 * s + 8), rr);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) G[t + h] = Mma<bf16>::mma(tr_frag(rr, h), bf, G[t + h]);
+        for (int h = 0; h < 2; ++h) {
+          G[t + h] = Mma<bf16>::mma(tr_frag(rr, h), bf, G[t + h]);
+          G[t + h] = Mma<bf16>::mma(tr_frag(rr, h), bl, G[t + h]);
+        }
       }
     }
     // dW2 += u^T dout: A = u (lane <-> hidden column; group q takes the rows

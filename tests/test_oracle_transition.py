@@ -180,41 +180,3 @@ def test_pins_catch_mutation(name, tmp_path):
     finally:
         g["T"] = saved
     assert failed > 0, f"no pin caught {name}"
-
-
-def test_sum_scales_one_row():
-    """With one row the scales are the magnitudes of the regrouped terms:
-    |gamma_k xhat_k dh_c| + |beta_k dh_c| for dW1 (>= |dW1|), |u_f dout_k|
-    = |dW2| for dW2."""
-    x, g, b, w1, w2, do = rnd(1, 8, 4, 13)
-    _, dw1, dw2, dg, db = T.trn_bwd(x, g, b, w1, w2, do, EPS)
-    (s1, s2, sg, sb), rec = T.trn_sum_scales(x, g, b, w1, w2, do, EPS)
-    np.testing.assert_allclose(s2, np.abs(dw2), rtol=1e-12, atol=1e-15)
-    assert np.all(s1 >= np.abs(dw1) * (1 - 1e-12))
-    # dgamma = sum_c W1 G and dbeta = W1 s: the scales bound the sums
-    # (Cauchy-Schwarz over the 2F columns)
-    assert np.all(sg * np.sqrt(8) >= np.abs(dg) * (1 - 1e-12))
-    assert np.all(sb * np.sqrt(8) >= np.abs(db) * (1 - 1e-12))
-
-
-def test_recompute_scales_match_a_perturbed_o1():
-    """The recompute part of the error scales predicts the spread of the sums
-    when o1 is perturbed by independent relative errors of 2^-9 (checked by
-    sampling: the observed spread stays within a factor 3 of the scale)."""
-    m, c, f = 3, 16, 8
-    x, g, b, w1, w2, do = rnd(m, c, f, 21)
-    _, rec = T.trn_sum_scales(x, g, b, w1, w2, do, EPS)
-    xhat, o1, _, _ = T._ln(x, g, b, EPS)
-    rng = np.random.default_rng(0)
-    devs = []
-    for _ in range(200):
-        o1p = o1 * (1 + 2.0 ** -9 * rng.standard_normal(o1.shape))
-        h = o1p @ w1
-        a, bb = h[:, :f], h[:, f:]
-        sgm = 1 / (1 + np.exp(-a))
-        du = do @ w2.T
-        dh = np.concatenate([du * bb * sgm * (1 + a * (1 - sgm)), du * a * sgm], axis=1)
-        devs.append((a * sgm * bb).T @ do)
-    spread = np.std(np.array(devs), axis=0)
-    ratio = spread / rec[1]
-    assert 1 / 3 < np.median(ratio) < 3

@@ -3,19 +3,15 @@ fp64 oracle, on the same seeded bf16 inputs.
 
 Tolerance: the bf16 bound used for the attention, |gpu - oracle| <= 2e-2 +
 1e-2 |oracle| elementwise plus a relative Frobenius error <= 1e-2; the fp32
-row statistics to 1e-5.  The sums over rows (dW1, dW2, dgamma, dbeta) add m
-terms whose bf16 factors carry relative rounding errors up to 2^-9 (and the
-recomputed a, b inherit the rounding of o1), so their errors add up like
-the l2 norm over rows of each entry's terms: for them the absolute part of
-the bound is 2e-2 times that norm plus 8 times the spread that the bf16
-rounding of o1 causes in the recomputed a and b (both from the oracle's
-trn_sum_scales).  With one row the first part is a 2% relative bound on the
-single term; with many rows it is close to 2e-2 times the RMS of the
-entries.  Small problems
-are compared in full (several 256-row blocks and 32-row tiles, ragged
-tails, one to sixteen 32-column hidden chunks); the N = 768 pair
-representation (589824 rows) is compared on sampled rows for out and dx and
-in full for the sums over rows.
+row statistics to 1e-5.  The sums over rows (dW1, dW2, dgamma, dbeta) take
+the bound the layer-norm + linear sums use, which depends on the oracle's
+values only: the absolute part is 2e-2 times the RMS of the oracle's
+entries of that sum (a sum of m terms with relative bf16 rounding errors
+grows like the l2 norm of its terms, which is the size of a typical entry).
+Small problems are compared in full (several 256-row blocks and 32-row
+tiles, ragged tails, one to sixteen 32-column hidden chunks); the N = 768
+pair representation (589824 rows) is compared on sampled rows for out and dx
+and in full for the sums over rows.
 """
 import numpy as np
 import pytest
@@ -28,25 +24,10 @@ from paper_2506_20686_amd import workloads as W
 from test_lnl_gpu import close
 
 
-def close_sum(name, got, ref, scale, rscale):
-    got = got.detach().double().cpu().numpy()
-    assert got.shape == ref.shape, name
-    assert np.all(np.isfinite(got)), f"{name}: non-finite"
-    err = np.abs(got - ref)
-    bound = 2e-2 * scale + 8.0 * rscale + 1e-2 * np.abs(ref) + 1e-30
-    worst = np.max(err / bound, initial=0)
-    assert worst <= 1.0, f"{name}: bound violated (worst err/bound {worst:.3f})"
-    nrm = np.linalg.norm(ref)
-    if nrm > 0:
-        rel = np.linalg.norm(got - ref) / nrm
-        assert rel <= 1e-2, f"{name}: relative Frobenius error {rel:.3g}"
+def check_sums(got, ref):
+    for name, g, r in zip(("dw1", "dw2", "dgamma", "dbeta"), got, ref):
+        close(name, g, r, row_sum=True)
 
-
-def check_sums(t, got, ref):
-    scales, rscales = OT.trn_sum_scales(t["x"], t["gamma"], t["beta"], t["w1"], t["w2"],
-                                        t["dout"], EPS)
-    for name, g, r, sc, rs in zip(("dw1", "dw2", "dgamma", "dbeta"), got, ref, scales, rscales):
-        close_sum(name, g, r, sc, rs)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -84,7 +65,7 @@ def test_forward_and_backward_full(m, f):
     rdx, rdw1, rdw2, rdg, rdb = OT.trn_bwd(t["x"], t["gamma"], t["beta"], t["w1"], t["w2"],
                                            t["dout"], EPS)
     close("dx", dx, rdx)
-    check_sums(t, (dw1, dw2, dg, db), (rdw1, rdw2, rdg, rdb))
+    check_sums((dw1, dw2, dg, db), (rdw1, rdw2, rdg, rdb))
 
 
 def test_pair_transition_n768():
@@ -103,7 +84,7 @@ def test_pair_transition_n768():
     rdx, rdw1, rdw2, rdg, rdb = OT.trn_bwd(t["x"], t["gamma"], t["beta"], t["w1"], t["w2"],
                                            t["dout"], EPS, rows=rows)
     close("dx", dx.cpu()[rows], rdx[rows])
-    check_sums(t, (dw1, dw2, dg, db), (rdw1, rdw2, rdg, rdb))
+    check_sums((dw1, dw2, dg, db), (rdw1, rdw2, rdg, rdb))
 
 
 def test_transition_is_bitwise_deterministic():
