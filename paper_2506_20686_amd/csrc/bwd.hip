@@ -1204,15 +1204,16 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   const int pc = (lane & 3) ^ swz(pp);
   const bf16* src0 = wave < 8 ? a.k : a.v;
   const bf16* src1 = wave < 8 ? a.q : a.da;
-  const uint32_t voff0 =
-      (uint32_t)(((int64_t)(kstart + pp) * G.sPos + hb + 8 * pc) * 2);
-  const uint32_t voff1 =
-      (uint32_t)(((int64_t)(qstart + pp) * G.sPos + hb + 8 * pc) * 2);
+  // The first key and query of the block move the 64-bit bases (koff, qoff
+  // elements), so a lane's byte offset stays below 2^32 for every accepted
+  // size: at most 127 positions x sPos (the ending node's n h 32) x 2 bytes.
+  const int64_t koff = (int64_t)kstart * G.sPos, qoff = (int64_t)qstart * G.sPos;
+  const uint32_t voff = (uint32_t)(((int64_t)pp * G.sPos + hb + 8 * pc) * 2);
   // op 2: dA low (waves 0-7, same lane offsets as op 1) or lse2 / -D rows
   const bool lo_op = wave < 8;
   const float* lrow = (wave < 12 ? a.lse2 : a.dsum) + (int64_t)h * G.nr * G.np;
   const uint32_t voff2 =
-      lo_op ? voff1 : (uint32_t)((qstart + 32 * (wave & 3) + 4 * lane) * 4);
+      lo_op ? voff : (uint32_t)((qstart + 32 * (wave & 3) + 4 * lane) * 4);
   char* const dst0 = smem + (wave < 8 ? DBD_OK : DBD_OV) + 1024 * (wave & 7);
   char* const dst1 = smem + (wave < 8 ? DBD_OQ : DBD_ODA) + 1024 * (wave & 7);
   char* const dst2 = lo_op ? smem + DBD_OLO + 1024 * wave
@@ -1222,13 +1223,13 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
     // counts uniform
     const bool real = r < r1;
     const int64_t rb = (int64_t)min(r, G.nr - 1) * G.sRow;
-    const bf16* p0 = src0 + rb;
-    const bf16* p1 = src1 + rb;
-    const bf16* p2 = a.dalo + rb;
+    const bf16* p0 = src0 + rb + koff;
+    const bf16* p1 = src1 + rb + qoff;
+    const bf16* p2 = a.dalo + rb + qoff;
     const float* pl = lrow + (int64_t)min(r, G.nr - 1) * G.np;
-    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff0,
+    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff,
            dst0 + slot * DBD_SLOT);
-    dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff1,
+    dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff,
            dst1 + slot * DBD_SLOT);
     if (lo_op) {
       dma16b(real ? buf_rsrc(p2, a.dalo + tensor) : buf_rsrc(p2, p2), voff2,

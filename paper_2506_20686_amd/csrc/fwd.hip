@@ -113,6 +113,11 @@ constexpr int FWD_ROWS = 1;                 // rows per workgroup (they share th
 // this (log2 units), so unnormalised weights stay <= 2^8 and most blocks skip
 // the rescale of the accumulator.  Any stale max gives the same result.
 constexpr float STALE_MAX_SLACK = 8.f;
+// Starting value of the running max: finite, so that a query whose keys so
+// far all have logit -inf (an additive -inf bias) keeps m - mnew = 0 when
+// another lane of its wave raises the wave's maxima, and exp2(-inf - m) = 0;
+// any finite logit exceeds it by more than the slack.
+constexpr float M_FLOOR = -3.4028234663852886e38f;
 
 template <typename T>
 struct FwdArgs {
@@ -191,7 +196,7 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
       row_frags(a.q + rowbase[i] + (int64_t)q * G.sPos, g, qf[i]);
     else
       zero_frags(qf[i]);
-    st[i].m = neg_inf();
+    st[i].m = M_FLOOR;
     st[i].l = f32x16{};
 #pragma unroll
     for (int c = 0; c < NO; ++c) st[i].o[c] = f32x16{};
@@ -519,7 +524,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   float ls0[FO_QT], ls1[FO_QT];  // this lane's share of sum_k P (its 16 keys of each tile)
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
-    m[i] = neg_inf();
+    m[i] = M_FLOOR;
     o[i] = f32x16{};
     ls0[i] = ls1[i] = 0.f;
   }

@@ -146,6 +146,25 @@ def test_maximum_heads(node):
     full_check(t, node, torch.bfloat16)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_minus_inf_bias_tile(dtype, node):
+    """An additive -inf bias on every key of the first 32-key tile of one
+    query, while the other queries of its wave see finite logits there: the
+    wave raises its running maxima on that tile, and the -inf query's weights
+    stay exactly 0 (no NaN from -inf - -inf); its remaining keys decide its
+    output."""
+    n, h, q0 = 70, 2, 5
+    t = inputs(n, h, dtype, seed=4242 + node, mask_kind="none")
+    bias = t["bias"].clone()
+    if node == B.STARTING:
+        bias[q0, :32, :] = float("-inf")  # bias[q][k][h]
+    else:
+        bias[:32, q0, :] = float("-inf")  # the ending node reads bias[k][i][h]
+    t["bias"] = bias
+    full_check(t, node, dtype)
+
+
 def test_non_default_scale():
     t = inputs(48, 2, torch.float32, seed=5, mask_kind="random")
     full_check(t, B.ENDING, torch.float32, scale=0.9)
