@@ -64,7 +64,8 @@ typedef enum {
   TRIATTN_ERR_INVALID_ARG = 1, /* null pointer, bad enum, size or scale out of range */
   TRIATTN_ERR_UNSUPPORTED = 2, /* a value the library does not implement (e.g. d = 128) */
   TRIATTN_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
-  TRIATTN_ERR_HIP = 4          /* a HIP launch reported an error */
+  TRIATTN_ERR_HIP = 4,         /* a HIP launch reported an error */
+  TRIATTN_ERR_TOO_LARGE = 5    /* more scratch than tri_attn_fwd_noalloc holds */
 } triattn_status;
 
 typedef enum { TRIATTN_STARTING = 0, TRIATTN_ENDING = 1 } triattn_node;
@@ -82,6 +83,25 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                  const void* q, const void* k, const void* v, const void* g, const void* bias,
                  const uint8_t* mask, void* out, float* lse, void* workspace,
                  size_t workspace_bytes, void* stream);
+
+/* The forward for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, results (bitwise) and rules as tri_attn_fwd, without the
+ * workspace: the library keeps it in a device array of
+ * TRIATTN_FWD_NOALLOC_SCRATCH_BYTES that each GPU it runs on holds from the
+ * library's first use until the process ends; the call itself allocates and
+ * frees nothing.  Sizes whose forward workspace (tri_attn_fwd_workspace_bytes)
+ * exceeds the array return TRIATTN_ERR_TOO_LARGE (N = 768 at h = 4, d = 32
+ * needs about 9.5 MiB; d = 16 needs its padded copies too).  `stream` must
+ * belong to the current device (TRIATTN_ERR_INVALID_ARG otherwise).  Every
+ * call on one GPU shares that GPU's array: calls that may overlap on one GPU
+ * (different streams, no ordering between them) race and must not be made;
+ * calls on one stream are ordered and safe. */
+#define TRIATTN_FWD_NOALLOC_SCRATCH_BYTES (32u << 20)
+int tri_attn_fwd_noalloc(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                         const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, void* out, float* lse,
+                         void* stream);
 
 /* Bytes of device workspace tri_attn_bwd needs for these sizes. */
 int tri_attn_bwd_workspace_bytes(int node, int dtype, int64_t n, int64_t h, int64_t d,

@@ -18,7 +18,8 @@ import torch
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libtriattn.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_TOO_LARGE = 0, 1, 2, 3, 4, 5
+FWD_NOALLOC_SCRATCH_BYTES = 32 << 20  # TRIATTN_FWD_NOALLOC_SCRATCH_BYTES
 STARTING, ENDING = 0, 1
 F32, BF16 = 0, 1
 HEAD_DIM = 32
@@ -46,6 +47,8 @@ def lib():
         L.tri_attn_bwd_workspace_bytes.argtypes = L.tri_attn_fwd_workspace_bytes.argtypes
         L.tri_attn_fwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 9 + [_sz, _vp]
         L.tri_attn_bwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz, _vp]
+        L.tri_attn_fwd_noalloc.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 9
+        L.tri_attn_fwd_noalloc.restype = _int
         L.tri_attn_rows_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _i64, _i64,
                                                         ctypes.POINTER(_sz)]
         L.tri_attn_rows_bwd_workspace_bytes.argtypes = L.tri_attn_rows_fwd_workspace_bytes.argtypes
@@ -147,6 +150,13 @@ def tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, 
     """Raw call: every tensor argument is an integer device address (or None)."""
     return lib().tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
                               workspace, workspace_bytes, stream)
+
+
+def tri_attn_fwd_noalloc(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
+                         stream) -> int:
+    """Raw call: every tensor argument is an integer device address (or None)."""
+    return lib().tri_attn_fwd_noalloc(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out,
+                                      lse, stream)
 
 
 def tri_attn_bwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, dout, dq, dk,
@@ -383,6 +393,30 @@ def fwd(q, k, v, g, bias, mask=None, node: int = STARTING, scale: Optional[float
         st = tri_attn_fwd(node, dt, n, h, d, *args)
     if st != OK:
         raise TriAttnError(st, "tri_attn_fwd_batched" if lead else "tri_attn_fwd")
+    return out, lse
+
+
+def fwd_noalloc(q, k, v, g, bias, mask=None, node: int = STARTING,
+                scale: Optional[float] = None, out: Optional[torch.Tensor] = None,
+                lse: Optional[torch.Tensor] = None):
+    """Triangle attention forward through the allocation-free entry point (the
+    library's own scratch array instead of a workspace).  out and lse may be
+    passed in; otherwise they are allocated here (the library allocates
+    nothing).  Unbatched only."""
+    lead, n, h, d, dt, dev = _common(q, k, v, g, bias, mask)
+    if lead:
+        raise ValueError("fwd_noalloc takes one pair map (no batch axis)")
+    scale = default_scale(d) if scale is None else float(scale)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((n, n, h), dtype=torch.float32, device=dev)
+    _check("out", out, (n, n, h, d), q.dtype, dev)
+    _check("lse", lse, (n, n, h), torch.float32, dev)
+    st = tri_attn_fwd_noalloc(node, dt, n, h, d, scale, _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                              _ptr(bias), _ptr(mask), _ptr(out), _ptr(lse), _stream(dev))
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_fwd_noalloc")
     return out, lse
 
 

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "kernels.h"
@@ -286,6 +287,72 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
                                   dk, dv, dg, dbias, workspace, s);
   return bwd_one<float>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, dout, dq, dk, dv, dg,
                         dbias, workspace, s);
+}
+
+}  // extern "C"
+
+// ---- the forward for callers that cannot allocate ------------------------------------------
+//
+// Its workspace (bias planes, key bits) lives in this file-scope device array;
+// each GPU the library runs on holds its own copy until the process ends.  In
+// host code `scratch` names a host-side stand-in, not the device array: the
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current, and only that address reaches the kernels.
+static __device__ __align__(256) char scratch[TRIATTN_FWD_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[MAX_DEVICES] = {};  // device address of `scratch`, per device
+
+// Device address of this device's scratch array (the stream's device must be
+// the current one).
+int scratch_address(hipStream_t s, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return TRIATTN_ERR_HIP;
+  if (s != nullptr) {
+    hipDevice_t sd = -1;
+    if (hipStreamGetDevice(s, &sd) != hipSuccess) return TRIATTN_ERR_HIP;
+    if (sd != dev) return TRIATTN_ERR_INVALID_ARG;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+      return TRIATTN_ERR_HIP;
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return TRIATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tri_attn_fwd_noalloc(int node, int dtype, int64_t n, int64_t h, int64_t d, float scale,
+                         const void* q, const void* k, const void* v, const void* g,
+                         const void* bias, const uint8_t* mask, void* out, float* lse,
+                         void* stream) {
+  int st = check_shape(node, dtype, n, h, d, true);
+  if (st != TRIATTN_OK) return st;
+  if (!(isfinite(scale) && scale > 0.f)) return TRIATTN_ERR_INVALID_ARG;
+  const void* ptrs[] = {q, k, v, g, bias, out, lse};
+  for (const void* p : ptrs)
+    if (p == nullptr || !aligned16(p)) return TRIATTN_ERR_INVALID_ARG;
+  const Whole W = whole_plan(false, dtype, n, h, d);
+  if (W.total > (size_t)TRIATTN_FWD_NOALLOC_SCRATCH_BYTES) return TRIATTN_ERR_TOO_LARGE;
+  hipStream_t s = (hipStream_t)stream;
+  void* ws = nullptr;
+  st = scratch_address(s, &ws);
+  if (st != TRIATTN_OK) return st;
+  // every byte of the workspace the forward reads is written first by its
+  // preparation kernels (bias planes, key bits), so nothing needs clearing
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  if (dtype == TRIATTN_BF16)
+    return fwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, ws, s);
+  return fwd_one<float>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, ws, s);
 }
 
 // ---- a batch of pair maps -----------------------------------------------------------------
@@ -825,6 +892,8 @@ const char* tri_attn_status_string(int status) {
     case TRIATTN_ERR_UNSUPPORTED: return "unsupported argument value";
     case TRIATTN_ERR_WORKSPACE: return "workspace missing or too small";
     case TRIATTN_ERR_HIP: return "HIP launch error";
+    case TRIATTN_ERR_TOO_LARGE:
+      return "problem needs more scratch memory than the allocation-free entry point holds";
     default: return "unknown status";
   }
 }

@@ -36,7 +36,8 @@ def test_exports_every_declared_symbol(lib):
 
 def test_status_strings(lib):
     assert B.tri_attn_status_string(B.OK) == "ok"
-    for s in (B.ERR_INVALID_ARG, B.ERR_UNSUPPORTED, B.ERR_WORKSPACE, B.ERR_HIP):
+    for s in (B.ERR_INVALID_ARG, B.ERR_UNSUPPORTED, B.ERR_WORKSPACE, B.ERR_HIP,
+              B.ERR_TOO_LARGE):
         assert B.tri_attn_status_string(s) not in ("ok", "unknown status")
     assert B.tri_attn_status_string(99) == "unknown status"
 
@@ -460,3 +461,19 @@ def test_d64_workspace_scales_the_pair_buffers(lib):
         st, f32_ = ws_bytes(lib.tri_attn_fwd_workspace_bytes, 0, dtype, n, h, 32)
         st, f64_ = ws_bytes(lib.tri_attn_fwd_workspace_bytes, 0, dtype, n, h, 64)
         assert f32_ == f64_
+
+
+def test_noalloc_forward_rejects_before_any_hip_call(lib):
+    """The allocation-free forward checks sizes, pointers and its scratch
+    limit before it looks up the scratch array or launches anything."""
+    f = lib.tri_attn_fwd_noalloc
+    good = (P,) * 5
+    sc = 0.1767767
+    assert f(0, B.BF16, 0, 1, 32, sc, *good, None, P, P, None) == B.ERR_INVALID_ARG
+    assert f(0, B.BF16, 8, 1, 128, sc, *good, None, P, P, None) == B.ERR_UNSUPPORTED
+    assert f(0, B.BF16, 8, 1, 32, -1.0, *good, None, P, P, None) == B.ERR_INVALID_ARG
+    assert f(0, B.BF16, 8, 1, 32, sc, None, P, P, P, P, None, P, P, None) == B.ERR_INVALID_ARG
+    assert f(0, B.BF16, 8, 1, 32, sc, P + 8, P, P, P, P, None, P, P, None) == B.ERR_INVALID_ARG
+    # bias planes of n = 2048, h = 4 alone are 64 MiB, beyond the 32 MiB array
+    assert f(0, B.BF16, 2048, 4, 32, sc, *good, None, P, P, None) == B.ERR_TOO_LARGE
+    assert f(1, B.F32, 8192, 64, 32, sc, *good, None, P, P, None) == B.ERR_TOO_LARGE
