@@ -30,6 +30,11 @@
  *     Tensor pointers must be 16-byte aligned.  mask may be NULL (all valid).
  *   - A masked key gets weight exactly 0.  A query with no valid key gets
  *     out = 0, lse = -inf and contributes nothing to any gradient.
+ *   - Inputs must be finite, except that bias entries may be -inf: an
+ *     additive -inf excludes that key for that query like the mask does (a
+ *     query whose valid keys all carry -inf is treated as one with no valid
+ *     key).  Device code is compiled on the assumption that no NaN reaches it
+ *     (-fno-honor-nans), so a NaN input gives unspecified results.
  *   - dtype TRIATTN_BF16: bfloat16 tensors, fp32 accumulation, outputs
  *     rounded to nearest even.  TRIATTN_F32: fp32 throughout.
  *   - d must be 32; the whole-map and batched calls also take d = 16, which
