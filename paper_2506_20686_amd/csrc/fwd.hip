@@ -118,6 +118,10 @@ constexpr float STALE_MAX_SLACK = 8.f;
 // another lane of its wave raises the wave's maxima, and exp2(-inf - m) = 0;
 // any finite logit exceeds it by more than the slack.
 constexpr float M_FLOOR = -3.4028234663852886e38f;
+// Largest per-lane tile sum of weights (32 keys, relative to the running max)
+// the bf16 forward accepts without raising the max: weights stay below 2^64,
+// so over at most 256 tiles the sums and the weighted values stay finite.
+constexpr float WEIGHT_LIMIT = 1.8446744e19f;  // 2^64
 
 template <typename T>
 struct FwdArgs {
@@ -587,11 +591,52 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       tr[1] = ds_read_tr<S * FO_SLOT + 8 * 64>(rv8);
       tr[2] = ds_read_tr<S * FO_SLOT + 16 * 64>(rv);
       tr[3] = ds_read_tr<S * FO_SLOT + 24 * 64>(rv8);
+      // P = exp2(S c1 - m) against the running max m as it stands (in place of
+      // S), and the tile's row sums of the bf16 P the MFMA uses (dot products
+      // with (1, 1)).  The max is not formed per tile: a tile whose weights
+      // grow past 2^64 (or overflow: the first tile, while m is still the
+      // floor) recomputes its logits, raises m to their max, rescales the
+      // state and is redone; other tiles only have weights below 2^64, which
+      // fp32 sums and bf16 operands hold as exactly as weights below 1.
+      F pf[FO_QT][M::PCH];
+      float t0[FO_QT], t1[FO_QT];
+      auto weights = [&](int i) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          s[i][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i][v], c1, -m[i]));
+        acc_frags(s[i], pf[i]);
+        t0[i] = 0.f;
+        t1[i] = 0.f;
+#pragma unroll
+        for (int u = 0; u < M::PCH; ++u) {
+          t0[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 0, 1), one2, t0[i], false);
+          t1[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 2, 3), one2, t1[i], false);
+          t0[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 4, 5), one2, t0[i], false);
+          t1[i] = __builtin_amdgcn_fdot2_f32_bf16(
+              __builtin_shufflevector(pf[i][u], pf[i][u], 6, 7), one2, t1[i], false);
+        }
+      };
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
         if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
-        const float mx = wave_xor32_max(max16(s[i])) * c1;
-        if (__any(mx > m[i] + STALE_MAX_SLACK)) {
+        weights(i);
+        if (__any(!(t0[i] + t1[i] <= WEIGHT_LIMIT))) {
+          // the tile's logits again (bias and K from the slot, Q at hand)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const f32x4 y = lds_load16<f32x4>(rb + S * FO_SLOT + i * 4096 + 1024 * j);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
+          }
+          {
+            const F k0r = lds_load16<F>(rk0 + S * FO_SLOT), k1r = lds_load16<F>(rk1 + S * FO_SLOT);
+            s[i] = M::mma(k1r, qf[i][1], M::mma(k0r, qf[i][0], s[i]));
+          }
+          if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
+          const float mx = wave_xor32_max(max16(s[i])) * c1;
           const float mnew = fmaxf(m[i], mx);
           const float alpha = __builtin_amdgcn_exp2f(m[i] - mnew);
           ls0[i] *= alpha;
@@ -599,36 +644,16 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) o[i][v] *= alpha;
           m[i] = mnew;
+          weights(i);
         }
-      }
-      F pf[FO_QT][M::PCH];
-#pragma unroll
-      for (int i = 0; i < FO_QT; ++i) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          s[i][v] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[i][v], c1, -m[i]));
-        acc_frags(s[i], pf[i]);
       }
       tr_wait(tr);
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
 #pragma unroll
         for (int u = 0; u < M::PCH; ++u) o[i] = M::mma(tr_frag(tr, u), pf[i][u], o[i]);
-      }
-      // row sums of the bf16 P the MFMA used: dot products with (1, 1)
-#pragma unroll
-      for (int i = 0; i < FO_QT; ++i) {
-#pragma unroll
-        for (int u = 0; u < M::PCH; ++u) {
-          ls0[i] = __builtin_amdgcn_fdot2_f32_bf16(
-              __builtin_shufflevector(pf[i][u], pf[i][u], 0, 1), one2, ls0[i], false);
-          ls1[i] = __builtin_amdgcn_fdot2_f32_bf16(
-              __builtin_shufflevector(pf[i][u], pf[i][u], 2, 3), one2, ls1[i], false);
-          ls0[i] = __builtin_amdgcn_fdot2_f32_bf16(
-              __builtin_shufflevector(pf[i][u], pf[i][u], 4, 5), one2, ls0[i], false);
-          ls1[i] = __builtin_amdgcn_fdot2_f32_bf16(
-              __builtin_shufflevector(pf[i][u], pf[i][u], 6, 7), one2, ls1[i], false);
-        }
+        ls0[i] += t0[i];
+        ls1[i] += t1[i];
       }
     };
     issue(0);
