@@ -75,6 +75,10 @@ def parse():
                          "(N = 32 fp32 ... N = 1536, each node variant) and report its fwd and "
                          "bwd time, TFLOP/s and peak HBM bytes in the same JSON line "
                          "(0 skips it, as the profiling runs do)")
+    ap.add_argument("--mfma-probe", type=int, default=0,
+                    help="only run the library's MFMA-only calibration kernel this many times "
+                         "(1024 workgroups of 4 waves, 2000 rounds of 8 bf16 32x32x16 MFMAs per "
+                         "wave): the reference kernel for the MFMA-activity counters")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device-to-device copy of this many bytes 5 times "
                          "(reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -92,6 +96,33 @@ def copy_calibration(nbytes):
         dst.copy_(src)
     torch.cuda.synchronize(dev)
     print(json.dumps({"copy_bytes": src.numel() * 4, "launches": 5}), flush=True)
+
+
+def mfma_calibration(launches, blocks=1024, iters=2000):
+    """The library's MFMA-only kernel (one workgroup of 4 waves per SIMD quad,
+    `iters` rounds of 8 bf16 32x32x16 MFMAs per wave): under rocprofv3 --pmc the
+    MFMA-busy counter of a dispatch, divided by the cycles its MFMAs need at
+    the dense rate (32 per MFMA on each SIMD), calibrates that counter."""
+    import torch
+
+    from paper_2506_20686_amd import binding as B
+    dev = torch.device("cuda:0")
+    out = torch.empty(blocks * 256, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for i in range(launches + 1):
+        if i == 1:
+            ev[0].record()
+        st = B.tri_attn_mfma_probe(blocks, iters, out.data_ptr(), stream)
+        if st != B.OK:
+            raise B.TriAttnError(st, "tri_attn_mfma_probe")
+    ev[1].record()
+    torch.cuda.synchronize(dev)
+    ms = ev[0].elapsed_time(ev[1]) / max(1, launches)
+    mfmas = blocks * 4 * iters * 8
+    print(json.dumps({"mfma_probe_launches": launches, "blocks": blocks, "iters": iters,
+                      "mfma_per_launch": mfmas, "ms_per_launch": round(ms, 5),
+                      "tflops": round(mfmas * 32768 / (ms * 1e-3) / 1e12, 2)}), flush=True)
 
 
 # Sources whose change can change a kernel family's memory traffic (its
@@ -128,41 +159,101 @@ def recorded_traffic(kernel, workload, family="tri"):
     return float(m.group(1))
 
 
-def cpu_baseline(w, t, target_s, row_range=None):
-    """Time the fp64 oracle (as it stands) on rows of the starting node: the
-    forward and the per-row gradients (dQ, dK, dV, dG) of R rows, nominal
-    14 N^2 H d flop per row.  R is sized from a trial of one row per thread;
-    row_range = (r0, rows) draws them from that range only."""
+def host_cpu():
+    """CPU model and logical core count of the host running the benchmark."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
+
+
+class native_oracle:
+    """The oracle's sources built for this host (-O3 -march=native, OpenMP) and
+    swapped in for the duration of a `with` block; the tests use the generic build."""
+
+    def __enter__(self):
+        import oracle
+        from oracle import build as ob
+        self.flags = " ".join(ob.NATIVE_FLAGS)
+        self.prev = oracle.use_library(oracle.load(ob.build_native()))
+        return self
+
+    def __exit__(self, *exc):
+        import oracle
+        oracle.use_library(self.prev)
+
+
+def cpu_baseline(w, t, target_s, row_range=None, whole=()):
+    """Time the fp64 oracle (as it stands, built -O3 -march=native for this
+    host) on a sample of the workload.  A whole fwd+bwd is the forward of every
+    row, the per-row gradients (dQ, dK, dV, dG) of every row and the bias
+    gradient of every query (a sum over all rows); the sample takes R evenly
+    spaced rows and R evenly spaced bias-gradient queries, R / N of that work,
+    nominal 14 N^2 H d flop per row.  R is sized from a trial of one row and
+    one query per oracle thread to about target_s seconds.  row_range = (r0,
+    rows) draws the rows from that range and leaves the bias gradient out (the
+    oracle sums it over every row of the map, not over a range's).  `whole`
+    lists small workloads timed in full as well."""
     import numpy as np
 
     import oracle
+    from paper_2506_20686_amd import workloads as W
 
-    arr = {k: np.ascontiguousarray(t[k].double().numpy()) for k in ("q", "k", "v", "g", "bias",
-                                                                    "dout")}
-    mask = t["mask"].numpy()
+    def arrays(tt):
+        arr = {k: np.ascontiguousarray(tt[k].double().numpy())
+               for k in ("q", "k", "v", "g", "bias", "dout")}
+        m = tt.get("mask")
+        return arr, (None if m is None else m.numpy())
 
-    def run(rows):
+    def run(ww, tt, node, rows, qs):
+        arr, mask = arrays(tt)
         t0 = time.perf_counter()
-        oracle.fwd(0, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], mask, rows=rows)
-        oracle.bwd(0, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], arr["dout"], mask,
-                   rows=rows, db_queries=[])
+        oracle.fwd(node, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], mask, rows=rows)
+        oracle.bwd(node, arr["q"], arr["k"], arr["v"], arr["g"], arr["bias"], arr["dout"], mask,
+                   rows=rows, db_queries=qs)
         return time.perf_counter() - t0
 
-    # the oracle spreads rows over its threads: size the sample from a trial
-    # with one row per thread
-    r0, span = (0, w.n) if row_range is None else row_range
-    nt = max(1, min(span, oracle.max_threads()))
-    trial = run(list(range(r0, r0 + nt)))
-    rows = max(nt, min(span, int(nt * target_s / max(trial, 1e-3)) // nt * nt))
-    sel = [r0 + int(i * span / rows) for i in range(rows)]
-    dt = run(sel)
-    flop = 14.0 * w.n ** 2 * w.h * w.d * rows
-    where = f"{w.n} rows" if row_range is None else f"rows {r0}..{r0 + span - 1} of {w.n}"
-    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(),
-            "kind": "oracle", "seconds": round(dt, 3),
-            "sample": f"starting node of {w.name}: forward + per-row gradients (dQ, dK, dV, dG) "
-                      f"of {rows} of {where}, fp64, nominal 14*N^2*H*d flop per row; "
-                      f"dB (a row sum of the same dS) not included"}
+    with native_oracle() as nat:
+        node = w.nodes[0]
+        r0, span = (0, w.n) if row_range is None else row_range
+        nt = max(1, min(span, oracle.max_threads()))
+        with_db = row_range is None
+
+        def sample(count):
+            rows = [r0 + int(i * span / count) for i in range(count)]
+            qs = [int(i * w.n / count) for i in range(count)] if with_db else []
+            return run(w, t, node, rows, qs)
+
+        trial = sample(nt)
+        rows = max(nt, min(span, int(nt * target_s / max(trial, 1e-3)) // nt * nt))
+        dt = sample(rows)
+        flop = 14.0 * w.n ** 2 * w.h * w.d * rows
+        where = f"{w.n} rows" if row_range is None else f"rows {r0}..{r0 + span - 1} of {w.n}"
+        res = {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.max_threads(),
+               "kind": "oracle", "seconds": round(dt, 3), "build": f"gcc {nat.flags}",
+               **host_cpu(),
+               "sample": (f"{W.NODE_NAMES[node]} node of {w.name}: forward and per-row gradients "
+                          f"(dQ, dK, dV, dG) of {rows} of {where}" +
+                          (f", and the bias gradient of {rows} of {w.n} query indices (each a "
+                           f"sum over all {w.n} rows): {rows}/{w.n} of one node's fwd+bwd"
+                           if with_db else "; the range's bias-gradient term not included") +
+                          ", fp64, nominal 14*N^2*H*d flop per row")}
+        timed = {}
+        for wname in whole:
+            ww = W.WORKLOADS[wname]
+            tt = W.workload_inputs(ww)
+            sec = run(ww, tt, tt["node"], None, None)
+            timed[wname] = {"seconds": round(sec, 3),
+                            "tflops": round(ww.flops_fwd_bwd / sec / 1e12, 6)}
+        if timed:
+            res["whole"] = timed
+    return res
 
 
 def lnl_kernel_bytes(m, cols, k=128):
@@ -641,6 +732,9 @@ def main():
     if args.copy_bytes > 0:
         copy_calibration(args.copy_bytes)
         return
+    if args.mfma_probe > 0:
+        mfma_calibration(args.mfma_probe)
+        return
 
     import torch
 
@@ -784,7 +878,10 @@ def main():
         h0 = host[w.nodes[0]]
         if w.batch > 1:  # sample 0
             h0 = {k: (v[0] if hasattr(v, "dim") else v) for k, v in h0.items()}
-        out["cpu_baseline"] = cpu_baseline(w, h0, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(
+            w, h0, args.cpu_seconds,
+            whole=("tri_start_fp32_n32", "tri_start_bf16_n256_pad10") if name == W.HEADLINE
+            else ())
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

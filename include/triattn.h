@@ -301,6 +301,13 @@ int tri_attn_timing_read(int index, const char** name, double* total_ms, int64_t
  * events); returns TRIATTN_ERR_HIP if an event call had failed. */
 int tri_attn_timing_reset(void);
 
+/* Calibration kernel for the MFMA-activity counters (not part of the paper's
+ * method): `blocks` workgroups of 4 waves, each wave running `iters` rounds of
+ * eight bf16 v_mfma_f32_32x32x16 (32768 flop each) and nothing else, then
+ * writing one float per thread to out [blocks * 256] (device memory).
+ * 1 <= blocks <= 2^20, 1 <= iters <= 2^24; asynchronous on `stream`. */
+int tri_attn_mfma_probe(int64_t blocks, int64_t iters, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -49,6 +49,8 @@ def lib():
         L.tri_attn_bwd.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 15 + [_sz, _vp]
         L.tri_attn_fwd_noalloc.argtypes = [_int, _int, _i64, _i64, _i64, _f] + [_vp] * 9
         L.tri_attn_fwd_noalloc.restype = _int
+        L.tri_attn_mfma_probe.argtypes = [_i64, _i64, _vp, _vp]
+        L.tri_attn_mfma_probe.restype = _int
         L.tri_attn_rows_fwd_workspace_bytes.argtypes = [_int, _i64, _i64, _i64, _i64,
                                                         ctypes.POINTER(_sz)]
         L.tri_attn_rows_bwd_workspace_bytes.argtypes = L.tri_attn_rows_fwd_workspace_bytes.argtypes
@@ -150,6 +152,11 @@ def tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse, 
     """Raw call: every tensor argument is an integer device address (or None)."""
     return lib().tri_attn_fwd(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,
                               workspace, workspace_bytes, stream)
+
+
+def tri_attn_mfma_probe(blocks: int, iters: int, out, stream) -> int:
+    """Raw call of the MFMA counter-calibration kernel (out: device address)."""
+    return lib().tri_attn_mfma_probe(blocks, iters, out, stream)
 
 
 def tri_attn_fwd_noalloc(node, dtype, n, h, d, scale, q, k, v, g, bias, mask, out, lse,

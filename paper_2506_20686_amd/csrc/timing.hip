@@ -5,6 +5,7 @@
 #include <mutex>
 #include <vector>
 
+#include "common.h"
 #include "timing.h"
 #include "triattn.h"
 
@@ -125,3 +126,47 @@ int tri_attn_timing_read(int index, const char** name, double* total_ms, int64_t
 }
 
 }  // extern "C"
+
+// ---- MFMA counter calibration -------------------------------------------------------
+//
+// A kernel whose only work is bf16 MFMA: every wave runs `iters` rounds of
+// eight v_mfma_f32_32x32x16_bf16 over four independent accumulator chains
+// (4 waves per block, one per SIMD).  Profiled beside the attention kernels it
+// gives the reading of the MFMA-activity counters for a known amount of MFMA
+// work at full occupancy of the matrix cores.
+namespace triattn {
+namespace {
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void mfma_probe_kernel(float* out, int iters) {
+  bf16x8 a, b;
+  const float x = 1.f + 1e-3f * (float)threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (bf16)(x + (float)i);
+    b[i] = (bf16)(x - (float)i);
+  }
+  f32x16 acc[4] = {};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      acc[k & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[k & 3], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) s += acc[m][v];
+  out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+}  // namespace
+}  // namespace triattn
+
+extern "C" int tri_attn_mfma_probe(int64_t blocks, int64_t iters, float* out, void* stream) {
+  if (blocks < 1 || blocks > (1 << 20) || iters < 1 || iters > (1 << 24) || out == nullptr)
+    return TRIATTN_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(triattn::mfma_probe_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                     (hipStream_t)stream, out, (int)iters);
+  return hipGetLastError() == hipSuccess ? TRIATTN_OK : TRIATTN_ERR_HIP;
+}

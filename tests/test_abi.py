@@ -477,3 +477,12 @@ def test_noalloc_forward_rejects_before_any_hip_call(lib):
     # bias planes of n = 2048, h = 4 alone are 64 MiB, beyond the 32 MiB array
     assert f(0, B.BF16, 2048, 4, 32, sc, *good, None, P, P, None) == B.ERR_TOO_LARGE
     assert f(1, B.F32, 8192, 64, 32, sc, *good, None, P, P, None) == B.ERR_TOO_LARGE
+
+
+def test_mfma_probe_rejects_bad_sizes(lib):
+    """The MFMA counter-calibration kernel checks its sizes before launching."""
+    f = lib.tri_attn_mfma_probe
+    assert f(0, 10, P, None) == B.ERR_INVALID_ARG
+    assert f(1, 0, P, None) == B.ERR_INVALID_ARG
+    assert f((1 << 20) + 1, 10, P, None) == B.ERR_INVALID_ARG
+    assert f(1, 10, None, None) == B.ERR_INVALID_ARG
