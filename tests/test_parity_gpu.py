@@ -197,6 +197,23 @@ def test_workload_sampled(name, node):
     close("dbias", grads[4], rg[4], w.dtype, bsel)
 
 
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_workload_dbias_block(node):
+    """The N = 768 workload in the benchmark's launch configuration: the bias
+    gradient of 128 consecutive queries (one whole 128-query block of the
+    bias-gradient kernel, across all six of its 128-key blocks) against the
+    oracle, which sums dS over all 768 rows for each of them."""
+    w = W.WORKLOADS[W.HEADLINE]
+    t = W.workload_inputs(w, node)
+    print(f"\n[dbias block node={node}]", flush=True)
+    out, lse, grads = run_gpu(t, node)
+    qs = list(range(256, 384))
+    rg = oracle.bwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["dout"], t["mask"],
+                    rows=[], db_queries=qs)
+    bsel = (qs,) if node == B.STARTING else (slice(None), qs)
+    close("dbias", grads[4], rg[4], w.dtype, bsel)
+
+
 # ---- properties that hold at any size ----------------------------------------------
 
 @pytest.mark.parametrize("name,node", [("tri_start_bf16_n256_pad10", B.STARTING),
