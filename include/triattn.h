@@ -37,11 +37,12 @@
  *     (-fno-honor-nans), so a NaN input gives unspecified results.
  *   - dtype TRIATTN_BF16: bfloat16 tensors, fp32 accumulation, outputs
  *     rounded to nearest even.  TRIATTN_F32: fp32 throughout.
- *   - d must be 32; the whole-map and batched calls also take d = 16, which
- *     they run through the d = 32 kernels on zero-padded copies held in the
- *     workspace (zero channels add exact zeros: the results are those of
- *     d = 16), and d = 64, which runs register-staged kernels built for 64
- *     channels.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
+ *   - d must be 32; the whole-map and batched calls also take d = 16 and
+ *     d = 64.  bf16 d = 16 runs the 32-channel kernels' 16-channel variants
+ *     on the tensors as they are; fp32 d = 16 runs the d = 32 kernels on
+ *     zero-padded copies held in the workspace (zero channels add exact
+ *     zeros: the results are those of d = 16).  d = 64 runs register-staged
+ *     kernels built for 64 channels.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
  *     positive (1/sqrt(d) is the usual choice).
  *   - The library never allocates or frees memory and never synchronises:
  *     work is enqueued on `stream` (a hipStream_t; NULL is the default stream)
@@ -97,7 +98,7 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
  * library's first use until the process ends; the call itself allocates and
  * frees nothing.  Sizes whose forward workspace (tri_attn_fwd_workspace_bytes)
  * exceeds the array return TRIATTN_ERR_TOO_LARGE (N = 768 at h = 4, d = 32
- * needs about 9.5 MiB; d = 16 needs its padded copies too).  `stream` must
+ * needs about 9.5 MiB; fp32 d = 16 needs its padded copies too).  `stream` must
  * belong to the current device (TRIATTN_ERR_INVALID_ARG otherwise).  Every
  * call on one GPU shares that GPU's array: calls that may overlap on one GPU
  * (different streams, no ordering between them) race and must not be made;
@@ -135,8 +136,8 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
  * index), which keeps the GPU full when one sample's grid is small.  With the
  * unbatched workspace size (tri_attn_fwd_workspace_bytes /
  * tri_attn_bwd_workspace_bytes for n, h, d) the samples run one after another
- * on `stream` and share it.  d = 16 always runs sample by sample, and so do
- * batches above 65535.  The base pointers follow the unbatched rules;
+ * on `stream` and share it.  fp32 d = 16 always runs sample by sample, and so
+ * do batches above 65535.  The base pointers follow the unbatched rules;
  * 1 <= batch <= 2^20.  The per-sample slices of bias, dbias, lse and mask need
  * only element alignment. */
 int tri_attn_fwd_batched_workspace_bytes(int node, int dtype, int64_t batch, int64_t n,

@@ -29,9 +29,16 @@ int check_shape(int node, int dtype, int64_t n, int64_t h, int64_t d, bool whole
   return TRIATTN_OK;
 }
 
-// Channels per head the kernels run with: 64 for d = 64, else 32 (d = 16 is
+// Channels per head the kernels run with: 64 for d = 64, 16 for bf16 d = 16
+// (the DMA kernels read 16-channel heads directly), else 32 (fp32 d = 16 is
 // padded to 32).
-int64_t kernel_d(int64_t d) { return d == 64 ? 64 : triattn::HEAD_DIM; }
+int64_t kernel_d(int64_t d, int dtype) {
+  if (d == 64) return 64;
+  if (d == 16 && dtype == TRIATTN_BF16) return 16;
+  return triattn::HEAD_DIM;
+}
+// fp32 d = 16 runs on zero-padded 32-channel copies held in the workspace.
+bool padded16(int64_t d, int dtype) { return d == 16 && dtype != TRIATTN_BF16; }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -171,9 +178,9 @@ struct Whole {
 };
 
 Whole whole_plan(bool bwd, int dtype, int64_t n, int64_t h, int64_t d) {
-  Whole w{plan(bwd, dtype, n, n, h, kernel_d(d)), 0, 0, 0};
+  Whole w{plan(bwd, dtype, n, n, h, kernel_d(d, dtype)), 0, 0, 0};
   w.pad0 = w.L.total;
-  const int npad = d == 16 ? (bwd ? 10 : 5) : 0;
+  const int npad = padded16(d, dtype) ? (bwd ? 10 : 5) : 0;
   w.pad_bytes = round256((size_t)n * n * h * triattn::HEAD_DIM * (dtype == TRIATTN_BF16 ? 2 : 4));
   w.total = w.pad0 + (size_t)npad * w.pad_bytes;
   return w;
@@ -183,7 +190,7 @@ template <typename T>
 int fwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, const void* k,
             const void* v, const void* gate, const void* bias, const uint8_t* mask, void* out,
             float* lse, void* ws, hipStream_t s) {
-  if (d != 16)
+  if (!padded16(d, std::is_same<T, float>::value ? TRIATTN_F32 : TRIATTN_BF16))
     return run_fwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, ws, s);
   const int64_t rows = (int64_t)g.n * g.n * g.H;
   char* p[5];
@@ -203,7 +210,7 @@ int bwd_one(int node, const Geom& g, const Whole& W, int64_t d, const void* q, c
             const void* v, const void* gate, const void* bias, const uint8_t* mask,
             const void* out, const float* lse, const void* dout, void* dq, void* dk, void* dv,
             void* dg, void* dbias, void* ws, hipStream_t s) {
-  if (d != 16)
+  if (!padded16(d, std::is_same<T, float>::value ? TRIATTN_F32 : TRIATTN_BF16))
     return run_bwd<T>(node, g, W.L, q, k, v, gate, bias, mask, out, lse, dout, dq, dk, dv, dg,
                       dbias, nullptr, ws, s);
   const int64_t rows = (int64_t)g.n * g.n * g.H;
@@ -258,7 +265,7 @@ int tri_attn_fwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const Whole W = whole_plan(false, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d, dtype));
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return fwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, workspace,
@@ -280,7 +287,7 @@ int tri_attn_bwd(int node, int dtype, int64_t n, int64_t h, int64_t d, float sca
   const Whole W = whole_plan(true, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d, dtype));
   hipStream_t s = (hipStream_t)stream;
   if (dtype == TRIATTN_BF16)
     return bwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, dout, dq,
@@ -349,7 +356,7 @@ int tri_attn_fwd_noalloc(int node, int dtype, int64_t n, int64_t h, int64_t d, f
   if (st != TRIATTN_OK) return st;
   // every byte of the workspace the forward reads is written first by its
   // preparation kernels (bias planes, key bits), so nothing needs clearing
-  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d, dtype));
   if (dtype == TRIATTN_BF16)
     return fwd_one<triattn::bf16>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, ws, s);
   return fwd_one<float>(node, geo, W, d, q, k, v, g, bias, mask, out, lse, ws, s);
@@ -376,13 +383,15 @@ BatchStrides batch_strides(int dtype, int64_t n, int64_t h, int64_t d) {
 
 // Batched calls run all samples in one launch per kernel (the sample is the
 // grid's z index, each sample with its own copy of the workspace) when the
-// workspace holds `batch` copies; otherwise, and for d = 16 (which goes
+// workspace holds `batch` copies; otherwise, and for fp32 d = 16 (which goes
 // through per-sample zero-padded copies), sample by sample.
 constexpr int64_t MAX_GRID_BATCH = 65535;  // grid z extent
-bool one_grid(int64_t batch, int64_t d) { return batch > 1 && batch <= MAX_GRID_BATCH && d != 16; }
+bool one_grid(int64_t batch, int64_t d, int dtype) {
+  return batch > 1 && batch <= MAX_GRID_BATCH && !padded16(d, dtype);
+}
 size_t batched_bytes(bool bwd, int dtype, int64_t batch, int64_t n, int64_t h, int64_t d) {
   const size_t one = whole_plan(bwd, dtype, n, h, d).total;
-  return one_grid(batch, d) ? (size_t)batch * one : one;
+  return one_grid(batch, d, dtype) ? (size_t)batch * one : one;
 }
 // The geometry of a one-launch batch: per-sample strides of the tensors and
 // of the workspace.
@@ -431,10 +440,10 @@ int tri_attn_fwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Whole W = whole_plan(false, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d, dtype));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
-  if (one_grid(batch, d) && workspace_bytes / (size_t)batch >= W.total) {
+  if (one_grid(batch, d, dtype) && workspace_bytes / (size_t)batch >= W.total) {
     const Geom gb = batched_geom(geo, batch, S, mask != nullptr, W.total);
     return dtype == TRIATTN_BF16
                ? fwd_one<triattn::bf16>(node, gb, W, d, q, k, v, g, bias, mask, out, lse,
@@ -474,10 +483,10 @@ int tri_attn_bwd_batched(int node, int dtype, int64_t batch, int64_t n, int64_t 
   const Whole W = whole_plan(true, dtype, n, h, d);
   if (workspace == nullptr || !aligned16(workspace) || workspace_bytes < W.total)
     return TRIATTN_ERR_WORKSPACE;
-  const Geom geo = geom(node, n, n, h, scale, kernel_d(d));
+  const Geom geo = geom(node, n, n, h, scale, kernel_d(d, dtype));
   const BatchStrides S = batch_strides(dtype, n, h, d);
   hipStream_t s = (hipStream_t)stream;
-  if (one_grid(batch, d) && workspace_bytes / (size_t)batch >= W.total) {
+  if (one_grid(batch, d, dtype) && workspace_bytes / (size_t)batch >= W.total) {
     const Geom gb = batched_geom(geo, batch, S, mask != nullptr, W.total);
     return dtype == TRIATTN_BF16
                ? bwd_one<triattn::bf16>(node, gb, W, d, q, k, v, g, bias, mask, out, lse, dout,

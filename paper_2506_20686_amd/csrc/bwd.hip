@@ -38,9 +38,9 @@ constexpr bool kSplitDA = std::is_same<T, bf16>::value;
 
 // ---- elementwise preparation -------------------------------------------------------
 
-// Four threads per (pair, head): thread t handles channels 32 c + 8 (t % 4)
-// .. +7 for c < D / 32, so every load and store is 16 contiguous bytes (bf16)
-// and a wave covers 16 whole (pair, head) rows.  All of a thread's loads are
+// Four threads per (pair, head) (two for D = 16): thread t handles channels
+// 8 TPH c + 8 (t % TPH) .. +7 for c < NC, so every load and store is 16
+// contiguous bytes (bf16) and a wave covers 16 (32) whole (pair, head) rows.  All of a thread's loads are
 // issued before its first store (the compiler may not move loads past stores
 // to memory that could alias them).  Grid: x over the (b, h) entries of one
 // pair row a = blockIdx.y (all index arithmetic in 32 bits but the row
@@ -90,21 +90,23 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
   da = ws_at_sample(da, G.bWs);
   dalo = ws_at_sample(dalo, G.bWs);
   lse2 = ws_at_sample(lse2, G.bWs);
-  constexpr int NC = D / 32;  // 8-channel chunks per thread
+  constexpr int TPH = D == 16 ? 2 : 4;  // threads per (pair, head)
+  constexpr int NC = D / (8 * TPH);     // 8-channel chunks per thread
+  constexpr int CS = 8 * TPH;           // channel stride between a thread's chunks
   const uint32_t tix = blockIdx.x * 256u + threadIdx.x;
-  const uint32_t in_row = tix >> 2;  // b * H + h
+  const uint32_t in_row = tix / TPH;  // b * H + h
   if (in_row >= (uint32_t)(G.n * G.H)) return;
   const int pa = blockIdx.y;
   const int64_t idx = (int64_t)pa * (G.n * G.H) + in_row;  // (a, b, h)
-  const int64_t base = idx * D + 8 * (tix & 3);
+  const int64_t base = idx * D + 8 * (tix % TPH);
   Vec8<T> go[NC], oo[NC], gg[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    go[c] = load8(dout + base + 32 * c);
-    oo[c] = load8(out + base + 32 * c);
-    gg[c] = load8(gate + base + 32 * c);
+    go[c] = load8(dout + base + CS * c);
+    oo[c] = load8(out + base + CS * c);
+    gg[c] = load8(gate + base + CS * c);
   }
-  const float l = (tix & 3) == 0 ? lse[idx] : 0.f;
+  const float l = tix % TPH == 0 ? lse[idx] : 0.f;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     float dgv[8], dav[8], lo[8];
@@ -115,11 +117,11 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(Geom G, int node, const T
       dav[e] = go[c].x[e] * sg;
       lo[e] = dav[e] - (float)(bf16)dav[e];
     }
-    store8(dg + base + 32 * c, dgv);
-    store8(da + base + 32 * c, dav);
-    if constexpr (kSplitDA<T>) store8(dalo + base + 32 * c, lo);
+    store8(dg + base + CS * c, dgv);
+    store8(da + base + CS * c, dav);
+    if constexpr (kSplitDA<T>) store8(dalo + base + CS * c, lo);
   }
-  if ((tix & 3) == 0) {
+  if (tix % TPH == 0) {
     const int b = (int)(in_row / (uint32_t)G.H), h = (int)(in_row - (uint32_t)b * G.H);
     const int row = node == 0 ? pa : b, qi = node == 0 ? b : pa;
     lse2[((int64_t)h * G.nr + row) * G.np + qi] = l == neg_inf() ? pos_inf() : l * LOG2E;
@@ -359,6 +361,8 @@ constexpr int QD_OPS = QD_UNITS / QD_WAVES;             // DMA ops per thread pe
 static_assert(QD_UNITS % QD_WAVES == 0, "DMA units must split evenly over the waves");
 static_assert(QD_SLOTS * QD_SLOT <= 65536, "slot offsets must fit the LDS immediate");
 
+// D = 16 or 32 channels per head (see dma.h for 16).
+template <int D>
 __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4, 4))) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
   to_sample(a);
   using M = Mma<bf16>;
@@ -385,14 +389,14 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   __shared__ __align__(16) char smem[QD_SLOTS * QD_SLOT];
 
   // ---- this lane's query: Q, dA (hi, lo) fragments and lse2
-  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t hb = (int64_t)h * D;
   const int64_t rowbase = (int64_t)r * G.sRow + hb;
   F qf[M::KCH], daf[M::KCH], dalf[M::KCH];
   float l2 = pos_inf();
   if (active && qok) {
-    row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
-    row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
-    row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    row_frags_d<D>(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
+    row_frags_d<D>(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
+    row_frags_d<D>(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
     l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
     zero_frags(qf);
@@ -408,13 +412,14 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   // u % 2 (keys 16 (u % 2) + lane / 4) of tile u / 2 of [K rows, V rows];
   // otherwise quarter v % 4 of bias tile v / 4, v = u - 4 QD_ROWS.  Lane
   // offsets are fixed; the source bases advance by one key tile per issue.
-  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const void* src[QD_OPS];
   const void* srcend[QD_OPS];
   int64_t adv[QD_OPS];  // bytes per tile
   uint32_t voff[QD_OPS];
   char* dst[QD_OPS];
+  bool dok[QD_OPS];  // this lane has a chunk to copy (not: channels 16..31 of a 16-channel head)
 #pragma unroll
   for (int j = 0; j < QD_OPS; ++j) {
     const int u = QD_OPS * wave + j;
@@ -427,6 +432,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
       adv[j] = tstep * 2;
       voff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
       dst[j] = smem + blk * QD_BLK + 1024 * half;
+      dok[j] = chunk_exists<D>(p, lane & 3);
     } else {
       const int v = u - 4 * QD_ROWS, tl = v >> 2, qu = v & 3;
       src[j] = a.bt + ((int64_t)h * nkt + qb * QD_QT + tl) * nkt * 1024;
@@ -434,6 +440,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
       adv[j] = 4096;
       voff[j] = (uint32_t)(1024 * qu + 16 * lane);
       dst[j] = smem + QD_BIAS + tl * 4096 + 1024 * qu;
+      dok[j] = true;
     }
   }
   int issued = 0;
@@ -443,8 +450,9 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
     const bool real = issued < nkt;
 #pragma unroll
     for (int j = 0; j < QD_OPS; ++j) {
-      dma16b(real ? buf_rsrc(src[j], srcend[j]) : buf_rsrc(src[j], src[j]), voff[j],
-             dst[j] + slot * QD_SLOT);
+      if (dok[j])
+        dma16b(real ? buf_rsrc(src[j], srcend[j]) : buf_rsrc(src[j], src[j]), voff[j],
+               dst[j] + slot * QD_SLOT);
       if (issued + 1 < nkt) src[j] = (const char*)src[j] + adv[j];
     }
     ++issued;
@@ -513,8 +521,12 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
         for (int e = 0; e < 4; ++e) sv[4 * j + e] = y[e];
       }
       {
-        const F k0 = lds_load16<F>(rk0 + so + QD_K), k1 = lds_load16<F>(rk1 + so + QD_K);
-        sv = M::mma(k1, qf[1], M::mma(k0, qf[0], sv));
+        const F k0 = lds_load16<F>(rk0 + so + QD_K);
+        sv = M::mma(k0, qf[0], sv);
+        if constexpr (D == 32) {
+          const F k1 = lds_load16<F>(rk1 + so + QD_K);
+          sv = M::mma(k1, qf[1], sv);
+        }
       }
       if (bits != 0xffffffffu) mask_rows(sv, bits, g);
 #pragma unroll
@@ -522,11 +534,12 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
       // dP^T = V dA^T (hi and lo parts), then P dP and its running sum D
       f32x16 dp;
       {
-        const F v0 = lds_load16<F>(rk0 + so + QD_V), v1 = lds_load16<F>(rk1 + so + QD_V);
+        const F v0 = lds_load16<F>(rk0 + so + QD_V);
+        const F v1 = D == 32 ? lds_load16<F>(rk1 + so + QD_V) : F{};
         dp = M::mma(v0, daf[0], f32x16{});
-        dp = M::mma(v1, daf[1], dp);
+        if constexpr (D == 32) dp = M::mma(v1, daf[1], dp);
         dp = M::mma(v0, dalf[0], dp);
-        dp = M::mma(v1, dalf[1], dp);
+        if constexpr (D == 32) dp = M::mma(v1, dalf[1], dp);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -570,7 +583,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   if (g == 0) a.dsum[((int64_t)h * G.nr + r) * G.np + q] = -dsum;  // stored negated
   const int64_t gb = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < D / 8; ++j) {  // the quads of channels 8 j + 4 g .. +3 < D
     f32x4 x;
 #pragma unroll
     for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
@@ -781,6 +794,8 @@ constexpr int KD_BIAS = 3 * KD_SLOTS * KD_TS, KD_BS = 4 * 4096;
 constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
 constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 57 KB at 2 rows, 2 slots
 
+// D = 16 or 32 channels per head (see dma.h for 16).
+template <int D>
 __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a) {
   to_sample(a);
   using M = Mma<bf16>;
@@ -809,12 +824,12 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
 
   // ---- the wave's keys: K and V fragments (zero for invalid keys, so that
   // non-finite values there cannot reach the products)
-  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t hb = (int64_t)h * D;
   const int64_t rowbase = (int64_t)r * G.sRow + hb;
   F kf[M::KCH], vf[M::KCH];
   if (kvalid) {
-    row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
-    row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
+    row_frags_d<D>(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
+    row_frags_d<D>(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
   } else {
     zero_frags(kf);
     zero_frags(vf);
@@ -827,9 +842,10 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   // positions 16 (w % 2) + lane / 4.  Op 1: the low part of dA of row
   // w / 2 (waves 0-7), or lse2 (waves 8-11) / -D (waves 12-15) of row w % 4,
   // 128 bytes (lanes 0..7).  Op 2: bias tile w / 4, quarter w % 4.
-  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const int p16 = 16 * (wave & 1) + (lane >> 2);
   const uint32_t pvoff = (uint32_t)(((int64_t)p16 * G.sPos + hb + 8 * ((lane & 3) ^ swz(p16))) * 2);
+  const bool pok = chunk_exists<D>(p16, lane & 3);  // a chunk to copy for ops 0 and 1 (dA low)
   const int64_t tstep = (int64_t)TILE * G.sPos;  // elements per query tile
   const int orow = (wave % KD_HALF) >> 1;       // op 0 / op 1 (dA low) row
   const bf16* src0 = wave < KD_HALF ? a.q : a.da;
@@ -862,11 +878,14 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     // tiles past the last copy nothing (empty resources) but keep the wait
     // counts uniform
     const bool real = issued < nkt;
-    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff,
-           dst0 + slot * dst0_stride);
-    if (lo_op)
-      dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff,
-             dst1 + slot * dst1_stride);
+    if (pok)
+      dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff,
+             dst0 + slot * dst0_stride);
+    if (lo_op) {
+      if (pok)
+        dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff,
+               dst1 + slot * dst1_stride);
+    }
     else if (lane < 8)
       dma16b(real ? buf_rsrc(pl, plend) : buf_rsrc(pl, pl), lvoff, dst1 + slot * dst1_stride);
     const rsrc_t rbias = real ? buf_rsrc(pb, pbend) : buf_rsrc(pb, pb);
@@ -927,21 +946,27 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
 #pragma unroll
         for (int v = 0; v < 16; ++v) bias[v] += kmask;  // -inf for an invalid key
       }
-      const F q0 = lds_load16<F>(rq0 + so + KD_Q), q1 = lds_load16<F>(rq1 + so + KD_Q);
-      sv = M::mma(q1, kf[1], M::mma(q0, kf[0], bias));
+      const F q0 = lds_load16<F>(rq0 + so + KD_Q);
+      sv = M::mma(q0, kf[0], bias);
+      if constexpr (D == 32) {
+        const F q1 = lds_load16<F>(rq1 + so + KD_Q);
+        sv = M::mma(q1, kf[1], sv);
+      }
     }
     // P = exp2(S c1 - lse2[query])
     const f32x16 l2 = quads(rl + S * KD_LS);
 #pragma unroll
     for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2[v]));
     // dP - D = dA V^T - D (hi and lo parts of dA), then dS = P (dP - D)
-    const F d0 = lds_load16<F>(rq0 + so + KD_DA), d1 = lds_load16<F>(rq1 + so + KD_DA);
-    const F e0 = lds_load16<F>(rq0 + so + KD_LO), e1 = lds_load16<F>(rq1 + so + KD_LO);
+    const F d0 = lds_load16<F>(rq0 + so + KD_DA);
+    const F d1 = D == 32 ? lds_load16<F>(rq1 + so + KD_DA) : F{};
+    const F e0 = lds_load16<F>(rq0 + so + KD_LO);
+    const F e1 = D == 32 ? lds_load16<F>(rq1 + so + KD_LO) : F{};
     f32x16 dp = quads(rl + S * KD_LS + KD_ROWS * 128);  // -D
     dp = M::mma(d0, vf[0], dp);
-    dp = M::mma(d1, vf[1], dp);
+    if constexpr (D == 32) dp = M::mma(d1, vf[1], dp);
     dp = M::mma(e0, vf[0], dp);
-    dp = M::mma(e1, vf[1], dp);
+    if constexpr (D == 32) dp = M::mma(e1, vf[1], dp);
 #pragma unroll
     for (int v = 0; v < 16; ++v) dp[v] *= sv[v];
     // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the tile's queries)
@@ -979,7 +1004,7 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   if (!active || key >= G.n) return;
   const int64_t gb = rowbase + (int64_t)key * G.sPos;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < D / 8; ++j) {  // the quads of channels 8 j + 4 g .. +3 < D
     const int c0 = 8 * j + 4 * g;
     f32x4 x, y;
 #pragma unroll
@@ -1157,6 +1182,8 @@ constexpr int DBD_SLOT = DBD_LD + 1024;
 constexpr int DBD_SLOTS = 3;
 constexpr int DBD_OPS = 3;                    // DMA ops per thread per row
 
+// D = 16 or 32 channels per head (see dma.h for 16).
+template <int D>
 __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
   to_sample(a);
   using M = Mma<bf16>;
@@ -1198,10 +1225,11 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   // or -D (waves 12-15), 128 bytes per wave (lanes 0..7).
   const int r0 = rc * a.rpc, r1 = min(G.nr, r0 + a.rpc);
   const int nr = max(r1 - r0, 0);
-  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
-  const int hb = h * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
+  const int hb = h * D;
   const int pp = 16 * (wave & 7) + (lane >> 2);  // position (key or query) of this lane
   const int pc = (lane & 3) ^ swz(pp);
+  const bool pok = chunk_exists<D>(pp, lane & 3);  // a chunk to copy for the position ops
   const bf16* src0 = wave < 8 ? a.k : a.v;
   const bf16* src1 = wave < 8 ? a.q : a.da;
   // The first key and query of the block move the 64-bit bases (koff, qoff
@@ -1227,13 +1255,16 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
     const bf16* p1 = src1 + rb + qoff;
     const bf16* p2 = a.dalo + rb + qoff;
     const float* pl = lrow + (int64_t)min(r, G.nr - 1) * G.np;
-    dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff,
-           dst0 + slot * DBD_SLOT);
-    dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff,
-           dst1 + slot * DBD_SLOT);
+    if (pok) {
+      dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff,
+             dst0 + slot * DBD_SLOT);
+      dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff,
+             dst1 + slot * DBD_SLOT);
+    }
     if (lo_op) {
-      dma16b(real ? buf_rsrc(p2, a.dalo + tensor) : buf_rsrc(p2, p2), voff2,
-             dst2 + slot * DBD_SLOT);
+      if (pok)
+        dma16b(real ? buf_rsrc(p2, a.dalo + tensor) : buf_rsrc(p2, p2), voff2,
+               dst2 + slot * DBD_SLOT);
     } else if (lane < 8) {
       dma16b(real ? buf_rsrc(pl, pl + G.np) : buf_rsrc(pl, pl), voff2,
              dst2 + slot * DBD_SLOT);
@@ -1280,22 +1311,30 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
     const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT + 512);
     if (!qok) l2 = pos_inf();
     const F q0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OQ);
-    const F q1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OQ);
     const F k0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OK);
-    const F k1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OK);
-    f32x16 sv = M::mma(k1, q1, M::mma(k0, q0, binit));  // S^T = bias + K Q^T
+    f32x16 sv = M::mma(k0, q0, binit);  // S^T = bias + K Q^T
+    if constexpr (D == 32) {
+      const F q1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OQ);
+      const F k1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OK);
+      sv = M::mma(k1, q1, sv);
+    }
     if (wb != 0xffffffffu) mask_rows(sv, wb, g);
     const F d0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_ODA);
-    const F d1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_ODA);
     const F e0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OLO);
-    const F e1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OLO);
     const F v0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OV);
-    const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
     f32x16 dpv = splat16(nd);  // dP^T - D = V dA^T - D (hi and lo parts)
     dpv = M::mma(v0, d0, dpv);
-    dpv = M::mma(v1, d1, dpv);
+    if constexpr (D == 32) {
+      const F d1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_ODA);
+      const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
+      dpv = M::mma(v1, d1, dpv);
+    }
     dpv = M::mma(v0, e0, dpv);
-    dpv = M::mma(v1, e1, dpv);
+    if constexpr (D == 32) {
+      const F e1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OLO);
+      const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
+      dpv = M::mma(v1, e1, dpv);
+    }
 #pragma unroll
     for (int v = 0; v < 16; ++v)
       acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
@@ -1359,12 +1398,18 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   T* da = (T*)ws.da;
   T* dalo = (T*)ws.dalo;
   const bool d64 = g.d == 64;  // register-staged kernels with 64 channels per head
+  const bool d16 = g.d == 16;  // bf16 only: the DMA kernels with 16 channels per head
+  if (d16 && !std::is_same<T, bf16>::value) return hipErrorInvalidValue;
   {
     KernelTimer t(K_BWD_PREP, s);
     const dim3 grid((unsigned)((4 * g.n * g.H + 255) / 256), (unsigned)g.nr, (unsigned)g.batch);
     if (d64)
       hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), grid, dim3(256), 0, s, g, node, out, lse, gate,
                          dout, dg, da, dalo, ws.lse2);
+    else if (d16)  // two threads per (pair, head): half the grid
+      hipLaunchKernelGGL((bwd_prep_kernel<T, 16>),
+                         dim3((unsigned)((2 * g.n * g.H + 255) / 256), (unsigned)g.nr, (unsigned)g.batch),
+                         dim3(256), 0, s, g, node, out, lse, gate, dout, dg, da, dalo, ws.lse2);
     else
       hipLaunchKernelGGL((bwd_prep_kernel<T, 32>), grid, dim3(256), 0, s, g, node, out, lse, gate,
                          dout, dg, da, dalo, ws.lse2);
@@ -1386,7 +1431,10 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
       const int64_t nwg = (int64_t)nqb * ((g.nr + QD_ROWS - 1) / QD_ROWS) * g.H;
-      hipLaunchKernelGGL(dq_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
+      if (d16)
+        hipLaunchKernelGGL(dq_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
+      else
+        hipLaunchKernelGGL(dq_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
     } else {
       hipLaunchKernelGGL((dq_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
@@ -1397,7 +1445,10 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
       hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int64_t nwg = (int64_t)a.nblk * ((g.nr + KD_ROWS - 1) / KD_ROWS) * g.H;
-      hipLaunchKernelGGL(dkdv_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
+      if (d16)
+        hipLaunchKernelGGL(dkdv_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
+      else
+        hipLaunchKernelGGL(dkdv_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
     } else {
       hipLaunchKernelGGL((dkdv_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
@@ -1410,7 +1461,10 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     } else if constexpr (std::is_same<T, bf16>::value) {
       const int nkb = (g.n + DBD_K - 1) / DBD_K;
       const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
-      hipLaunchKernelGGL(db_dma_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
+      if (d16)
+        hipLaunchKernelGGL(db_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
+      else
+        hipLaunchKernelGGL(db_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
     } else {
       hipLaunchKernelGGL((db_kernel<T, 32>), dim3((unsigned)ndb, 1, (unsigned)g.batch), dim3(64 * DB_WAVES), 0, s, a);
     }

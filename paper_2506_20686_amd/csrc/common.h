@@ -92,6 +92,14 @@ __device__ inline void row_frags(const float* p, int g, float (&f)[N]) {
     for (int e = 0; e < 4; ++e) f[4 * i + e] = x[e];
   }
 }
+// bf16 row fragments of a row of D = 16 or 32 channels: slot 1 (channels
+// 16..31) is zero when D = 16 (its products are skipped as well).
+template <int D>
+__device__ inline void row_frags_d(const bf16* p, int g, bf16x8 (&f)[2]) {
+  static_assert(D == 16 || D == 32, "16 or 32 channels");
+  f[0] = *(const bf16x8*)(p + 8 * g);
+  f[1] = D == 32 ? *(const bf16x8*)(p + 16 + 8 * g) : bf16x8{};
+}
 template <typename F, int N>
 __device__ inline void zero_frags(F (&f)[N]) {
 #pragma unroll

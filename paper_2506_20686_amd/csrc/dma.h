@@ -43,6 +43,19 @@ namespace triattn {
 // differ in bit 1.
 __device__ inline int swz(int p) { return ((((p >> 1) ^ (p >> 3)) & 1) << 1) | ((p >> 2) & 1); }
 
+// Heads of 16 channels use the same 64-byte LDS rows: the DMA lanes of
+// chunks 2 and 3 (channels 16..31) stay idle, so those LDS bytes hold
+// whatever was there.  They only ever meet products whose results are
+// dropped: every contraction over channels skips its second 16-channel step,
+// and output rows (channels) 16..31 are never stored.
+//
+// Whether the DMA lane that fills slot s of position p has a chunk to copy.
+template <int D>
+__device__ inline bool chunk_exists(int p, int s) {
+  static_assert(D == 16 || D == 32, "16 or 32 channels");
+  return D == 32 || ((s ^ swz(p)) < 2);
+}
+
 // Byte offset of channels 8 c .. 8 c + 7 of position p in a block.
 __device__ inline int blk_off(int p, int c) { return p * 64 + 16 * (c ^ swz(p)); }
 

@@ -424,6 +424,9 @@ constexpr int FO_BIAS = 2 * FO_ROWS * FO_ROWBLK;    // then the 4 bias tiles (fp
 constexpr int FO_SLOT = FO_BIAS + 4 * 4096;         // 32 KB
 constexpr int FO_SLOTS = 2;
 
+//
+// D = 16 or 32 channels per head (see dma.h for 16).
+template <int D>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void fwd_dma_kernel(FwdArgs<bf16> a) {
   to_sample(a);
@@ -445,7 +448,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
 
   __shared__ __align__(16) char smem[FO_SLOTS * FO_SLOT];
 
-  const int64_t hb = (int64_t)h * HEAD_DIM;
+  const int64_t hb = (int64_t)h * D;
   const int64_t myrow = (int64_t)min(row, last) * G.sRow + hb;
   // query tiles 2 qh + i of the block: lane <-> query
   int qv[FO_QT];
@@ -457,7 +460,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     qv[i] = q0 + l32;
     act[i] = rok && q0 < G.n;
     if (act[i] && qv[i] < G.n)
-      row_frags(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
+      row_frags_d<D>(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
     else
       zero_frags(qf[i]);
   }
@@ -476,15 +479,17 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   // counts uniform.
   const int dblk = wave;  // K0..K3, V0..V3
   const int dp = lane >> 2;
-  const int64_t tensor = (int64_t)G.nr * G.n * G.H * HEAD_DIM;
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const bf16* dsrc = dblk < 4 ? a.k : a.v;
   const bf16* dptr = dsrc + (int64_t)min(r0 + (dblk & 3), last) * G.sRow + hb;
   const bf16* const dend = dsrc + tensor;
   uint32_t dvoff[2];
+  bool dok[2];  // this lane's chunk exists (always for 32 channels)
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int p = 16 * j + dp;
     dvoff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
+    dok[j] = chunk_exists<D>(p, lane & 3);
   }
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const float* bptr = a.bt + ((int64_t)h * nkt + (int64_t)qb * 4) * nkt * 1024;
@@ -501,8 +506,8 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   auto issue = [&](int slot) {
     const bool real = issued < nkt;
     const rsrc_t rk = real ? buf_rsrc(dptr, dend) : buf_rsrc(dptr, dptr);
-    dma16b(rk, dvoff[0], kvdst + slot * FO_SLOT);
-    dma16b(rk, dvoff[1], kvdst + slot * FO_SLOT + 1024);
+    if (dok[0]) dma16b(rk, dvoff[0], kvdst + slot * FO_SLOT);
+    if (dok[1]) dma16b(rk, dvoff[1], kvdst + slot * FO_SLOT + 1024);
     const rsrc_t rb = real ? buf_rsrc(bptr, bend) : buf_rsrc(bptr, bptr);
     dma16b(rb, bvoff0, bdst0 + slot * FO_SLOT);
     dma16b(rb, bvoff1, bdst1 + slot * FO_SLOT);
@@ -574,7 +579,8 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       issue(S ^ 1);  // tile t + 1 into the other slot
       const uint32_t wb = ri == 0 ? wr[0] : ri == 1 ? wr[1] : ri == 2 ? wr[2] : wr[3];
       if (!active || wb == 0u) return;
-      const F k0 = lds_load16<F>(rk0 + S * FO_SLOT), k1 = lds_load16<F>(rk1 + S * FO_SLOT);
+      const F k0 = lds_load16<F>(rk0 + S * FO_SLOT);
+      const F k1 = D == 32 ? lds_load16<F>(rk1 + S * FO_SLOT) : F{};
       f32x16 s[FO_QT];
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
@@ -584,7 +590,8 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
         }
-        s[i] = M::mma(k1, qf[i][1], M::mma(k0, qf[i][0], s[i]));  // S^T = bias + K Q^T
+        s[i] = M::mma(k0, qf[i][0], s[i]);  // S^T = bias + K Q^T
+        if constexpr (D == 32) s[i] = M::mma(k1, qf[i][1], s[i]);
       }
       s16x4 tr[4];
       tr[0] = ds_read_tr<S * FO_SLOT>(rv);
@@ -632,8 +639,12 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
             for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
           }
           {
-            const F k0r = lds_load16<F>(rk0 + S * FO_SLOT), k1r = lds_load16<F>(rk1 + S * FO_SLOT);
-            s[i] = M::mma(k1r, qf[i][1], M::mma(k0r, qf[i][0], s[i]));
+            const F k0r = lds_load16<F>(rk0 + S * FO_SLOT);
+            s[i] = M::mma(k0r, qf[i][0], s[i]);
+            if constexpr (D == 32) {
+              const F k1r = lds_load16<F>(rk1 + S * FO_SLOT);
+              s[i] = M::mma(k1r, qf[i][1], s[i]);
+            }
           }
           if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
           const float mx = wave_xor32_max(max16(s[i])) * c1;
@@ -672,13 +683,14 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   if (!active) return;
   // every gate load is issued before the first store (a store to memory that
   // could alias a later load keeps the compiler from moving the load up)
-  f32x4 gv[FO_QT][4];
+  constexpr int NQ = D / 8;  // accumulator quads holding channels (8 j + 4 g .. +3 < D)
+  f32x4 gv[FO_QT][NQ];
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
     const bool ok = act[i] && qv[i] < G.n;
     const int64_t gbase = myrow + (int64_t)(ok ? qv[i] : 0) * G.sPos;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) gv[i][j] = load4(a.gate + gbase + 8 * j + 4 * g);
+    for (int j = 0; j < NQ; ++j) gv[i][j] = load4(a.gate + gbase + 8 * j + 4 * g);
   }
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
@@ -687,7 +699,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
     const int64_t gbase = myrow + (int64_t)qv[i] * G.sPos;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NQ; ++j) {
       const int c0 = 8 * j + 4 * g;
       f32x4 ov;
 #pragma unroll
@@ -707,13 +719,17 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
                       const T* gate, T* out, float* lse, hipStream_t s) {
   FwdArgs<T> a{g, p.bt, p.kbits, p.rowfull, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
+  if (g.d == 16 && !std::is_same<T, bf16>::value) return hipErrorInvalidValue;  // bf16 only
   if (g.d == 64) {
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
   } else if constexpr (std::is_same<T, bf16>::value) {
     const int64_t nwd = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL(fwd_dma_kernel, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+    if (g.d == 16)
+      hipLaunchKernelGGL(fwd_dma_kernel<16>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL(fwd_dma_kernel<32>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
   } else {
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL((fwd_kernel<T, 32>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);

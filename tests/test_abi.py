@@ -410,8 +410,8 @@ def test_batched_workspace_is_the_unbatched_one(lib):
 
 def test_batched_workspace_sizes(lib):
     """One launch per kernel for a batch needs one unbatched workspace per
-    sample; d = 16 (per-sample padded copies) and a batch of one need the
-    unbatched size; the size calls reject what the batched calls reject."""
+    sample; fp32 d = 16 (per-sample padded copies) and a batch of one need
+    the unbatched size; the size calls reject what the batched calls reject."""
     fns = ((lib.tri_attn_fwd_batched_workspace_bytes, lib.tri_attn_fwd_workspace_bytes),
            (lib.tri_attn_bwd_batched_workspace_bytes, lib.tri_attn_bwd_workspace_bytes))
     for fb, f1 in fns:
@@ -420,8 +420,9 @@ def test_batched_workspace_sizes(lib):
                 for d in (16, 32, 64):
                     st, one = ws_bytes(f1, node, dtype, 37, 3, d)
                     assert st == B.OK
-                    for batch, k in ((1, 1), (4, 1 if d == 16 else 4),
-                                     (65535, 1 if d == 16 else 65535), (65536, 1)):
+                    padded = d == 16 and dtype == B.F32
+                    for batch, k in ((1, 1), (4, 1 if padded else 4),
+                                     (65535, 1 if padded else 65535), (65536, 1)):
                         out = ctypes.c_size_t(0)
                         assert fb(node, dtype, batch, 37, 3, d, ctypes.byref(out)) == B.OK
                         assert out.value == k * one, (node, dtype, d, batch)
@@ -432,19 +433,29 @@ def test_batched_workspace_sizes(lib):
         assert fb(0, B.BF16, 2, 37, 3, 48, ctypes.byref(out)) != B.OK
 
 
-def test_d16_workspace_adds_padded_copies(lib):
-    """d = 16 runs the d = 32 kernels on zero-padded copies kept in the
-    workspace: 5 (forward) and 10 (backward) tensors of [n][n][h][32]."""
-    for dtype, el in ((B.BF16, 2), (B.F32, 4)):
-        for node in (0, 1):
-            n, h = 40, 3
-            pad = -(-n * n * h * 32 * el // 256) * 256
-            for fn, k in ((lib.tri_attn_fwd_workspace_bytes, 5),
-                          (lib.tri_attn_bwd_workspace_bytes, 10)):
-                st, b32 = ws_bytes(fn, node, dtype, n, h, 32)
-                st16, b16 = ws_bytes(fn, node, dtype, n, h, 16)
-                assert st == st16 == B.OK
-                assert b16 == b32 + k * pad
+def test_d16_workspace(lib):
+    """fp32 d = 16 runs the d = 32 kernels on zero-padded copies kept in the
+    workspace: 5 (forward) and 10 (backward) tensors of [n][n][h][32].  bf16
+    d = 16 reads the 16-channel tensors directly: the forward workspace is
+    that of d = 32, the backward's dA buffers (hi and lo) are half as large."""
+    n, h = 40, 3
+    for node in (0, 1):
+        el = 4
+        pad = -(-n * n * h * 32 * el // 256) * 256
+        for fn, k in ((lib.tri_attn_fwd_workspace_bytes, 5),
+                      (lib.tri_attn_bwd_workspace_bytes, 10)):
+            st, b32 = ws_bytes(fn, node, B.F32, n, h, 32)
+            st16, b16 = ws_bytes(fn, node, B.F32, n, h, 16)
+            assert st == st16 == B.OK
+            assert b16 == b32 + k * pad
+        pair32 = -(-n * n * h * 32 * 2 // 256) * 256
+        pair16 = -(-n * n * h * 16 * 2 // 256) * 256
+        st, f32_ = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, n, h, 32)
+        st16, f16 = ws_bytes(lib.tri_attn_fwd_workspace_bytes, node, B.BF16, n, h, 16)
+        assert st == st16 == B.OK and f16 == f32_
+        st, b32 = ws_bytes(lib.tri_attn_bwd_workspace_bytes, node, B.BF16, n, h, 32)
+        st16, b16 = ws_bytes(lib.tri_attn_bwd_workspace_bytes, node, B.BF16, n, h, 16)
+        assert st == st16 == B.OK and b16 == b32 - 2 * (pair32 - pair16)
 
 
 def test_d64_workspace_scales_the_pair_buffers(lib):
