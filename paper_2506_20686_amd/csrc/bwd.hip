@@ -783,23 +783,34 @@ constexpr int KD_HALF = KD_WAVES / 2;              // waves per half of the DMA 
 constexpr int KD_BLK = 32 * 64;                        // 2 KB: 32 positions x 32 channels
 constexpr int KD_SLOTS = KD_SLOTS_CFG;
 constexpr int KD_BOPS = 16 / KD_WAVES;                 // bias DMA ops per wave per tile
-constexpr int KD_OPS = 2 + KD_BOPS;                    // DMA ops per thread per tile
 // LDS regions, each holding its piece of every ring slot (so that slot
 // offsets stay small enough for the immediate field of LDS instructions):
-// Q, dA and dA low [slot][row] tiles, bias [slot][key tile] (4 KB each),
-// lse2 / -D [slot][2][row][32].
-constexpr int KD_TS = KD_ROWS * KD_BLK;                // 4 KB at 2 rows: one slot of a tile region
-constexpr int KD_Q = 0, KD_DA = KD_SLOTS * KD_TS, KD_LO = 2 * KD_SLOTS * KD_TS;
-constexpr int KD_BIAS = 3 * KD_SLOTS * KD_TS, KD_BS = 4 * 4096;
-constexpr int KD_L2 = KD_BIAS + KD_SLOTS * KD_BS, KD_LS = 2 * KD_ROWS * 128;
-constexpr int KD_LDS = KD_L2 + KD_SLOTS * KD_LS;       // 57 KB at 2 rows, 2 slots
+// Q, dA and dA low [slot][channel half][row] tiles, bias [slot][key tile]
+// (4 KB each), lse2 / -D [slot][2][row][32].  A 64-channel head keeps each
+// position as two 32-channel halves, each a block of the usual layout; 16-
+// and 32-channel heads have one.
+template <int D>
+struct KdL {
+  static constexpr int NH = D == 64 ? 2 : 1;         // 32-channel halves per position
+  static constexpr int HT = KD_ROWS * KD_BLK;        // one half's tiles of the rows
+  static constexpr int TS = NH * HT;                 // one slot of a tile region
+  static constexpr int Q = 0, DA = KD_SLOTS * TS, LO = 2 * KD_SLOTS * TS;
+  static constexpr int BIAS = 3 * KD_SLOTS * TS, BS = 4 * 4096;
+  static constexpr int L2 = BIAS + KD_SLOTS * BS, LS = 2 * KD_ROWS * 128;
+  static constexpr int LDS = L2 + KD_SLOTS * LS;     // 57 KB (D <= 32) or 81 KB (D = 64)
+};
 
-// D = 16 or 32 channels per head (see dma.h for 16).
+// D = 16, 32 or 64 channels per head (see dma.h for 16).  At 64 the LDS
+// ring (81 KB) leaves one workgroup per CU, two waves per SIMD.
 template <int D>
 __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a) {
   to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
+  using L = KdL<D>;
+  constexpr int NH = L::NH;
+  constexpr int KC = D == 16 ? 1 : D / 16;     // 16-channel MFMA steps of a contraction over channels
+  constexpr int KA = D == 64 ? 4 : 2;          // fragment slots held per operand row
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int nrg = (G.nr + KD_ROWS - 1) / KD_ROWS;
@@ -820,16 +831,21 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   const bool work = bits != 0u;
   const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) char smem[KD_LDS];
+  __shared__ __align__(16) char smem[L::LDS];
 
   // ---- the wave's keys: K and V fragments (zero for invalid keys, so that
   // non-finite values there cannot reach the products)
   const int64_t hb = (int64_t)h * D;
   const int64_t rowbase = (int64_t)r * G.sRow + hb;
-  F kf[M::KCH], vf[M::KCH];
+  F kf[KA], vf[KA];
   if (kvalid) {
-    row_frags_d<D>(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
-    row_frags_d<D>(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
+    if constexpr (D == 64) {
+      row_frags(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
+      row_frags(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
+    } else {
+      row_frags_d<D>(a.k + rowbase + (int64_t)key * G.sPos, g, kf);
+      row_frags_d<D>(a.v + rowbase + (int64_t)key * G.sPos, g, vf);
+    }
   } else {
     zero_frags(kf);
     zero_frags(vf);
@@ -839,28 +855,28 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
 
   // ---- DMA lanes (lane offsets fixed, bases advanced per tile in scalar
   // registers).  Op 0: Q (waves 0-7) or dA (waves 8-15) of row (w % 8) / 2,
-  // positions 16 (w % 2) + lane / 4.  Op 1: the low part of dA of row
-  // w / 2 (waves 0-7), or lse2 (waves 8-11) / -D (waves 12-15) of row w % 4,
-  // 128 bytes (lanes 0..7).  Op 2: bias tile w / 4, quarter w % 4.
+  // positions 16 (w % 2) + lane / 4, one op per 32-channel half.  Op 1: the
+  // low part of dA of row w / 2 (waves 0-7, per half), or lse2 (waves 8-11)
+  // / -D (waves 12-15) of row w % 4, 128 bytes (lanes 0..7).  Op 2: bias tile
+  // w / 4, quarter w % 4.
   const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const int p16 = 16 * (wave & 1) + (lane >> 2);
   const uint32_t pvoff = (uint32_t)(((int64_t)p16 * G.sPos + hb + 8 * ((lane & 3) ^ swz(p16))) * 2);
-  const bool pok = chunk_exists<D>(p16, lane & 3);  // a chunk to copy for ops 0 and 1 (dA low)
+  const bool pok = chunk_exists<D == 16 ? 16 : 32>(p16, lane & 3);  // a chunk to copy for ops 0 and 1 (dA low)
   const int64_t tstep = (int64_t)TILE * G.sPos;  // elements per query tile
   const int orow = (wave % KD_HALF) >> 1;       // op 0 / op 1 (dA low) row
   const bf16* src0 = wave < KD_HALF ? a.q : a.da;
   const bf16* p0 = src0 + (int64_t)min(r0 + orow, last) * G.sRow;
   const bf16* p1 = a.dalo + (int64_t)min(r0 + orow, last) * G.sRow;
-  char* const dst0 = smem + (wave < KD_HALF ? KD_Q : KD_DA) + orow * KD_BLK + 1024 * (wave & 1);
-  constexpr int dst0_stride = KD_TS;
+  char* const dst0 = smem + (wave < KD_HALF ? L::Q : L::DA) + orow * KD_BLK + 1024 * (wave & 1);
   const bool lo_op = wave < KD_HALF;
   const int lidx = wave - KD_HALF;                 // lse2 rows, then -D rows
   const float* pl = (lidx < KD_ROWS ? a.lse2 : a.dsum) +
                     ((int64_t)h * G.nr + min(r0 + lidx % KD_ROWS, last)) * G.np;
   const float* const plend = pl + G.np;
-  char* const dst1 = lo_op ? smem + KD_LO + orow * KD_BLK + 1024 * (wave & 1)
-                           : smem + KD_L2 + 128 * lidx;
-  const int dst1_stride = lo_op ? KD_TS : KD_LS;
+  char* const dst1 = lo_op ? smem + L::LO + orow * KD_BLK + 1024 * (wave & 1)
+                           : smem + L::L2 + 128 * lidx;
+  const int dst1_stride = lo_op ? L::TS : L::LS;
   const uint32_t lvoff = 16u * (uint32_t)lane;
   // bias op j of wave w: quarter (KD_BOPS w + j) % 4 of key tile (KD_BOPS w + j) / 4
   const float* pb = a.btT + ((int64_t)h * nkt + kbk * 4) * nkt * 1024;
@@ -871,26 +887,30 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   for (int j = 0; j < KD_BOPS; ++j) {
     const int u = KD_BOPS * wave + j, tl = u >> 2;
     bvoff[j] = (uint32_t)(((int64_t)tl * nkt * 1024 + 256 * (u & 3)) * 4 + 16 * lane);
-    dst2[j] = smem + KD_BIAS + tl * 4096 + 1024 * (u & 3);
+    dst2[j] = smem + L::BIAS + tl * 4096 + 1024 * (u & 3);
   }
   int issued = 0;
   auto issue = [&](int slot) {
     // tiles past the last copy nothing (empty resources) but keep the wait
     // counts uniform
     const bool real = issued < nkt;
-    if (pok)
-      dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff,
-             dst0 + slot * dst0_stride);
-    if (lo_op) {
+#pragma unroll
+    for (int c = 0; c < NH; ++c)  // channel half c: 32 channels (64 bytes) further on
       if (pok)
-        dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff,
-               dst1 + slot * dst1_stride);
-    }
-    else if (lane < 8)
+        dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff + 64 * c,
+               dst0 + slot * L::TS + c * L::HT);
+    if (lo_op) {
+#pragma unroll
+      for (int c = 0; c < NH; ++c)
+        if (pok)
+          dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff + 64 * c,
+                 dst1 + slot * dst1_stride + c * L::HT);
+    } else if (lane < 8) {
       dma16b(real ? buf_rsrc(pl, plend) : buf_rsrc(pl, pl), lvoff, dst1 + slot * dst1_stride);
+    }
     const rsrc_t rbias = real ? buf_rsrc(pb, pbend) : buf_rsrc(pb, pb);
 #pragma unroll
-    for (int j = 0; j < KD_BOPS; ++j) dma16b(rbias, bvoff[j], dst2[j] + slot * KD_BS);
+    for (int j = 0; j < KD_BOPS; ++j) dma16b(rbias, bvoff[j], dst2[j] + slot * L::BS);
     if (issued + 1 < nkt) {
       p0 += tstep;
       p1 += tstep;
@@ -900,7 +920,7 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     ++issued;
   };
 
-  // ---- LDS read addresses (slot 0)
+  // ---- LDS read addresses (slot 0, channel half 0)
   const uint32_t base = lds_addr(smem);
   const int sw = swz(l32);
   const uint32_t rq0 = base + ri * KD_BLK + l32 * 64 + 16 * (g ^ sw);
@@ -908,11 +928,11 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   const TrAddr ta(lane);
   const uint32_t rtr = base + ri * KD_BLK + ta.off(0);
   const uint32_t rtr8 = base + ri * KD_BLK + ta.off(8) - 8 * 64;
-  const uint32_t rta = rtr + KD_DA, rta8 = rtr8 + KD_DA;
-  const uint32_t rb = base + KD_BIAS + (wave & 3) * 4096 + lane * 16;
-  const uint32_t rl = base + KD_L2 + ri * 128 + 16 * g;  // + 32 j: lse2 quad j; + 512: -D
+  const uint32_t rta = rtr + L::DA, rta8 = rtr8 + L::DA;
+  const uint32_t rb = base + L::BIAS + (wave & 3) * 4096 + lane * 16;
+  const uint32_t rl = base + L::L2 + ri * 128 + 16 * g;  // + 32 j: lse2 quad j; + 512: -D
 
-  f32x16 dkt = {}, dvt = {};
+  f32x16 dkt[NH] = {}, dvt[NH] = {};
   const float kmask = kvalid ? 0.f : neg_inf();
   auto quads = [&](uint32_t at) {
     f32x16 x;
@@ -924,11 +944,15 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     }
     return x;
   };
+  // row fragment t (channels 16 t + 8 g .. +7) of this wave's row in a tile region
+  auto rfrag = [&](uint32_t region, int t) {
+    return lds_load16<F>((t & 1 ? rq1 : rq0) + (t >> 1) * L::HT + region);
+  };
 
   auto step = [&](auto slot) {
     constexpr int S = decltype(slot)::value;
-    constexpr uint32_t so = S * KD_TS;  // slot offset inside the Q, dA and dA-low regions
-    wait_vm<(KD_SLOTS - 2) * KD_OPS>();  // tile t has landed (tiles after it may be in flight)
+    constexpr uint32_t so = S * L::TS;  // slot offset inside the Q, dA and dA-low regions
+    wait_vm<0>();  // tile t has landed
     lds_barrier();
     issue((S + KD_SLOTS - 1) % KD_SLOTS);  // tile t + KD_SLOTS - 1 into the slot of tile t - 1
     if (!work) return;
@@ -938,7 +962,7 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
       f32x16 bias;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const f32x4 y = lds_load16<f32x4>(rb + S * KD_BS + 1024 * j);
+        const f32x4 y = lds_load16<f32x4>(rb + S * L::BS + 1024 * j);
 #pragma unroll
         for (int e = 0; e < 4; ++e) bias[4 * j + e] = y[e];
       }
@@ -946,49 +970,49 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
 #pragma unroll
         for (int v = 0; v < 16; ++v) bias[v] += kmask;  // -inf for an invalid key
       }
-      const F q0 = lds_load16<F>(rq0 + so + KD_Q);
-      sv = M::mma(q0, kf[0], bias);
-      if constexpr (D == 32) {
-        const F q1 = lds_load16<F>(rq1 + so + KD_Q);
-        sv = M::mma(q1, kf[1], sv);
-      }
+      sv = M::mma(rfrag(so + L::Q, 0), kf[0], bias);
+#pragma unroll
+      for (int t = 1; t < KC; ++t) sv = M::mma(rfrag(so + L::Q, t), kf[t], sv);
     }
     // P = exp2(S c1 - lse2[query])
-    const f32x16 l2 = quads(rl + S * KD_LS);
+    const f32x16 l2 = quads(rl + S * L::LS);
 #pragma unroll
     for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2[v]));
     // dP - D = dA V^T - D (hi and lo parts of dA), then dS = P (dP - D)
-    const F d0 = lds_load16<F>(rq0 + so + KD_DA);
-    const F d1 = D == 32 ? lds_load16<F>(rq1 + so + KD_DA) : F{};
-    const F e0 = lds_load16<F>(rq0 + so + KD_LO);
-    const F e1 = D == 32 ? lds_load16<F>(rq1 + so + KD_LO) : F{};
-    f32x16 dp = quads(rl + S * KD_LS + KD_ROWS * 128);  // -D
-    dp = M::mma(d0, vf[0], dp);
-    if constexpr (D == 32) dp = M::mma(d1, vf[1], dp);
-    dp = M::mma(e0, vf[0], dp);
-    if constexpr (D == 32) dp = M::mma(e1, vf[1], dp);
+    f32x16 dp = quads(rl + S * L::LS + KD_ROWS * 128);  // -D
+#pragma unroll
+    for (int t = 0; t < KC; ++t) dp = M::mma(rfrag(so + L::DA, t), vf[t], dp);
+#pragma unroll
+    for (int t = 0; t < KC; ++t) dp = M::mma(rfrag(so + L::LO, t), vf[t], dp);
 #pragma unroll
     for (int v = 0; v < 16; ++v) dp[v] *= sv[v];
-    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the tile's queries)
-    s16x4 xa[4], xq[4];
-    xa[0] = ds_read_tr<so>(rta);
-    xa[1] = ds_read_tr<so + 8 * 64>(rta8);
-    xa[2] = ds_read_tr<so + 16 * 64>(rta);
-    xa[3] = ds_read_tr<so + 24 * 64>(rta8);
-    xq[0] = ds_read_tr<so + KD_Q>(rtr);
-    xq[1] = ds_read_tr<so + KD_Q + 8 * 64>(rtr8);
-    xq[2] = ds_read_tr<so + KD_Q + 16 * 64>(rtr);
-    xq[3] = ds_read_tr<so + KD_Q + 24 * 64>(rtr8);
+    // dV^T += dA^T P,  dK^T += Q^T dS (contraction over the tile's queries),
+    // one 32-channel half at a time
     F pf[M::PCH], sf[M::PCH];
     acc_frags(sv, pf);
     acc_frags(dp, sf);
-    tr_wait(xa);
-    tr_wait(xq);
+    auto half = [&](auto cc) {
+      constexpr int c = decltype(cc)::value;
+      constexpr uint32_t ho = so + c * L::HT;
+      s16x4 xa[4], xq[4];
+      xa[0] = ds_read_tr<ho>(rta);
+      xa[1] = ds_read_tr<ho + 8 * 64>(rta8);
+      xa[2] = ds_read_tr<ho + 16 * 64>(rta);
+      xa[3] = ds_read_tr<ho + 24 * 64>(rta8);
+      xq[0] = ds_read_tr<ho + L::Q>(rtr);
+      xq[1] = ds_read_tr<ho + L::Q + 8 * 64>(rtr8);
+      xq[2] = ds_read_tr<ho + L::Q + 16 * 64>(rtr);
+      xq[3] = ds_read_tr<ho + L::Q + 24 * 64>(rtr8);
+      tr_wait(xa);
+      tr_wait(xq);
 #pragma unroll
-    for (int u = 0; u < M::PCH; ++u) {
-      dvt = M::mma(tr_frag(xa, u), pf[u], dvt);
-      dkt = M::mma(tr_frag(xq, u), sf[u], dkt);
-    }
+      for (int u = 0; u < M::PCH; ++u) {
+        dvt[c] = M::mma(tr_frag(xa, u), pf[u], dvt[c]);
+        dkt[c] = M::mma(tr_frag(xq, u), sf[u], dkt[c]);
+      }
+    };
+    half(std::integral_constant<int, 0>{});
+    if constexpr (NH == 2) half(std::integral_constant<int, 1>{});
   };
 
 #pragma unroll
@@ -1004,19 +1028,20 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   if (!active || key >= G.n) return;
   const int64_t gb = rowbase + (int64_t)key * G.sPos;
 #pragma unroll
-  for (int j = 0; j < D / 8; ++j) {  // the quads of channels 8 j + 4 g .. +3 < D
-    const int c0 = 8 * j + 4 * g;
-    f32x4 x, y;
+  for (int c = 0; c < NH; ++c)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      x[e] = dvt[4 * j + e];
-      y[e] = dkt[4 * j + e] * G.scale;
+    for (int j = 0; j < (D == 16 ? 2 : 4); ++j) {  // the quads of channels 32 c + 8 j + 4 g .. +3 < D
+      const int c0 = 32 * c + 8 * j + 4 * g;
+      f32x4 x, y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = dvt[c][4 * j + e];
+        y[e] = dkt[c][4 * j + e] * G.scale;
+      }
+      store4(a.dv + gb + c0, x);
+      store4(a.dk + gb + c0, y);
     }
-    store4(a.dv + gb + c0, x);
-    store4(a.dk + gb + c0, y);
-  }
 }
-
 
 // ---- dBias ---------------------------------------------------------------------------
 
@@ -1441,14 +1466,16 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   }
   {
     KernelTimer t(K_DKDV, s);
-    if (d64) {
-      hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
-    } else if constexpr (std::is_same<T, bf16>::value) {
+    if constexpr (std::is_same<T, bf16>::value) {
       const int64_t nwg = (int64_t)a.nblk * ((g.nr + KD_ROWS - 1) / KD_ROWS) * g.H;
-      if (d16)
+      if (d64)
+        hipLaunchKernelGGL(dkdv_dma_kernel<64>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
+      else if (d16)
         hipLaunchKernelGGL(dkdv_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
       else
         hipLaunchKernelGGL(dkdv_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * KD_WAVES), 0, s, a);
+    } else if (d64) {
+      hipLaunchKernelGGL((dkdv_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     } else {
       hipLaunchKernelGGL((dkdv_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
