@@ -41,8 +41,9 @@
  *     d = 64.  bf16 d = 16 runs the 32-channel kernels' 16-channel variants
  *     on the tensors as they are; fp32 d = 16 runs the d = 32 kernels on
  *     zero-padded copies held in the workspace (zero channels add exact
- *     zeros: the results are those of d = 16).  d = 64 runs register-staged
- *     kernels built for 64 channels.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
+ *     zeros: the results are those of d = 16).  bf16 d = 64 runs the DMA
+ *     kernels' 64-channel variants, fp32 d = 64 register-staged kernels built
+ *     for 64 channels.  1 <= n <= 8192, 1 <= h <= 64.  scale must be finite and
  *     positive (1/sqrt(d) is the usual choice).
  *   - The library never allocates or frees memory and never synchronises:
  *     work is enqueued on `stream` (a hipStream_t; NULL is the default stream)

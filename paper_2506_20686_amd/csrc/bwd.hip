@@ -353,20 +353,36 @@ __global__ __launch_bounds__(256, 2) void dq_kernel(BwdArgs<T> a) {
 constexpr int QD_ROWS = QD_ROWS_CFG, QD_QT = QD_QT_CFG, QD_SLOTS = QD_SLOTS_CFG;
 constexpr int QD_WAVES = QD_ROWS * QD_QT;
 constexpr int QD_BLK = 32 * 64;                         // 2 KB: 32 keys x 32 channels
-constexpr int QD_K = 0, QD_V = QD_ROWS * QD_BLK;        // [row] tiles
-constexpr int QD_BIAS = 2 * QD_ROWS * QD_BLK;           // QD_QT query tiles x 4 KB
-constexpr int QD_SLOT = QD_BIAS + QD_QT * 4096;
-constexpr int QD_UNITS = 4 * (QD_ROWS + QD_QT);         // 1 KB DMA units per tile
-constexpr int QD_OPS = QD_UNITS / QD_WAVES;             // DMA ops per thread per tile
-static_assert(QD_UNITS % QD_WAVES == 0, "DMA units must split evenly over the waves");
-static_assert(QD_SLOTS * QD_SLOT <= 65536, "slot offsets must fit the LDS immediate");
-
-// D = 16 or 32 channels per head (see dma.h for 16).
+// Slot layout: K tiles [channel half][row], V tiles [channel half][row], then
+// QD_QT bias tiles (fp32, 4 KB each).  A 64-channel head keeps each position
+// as two 32-channel halves (24 KB slots, two waves per SIMD); 16- and
+// 32-channel heads have one (16 KB slots, four waves per SIMD).
 template <int D>
-__global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4, 4))) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
+struct QdL {
+  static constexpr int NH = D == 64 ? 2 : 1;         // 32-channel halves per position
+  static constexpr int HQ = QD_ROWS * QD_BLK;        // one half's tiles of the rows
+  static constexpr int K = 0, V = NH * HQ;
+  static constexpr int BIAS = 2 * NH * HQ;
+  static constexpr int SLOT = BIAS + QD_QT * 4096;
+  static constexpr int KVU = 4 * QD_ROWS * NH;       // 1 KB K/V DMA units per tile
+  static constexpr int UNITS = KVU + 4 * QD_QT;      // and the bias quarters
+  static constexpr int OPS = UNITS / QD_WAVES;       // DMA ops per thread per tile
+  static constexpr int WPE = D == 64 ? 2 : 4;        // waves per SIMD
+  static_assert(UNITS % QD_WAVES == 0, "DMA units must split evenly over the waves");
+  static_assert(QD_SLOTS * SLOT <= 65536, "slot offsets must fit the LDS immediate");
+};
+
+// D = 16, 32 or 64 channels per head (see dma.h for 16).
+template <int D>
+__global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(QdL<D>::WPE, QdL<D>::WPE))) void dq_dma_kernel(BwdArgs<bf16> a, int nqb) {
   to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
+  using L = QdL<D>;
+  constexpr int NH = L::NH;
+  constexpr int QD_OPS = L::OPS;
+  constexpr int KC = D == 16 ? 1 : D / 16;  // 16-channel MFMA steps of a contraction over channels
+  constexpr int KA = D == 64 ? 4 : 2;       // fragment slots per operand row
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int nrg = (G.nr + QD_ROWS - 1) / QD_ROWS;
@@ -386,17 +402,23 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   const int nrows = min(QD_ROWS, G.nr - r0);  // rows of this group that exist
   const float c1 = G.scale * LOG2E;
 
-  __shared__ __align__(16) char smem[QD_SLOTS * QD_SLOT];
+  __shared__ __align__(16) char smem[QD_SLOTS * L::SLOT];
 
   // ---- this lane's query: Q, dA (hi, lo) fragments and lse2
   const int64_t hb = (int64_t)h * D;
   const int64_t rowbase = (int64_t)r * G.sRow + hb;
-  F qf[M::KCH], daf[M::KCH], dalf[M::KCH];
+  F qf[KA], daf[KA], dalf[KA];
   float l2 = pos_inf();
   if (active && qok) {
-    row_frags_d<D>(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
-    row_frags_d<D>(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
-    row_frags_d<D>(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    if constexpr (D == 64) {
+      row_frags(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
+      row_frags(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
+      row_frags(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    } else {
+      row_frags_d<D>(a.q + rowbase + (int64_t)q * G.sPos, g, qf);
+      row_frags_d<D>(a.da + rowbase + (int64_t)q * G.sPos, g, daf);
+      row_frags_d<D>(a.dalo + rowbase + (int64_t)q * G.sPos, g, dalf);
+    }
     l2 = a.lse2[((int64_t)h * G.nr + r) * G.np + q];
   } else {
     zero_frags(qf);
@@ -408,10 +430,11 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   // the plain register loads above stay in flight with the first DMAs: the
   // first step's full wait (vmcnt 0) precedes every use of their registers
 
-  // ---- DMA lanes.  Unit u = QD_OPS w + j of wave w: u < 4 QD_ROWS: half
-  // u % 2 (keys 16 (u % 2) + lane / 4) of tile u / 2 of [K rows, V rows];
-  // otherwise quarter v % 4 of bias tile v / 4, v = u - 4 QD_ROWS.  Lane
-  // offsets are fixed; the source bases advance by one key tile per issue.
+  // ---- DMA lanes.  Unit u = QD_OPS w + j of wave w: u < KVU: keys
+  // 16 (u % 2) + lane / 4 of tile b = (u / 2) % (2 QD_ROWS) of [K rows, V
+  // rows], channel half (u / 2) / (2 QD_ROWS); otherwise quarter v % 4 of
+  // bias tile v / 4, v = u - KVU.  Lane offsets are fixed; the source bases
+  // advance by one key tile per issue.
   const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const void* src[QD_OPS];
@@ -423,23 +446,24 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
 #pragma unroll
   for (int j = 0; j < QD_OPS; ++j) {
     const int u = QD_OPS * wave + j;
-    if (u < 4 * QD_ROWS) {
-      const int blk = u >> 1, half = u & 1;
+    if (u < L::KVU) {
+      const int blk = (u >> 1) % (2 * QD_ROWS), c = (u >> 1) / (2 * QD_ROWS), half = u & 1;
       const bf16* t = blk < QD_ROWS ? a.k : a.v;
       const int p = 16 * half + (lane >> 2);
       src[j] = t + (int64_t)min(r0 + blk % QD_ROWS, last) * G.sRow + hb;
       srcend[j] = t + tensor;
       adv[j] = tstep * 2;
-      voff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
-      dst[j] = smem + blk * QD_BLK + 1024 * half;
-      dok[j] = chunk_exists<D>(p, lane & 3);
+      voff[j] = (uint32_t)(((int64_t)p * G.sPos + 32 * c + 8 * ((lane & 3) ^ swz(p))) * 2);
+      dst[j] = smem + (blk < QD_ROWS ? L::K : L::V) + c * L::HQ + (blk % QD_ROWS) * QD_BLK +
+               1024 * half;
+      dok[j] = chunk_exists<D == 16 ? 16 : 32>(p, lane & 3);
     } else {
-      const int v = u - 4 * QD_ROWS, tl = v >> 2, qu = v & 3;
+      const int v = u - L::KVU, tl = v >> 2, qu = v & 3;
       src[j] = a.bt + ((int64_t)h * nkt + qb * QD_QT + tl) * nkt * 1024;
       srcend[j] = a.bt + (int64_t)G.H * nkt * nkt * 1024;
       adv[j] = 4096;
       voff[j] = (uint32_t)(1024 * qu + 16 * lane);
-      dst[j] = smem + QD_BIAS + tl * 4096 + 1024 * qu;
+      dst[j] = smem + L::BIAS + tl * 4096 + 1024 * qu;
       dok[j] = true;
     }
   }
@@ -452,7 +476,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
     for (int j = 0; j < QD_OPS; ++j) {
       if (dok[j])
         dma16b(real ? buf_rsrc(src[j], srcend[j]) : buf_rsrc(src[j], src[j]), voff[j],
-               dst[j] + slot * QD_SLOT);
+               dst[j] + slot * L::SLOT);
       if (issued + 1 < nkt) src[j] = (const char*)src[j] + adv[j];
     }
     ++issued;
@@ -464,11 +488,15 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   const uint32_t rk0 = base + ri * QD_BLK + l32 * 64 + 16 * (g ^ sw);
   const uint32_t rk1 = base + ri * QD_BLK + l32 * 64 + 16 * ((2 + g) ^ sw);
   const TrAddr ta(lane);
-  const uint32_t rtr = base + QD_K + ri * QD_BLK + ta.off(0);
-  const uint32_t rtr8 = base + QD_K + ri * QD_BLK + ta.off(8) - 8 * 64;
-  const uint32_t rb = base + QD_BIAS + qtl * 4096 + lane * 16;
+  const uint32_t rtr = base + L::K + ri * QD_BLK + ta.off(0);
+  const uint32_t rtr8 = base + L::K + ri * QD_BLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + L::BIAS + qtl * 4096 + lane * 16;
+  // K (region L::K) or V (L::V) fragment t (channels 16 t + 8 g .. +7) of this wave's row
+  auto rfrag = [&](uint32_t region, int t) {
+    return lds_load16<F>((t & 1 ? rk1 : rk0) + (t >> 1) * L::HQ + region);
+  };
 
-  f32x16 xt = {}, yt = {};
+  f32x16 xt[NH] = {}, yt[NH] = {};
   float dpart = 0.f;
 
   // the loop; FULL: every key of every row of the group is valid
@@ -476,7 +504,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
     constexpr bool FULL = decltype(full_c)::value;
     auto step = [&](int t, auto slot) {
       constexpr int S = decltype(slot)::value;
-      constexpr uint32_t so = S * QD_SLOT;
+      constexpr uint32_t so = S * L::SLOT;
       uint32_t wr[QD_ROWS];  // key bits of tile t per row (0 for a row past the end)
 #pragma unroll
       for (int i = 0; i < QD_ROWS; ++i)
@@ -498,9 +526,11 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
             for (int i = 0; i < QD_ROWS; ++i)
               if ((tid >> 5) == i) wb = wr[i];
             if (!((wb >> (tid & 31)) & 1u)) {
-              char* z = smem + so + QD_V + (tid >> 5) * QD_BLK + 64 * (tid & 31);
+              char* z = smem + so + L::V + (tid >> 5) * QD_BLK + 64 * (tid & 31);
 #pragma unroll
-              for (int e = 0; e < 4; ++e) *(f32x4*)(z + 16 * e) = f32x4{};
+              for (int c = 0; c < NH; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) *(f32x4*)(z + c * L::HQ + 16 * e) = f32x4{};
             }
           }
           __syncthreads();
@@ -520,26 +550,22 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
 #pragma unroll
         for (int e = 0; e < 4; ++e) sv[4 * j + e] = y[e];
       }
-      {
-        const F k0 = lds_load16<F>(rk0 + so + QD_K);
-        sv = M::mma(k0, qf[0], sv);
-        if constexpr (D == 32) {
-          const F k1 = lds_load16<F>(rk1 + so + QD_K);
-          sv = M::mma(k1, qf[1], sv);
-        }
-      }
+#pragma unroll
+      for (int t = 0; t < KC; ++t) sv = M::mma(rfrag(so + L::K, t), qf[t], sv);
       if (bits != 0xffffffffu) mask_rows(sv, bits, g);
 #pragma unroll
       for (int v = 0; v < 16; ++v) sv[v] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2));
       // dP^T = V dA^T (hi and lo parts), then P dP and its running sum D
       f32x16 dp;
       {
-        const F v0 = lds_load16<F>(rk0 + so + QD_V);
-        const F v1 = D == 32 ? lds_load16<F>(rk1 + so + QD_V) : F{};
-        dp = M::mma(v0, daf[0], f32x16{});
-        if constexpr (D == 32) dp = M::mma(v1, daf[1], dp);
-        dp = M::mma(v0, dalf[0], dp);
-        if constexpr (D == 32) dp = M::mma(v1, dalf[1], dp);
+        F vf[KA];
+#pragma unroll
+        for (int t = 0; t < KC; ++t) vf[t] = rfrag(so + L::V, t);
+        dp = M::mma(vf[0], daf[0], f32x16{});
+#pragma unroll
+        for (int t = 1; t < KC; ++t) dp = M::mma(vf[t], daf[t], dp);
+#pragma unroll
+        for (int t = 0; t < KC; ++t) dp = M::mma(vf[t], dalf[t], dp);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -547,20 +573,26 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
         dpart += dp[v];
       }
       // X^T += K^T (P dP)^T,  Y^T += K^T P^T (contraction over the tile's keys)
-      s16x4 xk[4];
-      xk[0] = ds_read_tr<so>(rtr);
-      xk[1] = ds_read_tr<so + 8 * 64>(rtr8);
-      xk[2] = ds_read_tr<so + 16 * 64>(rtr);
-      xk[3] = ds_read_tr<so + 24 * 64>(rtr8);
       F pf[M::PCH], xf[M::PCH];
       acc_frags(dp, xf);
       acc_frags(sv, pf);
-      tr_wait(xk);
+      auto half = [&](auto cc) {  // K^T fragments of channel half c
+        constexpr int c = decltype(cc)::value;
+        constexpr uint32_t ho = so + c * L::HQ;
+        s16x4 xk[4];
+        xk[0] = ds_read_tr<ho>(rtr);
+        xk[1] = ds_read_tr<ho + 8 * 64>(rtr8);
+        xk[2] = ds_read_tr<ho + 16 * 64>(rtr);
+        xk[3] = ds_read_tr<ho + 24 * 64>(rtr8);
+        tr_wait(xk);
 #pragma unroll
-      for (int u = 0; u < M::PCH; ++u) {
-        xt = M::mma(tr_frag(xk, u), xf[u], xt);
-        yt = M::mma(tr_frag(xk, u), pf[u], yt);
-      }
+        for (int u = 0; u < M::PCH; ++u) {
+          xt[c] = M::mma(tr_frag(xk, u), xf[u], xt[c]);
+          yt[c] = M::mma(tr_frag(xk, u), pf[u], yt[c]);
+        }
+      };
+      half(std::integral_constant<int, 0>{});
+      if constexpr (NH == 2) half(std::integral_constant<int, 1>{});
     };
 #pragma unroll
     for (int j = 0; j < QD_SLOTS - 1; ++j) issue(j);
@@ -583,12 +615,14 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(4
   if (g == 0) a.dsum[((int64_t)h * G.nr + r) * G.np + q] = -dsum;  // stored negated
   const int64_t gb = rowbase + (int64_t)q * G.sPos;
 #pragma unroll
-  for (int j = 0; j < D / 8; ++j) {  // the quads of channels 8 j + 4 g .. +3 < D
-    f32x4 x;
+  for (int c = 0; c < NH; ++c)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = (xt[4 * j + e] - dsum * yt[4 * j + e]) * G.scale;
-    store4(a.dq + gb + 8 * j + 4 * g, x);
-  }
+    for (int j = 0; j < (D == 16 ? 2 : 4); ++j) {  // the quads of channels 32 c + 8 j + 4 g .. +3 < D
+      f32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = (xt[c][4 * j + e] - dsum * yt[c][4 * j + e]) * G.scale;
+      store4(a.dq + gb + 32 * c + 8 * j + 4 * g, x);
+    }
 }
 
 
@@ -1387,6 +1421,192 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   }
 }
 
+// bf16 dB for 64 channels per head.  A position's 128 bytes are staged as
+// two 32-channel half-rows (the usual 64-byte block layout each), so a
+// 128 x 128 block's row (80 KB) would leave no room for a second ring slot;
+// the block is 64 queries x 128 keys instead: 8 waves, wave w owns query
+// tile w % 2 and key tile w / 2, one workgroup per CU (two waves per SIMD).
+// Per row, K and V of the 128 keys, Q, dA and its low part of the 64
+// queries, lse2 and -D (56.5 KB) land in LDS by DMA through a two-slot ring,
+// one row ahead.  LDS is laid out by region, each holding both slots, so
+// that slot offsets stay small.
+constexpr int D6_Q = 64, D6_K = 128, D6_WAVES = 8;
+constexpr int D6_KH = D6_K * 64;                 // one channel half of the block's K (or V): 8 KB
+constexpr int D6_QH = D6_Q * 64;                 // one channel half of its Q (dA, dA low): 4 KB
+constexpr int D6_OK = 0, D6_OV = 2 * 2 * D6_KH;  // [slot][half] regions
+constexpr int D6_OQ = 2 * D6_OV, D6_ODA = D6_OQ + 2 * 2 * D6_QH, D6_OLO = D6_ODA + 2 * 2 * D6_QH;
+constexpr int D6_OL = D6_OLO + 2 * 2 * D6_QH;    // [slot]: lse2 [64], then -D [64]
+constexpr int D6_LDS = D6_OL + 2 * 512;
+
+__global__ __launch_bounds__(64 * D6_WAVES) void db_dma64_kernel(BwdArgs<bf16> a, int nkb) {
+  to_sample(a);
+  using M = Mma<bf16>;
+  using F = bf16x8;
+  constexpr int D = 64;
+  const Geom& G = a.g;
+  const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int nqb = (G.n + D6_Q - 1) / D6_Q;
+  const int kbk = w % nkb;
+  const int qb = (w / nkb) % nqb;
+  const int rc = (w / (nkb * nqb)) % a.nrc;
+  const int h = w / (nkb * nqb * a.nrc);
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qtl = wave & 1, ktl = wave >> 1;
+  const int qstart = qb * D6_Q, kstart = kbk * D6_K;
+  const int q = qstart + qtl * TILE + l32;  // this lane's query
+  const int kt = kstart / TILE + ktl;       // this wave's key tile
+  const bool active = qstart + qtl * TILE < G.n && kt < G.nkt;
+  const bool qok = q < G.n;
+  const int nkt = G.nkt;
+  const float c1 = G.scale * LOG2E;
+
+  __shared__ __align__(16) char smem[D6_LDS];
+
+  f32x16 binit, acc = {};
+  {
+    const int qt = active ? qstart / TILE + qtl : 0;
+    binit = load_frag_tile(frag_tile(a.bt, h, qt, min(kt, nkt - 1), nkt), lane);
+  }
+  // the bias tile is a plain register load: let it complete before any DMA
+  // is issued
+  wait_vm<0>();
+
+  // ---- DMA lanes (lane offsets fixed, row bases in scalar registers).
+  // K, V: keys 16 w + lane / 4 of the block, both channel halves (2 ops
+  // each).  Q, dA, dA low: queries 16 (w % 4) + lane / 4, channel half w / 4
+  // (1 op each).  lse2 (waves 0, 1) or -D (waves 2, 3): queries
+  // 32 (w % 2) .. +31, 128 bytes (lanes 0..7).
+  const int r0 = rc * a.rpc, r1 = min(G.nr, r0 + a.rpc);
+  const int nr = max(r1 - r0, 0);
+  const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
+  const int hb = h * D;
+  const int pk = 16 * wave + (lane >> 2);        // key position of this lane
+  const int pq = 16 * (wave & 3) + (lane >> 2);  // query position of this lane
+  const int cq = wave >> 2;                      // channel half of the Q, dA, dA-low ops
+  // The first key and query of the block move the 64-bit bases, so a lane's
+  // byte offset stays below 2^32 for every accepted size.
+  const int64_t koff = (int64_t)kstart * G.sPos, qoff = (int64_t)qstart * G.sPos;
+  const uint32_t kvoff = (uint32_t)(((int64_t)pk * G.sPos + hb + 8 * ((lane & 3) ^ swz(pk))) * 2);
+  const uint32_t qvoff =
+      (uint32_t)(((int64_t)pq * G.sPos + hb + 32 * cq + 8 * ((lane & 3) ^ swz(pq))) * 2);
+  const bool l_op = wave < 4;
+  const float* lrow = (wave < 2 ? a.lse2 : a.dsum) + (int64_t)h * G.nr * G.np;
+  const uint32_t lvoff = (uint32_t)((qstart + 32 * (wave & 1) + 4 * lane) * 4);
+  char* const dK = smem + D6_OK + 1024 * wave;  // + slot 2 D6_KH + half D6_KH
+  char* const dV = smem + D6_OV + 1024 * wave;
+  const int qo = cq * D6_QH + 1024 * (wave & 3);  // + slot 2 D6_QH
+  char* const dL = smem + D6_OL + 128 * wave;     // + slot 512
+  auto issue = [&](int r, int slot) {
+    // rows past the chunk copy nothing (empty resources) but keep the wait
+    // counts uniform
+    const bool real = r < r1;
+    const int64_t rb = (int64_t)min(r, G.nr - 1) * G.sRow;
+    const bf16* pkk = a.k + rb + koff;
+    const bf16* pvv = a.v + rb + koff;
+    const bf16* pqq = a.q + rb + qoff;
+    const bf16* paa = a.da + rb + qoff;
+    const bf16* pll = a.dalo + rb + qoff;
+    const float* p5 = lrow + (int64_t)min(r, G.nr - 1) * G.np;
+    const rsrc_t rk = real ? buf_rsrc(pkk, a.k + tensor) : buf_rsrc(pkk, pkk);
+    const rsrc_t rv = real ? buf_rsrc(pvv, a.v + tensor) : buf_rsrc(pvv, pvv);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      dma16b(rk, kvoff + 64 * c, dK + (2 * slot + c) * D6_KH);
+      dma16b(rv, kvoff + 64 * c, dV + (2 * slot + c) * D6_KH);
+    }
+    dma16b(real ? buf_rsrc(pqq, a.q + tensor) : buf_rsrc(pqq, pqq), qvoff,
+           smem + D6_OQ + 2 * slot * D6_QH + qo);
+    dma16b(real ? buf_rsrc(paa, a.da + tensor) : buf_rsrc(paa, paa), qvoff,
+           smem + D6_ODA + 2 * slot * D6_QH + qo);
+    dma16b(real ? buf_rsrc(pll, a.dalo + tensor) : buf_rsrc(pll, pll), qvoff,
+           smem + D6_OLO + 2 * slot * D6_QH + qo);
+    if (l_op && lane < 8)
+      dma16b(real ? buf_rsrc(p5, p5 + G.np) : buf_rsrc(p5, p5), lvoff, dL + 512 * slot);
+  };
+
+  // ---- LDS read addresses (slot 0, channel half 0)
+  const uint32_t base = lds_addr(smem);
+  const int sw = swz(l32);
+  const uint32_t qpos = base + (uint32_t)(qtl * TILE + l32) * 64;
+  const uint32_t rq0 = qpos + 16 * (g ^ sw), rq1 = qpos + 16 * ((2 + g) ^ sw);
+  const uint32_t kpos = base + (uint32_t)(ktl * TILE + l32) * 64;
+  const uint32_t rk0 = kpos + 16 * (g ^ sw), rk1 = kpos + 16 * ((2 + g) ^ sw);
+  const uint32_t rl = base + D6_OL + (qtl * TILE + l32) * 4;
+  const uint32_t* kbrow = a.kbits + kstart / TILE;
+  // fragment t (channels 16 t + 8 g .. +7) of this lane's query (q) or key (k) row
+  auto qfrag = [&](uint32_t region, int t) {
+    return lds_load16<F>((t & 1 ? rq1 : rq0) + (t >> 1) * D6_QH + region);
+  };
+  auto kfrag = [&](uint32_t region, int t) {
+    return lds_load16<F>((t & 1 ? rk1 : rk0) + (t >> 1) * D6_KH + region);
+  };
+
+  auto step = [&](int r, auto slot) {
+    constexpr int S = decltype(slot)::value;
+    const uint32_t wb = kt < nkt ? const_load(kbrow + (int64_t)r * nkt + ktl) : 0u;
+    wait_vm<0>();  // row r has landed
+    lds_barrier();
+    {
+      // key bits of the block's 4 tiles: the same in every wave, so the
+      // branch below (it holds a barrier) is uniform across the workgroup
+      uint32_t all = 0xffffffffu;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        all &= kstart / TILE + j < nkt ? const_load(kbrow + (int64_t)r * nkt + j) : 0xffffffffu;
+      if (all != 0xffffffffu) {
+        // zero V rows of keys invalid for the row (P = 0 there, and 0 times
+        // a non-finite dP would not be); thread t: key t / 4, 16 bytes of
+        // each channel half
+        const int j = tid >> 7;
+        const uint32_t b = kstart / TILE + j < nkt ? const_load(kbrow + (int64_t)r * nkt + j) : 0u;
+        if (!((b >> ((tid >> 2) & 31)) & 1u)) {
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+            *(f32x4*)(smem + D6_OV + (2 * S + c) * D6_KH + 16 * tid) = f32x4{};
+        }
+        __syncthreads();
+      }
+    }
+    issue(r + 1, S ^ 1);  // row r + 1 into the slot of row r - 1
+    if (!active || wb == 0u) return;
+    constexpr uint32_t ks = 2 * S * D6_KH, qs = 2 * S * D6_QH;
+    float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + 512 * S);
+    const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + 512 * S + 256);
+    if (!qok) l2 = pos_inf();
+    f32x16 sv = binit;  // S^T = bias + K Q^T
+#pragma unroll
+    for (int t = 0; t < 4; ++t) sv = M::mma(kfrag(D6_OK + ks, t), qfrag(D6_OQ + qs, t), sv);
+    if (wb != 0xffffffffu) mask_rows(sv, wb, g);
+    f32x16 dpv = splat16(nd);  // dP^T - D = V dA^T - D (hi and lo parts)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) dpv = M::mma(kfrag(D6_OV + ks, t), qfrag(D6_ODA + qs, t), dpv);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) dpv = M::mma(kfrag(D6_OV + ks, t), qfrag(D6_OLO + qs, t), dpv);
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
+  };
+
+  issue(r0, 0);
+  for (int i = 0; i < nr; i += 2) {
+    step(r0 + i, slot_c<0>{});
+    if (i + 1 >= nr) break;
+    step(r0 + i + 1, slot_c<1>{});
+  }
+  wait_vm<0>();  // the copies past the end must land before the workgroup ends
+  if (!active) return;
+  float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + qstart + qtl * TILE + l32) * G.np +
+                kt * TILE + 4 * g;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    f32x4 x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = acc[4 * j + e];
+    *(f32x4*)(slab + 8 * j) = x;
+  }
+}
+
 
 // dbias at (query q, key k, head h) = sum of the slabs in chunk order; the
 // starting node stores it at [q][k][h], the ending node at [k][q][h].  One
@@ -1451,15 +1671,17 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     // the dQ kernel first: it produces D for the other two
     KernelTimer t(K_DQ, s);
-    if (d64) {
-      hipLaunchKernelGGL((dq_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
-    } else if constexpr (std::is_same<T, bf16>::value) {
+    if constexpr (std::is_same<T, bf16>::value) {
       const int nqb = (g.n + 32 * QD_QT - 1) / (32 * QD_QT);
       const int64_t nwg = (int64_t)nqb * ((g.nr + QD_ROWS - 1) / QD_ROWS) * g.H;
-      if (d16)
+      if (d64)
+        hipLaunchKernelGGL(dq_dma_kernel<64>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
+      else if (d16)
         hipLaunchKernelGGL(dq_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
       else
         hipLaunchKernelGGL(dq_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * QD_WAVES), 0, s, a, nqb);
+    } else if (d64) {
+      hipLaunchKernelGGL((dq_kernel<T, 64>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     } else {
       hipLaunchKernelGGL((dq_kernel<T, 32>), dim3((unsigned)nrow, 1, (unsigned)g.batch), dim3(256), 0, s, a);
     }
@@ -1483,15 +1705,21 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   {
     const int64_t ndb = (int64_t)a.nblk * a.nblk * ws.nrc * g.H;
     KernelTimer t(K_DB, s);
-    if (d64) {
+    if constexpr (std::is_same<T, bf16>::value) {
+      if (d64) {
+        const int nkb = (g.n + D6_K - 1) / D6_K;
+        const int64_t nwg = (int64_t)((g.n + D6_Q - 1) / D6_Q) * nkb * ws.nrc * g.H;
+        hipLaunchKernelGGL(db_dma64_kernel, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * D6_WAVES), 0, s, a, nkb);
+      } else {
+        const int nkb = (g.n + DBD_K - 1) / DBD_K;
+        const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
+        if (d16)
+          hipLaunchKernelGGL(db_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
+        else
+          hipLaunchKernelGGL(db_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
+      }
+    } else if (d64) {
       hipLaunchKernelGGL((db_kernel<T, 64>), dim3((unsigned)ndb, 1, (unsigned)g.batch), dim3(64 * DB_WAVES), 0, s, a);
-    } else if constexpr (std::is_same<T, bf16>::value) {
-      const int nkb = (g.n + DBD_K - 1) / DBD_K;
-      const int64_t nwg = (int64_t)((g.n + DBD_Q - 1) / DBD_Q) * nkb * ws.nrc * g.H;
-      if (d16)
-        hipLaunchKernelGGL(db_dma_kernel<16>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
-      else
-        hipLaunchKernelGGL(db_dma_kernel<32>, dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(64 * DBD_WAVES), 0, s, a, nkb);
     } else {
       hipLaunchKernelGGL((db_kernel<T, 32>), dim3((unsigned)ndb, 1, (unsigned)g.batch), dim3(64 * DB_WAVES), 0, s, a);
     }

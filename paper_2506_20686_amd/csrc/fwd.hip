@@ -419,19 +419,34 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
 constexpr int FO_ROWS = 4;
 constexpr int FO_QT = 2;                            // query tiles per wave
 constexpr int FO_ROWBLK = 32 * 64;                  // one row's K (or V) tile: 32 keys x 64 B
-constexpr int FO_V0 = FO_ROWS * FO_ROWBLK;          // V tiles follow the K tiles
-constexpr int FO_BIAS = 2 * FO_ROWS * FO_ROWBLK;    // then the 4 bias tiles (fp32, 4 KB each)
-constexpr int FO_SLOT = FO_BIAS + 4 * 4096;         // 32 KB
 constexpr int FO_SLOTS = 2;
+// Slot layout: K tiles [channel half][row], V tiles [channel half][row], then
+// the 4 bias tiles (fp32, 4 KB each).  A 64-channel head keeps each position
+// as two 32-channel halves, each a block of the usual layout: 48 KB slots,
+// one workgroup per CU and two waves per SIMD; 16- and 32-channel heads have
+// one half: 32 KB slots, four waves per SIMD.
+template <int D>
+struct FoL {
+  static constexpr int NH = D == 64 ? 2 : 1;       // 32-channel halves per position
+  static constexpr int HB = FO_ROWS * FO_ROWBLK;   // one half's K (or V) tiles of the rows
+  static constexpr int V0 = NH * HB;               // V tiles follow the K tiles
+  static constexpr int BIAS = 2 * NH * HB;
+  static constexpr int SLOT = BIAS + 4 * 4096;
+  static constexpr int WPE = D == 64 ? 2 : 4;      // waves per SIMD
+};
 
 //
-// D = 16 or 32 channels per head (see dma.h for 16).
+// D = 16, 32 or 64 channels per head (see dma.h for 16).
 template <int D>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(FoL<D>::WPE, FoL<D>::WPE)))
 void fwd_dma_kernel(FwdArgs<bf16> a) {
   to_sample(a);
   using M = Mma<bf16>;
   using F = bf16x8;
+  using L = FoL<D>;
+  constexpr int NH = L::NH;
+  constexpr int KC = D == 16 ? 1 : D / 16;  // 16-channel MFMA steps of a contraction over channels
+  constexpr int KA = D == 64 ? 4 : 2;       // fragment slots per operand row
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
   const int nrg = (G.nr + FO_ROWS - 1) / FO_ROWS;
@@ -446,23 +461,27 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const float c1 = G.scale * LOG2E;
   const int nrows = min(FO_ROWS, G.nr - r0);  // rows of this group that exist
 
-  __shared__ __align__(16) char smem[FO_SLOTS * FO_SLOT];
+  __shared__ __align__(16) char smem[FO_SLOTS * L::SLOT];
 
   const int64_t hb = (int64_t)h * D;
   const int64_t myrow = (int64_t)min(row, last) * G.sRow + hb;
   // query tiles 2 qh + i of the block: lane <-> query
   int qv[FO_QT];
   bool act[FO_QT];
-  F qf[FO_QT][M::KCH];
+  F qf[FO_QT][KA];
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
     const int q0 = qb * FWD_QBLK + (FO_QT * qh + i) * TILE;
     qv[i] = q0 + l32;
     act[i] = rok && q0 < G.n;
-    if (act[i] && qv[i] < G.n)
-      row_frags_d<D>(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
-    else
+    if (act[i] && qv[i] < G.n) {
+      if constexpr (D == 64)
+        row_frags(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
+      else
+        row_frags_d<D>(a.q + myrow + (int64_t)qv[i] * G.sPos, g, qf[i]);
+    } else {
       zero_frags(qf[i]);
+    }
   }
   const bool active = act[0];  // tile 1 active implies tile 0 active
   bool rows_full = true;
@@ -489,7 +508,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   for (int j = 0; j < 2; ++j) {
     const int p = 16 * j + dp;
     dvoff[j] = (uint32_t)(((int64_t)p * G.sPos + 8 * ((lane & 3) ^ swz(p))) * 2);
-    dok[j] = chunk_exists<D>(p, lane & 3);
+    dok[j] = chunk_exists<D == 16 ? 16 : 32>(p, lane & 3);
   }
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const float* bptr = a.bt + ((int64_t)h * nkt + (int64_t)qb * 4) * nkt * 1024;
@@ -499,18 +518,21 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       (uint32_t)(((int64_t)bt0 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
   const uint32_t bvoff1 =
       (uint32_t)(((int64_t)bt1 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
-  char* const kvdst = smem + dblk * FO_ROWBLK;
-  char* const bdst0 = smem + FO_BIAS + bt0 * 4096 + 1024 * (wave & 3);
-  char* const bdst1 = smem + FO_BIAS + bt1 * 4096 + 1024 * (wave & 3);
+  char* const kvdst = smem + (dblk < 4 ? 0 : L::V0) + (dblk & 3) * FO_ROWBLK;
+  char* const bdst0 = smem + L::BIAS + bt0 * 4096 + 1024 * (wave & 3);
+  char* const bdst1 = smem + L::BIAS + bt1 * 4096 + 1024 * (wave & 3);
   int issued = 0;
   auto issue = [&](int slot) {
     const bool real = issued < nkt;
     const rsrc_t rk = real ? buf_rsrc(dptr, dend) : buf_rsrc(dptr, dptr);
-    if (dok[0]) dma16b(rk, dvoff[0], kvdst + slot * FO_SLOT);
-    if (dok[1]) dma16b(rk, dvoff[1], kvdst + slot * FO_SLOT + 1024);
+#pragma unroll
+    for (int c = 0; c < NH; ++c) {  // channel half c: 32 channels (64 bytes) further on
+      if (dok[0]) dma16b(rk, dvoff[0] + 64 * c, kvdst + slot * L::SLOT + c * L::HB);
+      if (dok[1]) dma16b(rk, dvoff[1] + 64 * c, kvdst + slot * L::SLOT + c * L::HB + 1024);
+    }
     const rsrc_t rb = real ? buf_rsrc(bptr, bend) : buf_rsrc(bptr, bptr);
-    dma16b(rb, bvoff0, bdst0 + slot * FO_SLOT);
-    dma16b(rb, bvoff1, bdst1 + slot * FO_SLOT);
+    dma16b(rb, bvoff0, bdst0 + slot * L::SLOT);
+    dma16b(rb, bvoff1, bdst1 + slot * L::SLOT);
     if (issued + 1 < nkt) {
       dptr += tstep;
       bptr += 1024;
@@ -524,17 +546,22 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const uint32_t rk0 = base + ri * FO_ROWBLK + l32 * 64 + 16 * (g ^ sw);
   const uint32_t rk1 = base + ri * FO_ROWBLK + l32 * 64 + 16 * ((2 + g) ^ sw);
   const TrAddr ta(lane);
-  const uint32_t rv = base + FO_V0 + ri * FO_ROWBLK + ta.off(0);
-  const uint32_t rv8 = base + FO_V0 + ri * FO_ROWBLK + ta.off(8) - 8 * 64;
-  const uint32_t rb = base + FO_BIAS + FO_QT * qh * 4096 + lane * 16;
+  const uint32_t rv = base + L::V0 + ri * FO_ROWBLK + ta.off(0);
+  const uint32_t rv8 = base + L::V0 + ri * FO_ROWBLK + ta.off(8) - 8 * 64;
+  const uint32_t rb = base + L::BIAS + FO_QT * qh * 4096 + lane * 16;
+  // K fragment t (channels 16 t + 8 g .. +7) of this wave's row in slot S
+  auto kfrag = [&](uint32_t so, int t) {
+    return lds_load16<F>((t & 1 ? rk1 : rk0) + (t >> 1) * L::HB + so);
+  };
 
   float m[FO_QT];
-  f32x16 o[FO_QT];
+  f32x16 o[FO_QT][NH];
   float ls0[FO_QT], ls1[FO_QT];  // this lane's share of sum_k P (its 16 keys of each tile)
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
     m[i] = M_FLOOR;
-    o[i] = f32x16{};
+#pragma unroll
+    for (int c = 0; c < NH; ++c) o[i][c] = f32x16{};
     ls0[i] = ls1[i] = 0.f;
   }
   const bf16x2 one2 = {(bf16)1.f, (bf16)1.f};
@@ -547,9 +574,11 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       const int rr = tid >> 5;
       const uint32_t wb = rr == 0 ? wr[0] : rr == 1 ? wr[1] : rr == 2 ? wr[2] : wr[3];
       if (!((wb >> (tid & 31)) & 1u)) {
-        char* z = smem + S * FO_SLOT + FO_V0 + rr * FO_ROWBLK + 64 * (tid & 31);
+        char* z = smem + S * L::SLOT + L::V0 + rr * FO_ROWBLK + 64 * (tid & 31);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) *(f32x4*)(z + 16 * e) = f32x4{};
+        for (int c = 0; c < NH; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) *(f32x4*)(z + c * L::HB + 16 * e) = f32x4{};
       }
     }
   };
@@ -579,25 +608,32 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       issue(S ^ 1);  // tile t + 1 into the other slot
       const uint32_t wb = ri == 0 ? wr[0] : ri == 1 ? wr[1] : ri == 2 ? wr[2] : wr[3];
       if (!active || wb == 0u) return;
-      const F k0 = lds_load16<F>(rk0 + S * FO_SLOT);
-      const F k1 = D == 32 ? lds_load16<F>(rk1 + S * FO_SLOT) : F{};
+      F kfr[KA];
+#pragma unroll
+      for (int t = 0; t < KC; ++t) kfr[t] = kfrag(S * L::SLOT, t);
       f32x16 s[FO_QT];
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const f32x4 y = lds_load16<f32x4>(rb + S * FO_SLOT + i * 4096 + 1024 * j);
+          const f32x4 y = lds_load16<f32x4>(rb + S * L::SLOT + i * 4096 + 1024 * j);
 #pragma unroll
           for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
         }
-        s[i] = M::mma(k0, qf[i][0], s[i]);  // S^T = bias + K Q^T
-        if constexpr (D == 32) s[i] = M::mma(k1, qf[i][1], s[i]);
+#pragma unroll
+        for (int t = 0; t < KC; ++t) s[i] = M::mma(kfr[t], qf[i][t], s[i]);  // S^T = bias + K Q^T
       }
-      s16x4 tr[4];
-      tr[0] = ds_read_tr<S * FO_SLOT>(rv);
-      tr[1] = ds_read_tr<S * FO_SLOT + 8 * 64>(rv8);
-      tr[2] = ds_read_tr<S * FO_SLOT + 16 * 64>(rv);
-      tr[3] = ds_read_tr<S * FO_SLOT + 24 * 64>(rv8);
+      s16x4 tr[NH][4];
+      auto trread = [&](auto cc) {  // V^T fragments of channel half c
+        constexpr int c = decltype(cc)::value;
+        constexpr uint32_t ho = S * L::SLOT + c * L::HB;
+        tr[c][0] = ds_read_tr<ho>(rv);
+        tr[c][1] = ds_read_tr<ho + 8 * 64>(rv8);
+        tr[c][2] = ds_read_tr<ho + 16 * 64>(rv);
+        tr[c][3] = ds_read_tr<ho + 24 * 64>(rv8);
+      };
+      trread(std::integral_constant<int, 0>{});
+      if constexpr (NH == 2) trread(std::integral_constant<int, 1>{});
       // P = exp2(S c1 - m) against the running max m as it stands (in place of
       // S), and the tile's row sums of the bf16 P the MFMA uses (dot products
       // with (1, 1)).  The max is not formed per tile: a tile whose weights
@@ -634,18 +670,12 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
           // the tile's logits again (bias and K from the slot, Q at hand)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const f32x4 y = lds_load16<f32x4>(rb + S * FO_SLOT + i * 4096 + 1024 * j);
+            const f32x4 y = lds_load16<f32x4>(rb + S * L::SLOT + i * 4096 + 1024 * j);
 #pragma unroll
             for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
           }
-          {
-            const F k0r = lds_load16<F>(rk0 + S * FO_SLOT);
-            s[i] = M::mma(k0r, qf[i][0], s[i]);
-            if constexpr (D == 32) {
-              const F k1r = lds_load16<F>(rk1 + S * FO_SLOT);
-              s[i] = M::mma(k1r, qf[i][1], s[i]);
-            }
-          }
+#pragma unroll
+          for (int t = 0; t < KC; ++t) s[i] = M::mma(kfrag(S * L::SLOT, t), qf[i][t], s[i]);
           if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
           const float mx = wave_xor32_max(max16(s[i])) * c1;
           const float mnew = fmaxf(m[i], mx);
@@ -653,16 +683,21 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
           ls0[i] *= alpha;
           ls1[i] *= alpha;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) o[i][v] *= alpha;
+          for (int c = 0; c < NH; ++c)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[i][c][v] *= alpha;
           m[i] = mnew;
           weights(i);
         }
       }
-      tr_wait(tr);
+#pragma unroll
+      for (int c = 0; c < NH; ++c) tr_wait(tr[c]);
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
 #pragma unroll
-        for (int u = 0; u < M::PCH; ++u) o[i] = M::mma(tr_frag(tr, u), pf[i][u], o[i]);
+        for (int c = 0; c < NH; ++c)
+#pragma unroll
+          for (int u = 0; u < M::PCH; ++u) o[i][c] = M::mma(tr_frag(tr[c], u), pf[i][u], o[i][c]);
         ls0[i] += t0[i];
         ls1[i] += t1[i];
       }
@@ -683,14 +718,16 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   if (!active) return;
   // every gate load is issued before the first store (a store to memory that
   // could alias a later load keeps the compiler from moving the load up)
-  constexpr int NQ = D / 8;  // accumulator quads holding channels (8 j + 4 g .. +3 < D)
-  f32x4 gv[FO_QT][NQ];
+  constexpr int NQ = D == 16 ? 2 : 4;  // accumulator quads holding channels (32 c + 8 j + 4 g .. +3 < D)
+  f32x4 gv[FO_QT][NH][NQ];
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
     const bool ok = act[i] && qv[i] < G.n;
     const int64_t gbase = myrow + (int64_t)(ok ? qv[i] : 0) * G.sPos;
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) gv[i][j] = load4(a.gate + gbase + 8 * j + 4 * g);
+    for (int c = 0; c < NH; ++c)
+#pragma unroll
+      for (int j = 0; j < NQ; ++j) gv[i][c][j] = load4(a.gate + gbase + 32 * c + 8 * j + 4 * g);
   }
 #pragma unroll
   for (int i = 0; i < FO_QT; ++i) {
@@ -699,14 +736,16 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     const float inv = lt > 0.f ? fast_rcp(lt) : 0.f;
     const int64_t gbase = myrow + (int64_t)qv[i] * G.sPos;
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-      const int c0 = 8 * j + 4 * g;
-      f32x4 ov;
+    for (int c = 0; c < NH; ++c)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        ov[e] = o[i][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[i][j][e]));
-      store4(a.out + gbase + c0, ov);
-    }
+      for (int j = 0; j < NQ; ++j) {
+        const int c0 = 32 * c + 8 * j + 4 * g;
+        f32x4 ov;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          ov[e] = o[i][c][4 * j + e] * inv * fast_rcp(1.f + __expf(-gv[i][c][j][e]));
+        store4(a.out + gbase + c0, ov);
+      }
     if (g == 0)
       a.lse[(int64_t)row * G.lRow + (int64_t)qv[i] * G.lPos + h] =
           lt > 0.f ? (m[i] + log2f(lt)) * LN2 : neg_inf();
@@ -720,16 +759,18 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
   FwdArgs<T> a{g, p.bt, p.kbits, p.rowfull, q, k, v, gate, out, lse, (g.n + FWD_QBLK - 1) / FWD_QBLK};
   const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
   if (g.d == 16 && !std::is_same<T, bf16>::value) return hipErrorInvalidValue;  // bf16 only
-  if (g.d == 64) {
-    KernelTimer t(K_FWD, s);
-    hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
-  } else if constexpr (std::is_same<T, bf16>::value) {
+  if constexpr (std::is_same<T, bf16>::value) {
     const int64_t nwd = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
-    if (g.d == 16)
+    if (g.d == 64)
+      hipLaunchKernelGGL(fwd_dma_kernel<64>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+    else if (g.d == 16)
       hipLaunchKernelGGL(fwd_dma_kernel<16>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
     else
       hipLaunchKernelGGL(fwd_dma_kernel<32>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+  } else if (g.d == 64) {
+    KernelTimer t(K_FWD, s);
+    hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
   } else {
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL((fwd_kernel<T, 32>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);

@@ -1,7 +1,10 @@
-"""GPU parity of triangle attention with head dimension d = 64 (the
-register-staged kernels instantiated for 64 channels) against the fp64
-oracle, with the tolerances of the d = 32 tests, including a batched call
-and the run-to-run determinism."""
+"""GPU parity of triangle attention with head dimension d = 64 against the
+fp64 oracle, with the tolerances of the d = 32 tests, including a batched
+call and the run-to-run determinism.  bf16 runs the DMA kernels' 64-channel
+variants (positions staged as two 32-channel halves), fp32 the
+register-staged kernels instantiated for 64 channels.  The benchmark's
+d = 64 workload (N = 768) is checked on sampled rows and a whole 128-query
+block of the bias gradient."""
 import pytest
 import torch
 
@@ -26,7 +29,7 @@ def inputs64(n, h, dtype, seed, mask_kind="random"):
 
 
 def check(t, node, dtype, rows=None, db_queries=None):
-    d = {k: (v.to(DEV) if v is not None else None) for k, v in t.items()}
+    d = {k: (v.to(DEV) if isinstance(v, torch.Tensor) else v) for k, v in t.items()}
     out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], node)
     grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d["mask"], node)
     torch.cuda.synchronize()
@@ -86,3 +89,13 @@ def test_d64_batched_and_deterministic():
         close(f"out[{i}]", out[i], ro, torch.bfloat16)
         for name, a, r in zip(("dq", "dk", "dv", "dg", "dbias"), grads, rg):
             close(f"{name}[{i}]", a[i], r, torch.bfloat16)
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_d64_workload_sampled(node):
+    """The N = 768, h = 4, d = 64 benchmark workload in its launch configuration."""
+    w = W.WORKLOADS["tri_bf16_n768_d64"]
+    t = W.workload_inputs(w, node)
+    n = w.n
+    print(f"\n[d64 workload n={n} node={node}]", flush=True)
+    check(t, node, w.dtype, rows=[0, 1, 31, 32, n // 2, n - 1], db_queries=list(range(128, 256)))
