@@ -261,6 +261,28 @@ def test_ending_equals_transposed_starting_headline_size():
     _ending_vs_transposed_starting(W.workload_inputs(w, B.ENDING))
 
 
+def test_ending_large_tensor_offsets():
+    """The ending node at n = 1056, h = 64, d = 32 (bf16; 4.6 GB per pair
+    tensor).  The positions of a tile are n h 32 elements apart there, so the
+    byte offset of a block's first key or query times that stride passes 2^32:
+    a 32-bit lane offset that included it would wrap and read other keys.  The
+    kernels move their 64-bit bases to the block's first key and query
+    instead.  Checked bit for bit against the starting node on contiguous
+    transposed copies, whose strides are small (inputs drawn on the device)."""
+    n, h = 1056, 64
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(1056)
+
+    def rnd(*shape):
+        return torch.randn(*shape, generator=gen, device=DEV).to(torch.bfloat16)
+
+    print(f"\n[ending node n={n} h={h}]", flush=True)
+    t = {k: rnd(n, n, h, 32) for k in ("q", "k", "v", "g", "dout")}
+    t["bias"] = rnd(n, n, h)
+    t["mask"] = (torch.rand(n, n, generator=gen, device=DEV) < 0.9).to(torch.uint8)
+    _ending_vs_transposed_starting(t)
+
+
 def test_peak_memory_is_quadratic():
     w = W.WORKLOADS[W.HEADLINE]
     d = to_dev(W.workload_inputs(w, B.STARTING))
