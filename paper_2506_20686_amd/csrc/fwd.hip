@@ -416,29 +416,36 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
 // with the tile: no vector instruction is spent on addresses.  A workgroup
 // whose rows have every key valid (every row of an unmasked problem) runs a
 // loop without any mask step.
-constexpr int FO_ROWS = 4;
 constexpr int FO_QT = 2;                            // query tiles per wave
 constexpr int FO_ROWBLK = 32 * 64;                  // one row's K (or V) tile: 32 keys x 64 B
-constexpr int FO_SLOTS = 2;
-// Slot layout: K tiles [channel half][row], V tiles [channel half][row], then
-// the 4 bias tiles (fp32, 4 KB each).  A 64-channel head keeps each position
-// as two 32-channel halves, each a block of the usual layout: 48 KB slots,
-// one workgroup per CU and two waves per SIMD; 16- and 32-channel heads have
-// one half: 32 KB slots, four waves per SIMD.
+// Workgroup shape and LDS layout.  ROWS rows x 128 queries of one head, two
+// waves per row; a ring of SLOTS key tiles.  (8 rows of 16 waves with a
+// three-slot ring, 144 KB, measured 15% slower than 4 rows and two slots.)  LDS by region, each region
+// holding its piece of every slot (so that slot offsets stay small): K tiles
+// [slot][channel half][row], V tiles likewise, then the 4 bias tiles (fp32,
+// 4 KB each) [slot].  A 64-channel head keeps each position as two 32-channel
+// halves, each a block of the usual layout.
 template <int D>
 struct FoL {
   static constexpr int NH = D == 64 ? 2 : 1;       // 32-channel halves per position
-  static constexpr int HB = FO_ROWS * FO_ROWBLK;   // one half's K (or V) tiles of the rows
-  static constexpr int V0 = NH * HB;               // V tiles follow the K tiles
-  static constexpr int BIAS = 2 * NH * HB;
-  static constexpr int SLOT = BIAS + 4 * 4096;
+  static constexpr int ROWS = 4;
+  static constexpr int SLOTS = 2;
+  static constexpr int WAVES = 2 * ROWS;
+  static constexpr int HB = ROWS * FO_ROWBLK;      // one half's K (or V) tiles of the rows
+  static constexpr int KS = NH * HB;               // one slot of the K (or V) region
+  static constexpr int V0 = SLOTS * KS;            // the V region follows the K region
+  static constexpr int BIAS = 2 * SLOTS * KS;      // then the bias region
+  static constexpr int BS = 4 * 4096;              // one slot of it
+  static constexpr int LDS = BIAS + SLOTS * BS;
+  static constexpr int BOPS = 16 / WAVES;          // bias DMA ops (1 KB quarters) per wave per tile
+  static constexpr int OPS = 2 * NH + BOPS;        // DMA ops per wave per tile
   static constexpr int WPE = D == 64 ? 2 : 4;      // waves per SIMD
 };
 
 //
 // D = 16, 32 or 64 channels per head (see dma.h for 16).
 template <int D>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(FoL<D>::WPE, FoL<D>::WPE)))
+__global__ __launch_bounds__(64 * FoL<D>::WAVES) __attribute__((amdgpu_waves_per_eu(FoL<D>::WPE, FoL<D>::WPE)))
 void fwd_dma_kernel(FwdArgs<bf16> a) {
   to_sample(a);
   using M = Mma<bf16>;
@@ -449,6 +456,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   constexpr int KA = D == 64 ? 4 : 2;       // fragment slots per operand row
   const Geom& G = a.g;
   const int w = xcd_swizzle(blockIdx.x, gridDim.x);
+  constexpr int FO_ROWS = L::ROWS, FO_SLOTS = L::SLOTS;
   const int nrg = (G.nr + FO_ROWS - 1) / FO_ROWS;
   const int qb = w % a.nqb, rg = (w / a.nqb) % nrg, h = w / (a.nqb * nrg);
   const int r0 = rg * FO_ROWS;
@@ -461,7 +469,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const float c1 = G.scale * LOG2E;
   const int nrows = min(FO_ROWS, G.nr - r0);  // rows of this group that exist
 
-  __shared__ __align__(16) char smem[FO_SLOTS * L::SLOT];
+  __shared__ __align__(16) char smem[L::LDS];
 
   const int64_t hb = (int64_t)h * D;
   const int64_t myrow = (int64_t)min(row, last) * G.sRow + hb;
@@ -499,8 +507,8 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const int dblk = wave;  // K0..K3, V0..V3
   const int dp = lane >> 2;
   const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
-  const bf16* dsrc = dblk < 4 ? a.k : a.v;
-  const bf16* dptr = dsrc + (int64_t)min(r0 + (dblk & 3), last) * G.sRow + hb;
+  const bf16* dsrc = dblk < FO_ROWS ? a.k : a.v;
+  const bf16* dptr = dsrc + (int64_t)min(r0 + dblk % FO_ROWS, last) * G.sRow + hb;
   const bf16* const dend = dsrc + tensor;
   uint32_t dvoff[2];
   bool dok[2];  // this lane's chunk exists (always for 32 channels)
@@ -513,26 +521,28 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const int64_t tstep = (int64_t)TILE * G.sPos;
   const float* bptr = a.bt + ((int64_t)h * nkt + (int64_t)qb * 4) * nkt * 1024;
   const float* const bend = a.bt + (int64_t)G.H * nkt * nkt * 1024;
-  const int bt0 = wave >> 2, bt1 = 2 + (wave >> 2);  // bias tiles this wave copies
-  const uint32_t bvoff0 =
-      (uint32_t)(((int64_t)bt0 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
-  const uint32_t bvoff1 =
-      (uint32_t)(((int64_t)bt1 * nkt * 1024 + 256 * (wave & 3)) * 4 + 16 * lane);
-  char* const kvdst = smem + (dblk < 4 ? 0 : L::V0) + (dblk & 3) * FO_ROWBLK;
-  char* const bdst0 = smem + L::BIAS + bt0 * 4096 + 1024 * (wave & 3);
-  char* const bdst1 = smem + L::BIAS + bt1 * 4096 + 1024 * (wave & 3);
+  // bias op j of wave w: quarter u % 4 of tile u / 4, u = BOPS w + j
+  uint32_t bvoff[L::BOPS];
+  char* bdst[L::BOPS];
+#pragma unroll
+  for (int j = 0; j < L::BOPS; ++j) {
+    const int u = L::BOPS * wave + j, bt = u >> 2;
+    bvoff[j] = (uint32_t)(((int64_t)bt * nkt * 1024 + 256 * (u & 3)) * 4 + 16 * lane);
+    bdst[j] = smem + L::BIAS + bt * 4096 + 1024 * (u & 3);
+  }
+  char* const kvdst = smem + (dblk < FO_ROWS ? 0 : L::V0) + (dblk % FO_ROWS) * FO_ROWBLK;
   int issued = 0;
   auto issue = [&](int slot) {
     const bool real = issued < nkt;
     const rsrc_t rk = real ? buf_rsrc(dptr, dend) : buf_rsrc(dptr, dptr);
 #pragma unroll
     for (int c = 0; c < NH; ++c) {  // channel half c: 32 channels (64 bytes) further on
-      if (dok[0]) dma16b(rk, dvoff[0] + 64 * c, kvdst + slot * L::SLOT + c * L::HB);
-      if (dok[1]) dma16b(rk, dvoff[1] + 64 * c, kvdst + slot * L::SLOT + c * L::HB + 1024);
+      if (dok[0]) dma16b(rk, dvoff[0] + 64 * c, kvdst + slot * L::KS + c * L::HB);
+      if (dok[1]) dma16b(rk, dvoff[1] + 64 * c, kvdst + slot * L::KS + c * L::HB + 1024);
     }
     const rsrc_t rb = real ? buf_rsrc(bptr, bend) : buf_rsrc(bptr, bptr);
-    dma16b(rb, bvoff0, bdst0 + slot * L::SLOT);
-    dma16b(rb, bvoff1, bdst1 + slot * L::SLOT);
+#pragma unroll
+    for (int j = 0; j < L::BOPS; ++j) dma16b(rb, bvoff[j], bdst[j] + slot * L::BS);
     if (issued + 1 < nkt) {
       dptr += tstep;
       bptr += 1024;
@@ -567,14 +577,17 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
   const bf16x2 one2 = {(bf16)1.f, (bf16)1.f};
 
   // zero the V rows of keys invalid for a row in ring slot S (weight 0, and
-  // 0 times a non-finite value would not be); thread t < 128: row t / 32, key t % 32
+  // 0 times a non-finite value would not be); thread t < 32 ROWS: row t / 32, key t % 32
   auto zero_invalid_v = [&](auto slot, const uint32_t (&wr)[FO_ROWS]) {
     constexpr int S = decltype(slot)::value;
-    if (tid < 128) {
+    if (tid < 32 * FO_ROWS) {
       const int rr = tid >> 5;
-      const uint32_t wb = rr == 0 ? wr[0] : rr == 1 ? wr[1] : rr == 2 ? wr[2] : wr[3];
+      uint32_t wb = 0;
+#pragma unroll
+      for (int i = 0; i < FO_ROWS; ++i)
+        if (rr == i) wb = wr[i];
       if (!((wb >> (tid & 31)) & 1u)) {
-        char* z = smem + S * L::SLOT + L::V0 + rr * FO_ROWBLK + 64 * (tid & 31);
+        char* z = smem + S * L::KS + L::V0 + rr * FO_ROWBLK + 64 * (tid & 31);
 #pragma unroll
         for (int c = 0; c < NH; ++c)
 #pragma unroll
@@ -594,7 +607,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
         wr[i] = i < nrows ? (FULL ? in_range_bits(t, G.n)
                                   : const_load(a.kbits + (int64_t)(r0 + i) * nkt + t))
                           : 0u;
-      wait_vm<0>();  // tile t has landed
+      wait_vm<(FO_SLOTS - 2) * L::OPS>();  // tile t has landed (tiles after it may be in flight)
       lds_barrier();
       if (!FULL) {
         bool full = true;
@@ -605,18 +618,21 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
           __syncthreads();
         }
       }
-      issue(S ^ 1);  // tile t + 1 into the other slot
-      const uint32_t wb = ri == 0 ? wr[0] : ri == 1 ? wr[1] : ri == 2 ? wr[2] : wr[3];
+      issue((S + FO_SLOTS - 1) % FO_SLOTS);  // tile t + SLOTS - 1 into the slot of tile t - 1
+      uint32_t wb = 0;
+#pragma unroll
+      for (int i = 0; i < FO_ROWS; ++i)
+        if (ri == i) wb = wr[i];
       if (!active || wb == 0u) return;
       F kfr[KA];
 #pragma unroll
-      for (int t = 0; t < KC; ++t) kfr[t] = kfrag(S * L::SLOT, t);
+      for (int t = 0; t < KC; ++t) kfr[t] = kfrag(S * L::KS, t);
       f32x16 s[FO_QT];
 #pragma unroll
       for (int i = 0; i < FO_QT; ++i) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const f32x4 y = lds_load16<f32x4>(rb + S * L::SLOT + i * 4096 + 1024 * j);
+          const f32x4 y = lds_load16<f32x4>(rb + S * L::BS + i * 4096 + 1024 * j);
 #pragma unroll
           for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
         }
@@ -626,7 +642,7 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
       s16x4 tr[NH][4];
       auto trread = [&](auto cc) {  // V^T fragments of channel half c
         constexpr int c = decltype(cc)::value;
-        constexpr uint32_t ho = S * L::SLOT + c * L::HB;
+        constexpr uint32_t ho = S * L::KS + c * L::HB;
         tr[c][0] = ds_read_tr<ho>(rv);
         tr[c][1] = ds_read_tr<ho + 8 * 64>(rv8);
         tr[c][2] = ds_read_tr<ho + 16 * 64>(rv);
@@ -670,12 +686,12 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
           // the tile's logits again (bias and K from the slot, Q at hand)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const f32x4 y = lds_load16<f32x4>(rb + S * L::SLOT + i * 4096 + 1024 * j);
+            const f32x4 y = lds_load16<f32x4>(rb + S * L::BS + i * 4096 + 1024 * j);
 #pragma unroll
             for (int e = 0; e < 4; ++e) s[i][4 * j + e] = y[e];
           }
 #pragma unroll
-          for (int t = 0; t < KC; ++t) s[i] = M::mma(kfrag(S * L::SLOT, t), qf[i][t], s[i]);
+          for (int t = 0; t < KC; ++t) s[i] = M::mma(kfrag(S * L::KS, t), qf[i][t], s[i]);
           if (wb != 0xffffffffu) mask_rows(s[i], wb, g);
           const float mx = wave_xor32_max(max16(s[i])) * c1;
           const float mnew = fmaxf(m[i], mx);
@@ -702,11 +718,14 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
         ls1[i] += t1[i];
       }
     };
-    issue(0);
+#pragma unroll
+    for (int j = 0; j < FO_SLOTS - 1; ++j) issue(j);
     for (int t = 0; t < nkt; t += FO_SLOTS) {
       step(t, slot_c<0>{});
       if (t + 1 >= nkt) break;
-      step(t + 1, slot_c<1>{});
+      step(t + 1, slot_c<1 % FO_SLOTS>{});
+      if (FO_SLOTS < 3 || t + 2 >= nkt) continue;
+      step(t + 2, slot_c<2 % FO_SLOTS>{});
     }
   };
   if (rows_full)
@@ -760,14 +779,18 @@ hipError_t launch_fwd(const Geom& g, const Prep& p, const T* q, const T* k, cons
   const int64_t nwg = (int64_t)a.nqb * ((g.nr + FWD_ROWS - 1) / FWD_ROWS) * g.H;
   if (g.d == 16 && !std::is_same<T, bf16>::value) return hipErrorInvalidValue;  // bf16 only
   if constexpr (std::is_same<T, bf16>::value) {
-    const int64_t nwd = (int64_t)a.nqb * ((g.nr + FO_ROWS - 1) / FO_ROWS) * g.H;
     KernelTimer t(K_FWD, s);
+    auto go = [&](auto kernel, auto lay) {
+      using L = decltype(lay);
+      const int64_t nwd = (int64_t)a.nqb * ((g.nr + L::ROWS - 1) / L::ROWS) * g.H;
+      hipLaunchKernelGGL(kernel, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(64 * L::WAVES), 0, s, a);
+    };
     if (g.d == 64)
-      hipLaunchKernelGGL(fwd_dma_kernel<64>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+      go(fwd_dma_kernel<64>, FoL<64>{});
     else if (g.d == 16)
-      hipLaunchKernelGGL(fwd_dma_kernel<16>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+      go(fwd_dma_kernel<16>, FoL<16>{});
     else
-      hipLaunchKernelGGL(fwd_dma_kernel<32>, dim3((unsigned)nwd, 1, (unsigned)g.batch), dim3(512), 0, s, a);
+      go(fwd_dma_kernel<32>, FoL<32>{});
   } else if (g.d == 64) {
     KernelTimer t(K_FWD, s);
     hipLaunchKernelGGL((fwd_kernel<T, 64>), dim3((unsigned)nwg, 1, (unsigned)g.batch), dim3(256), 0, s, a);
