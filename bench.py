@@ -134,14 +134,23 @@ SOURCE_FAMILIES = {
 }
 
 
+def _code_only(text):
+    """C++ source without its comments and with runs of whitespace collapsed, so that
+    editing a comment leaves the hash of the code unchanged (the sources hold no string
+    literal with comment markers)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_hash(family="tri"):
-    """Hash of a kernel family's sources; a traffic figure measured on other sources is
-    stale."""
+    """Hash of the code (comments aside) of a kernel family's sources; a traffic figure
+    measured on other code is stale."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_20686_amd", "csrc")
     for name in sorted(SOURCE_FAMILIES[family]):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + _code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1241,7 +1241,8 @@ constexpr int DBD_SLOT = DBD_LD + 1024;
 constexpr int DBD_SLOTS = 3;
 constexpr int DBD_OPS = 3;                    // DMA ops per thread per row
 
-// D = 16 or 32 channels per head (see dma.h for 16).
+// D = 16 or 32 channels per head (see dma.h for 16; 64 channels use
+// db_dma64_kernel below).
 template <int D>
 __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) {
   to_sample(a);

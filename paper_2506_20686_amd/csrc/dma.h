@@ -1,7 +1,8 @@
 // Asynchronous staging of bf16 operand blocks through LDS on gfx950.
 //
 // A block is consecutive pair positions x 32 channels of one (row, head),
-// 64 bytes per position.  It is copied HBM -> LDS with
+// 64 bytes per position (a 64-channel head is staged as two blocks, one per
+// 32-channel half; a 16-channel head fills half of each position's row).  It is copied HBM -> LDS with
 // global_load_lds_dwordx4 (each lane moves 16 bytes straight into LDS, no
 // registers, no vector instructions) into a ring of slots, one or more
 // blocks ahead of the compute.

@@ -407,9 +407,10 @@ __global__ __launch_bounds__(256, 2) void fwd_kernel(FwdArgs<T> a) {
 // 2 (w % 2) and 2 (w % 2) + 1 of row r0 + w / 2, so every K and V fragment
 // it reads from LDS serves two query tiles.  Keys stream in tiles of 32
 // through a double-buffered DMA ring: per slot the K and V tiles of the 4
-// rows (16 KB) and the bias tiles of the 4 query tiles, shared by the rows
-// (16 KB).  64 KB of LDS and at most 128 VGPRs let two workgroups share a
-// CU (four waves per SIMD).
+// rows (16 KB; 32 KB for 64-channel heads) and the bias tiles of the 4 query
+// tiles, shared by the rows (16 KB).  With 16 or 32 channels, 64 KB of LDS
+// and at most 128 VGPRs let two workgroups share a CU (four waves per SIMD);
+// with 64, one workgroup (96 KB) runs per CU at two waves per SIMD.
 //
 // The loop is unrolled by the ring length, so every LDS read has a constant
 // slot offset, and the DMAs go through buffer resources whose base moves
