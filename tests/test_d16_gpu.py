@@ -132,3 +132,28 @@ def test_d16_batched_one_launch_equals_per_sample():
             assert torch.equal(out[i], o1) and torch.equal(lse[i], l1)
             for a, c in zip(grads, g1):
                 assert torch.equal(a[i], c)
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_d16_minus_inf_bias_tile(node):
+    """An additive -inf bias on every key of the first 32-key tile of one
+    query (the other queries of its wave see finite logits there) with 16
+    channels per head: the -inf query's weights stay exactly 0."""
+    n, h, q0 = 70, 2, 5
+    t = inputs16(n, h, torch.bfloat16, seed=4444 + node, masked=False)
+    bias = t["bias"].clone()
+    if node == B.STARTING:
+        bias[q0, :32, :] = float("-inf")  # bias[q][k][h]
+    else:
+        bias[:32, q0, :] = float("-inf")  # the ending node reads bias[k][i][h]
+    t["bias"] = bias
+    d = {k: (v.to(DEV) if v is not None else None) for k, v in t.items()}
+    out, lse = B.fwd(d["q"], d["k"], d["v"], d["g"], d["bias"], d["mask"], node)
+    grads = B.bwd(d["q"], d["k"], d["v"], d["g"], d["bias"], out, lse, d["dout"], d["mask"], node)
+    torch.cuda.synchronize()
+    ro, rl = oracle.fwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["mask"])
+    rg = oracle.bwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["dout"], t["mask"])
+    close("out", out, ro, torch.bfloat16)
+    close("lse", lse, rl, torch.bfloat16)
+    for name, a, r in zip(("dq", "dk", "dv", "dg", "dbias"), grads, rg):
+        close(name, a, r, torch.bfloat16)

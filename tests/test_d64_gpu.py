@@ -99,3 +99,19 @@ def test_d64_workload_sampled(node):
     n = w.n
     print(f"\n[d64 workload n={n} node={node}]", flush=True)
     check(t, node, w.dtype, rows=[0, 1, 31, 32, n // 2, n - 1], db_queries=list(range(128, 256)))
+
+
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_d64_minus_inf_bias_tile(node):
+    """An additive -inf bias on every key of the first 32-key tile of one
+    query (the other queries of its wave see finite logits there) with 64
+    channels per head: the -inf query's weights stay exactly 0."""
+    n, h, q0 = 70, 2, 5
+    t = inputs64(n, h, torch.bfloat16, seed=4343 + node, mask_kind="none")
+    bias = t["bias"].clone()
+    if node == B.STARTING:
+        bias[q0, :32, :] = float("-inf")  # bias[q][k][h]
+    else:
+        bias[:32, q0, :] = float("-inf")  # the ending node reads bias[k][i][h]
+    t["bias"] = bias
+    check(t, node, torch.bfloat16)
