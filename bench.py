@@ -128,7 +128,8 @@ def mfma_calibration(launches, blocks=1024, iters=2000):
 # Sources whose change can change a kernel family's memory traffic (its
 # kernels, the shared device headers, the host code that picks launch shapes).
 SOURCE_FAMILIES = {
-    "tri": ("fwd.hip", "bwd.hip", "api.hip", "common.h", "dma.h", "stage.h", "kernels.h"),
+    "tri": ("fwd.hip", "bwd.hip", "dkdv.hip", "bwd.h", "api.hip", "common.h", "dma.h", "stage.h",
+            "kernels.h"),
     "lnl": ("lnl.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
     "trn": ("trn.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
 }
@@ -146,11 +147,14 @@ def _code_only(text):
 def kernel_source_hash(family="tri"):
     """Hash of the code (comments aside) of a kernel family's sources; a traffic figure
     measured on other code is stale."""
+    from paper_2506_20686_amd import build as hip_build
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2506_20686_amd", "csrc")
     for name in sorted(SOURCE_FAMILIES[family]):
         with open(os.path.join(csrc, name), encoding="utf-8") as f:
             h.update(name.encode() + b"\0" + _code_only(f.read()).encode())
+    # the compile options shape the code as much as the sources do
+    h.update(repr((hip_build.FLAGS, hip_build.MAX_ILP, hip_build.ILP_FLAGS)).encode())
     return h.hexdigest()[:16]
 
 

@@ -6,7 +6,14 @@ hipcc cross-compiles for gfx950 without a GPU.  Packed-fp32 instructions are
 disabled for device code (some of their forms have given wrong results on
 these parts); the host pass warns that it does not know that feature, which
 is harmless.
+
+Each source compiles to its own object, then one link makes the library.
+The forward and backward sources (not the dK/dV kernels, which sit in a file
+of their own) are compiled with LLVM's "max-ilp" machine scheduler: measured
+on MI355X it made the forward 6%, dB 4% and dQ 1% faster, and dK/dV 27%
+slower (it raised dK/dV's registers past four waves per SIMD).
 """
+import concurrent.futures
 import glob
 import os
 import subprocess
@@ -16,34 +23,58 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libtriattn.so")
+OBJ_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # device code only: no NaN reaches the kernels' max/min, so fmaxf needs no
     # quieting of its operands (host-side argument checks keep NaN semantics)
     "-Xarch_device", "-fno-honor-nans",
     "-Wall", "-Wno-unused-function",
 ]
+# sources built with the instruction-level-parallelism scheduler
+MAX_ILP = ("fwd.hip", "bwd.hip")
+ILP_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]
+NOISE = "is not a recognized feature for this target"
 
 
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", CSRC,
-           *sources(), "-o", LIB + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if err.strip() and verbose:
-        print(err, file=sys.stderr)
+    err = "\n".join(l for l in res.stderr.splitlines() if NOISE not in l)
+    return res.returncode, err
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    """Compile every source (in parallel) and link the library; `extra` flags
+    go to every compile."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    jobs = []
+    for src in sources():
+        name = os.path.basename(src)
+        obj = os.path.join(OBJ_DIR, name + ".o")
+        flags = FLAGS + (ILP_FLAGS if name in MAX_ILP else []) + list(extra)
+        jobs.append(([HIPCC, *flags, *inc, "-c", src, "-o", obj], obj))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        results = list(ex.map(lambda j: _run(j[0]), jobs))
+    for (cmd, _), (rc, err) in zip(jobs, results):
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        if rc != 0:
+            raise RuntimeError(f"hipcc failed ({rc}):\n{err}")
+        if err.strip() and verbose:
+            print(err, file=sys.stderr)
+    link = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for _, o in jobs],
+            "-o", LIB + ".tmp"]
+    rc, err = _run(link)
+    if rc != 0:
+        raise RuntimeError(f"link failed ({rc}):\n{err}")
     os.replace(LIB + ".tmp", LIB)
     return LIB
 
