@@ -373,7 +373,12 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
   auto step = [&](auto slot) {
     constexpr int S = decltype(slot)::value;
     constexpr uint32_t so = S * L::TS;  // slot offset inside the Q, dA and dA-low regions
-    wait_vm<0>();  // tile t has landed
+    // tile t has landed (the tiles after it may be in flight: each wave issues
+    // the same number of DMA ops per tile when NH = 1)
+    if constexpr (NH == 1)
+      wait_vm<(KD_SLOTS - 2) * (2 + KD_BOPS)>();
+    else
+      wait_vm<0>();
     lds_barrier();
     issue((S + KD_SLOTS - 1) % KD_SLOTS);  // tile t + KD_SLOTS - 1 into the slot of tile t - 1
     if (!work) return;
