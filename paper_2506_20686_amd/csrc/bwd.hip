@@ -424,17 +424,36 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
       dok[j] = true;
     }
   }
+  // With one channel half, the units of a wave all come from one source (the
+  // K rows, the V rows or one bias tile): one walking resource serves them,
+  // the rows told apart by their lane offsets.  Otherwise each unit walks its own.
+  constexpr bool ONE = NH == 1;
+  constexpr int NW = ONE ? 1 : QD_OPS;
+  Walk wk[NW];
+#pragma unroll
+  for (int j = 0; j < NW; ++j) wk[j] = Walk(src[j], srcend[j], adv[j]);
+  if constexpr (ONE) {
+#pragma unroll
+    for (int j = 1; j < QD_OPS; ++j)
+      voff[j] += (uint32_t)((const char*)src[j] - (const char*)src[0]);
+  }
   int issued = 0;
   auto issue = [&](int slot) {
     // tiles past the last copy nothing (empty resources) but keep the wait
     // counts uniform
     const bool real = issued < nkt;
+    if constexpr (ONE) {
+      const rsrc_t rs = wk[0].rsrc(real);
 #pragma unroll
-    for (int j = 0; j < QD_OPS; ++j) {
-      if (dok[j])
-        dma16b(real ? buf_rsrc(src[j], srcend[j]) : buf_rsrc(src[j], src[j]), voff[j],
-               dst[j] + slot * L::SLOT);
-      if (issued + 1 < nkt) src[j] = (const char*)src[j] + adv[j];
+      for (int j = 0; j < QD_OPS; ++j)
+        if (dok[j]) dma16b(rs, voff[j], dst[j] + slot * L::SLOT);
+      wk[0].advance();
+    } else {
+#pragma unroll
+      for (int j = 0; j < QD_OPS; ++j) {
+        if (dok[j]) dma16b(wk[j].rsrc(real), voff[j], dst[j] + slot * L::SLOT);
+        wk[j].advance();
+      }
     }
     ++issued;
   };
@@ -812,29 +831,34 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   char* const dst1 = smem + (wave < 8 ? DBD_OQ : DBD_ODA) + 1024 * (wave & 7);
   char* const dst2 = lo_op ? smem + DBD_OLO + 1024 * wave
                            : smem + DBD_LD + 128 * (wave - 8);
-  auto issue = [&](int r, int slot) {
+  // Op bases at row r0, advanced by one row per issue (scalar adds only),
+  // with record counts fixed for the loop (see last_row_records; the lse2 /
+  // -D rows are whole rows of np floats).
+  const int64_t lastr = max(G.nr - 1 - r0, 0);
+  const char* b0 = (const char*)(src0 + (int64_t)r0 * G.sRow + koff);
+  const char* b1 = (const char*)(src1 + (int64_t)r0 * G.sRow + qoff);
+  const char* b2 = lo_op ? (const char*)(a.dalo + (int64_t)r0 * G.sRow + qoff)
+                         : (const char*)(lrow + (int64_t)r0 * G.np);
+  const int64_t rs = G.sRow * 2, rs2 = lo_op ? rs : (int64_t)G.np * 4;  // bytes per row
+  const uint32_t n0 = last_row_records(b0 + lastr * rs, src0 + tensor);
+  const uint32_t n1 = last_row_records(b1 + lastr * rs, src1 + tensor);
+  const uint32_t n2 = lo_op ? last_row_records(b2 + lastr * rs, a.dalo + tensor)
+                            : (uint32_t)G.np * 4;
+  const bool op2 = lo_op ? pok : lane < 8;
+  int next = r0;  // the row the next issue copies
+  auto issue = [&](int slot) {
     // rows past the chunk copy nothing (empty resources) but keep the wait
     // counts uniform
-    const bool real = r < r1;
-    const int64_t rb = (int64_t)min(r, G.nr - 1) * G.sRow;
-    const bf16* p0 = src0 + rb + koff;
-    const bf16* p1 = src1 + rb + qoff;
-    const bf16* p2 = a.dalo + rb + qoff;
-    const float* pl = lrow + (int64_t)min(r, G.nr - 1) * G.np;
+    const bool real = next < r1;
     if (pok) {
-      dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), voff,
-             dst0 + slot * DBD_SLOT);
-      dma16b(real ? buf_rsrc(p1, src1 + tensor) : buf_rsrc(p1, p1), voff,
-             dst1 + slot * DBD_SLOT);
+      dma16b(buf_rsrc_n(b0, real ? n0 : 0u), voff, dst0 + slot * DBD_SLOT);
+      dma16b(buf_rsrc_n(b1, real ? n1 : 0u), voff, dst1 + slot * DBD_SLOT);
     }
-    if (lo_op) {
-      if (pok)
-        dma16b(real ? buf_rsrc(p2, a.dalo + tensor) : buf_rsrc(p2, p2), voff2,
-               dst2 + slot * DBD_SLOT);
-    } else if (lane < 8) {
-      dma16b(real ? buf_rsrc(pl, pl + G.np) : buf_rsrc(pl, pl), voff2,
-             dst2 + slot * DBD_SLOT);
-    }
+    if (op2) dma16b(buf_rsrc_n(b2, real ? n2 : 0u), voff2, dst2 + slot * DBD_SLOT);
+    b0 += rs;
+    b1 += rs;
+    b2 += rs2;
+    ++next;
   };
 
   // ---- LDS read addresses (slot 0)
@@ -847,12 +871,23 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   const uint32_t rl = base + DBD_LD + (qtl * TILE + l32) * 4;
   const uint32_t* kbrow = a.kbits + kstart / TILE;
 
-  auto step = [&](int r, auto slot) {
+  // FULL: every key < n is valid for every row of the chunk.  The key bits
+  // of the wave's tile are then the same for every row, and keys past n
+  // read zeros (K, V) through the record counts, so no row needs its V rows
+  // cleared.
+  bool rows_full = true;
+  for (int rr = r0; rr < r1; rr += 64)
+    rows_full = rows_full && __all(rr + lane >= r1 || a.rowfull[rr + lane] != 0u);
+  const uint32_t wfull = kt < nkt ? in_range_bits(kt, G.n) : 0u;
+
+  auto step = [&](int r, auto slot, auto full_c) {
     constexpr int S = decltype(slot)::value;
-    const uint32_t wb = kt < nkt ? const_load(kbrow + (int64_t)r * nkt + ktl) : 0u;
+    constexpr bool FULL = decltype(full_c)::value;
+    const uint32_t wb =
+        FULL ? wfull : (kt < nkt ? const_load(kbrow + (int64_t)r * nkt + ktl) : 0u);
     wait_vm<DBD_OPS>();  // row r has landed (only row r + 1 is still in flight)
     lds_barrier();
-    {
+    if constexpr (!FULL) {
       // key bits of the block's 4 tiles: the same in every wave, so the
       // branch below (it holds a barrier) is uniform across the workgroup
       uint32_t all = 0xffffffffu;
@@ -871,7 +906,7 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
         __syncthreads();
       }
     }
-    issue(r + 2, (S + 2) % DBD_SLOTS);  // row r + 2 into the slot of row r - 1
+    issue((S + 2) % DBD_SLOTS);  // row r + 2 into the slot of row r - 1
     if (!active || wb == 0u) return;
     float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT);
     const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT + 512);
@@ -906,15 +941,21 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
       acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
   };
 
-  issue(r0, 0);
-  issue(r0 + 1, 1);
-  for (int i = 0; i < nr; i += DBD_SLOTS) {
-    step(r0 + i, slot_c<0>{});
-    if (i + 1 >= nr) break;
-    step(r0 + i + 1, slot_c<1>{});
-    if (i + 2 >= nr) break;
-    step(r0 + i + 2, slot_c<2>{});
-  }
+  issue(0);
+  issue(1);
+  auto run = [&](auto full_c) {
+    for (int i = 0; i < nr; i += DBD_SLOTS) {
+      step(r0 + i, slot_c<0>{}, full_c);
+      if (i + 1 >= nr) break;
+      step(r0 + i + 1, slot_c<1>{}, full_c);
+      if (i + 2 >= nr) break;
+      step(r0 + i + 2, slot_c<2>{}, full_c);
+    }
+  };
+  if (rows_full)
+    run(std::true_type{});
+  else
+    run(std::false_type{});
   wait_vm<0>();  // the copies past the end must land before the workgroup ends
   if (!active) return;
   float* slab = a.slabs + (((int64_t)rc * G.H + h) * G.np + qstart + qtl * TILE + l32) * G.np +
@@ -1004,32 +1045,44 @@ __global__ __launch_bounds__(64 * D6_WAVES) void db_dma64_kernel(BwdArgs<bf16> a
   char* const dV = smem + D6_OV + 1024 * wave;
   const int qo = cq * D6_QH + 1024 * (wave & 3);  // + slot 2 D6_QH
   char* const dL = smem + D6_OL + 128 * wave;     // + slot 512
+  // Op bases at row r0, advanced by one row per issue, with record counts
+  // fixed for the loop (see last_row_records; lse2 / -D rows are whole rows
+  // of np floats).
+  const int64_t lastr = max(G.nr - 1 - r0, 0);
+  const int64_t rs = G.sRow * 2;  // bytes per row
+  const char* bk = (const char*)(a.k + (int64_t)r0 * G.sRow + koff);
+  const char* bv = (const char*)(a.v + (int64_t)r0 * G.sRow + koff);
+  const char* bq = (const char*)(a.q + (int64_t)r0 * G.sRow + qoff);
+  const char* ba = (const char*)(a.da + (int64_t)r0 * G.sRow + qoff);
+  const char* bl = (const char*)(a.dalo + (int64_t)r0 * G.sRow + qoff);
+  const char* b5 = (const char*)(lrow + (int64_t)r0 * G.np);
+  const uint32_t nk = last_row_records(bk + lastr * rs, a.k + tensor);
+  const uint32_t nv = last_row_records(bv + lastr * rs, a.v + tensor);
+  const uint32_t nq = last_row_records(bq + lastr * rs, a.q + tensor);
+  const uint32_t na = last_row_records(ba + lastr * rs, a.da + tensor);
+  const uint32_t nl = last_row_records(bl + lastr * rs, a.dalo + tensor);
   auto issue = [&](int r, int slot) {
     // rows past the chunk copy nothing (empty resources) but keep the wait
-    // counts uniform
+    // counts uniform; rows are issued in order, one per call
     const bool real = r < r1;
-    const int64_t rb = (int64_t)min(r, G.nr - 1) * G.sRow;
-    const bf16* pkk = a.k + rb + koff;
-    const bf16* pvv = a.v + rb + koff;
-    const bf16* pqq = a.q + rb + qoff;
-    const bf16* paa = a.da + rb + qoff;
-    const bf16* pll = a.dalo + rb + qoff;
-    const float* p5 = lrow + (int64_t)min(r, G.nr - 1) * G.np;
-    const rsrc_t rk = real ? buf_rsrc(pkk, a.k + tensor) : buf_rsrc(pkk, pkk);
-    const rsrc_t rv = real ? buf_rsrc(pvv, a.v + tensor) : buf_rsrc(pvv, pvv);
+    const rsrc_t rk = buf_rsrc_n(bk, real ? nk : 0u);
+    const rsrc_t rv = buf_rsrc_n(bv, real ? nv : 0u);
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       dma16b(rk, kvoff + 64 * c, dK + (2 * slot + c) * D6_KH);
       dma16b(rv, kvoff + 64 * c, dV + (2 * slot + c) * D6_KH);
     }
-    dma16b(real ? buf_rsrc(pqq, a.q + tensor) : buf_rsrc(pqq, pqq), qvoff,
-           smem + D6_OQ + 2 * slot * D6_QH + qo);
-    dma16b(real ? buf_rsrc(paa, a.da + tensor) : buf_rsrc(paa, paa), qvoff,
-           smem + D6_ODA + 2 * slot * D6_QH + qo);
-    dma16b(real ? buf_rsrc(pll, a.dalo + tensor) : buf_rsrc(pll, pll), qvoff,
-           smem + D6_OLO + 2 * slot * D6_QH + qo);
+    dma16b(buf_rsrc_n(bq, real ? nq : 0u), qvoff, smem + D6_OQ + 2 * slot * D6_QH + qo);
+    dma16b(buf_rsrc_n(ba, real ? na : 0u), qvoff, smem + D6_ODA + 2 * slot * D6_QH + qo);
+    dma16b(buf_rsrc_n(bl, real ? nl : 0u), qvoff, smem + D6_OLO + 2 * slot * D6_QH + qo);
     if (l_op && lane < 8)
-      dma16b(real ? buf_rsrc(p5, p5 + G.np) : buf_rsrc(p5, p5), lvoff, dL + 512 * slot);
+      dma16b(buf_rsrc_n(b5, real ? (uint32_t)G.np * 4 : 0u), lvoff, dL + 512 * slot);
+    bk += rs;
+    bv += rs;
+    bq += rs;
+    ba += rs;
+    bl += rs;
+    b5 += (int64_t)G.np * 4;
   };
 
   // ---- LDS read addresses (slot 0, channel half 0)

@@ -310,34 +310,32 @@ __global__ __launch_bounds__(64 * KD_WAVES) void dkdv_dma_kernel(BwdArgs<bf16> a
     bvoff[j] = (uint32_t)(((int64_t)tl * nkt * 1024 + 256 * (u & 3)) * 4 + 16 * lane);
     dst2[j] = smem + L::BIAS + tl * 4096 + 1024 * (u & 3);
   }
+  Walk w0(p0, src0 + tensor, tstep * 2);
+  Walk w1 = lo_op ? Walk(p1, a.dalo + tensor, tstep * 2) : Walk(pl, plend, TILE * 4);
+  Walk wb(pb, pbend, 4096);
   int issued = 0;
   auto issue = [&](int slot) {
     // tiles past the last copy nothing (empty resources) but keep the wait
     // counts uniform
     const bool real = issued < nkt;
+    const rsrc_t r0s = w0.rsrc(real);
 #pragma unroll
     for (int c = 0; c < NH; ++c)  // channel half c: 32 channels (64 bytes) further on
-      if (pok)
-        dma16b(real ? buf_rsrc(p0, src0 + tensor) : buf_rsrc(p0, p0), pvoff + 64 * c,
-               dst0 + slot * L::TS + c * L::HT);
+      if (pok) dma16b(r0s, pvoff + 64 * c, dst0 + slot * L::TS + c * L::HT);
+    const rsrc_t r1s = w1.rsrc(real);
     if (lo_op) {
 #pragma unroll
       for (int c = 0; c < NH; ++c)
-        if (pok)
-          dma16b(real ? buf_rsrc(p1, a.dalo + tensor) : buf_rsrc(p1, p1), pvoff + 64 * c,
-                 dst1 + slot * dst1_stride + c * L::HT);
+        if (pok) dma16b(r1s, pvoff + 64 * c, dst1 + slot * dst1_stride + c * L::HT);
     } else if (lane < 8) {
-      dma16b(real ? buf_rsrc(pl, plend) : buf_rsrc(pl, pl), lvoff, dst1 + slot * dst1_stride);
+      dma16b(r1s, lvoff, dst1 + slot * dst1_stride);
     }
-    const rsrc_t rbias = real ? buf_rsrc(pb, pbend) : buf_rsrc(pb, pb);
+    const rsrc_t rbias = wb.rsrc(real);
 #pragma unroll
     for (int j = 0; j < KD_BOPS; ++j) dma16b(rbias, bvoff[j], dst2[j] + slot * L::BS);
-    if (issued + 1 < nkt) {
-      p0 += tstep;
-      p1 += tstep;
-      pl += TILE;
-      pb += 1024;
-    }
+    w0.advance();
+    w1.advance();
+    wb.advance();
     ++issued;
   };
 

@@ -66,18 +66,52 @@ __device__ inline void dma16(const void* src, void* dst_wave) {
   __builtin_amdgcn_global_load_lds(src, (TRIATTN_LDS void*)dst_wave, 16, 0, 0);
 }
 
-// Buffer resource over the bytes [base, end) (gfx9 raw buffer, stride 0).
-// A lane whose offset falls past `end` reads zeros, so the ragged tail of a
-// tensor needs no clamped addresses.  The record count saturates at 4 GiB - 1;
-// callers keep each lane's offset below 2^32 by moving `base` with the tile.
+// Buffer resource over `nrec` bytes from `base` (gfx9 raw buffer, stride 0).
+// A lane whose offset falls past the record count reads zeros, so the ragged
+// tail of a tensor needs no clamped addresses; nrec = 0 gives an empty
+// resource (every lane reads zeros and no memory is touched).  Record counts
+// saturate at 4 GiB - 1; callers keep each lane's offset below 2^32 by moving
+// `base` with the tile or row.
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
-__device__ inline rsrc_t buf_rsrc(const void* base, const void* end) {
-  // callers keep base <= end; the test on the high word stays scalar
-  const uint64_t len = (uint64_t)((const char*)end - (const char*)base);
-  const uint32_t nr = (len >> 32) != 0 ? 0xffffffffu : (uint32_t)len;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)nr,
+__device__ inline rsrc_t buf_rsrc_n(const void* base, uint32_t nrec) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)nrec,
                                            0x00020000);
 }
+
+// Record count for a resource whose base walks the rows of a pair tensor
+// ending at `end`: the bytes from the last row's base to `end`, saturated at
+// 4 GiB - 1.  A block reads the same offsets from every row's base.  Those
+// of positions below n stay under the count (they do in the last row, whose
+// last position ends the tensor); those of positions n and up reach past it
+// in either node's layout, so they read zeros in every row.
+__device__ inline uint32_t last_row_records(const void* last_base, const void* end) {
+  const int64_t len = (const char*)end - (const char*)last_base;
+  return len <= 0 ? 0u : (len >= 0xffffffffll ? 0xffffffffu : (uint32_t)len);
+}
+
+// A buffer resource that walks a tensor in fixed steps (one tile per
+// advance): the base moves by `step` bytes and the record count, the bytes
+// left to the tensor's end saturated at 4 GiB - 1, shrinks with it.  All of
+// it lives in scalar registers; an advance costs a few scalar adds.
+struct Walk {
+  const char* base;
+  uint64_t rem;  // bytes from base to the end (wraps once the base passes it)
+  int64_t step;
+  Walk() = default;
+  __device__ inline Walk(const void* b, const void* end, int64_t s)
+      : base((const char*)b), rem((uint64_t)((const char*)end - (const char*)b)), step(s) {}
+  // The resource for the current tile; real = false gives an empty one (the
+  // copy writes zeros and reads no memory), for tiles past the last.
+  __device__ inline rsrc_t rsrc(bool real) const {
+    const u32x2 r = __builtin_bit_cast(u32x2, rem);
+    const uint32_t n = r[1] != 0u ? 0xffffffffu : r[0];
+    return buf_rsrc_n(base, real ? n : 0u);
+  }
+  __device__ inline void advance() {
+    base += step;
+    rem -= (uint64_t)step;
+  }
+};
 
 // One 16-byte DMA lane through a buffer resource: lane i's 16 bytes at
 // `voff` land at dst_wave + 16 i.  The resource (and so the per-tile advance)

@@ -532,22 +532,21 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     bdst[j] = smem + L::BIAS + bt * 4096 + 1024 * (u & 3);
   }
   char* const kvdst = smem + (dblk < FO_ROWS ? 0 : L::V0) + (dblk % FO_ROWS) * FO_ROWBLK;
+  Walk wkv(dptr, dend, tstep * 2), wbias(bptr, bend, 4096);
   int issued = 0;
   auto issue = [&](int slot) {
     const bool real = issued < nkt;
-    const rsrc_t rk = real ? buf_rsrc(dptr, dend) : buf_rsrc(dptr, dptr);
+    const rsrc_t rk = wkv.rsrc(real);
 #pragma unroll
     for (int c = 0; c < NH; ++c) {  // channel half c: 32 channels (64 bytes) further on
       if (dok[0]) dma16b(rk, dvoff[0] + 64 * c, kvdst + slot * L::KS + c * L::HB);
       if (dok[1]) dma16b(rk, dvoff[1] + 64 * c, kvdst + slot * L::KS + c * L::HB + 1024);
     }
-    const rsrc_t rb = real ? buf_rsrc(bptr, bend) : buf_rsrc(bptr, bptr);
+    const rsrc_t rb = wbias.rsrc(real);
 #pragma unroll
     for (int j = 0; j < L::BOPS; ++j) dma16b(rb, bvoff[j], bdst[j] + slot * L::BS);
-    if (issued + 1 < nkt) {
-      dptr += tstep;
-      bptr += 1024;
-    }
+    wkv.advance();
+    wbias.advance();
     ++issued;
   };
 
