@@ -481,15 +481,20 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
     auto step = [&](int t, auto slot) {
       constexpr int S = decltype(slot)::value;
       constexpr uint32_t so = S * L::SLOT;
-      uint32_t wr[QD_ROWS];  // key bits of tile t per row (0 for a row past the end)
+      // key bits of tile t for this wave's row (0 for a row past the end)
+      uint32_t bits = 0;
+      if constexpr (FULL) {
+        bits = rok ? in_range_bits(t, G.n) : 0u;
+        wait_vm<(QD_SLOTS - 2) * QD_OPS>();  // tile t has landed
+        lds_barrier();
+        issue((S + QD_SLOTS - 1) % QD_SLOTS);  // tile t + QD_SLOTS - 1 into the slot of tile t - 1
+      } else {
+        uint32_t wr[QD_ROWS];  // per row of the group
 #pragma unroll
-      for (int i = 0; i < QD_ROWS; ++i)
-        wr[i] = i < nrows ? (FULL ? in_range_bits(t, G.n)
-                                  : const_load(a.kbits + (int64_t)(r0 + i) * nkt + t))
-                          : 0u;
-      wait_vm<(QD_SLOTS - 2) * QD_OPS>();  // tile t has landed
-      lds_barrier();
-      if (!FULL) {
+        for (int i = 0; i < QD_ROWS; ++i)
+          wr[i] = i < nrows ? const_load(a.kbits + (int64_t)(r0 + i) * nkt + t) : 0u;
+        wait_vm<(QD_SLOTS - 2) * QD_OPS>();
+        lds_barrier();
         bool full = true;
 #pragma unroll
         for (int i = 0; i < QD_ROWS; ++i) full = full && (i >= nrows || wr[i] == 0xffffffffu);
@@ -511,12 +516,11 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
           }
           __syncthreads();
         }
-      }
-      issue((S + QD_SLOTS - 1) % QD_SLOTS);  // tile t + QD_SLOTS - 1 into the slot of tile t - 1
-      uint32_t bits = 0;
+        issue((S + QD_SLOTS - 1) % QD_SLOTS);
 #pragma unroll
-      for (int i = 0; i < QD_ROWS; ++i)
-        if (ri == i) bits = wr[i];
+        for (int i = 0; i < QD_ROWS; ++i)
+          if (ri == i) bits = wr[i];
+      }
       if (!active || bits == 0u) return;
       // S^T = bias + K Q^T (lane <-> query, registers <-> keys)
       f32x16 sv;

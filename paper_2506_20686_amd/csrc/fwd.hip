@@ -30,76 +30,139 @@ namespace triattn {
 // ---- preparation ------------------------------------------------------------------
 
 // bias / scale over the zero-padded np x np map, in accumulator order (see
-// frag_tile): x = 32 t1 + l % 32 is the lane's column, y = 32 t2 + 8 j +
-// 4 (l / 32) + e its row.  bt holds bias(query x, key y) for the kernels
-// whose lanes own queries; btT holds bias(query y, key x) for the kernel
-// whose lanes own keys.  The starting node reads bias[q][k][h], the ending
-// node bias[k][q][h].
+// frag_tile): in tile (t1, t2), element 256 j + 4 l + e has x = 32 t1 + l % 32
+// as the lane's column and y = 32 t2 + 8 j + 4 (l / 32) + e as its row.  bt
+// holds bias(query x, key y) for the kernels whose lanes own queries; btT
+// holds bias(query y, key x) for the kernel whose lanes own keys.  The
+// starting node reads bias[q][k][h], the ending node bias[k][q][h].
+//
+// One workgroup per 32 x 32 block (query tile qa, key tile kb) of the map,
+// one head at a time: the block goes through LDS once and leaves as bt tile
+// (qa, kb) and btT tile (kb, qa), both written 16 bytes per thread.
 template <typename T>
 __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const T* bias,
                                                         float* bt, float* btT) {
   bias = at_sample(bias, G.bBias);
   bt = ws_at_sample(bt, G.bWs);
   btT = ws_at_sample(btT, G.bWs);
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t np = G.np, total = (int64_t)G.H * np * np;
-  if (idx >= total) return;
-  const int nt = G.nkt;
-  const int e = (int)(idx & 3), l = (int)((idx >> 2) & 63), j = (int)((idx >> 8) & 3);
-  const int64_t tt = idx >> 10;
-  const int t2 = (int)(tt % nt), t1 = (int)((tt / nt) % nt), h = (int)(tt / ((int64_t)nt * nt));
-  const int x = 32 * t1 + (l & 31), y = 32 * t2 + 8 * j + 4 * (l >> 5) + e;
-  const int n = G.n;
-  auto at = [&](int qi, int ki) -> int64_t {
-    return node == 0 ? ((int64_t)qi * n + ki) * G.H + h : ((int64_t)ki * n + qi) * G.H + h;
-  };
-  const bool in = x < n && y < n;
-  // both loads before either store
-  const float b0 = in ? (float)bias[at(x, y)] : 0.f;
-  const float b1 = in && btT ? (float)bias[at(y, x)] : 0.f;
-  bt[idx] = b0 / G.scale;
-  if (btT) btT[idx] = b1 / G.scale;
+  const int nt = G.nkt, n = G.n;
+  const int qa = blockIdx.x % nt, kb = blockIdx.x / nt;
+  const int tid = threadIdx.x;
+  __shared__ float tl[32][33];  // [query][key] of one head: bias / scale
+  // loads: query r, keys c0 .. c0 + 3 of the block
+  const int r = tid >> 3, c0 = 4 * (tid & 7);
+  const int q = 32 * qa + r;
+  // stores: element 4 tid .. 4 tid + 3 of a tile (j = tid / 64, l = tid % 64)
+  const int l = tid & 63, x = l & 31, y0 = 8 * (tid >> 6) + 4 * (l >> 5);
+  for (int h = 0; h < G.H; ++h) {
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int k = 32 * kb + c0 + e;
+      const int qc = min(q, n - 1), kc = min(k, n - 1);  // in bounds; zero outside the map
+      const int64_t at = node == 0 ? ((int64_t)qc * n + kc) * G.H + h : ((int64_t)kc * n + qc) * G.H + h;
+      const float b = (float)bias[at];
+      v[e] = q < n && k < n ? b : 0.f;
+    }
+    __syncthreads();  // the previous head's tile has been read
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tl[r][c0 + e] = v[e] / G.scale;
+    __syncthreads();
+    const f32x4 o = {tl[x][y0], tl[x][y0 + 1], tl[x][y0 + 2], tl[x][y0 + 3]};
+    *(f32x4*)(bt + (((int64_t)h * nt + qa) * nt + kb) * 1024 + 4 * tid) = o;
+    if (btT) {
+      const f32x4 p = {tl[y0][x], tl[y0 + 1][x], tl[y0 + 2][x], tl[y0 + 3][x]};
+      *(f32x4*)(btT + (((int64_t)h * nt + kb) * nt + qa) * 1024 + 4 * tid) = p;
+    }
+  }
 }
 
 // kbits[row][t]: bit e set iff key 32 t + e < n and mask(row, key) != 0.
-// rowfull[row] = 1 iff every key < n is valid for the row.  One workgroup
-// per row, thread t builds word t (nkt <= 256 for n <= 8192).  The starting
-// node reads mask[row][key], the ending node mask[key][row].
-__global__ __launch_bounds__(256) void prep_kbits_kernel(Geom G, int node, const uint8_t* mask,
-                                                         uint32_t* kbits, uint32_t* rowfull) {
+// rowfull[row] = 1 iff every key < n is valid for the row.
+//
+// Starting node, mask[row][key] (a row's keys contiguous): one workgroup per
+// row; each wave reads 64 consecutive keys per load and forms two words with
+// a ballot.
+__global__ __launch_bounds__(256) void prep_kbits_start_kernel(Geom G, const uint8_t* mask,
+                                                               uint32_t* kbits,
+                                                               uint32_t* rowfull) {
   mask = at_sample(mask, G.bMask);
   kbits = ws_at_sample(kbits, G.bWs);
   rowfull = ws_at_sample(rowfull, G.bWs);
-  const int row = blockIdx.x, t = threadIdx.x, n = G.n;
-  uint32_t bits = 0, want = 0;
-  if (t < G.nkt) {
-    for (int e = 0; e < 32; ++e) {
-      const int key = 32 * t + e;
-      if (key >= n) break;
-      const bool ok = mask == nullptr ||
-                      mask[node == 0 ? (int64_t)row * n + key : (int64_t)key * n + row] != 0;
-      bits |= (ok ? 1u : 0u) << e;
-      want |= 1u << e;
-    }
-    kbits[(int64_t)row * G.nkt + t] = bits;
+  const int row = blockIdx.x, n = G.n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  bool full = true;
+  for (int k0 = 64 * wave; k0 < G.np; k0 += 256) {
+    const int key = k0 + lane;
+    const bool in = key < n;
+    const bool ok = in && (mask == nullptr || mask[(int64_t)row * n + min(key, n - 1)] != 0);
+    const uint64_t b = __ballot(ok), want = __ballot(in);
+    full = full && b == want;
+    const int t = k0 >> 5;
+    if (lane == 0) kbits[(int64_t)row * G.nkt + t] = (uint32_t)b;
+    if (lane == 1 && t + 1 < G.nkt) kbits[(int64_t)row * G.nkt + t + 1] = (uint32_t)(b >> 32);
   }
-  const int full = __syncthreads_and(bits == want);
-  if (t == 0) rowfull[row] = full ? 1u : 0u;
+  const int all = __syncthreads_and(full);
+  if (threadIdx.x == 0) rowfull[row] = all ? 1u : 0u;
+}
+
+// Ending node, mask[key][row] (consecutive rows contiguous): one workgroup
+// per 64 rows, lane <-> row; wave w builds words w, w + 16, ... of the 64
+// rows, one 64-byte read of a key's row of the mask per bit.
+__global__ __launch_bounds__(1024) void prep_kbits_end_kernel(Geom G, const uint8_t* mask,
+                                                              uint32_t* kbits,
+                                                              uint32_t* rowfull) {
+  mask = at_sample(mask, G.bMask);
+  kbits = ws_at_sample(kbits, G.bWs);
+  rowfull = ws_at_sample(rowfull, G.bWs);
+  const int n = G.n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row = 64 * blockIdx.x + lane;
+  const bool rin = row < G.nr;
+  const int rowc = min(row, G.nr - 1);  // in-bounds address for lanes past the last row
+  bool full = true;
+  for (int t = wave; t < G.nkt; t += 16) {
+    const uint32_t want = in_range_bits(t, n);
+    uint32_t bits = rin ? want : 0u;
+    if (mask != nullptr) {
+      // every load first (addresses clamped in bounds), then the bits
+      uint8_t m[32];
+#pragma unroll
+      for (int e = 0; e < 32; ++e) m[e] = mask[(int64_t)min(32 * t + e, n - 1) * n + rowc];
+#pragma unroll
+      for (int e = 0; e < 32; ++e)
+        if (m[e] == 0) bits &= ~(1u << e);
+    }
+    if (rin) kbits[(int64_t)row * G.nkt + t] = bits;
+    full = full && bits == want;
+  }
+  __shared__ uint32_t part[16][64];
+  part[wave][lane] = full ? 1u : 0u;
+  __syncthreads();
+  if (wave == 0 && rin) {
+    uint32_t all = 1u;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) all &= part[w][lane];
+    rowfull[row] = all;
+  }
 }
 
 template <typename T>
 hipError_t launch_prep(const Geom& g, int node, const T* bias, const uint8_t* mask, const Prep& p,
                        hipStream_t s) {
-  const int64_t nb = ((int64_t)g.H * g.np * g.np + 255) / 256;
   {
     KernelTimer t(K_PREP_BIAS, s);
-    hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)nb, 1, (unsigned)g.batch), dim3(256), 0, s, g, node, bias,
-                       p.bt, p.btT);
+    hipLaunchKernelGGL(prep_bias_kernel<T>, dim3((unsigned)(g.nkt * g.nkt), 1, (unsigned)g.batch), dim3(256), 0, s,
+                       g, node, bias, p.bt, p.btT);
   }
   {
     KernelTimer t(K_PREP_KBITS, s);
-    hipLaunchKernelGGL(prep_kbits_kernel, dim3((unsigned)g.nr, 1, (unsigned)g.batch), dim3(256), 0, s, g, node, mask,
-                       p.kbits, p.rowfull);
+    if (node == 0)
+      hipLaunchKernelGGL(prep_kbits_start_kernel, dim3((unsigned)g.nr, 1, (unsigned)g.batch), dim3(256), 0, s, g,
+                         mask, p.kbits, p.rowfull);
+    else
+      hipLaunchKernelGGL(prep_kbits_end_kernel, dim3((unsigned)((g.nr + 63) / 64), 1, (unsigned)g.batch), dim3(1024),
+                         0, s, g, mask, p.kbits, p.rowfull);
   }
   return hipGetLastError();
 }
@@ -601,15 +664,19 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
     constexpr bool FULL = decltype(full_c)::value;
     auto step = [&](int t, auto slot) {
       constexpr int S = decltype(slot)::value;
-      uint32_t wr[FO_ROWS];  // key bits of tile t per row (0 for a row past the end)
+      // key bits of tile t for this wave's row (0 for a row past the end)
+      uint32_t wb = 0;
+      if constexpr (FULL) {
+        wb = rok ? in_range_bits(t, G.n) : 0u;
+        wait_vm<(FO_SLOTS - 2) * L::OPS>();  // tile t has landed (tiles after it may be in flight)
+        lds_barrier();
+      } else {
+        uint32_t wr[FO_ROWS];  // per row of the group
 #pragma unroll
-      for (int i = 0; i < FO_ROWS; ++i)
-        wr[i] = i < nrows ? (FULL ? in_range_bits(t, G.n)
-                                  : const_load(a.kbits + (int64_t)(r0 + i) * nkt + t))
-                          : 0u;
-      wait_vm<(FO_SLOTS - 2) * L::OPS>();  // tile t has landed (tiles after it may be in flight)
-      lds_barrier();
-      if (!FULL) {
+        for (int i = 0; i < FO_ROWS; ++i)
+          wr[i] = i < nrows ? const_load(a.kbits + (int64_t)(r0 + i) * nkt + t) : 0u;
+        wait_vm<(FO_SLOTS - 2) * L::OPS>();
+        lds_barrier();
         bool full = true;
 #pragma unroll
         for (int i = 0; i < FO_ROWS; ++i) full = full && (i >= nrows || wr[i] == 0xffffffffu);
@@ -617,12 +684,11 @@ void fwd_dma_kernel(FwdArgs<bf16> a) {
           zero_invalid_v(slot, wr);
           __syncthreads();
         }
+#pragma unroll
+        for (int i = 0; i < FO_ROWS; ++i)
+          if (ri == i) wb = wr[i];
       }
       issue((S + FO_SLOTS - 1) % FO_SLOTS);  // tile t + SLOTS - 1 into the slot of tile t - 1
-      uint32_t wb = 0;
-#pragma unroll
-      for (int i = 0; i < FO_ROWS; ++i)
-        if (ri == i) wb = wr[i];
       if (!active || wb == 0u) return;
       F kfr[KA];
 #pragma unroll
