@@ -1174,28 +1174,46 @@ __global__ __launch_bounds__(64 * D6_WAVES) void db_dma64_kernel(BwdArgs<bf16> a
 
 // dbias at (query q, key k, head h) = sum of the slabs in chunk order; the
 // starting node stores it at [q][k][h], the ending node at [k][q][h].  One
-// thread per (h, q, 4 consecutive keys): every slab read is 16 contiguous
-// bytes (the slab rows are np long, a multiple of 32).
+// workgroup per 32 x 32 block (query tile qa, key tile kb), four heads at a
+// time: every slab read is 16 contiguous bytes of a slab row, the sums pass
+// through LDS, and the stores run along the output's fastest axes (key, then
+// head for the starting node; query, then head for the ending node).
+constexpr int DBR_HG = 4;  // heads per pass
 template <typename T>
 __global__ __launch_bounds__(256) void db_reduce_kernel(Geom G, int node, int nrc,
                                                         const float* slabs, T* dbias) {
   slabs = ws_at_sample(slabs, G.bWs);
   dbias = at_sample(dbias, G.bBias);
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;  // (h, q, k / 4), k fastest
-  const int64_t n = G.n, nk4 = (n + 3) / 4;
-  if (idx >= (int64_t)G.H * n * nk4) return;
-  const int k0 = (int)(idx % nk4) * 4, q = (int)((idx / nk4) % n), h = (int)(idx / (n * nk4));
+  const int nt = G.nkt, n = G.n, tid = threadIdx.x;
+  const int qa = blockIdx.x % nt, kb = blockIdx.x / nt;
   const int64_t plane = (int64_t)G.np * G.np;
-  const float* p = slabs + (int64_t)h * plane + (int64_t)q * G.np + k0;
-  f32x4 s = *(const f32x4*)p;
-  for (int c = 1; c < nrc; ++c) s += *(const f32x4*)(p + (int64_t)c * G.H * plane);
+  __shared__ float tl[DBR_HG][32][33];
+  const int r = tid >> 3, c0 = 4 * (tid & 7);  // sums: query 32 qa + r, keys 32 kb + c0 .. +3
+  for (int h0 = 0; h0 < G.H; h0 += DBR_HG) {
+    const int hn = min(DBR_HG, G.H - h0);
+    if (h0 > 0) __syncthreads();  // the previous pass's stores have read the tile
+    for (int hh = 0; hh < hn; ++hh) {
+      const float* p = slabs + (int64_t)(h0 + hh) * plane + (int64_t)(32 * qa + r) * G.np + 32 * kb + c0;
+      f32x4 sum = *(const f32x4*)p;
+      for (int c = 1; c < nrc; ++c) sum += *(const f32x4*)(p + (int64_t)c * G.H * plane);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int k = k0 + e;
-    if (k >= n) break;
-    const int64_t at =
-        node == 0 ? ((int64_t)q * n + k) * G.H + h : ((int64_t)k * n + q) * G.H + h;
-    dbias[at] = (T)s[e];
+      for (int e = 0; e < 4; ++e) tl[hh][r][c0 + e] = sum[e];
+    }
+    __syncthreads();
+    // element e of the block: outer = e / 32, inner = e % 32 (consecutive threads along
+    // the output's key axis for the starting node, its query axis for the ending node)
+    for (int e = tid; e < 1024; e += 256) {
+      const int outer = e >> 5, inner = e & 31;
+      const int q = node == 0 ? outer : inner, k = node == 0 ? inner : outer;
+      const int qi = 32 * qa + q, ki = 32 * kb + k;
+      if (qi >= n || ki >= n) continue;
+      const int64_t at = (node == 0 ? ((int64_t)qi * n + ki) : ((int64_t)ki * n + qi)) * G.H + h0;
+      if (G.H % DBR_HG == 0) {  // four heads in one aligned store
+        store4(dbias + at, f32x4{tl[0][q][k], tl[1][q][k], tl[2][q][k], tl[3][q][k]});
+      } else {
+        for (int hh = 0; hh < hn; ++hh) dbias[at + hh] = (T)tl[hh][q][k];
+      }
+    }
   }
 }
 
@@ -1278,14 +1296,14 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
     }
   }
   {
-    const int64_t nred = (int64_t)g.H * g.n * ((g.n + 3) / 4);
+    const unsigned nblk = (unsigned)(g.nkt * g.nkt);
     KernelTimer t(K_DB_REDUCE, s);
     if (dbias_f32)
-      hipLaunchKernelGGL(db_reduce_kernel<float>, dim3((unsigned)((nred + 255) / 256), 1, (unsigned)g.batch), dim3(256),
-                         0, s, g, node, ws.nrc, ws.slabs, dbias_f32);
+      hipLaunchKernelGGL(db_reduce_kernel<float>, dim3(nblk, 1, (unsigned)g.batch), dim3(256), 0, s, g, node,
+                         ws.nrc, ws.slabs, dbias_f32);
     else
-      hipLaunchKernelGGL(db_reduce_kernel<T>, dim3((unsigned)((nred + 255) / 256), 1, (unsigned)g.batch), dim3(256), 0,
-                         s, g, node, ws.nrc, ws.slabs, dbias);
+      hipLaunchKernelGGL(db_reduce_kernel<T>, dim3(nblk, 1, (unsigned)g.batch), dim3(256), 0, s, g, node, ws.nrc,
+                         ws.slabs, dbias);
   }
   return hipGetLastError();
 }
