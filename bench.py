@@ -128,8 +128,8 @@ def mfma_calibration(launches, blocks=1024, iters=2000):
 # Sources whose change can change a kernel family's memory traffic (its
 # kernels, the shared device headers, the host code that picks launch shapes).
 SOURCE_FAMILIES = {
-    "tri": ("fwd.hip", "bwd.hip", "dkdv.hip", "bwd.h", "api.hip", "common.h", "dma.h", "stage.h",
-            "kernels.h"),
+    "tri": ("fwd.hip", "bwd.hip", "dkdv.hip", "dkdv_end.hip", "dkdv_dma.h", "bwd.h", "api.hip",
+            "common.h", "dma.h", "stage.h", "kernels.h"),
     "lnl": ("lnl.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
     "trn": ("trn.hip", "api.hip", "common.h", "dma.h", "kernels.h"),
 }

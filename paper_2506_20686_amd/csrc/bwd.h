@@ -55,8 +55,10 @@ __device__ inline void to_sample(BwdArgs<T>& a) {
 }
 
 // dK and dV (dkdv.hip): the DMA kernels for bf16 (16, 32 or 64 channels), the
-// register-staged ones for fp32.
+// register-staged ones for fp32.  node: 0 starting, 1 ending (the ending
+// node's bf16 kernels are built separately, dkdv_end.hip).
 template <typename T>
-hipError_t launch_dkdv(const BwdArgs<T>& a, hipStream_t s);
+hipError_t launch_dkdv(const BwdArgs<T>& a, int node, hipStream_t s);
+hipError_t launch_dkdv_dma_end(const BwdArgs<bf16>& a, hipStream_t s);
 
 }  // namespace triattn

@@ -1270,7 +1270,7 @@ hipError_t launch_bwd(const Geom& g, int node, const Prep& p, const BwdWs& ws, c
   }
   {
     KernelTimer t(K_DKDV, s);
-    const hipError_t e = launch_dkdv(a, s);
+    const hipError_t e = launch_dkdv(a, node, s);
     if (e != hipSuccess) return e;
   }
   {
