@@ -326,6 +326,18 @@ struct QdL {
   static constexpr int OPS = UNITS / QD_WAVES;       // DMA ops per thread per tile
   static constexpr int WPE = D == 64 ? 2 : 4;        // waves per SIMD
   static_assert(UNITS % QD_WAVES == 0, "DMA units must split evenly over the waves");
+  // source of unit u: K or V rows of channel half c, or bias tile t
+  static constexpr int source(int u) {
+    return u < KVU ? 2 * ((u >> 1) / (2 * QD_ROWS)) + ((u >> 1) % (2 * QD_ROWS) < QD_ROWS ? 0 : 1)
+                   : 2 * NH + (u - KVU) / 4;
+  }
+  // whether the OPS units of every wave share one source
+  static constexpr bool one_source() {
+    for (int w = 0; w < QD_WAVES; ++w)
+      for (int j = 1; j < OPS; ++j)
+        if (source(OPS * w + j) != source(OPS * w)) return false;
+    return true;
+  }
   static_assert(QD_SLOTS * SLOT <= 65536, "slot offsets must fit the LDS immediate");
 };
 
@@ -424,10 +436,11 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
       dok[j] = true;
     }
   }
-  // With one channel half, the units of a wave all come from one source (the
-  // K rows, the V rows or one bias tile): one walking resource serves them,
-  // the rows told apart by their lane offsets.  Otherwise each unit walks its own.
-  constexpr bool ONE = NH == 1;
+  // When the units of every wave come from one source (the K rows, the V rows
+  // or one bias tile, of one channel half), one walking resource serves a
+  // wave's units, the rows told apart by their lane offsets.  Otherwise each
+  // unit walks its own.
+  constexpr bool ONE = L::one_source();
   constexpr int NW = ONE ? 1 : QD_OPS;
   Walk wk[NW];
 #pragma unroll
