@@ -923,36 +923,37 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
         __syncthreads();
       }
     }
-    issue((S + 2) % DBD_SLOTS);  // row r + 2 into the slot of row r - 1
-    if (!active || wb == 0u) return;
-    float l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT);
-    const float nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT + 512);
-    if (!qok) l2 = pos_inf();
-    const F q0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OQ);
-    const F k0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OK);
-    f32x16 sv = M::mma(k0, q0, binit);  // S^T = bias + K Q^T
-    if constexpr (D == 32) {
-      const F q1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OQ);
-      const F k1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OK);
-      sv = M::mma(k1, q1, sv);
+    // the tile's operand reads first, then the DMA issue, then the products
+    const bool act = active && wb != 0u;
+    F q0{}, k0{}, q1{}, k1{}, d0{}, e0{}, v0{}, d1{}, e1{}, v1{};
+    float l2 = 0.f, nd = 0.f;
+    if (act) {
+      l2 = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT);
+      nd = *(const TRIATTN_LDS float*)(uintptr_t)(rl + S * DBD_SLOT + 512);
+      q0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OQ);
+      k0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OK);
+      d0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_ODA);
+      e0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OLO);
+      v0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OV);
+      if constexpr (D == 32) {
+        q1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OQ);
+        k1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OK);
+        d1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_ODA);
+        e1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OLO);
+        v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
+      }
     }
+    issue((S + 2) % DBD_SLOTS);  // row r + 2 into the slot of row r - 1
+    if (!act) return;
+    if (!qok) l2 = pos_inf();
+    f32x16 sv = M::mma(k0, q0, binit);  // S^T = bias + K Q^T
+    if constexpr (D == 32) sv = M::mma(k1, q1, sv);
     if (wb != 0xffffffffu) mask_rows(sv, wb, g);
-    const F d0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_ODA);
-    const F e0 = lds_load16<F>(rq0 + S * DBD_SLOT + DBD_OLO);
-    const F v0 = lds_load16<F>(rk0 + S * DBD_SLOT + DBD_OV);
     f32x16 dpv = splat16(nd);  // dP^T - D = V dA^T - D (hi and lo parts)
     dpv = M::mma(v0, d0, dpv);
-    if constexpr (D == 32) {
-      const F d1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_ODA);
-      const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
-      dpv = M::mma(v1, d1, dpv);
-    }
+    if constexpr (D == 32) dpv = M::mma(v1, d1, dpv);
     dpv = M::mma(v0, e0, dpv);
-    if constexpr (D == 32) {
-      const F e1 = lds_load16<F>(rq1 + S * DBD_SLOT + DBD_OLO);
-      const F v1 = lds_load16<F>(rk1 + S * DBD_SLOT + DBD_OV);
-      dpv = M::mma(v1, e1, dpv);
-    }
+    if constexpr (D == 32) dpv = M::mma(v1, e1, dpv);
 #pragma unroll
     for (int v = 0; v < 16; ++v)
       acc[v] += __builtin_amdgcn_exp2f(__builtin_fmaf(sv[v], c1, -l2)) * dpv[v];
