@@ -321,28 +321,52 @@ hipError_t launch_lnl_fwd(const LnlArgs& a, hipStream_t s) {
 // rows k of 16-byte chunks of 8 columns (chunk c of row k at slot c ^ (k % 8),
 // 72 chunk slots per row), each wave walking 32-row units.  do1^T tiles
 // [32 k][32 m] = W rows x dO2 rows^T: the dO2 B fragments (lane <-> row m,
-// 8 consecutive columns) come straight from HBM, D steps ahead.
+// 8 consecutive columns) come straight from HBM.  The 16-column steps of
+// the leading fast tiles (whole 32-column pieces of one output) form one
+// stream across the wave's units, LBX_AHEAD fragments in flight, so the next
+// unit's first fragments are in flight during this unit's epilogue; the
+// remaining steps read two 4-column pieces each.  No load sits in a branch:
+// a load whose result joins another value makes the wave wait for it there.
 constexpr int LBX_WAVES = 8;
 constexpr int LBX_PITCH = 72 * 16;
-constexpr int LBX_AHEAD = 4;  // dO2 fragments in flight per lane
+constexpr int LBX_AHEAD = 8;  // fast-step fragments in flight per lane (a multiple of 4)
+constexpr int LBX_SLOW_AHEAD = 2;  // other steps whose fragments are loaded at the unit's start
 
 __device__ inline uint32_t lbx_w_off(int k, int c) { return k * LBX_PITCH + 16 * (c ^ (k & 7)); }
 
-// dO2 fragment of 16-column step s for row m: columns 16 s + 8 g .. + 7.
-__device__ inline bf16x8 lbx_load_b(const LnlBwdArgs& a, const LnlQuad* quad, int s, int g,
-                                    int64_t m) {
+// dO2 fragment of fast step s (columns 16 s + 8 g .. + 7, inside one output)
+// for row mrow; zeros past the last row, or everywhere if !real.
+__device__ inline bf16x8 lbx_load_fast(const LnlBwdArgs& a, int s, int g, uint32_t mrow, bool real) {
   const LnlTile& tl = a.tile[s >> 1];
-  if (tl.fast) {
-    const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(tl.base, (short)0,
-                                                       (int)(uint32_t)(a.m * tl.w * 2), 0x00020000);
-    const uint32_t voff = ((uint32_t)m * (uint32_t)tl.w + (uint32_t)(tl.off + 16 * (s & 1) + 8 * g)) * 2u;
-    return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
-  }
+  const rsrc_t r = buf_rsrc_n(tl.base, real ? (uint32_t)(a.m * tl.w * 2) : 0u);
+  const uint32_t voff = (mrow * (uint32_t)tl.w + (uint32_t)(tl.off + 16 * (s & 1) + 8 * g)) * 2u;
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0));
+}
+
+// dO2 fragment of any step s for row m from two 4-column pieces of the quad
+// table.  Both loads are always issued (a missing piece reads x's first
+// bytes instead) and the pieces are zeroed after they arrive (lbx_slow_value).
+struct LbxSlow {
+  u32x2 lo, hi;
+  bool lok, hok;
+};
+__device__ inline LbxSlow lbx_load_slow(const LnlBwdArgs& a, const LnlQuad* quad, int s, int g,
+                                        int64_t m) {
   const int q = 2 * (2 * s + g);
   const LnlQuad e0 = quad[q], e1 = quad[q + 1];
   const bool ok = m < a.m;
-  const u32x2 lo = (ok && e0.p) ? *(const gu32x2*)(e0.p + m * e0.w) : u32x2{0u, 0u};
-  const u32x2 hi = (ok && e1.p) ? *(const gu32x2*)(e1.p + m * e1.w) : u32x2{0u, 0u};
+  LbxSlow r;
+  r.lok = ok && e0.p;
+  r.hok = ok && e1.p;
+  const gu32x2* dummy = (const gu32x2*)(gbf16*)a.x;
+  const gu32x2* p0 = r.lok ? (const gu32x2*)(e0.p + m * e0.w) : dummy;
+  const gu32x2* p1 = r.hok ? (const gu32x2*)(e1.p + m * e1.w) : dummy;
+  r.lo = *p0;
+  r.hi = *p1;
+  return r;
+}
+__device__ inline bf16x8 lbx_slow_value(const LbxSlow& r) {
+  const u32x2 lo = r.lok ? r.lo : u32x2{0u, 0u}, hi = r.hok ? r.hi : u32x2{0u, 0u};
   return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
 }
 
@@ -364,23 +388,41 @@ __device__ inline void lnl_quad_table(const int* start, int n_out, bf16* const* 
   }
 }
 
-__global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a) {
+// Steps [0, nf) of the fast-step stream: the 16-column steps of the leading
+// fast tiles, rounded down to a multiple of LBX_AHEAD (host side).
+// The dx kernel's 16-column steps: those holding a column below N.
+static int lbx_steps(const LnlBwdArgs& a) { return (a.ncols + 15) / 16; }
+
+static int lbx_fast_steps(const LnlBwdArgs& a) {
+  const int nsteps = lbx_steps(a);
+  int nt = 0;
+  while (2 * nt < nsteps && a.tile[nt].fast) ++nt;
+  return std::min(2 * nt, nsteps) / LBX_AHEAD * LBX_AHEAD;
+}
+
+// STREAM: at least one block of fast steps and at most LBX_SLOW_AHEAD other
+// steps, all loaded at the unit's start, so that no load of the unit loop is
+// conditional and the waits count the loads exactly (a wait that cannot count
+// them waits for all, the next unit's fragments included).
+template <bool STREAM>
+__global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a, int nf) {
   __shared__ __align__(16) char wk[LNL_K * LBX_PITCH];
   __shared__ __align__(16) LnlQuad quad[LNL_GROUP / 4];
   __shared__ __align__(16) float gam[LNL_K];
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 5, l32 = lane & 31;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nq = a.np / 4;
-  {  // W [K][N] into LDS (columns past N zero): all loads first
+  {  // W [K][N] into LDS (columns past N zero): all loads first, none in a
+     // branch (an element outside W reads W's first one and is zeroed)
     constexpr int NT = 64 * LBX_WAVES;
     constexpr int FILL = (LNL_K * (LNL_GROUP / 4) + NT - 1) / NT;
     u32x2 wv[FILL];
 #pragma unroll
     for (int i = 0; i < FILL; ++i) {
       const int idx = tid + i * NT, k = idx / nq, q = idx - k * nq;
-      wv[i] = (idx < LNL_K * nq && 4 * q < a.ncols)
-                  ? *(const u32x2*)(a.w + (int64_t)k * a.ncols + 4 * q)
-                  : u32x2{0u, 0u};
+      const bool ok = idx < LNL_K * nq && 4 * q < a.ncols;
+      const u32x2 v = *(const u32x2*)(a.w + (ok ? (int64_t)k * a.ncols + 4 * q : 0));
+      wv[i] = ok ? v : u32x2{0u, 0u};
     }
 #pragma unroll
     for (int i = 0; i < FILL; ++i) {
@@ -392,76 +434,144 @@ __global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a
   if (tid < LNL_K) gam[tid] = (float)a.gamma[tid];
   __syncthreads();
 
-  // A fragment of (k tile kt, step s): lane row k = 32 kt + l32, chunk
+  // The rows of a k tile enter the A operand permuted: operand row
+  // r = 8 j + 4 h + i (the accumulator rows that lane half h holds) reads W
+  // row 16 (j / 2) + 8 h + 4 (j % 2) + i, so that a lane ends up with two runs
+  // of 8 consecutive features per k tile (k = 32 kt + 16 a + 8 g + e in
+  // acc[kt][8 a + e]) and reads x and writes dx 16 bytes at a time.
+  const int wrow = 16 * (l32 >> 4) + 8 * ((l32 >> 2) & 1) + 4 * ((l32 >> 3) & 1) + (l32 & 3);
+  // A fragment of (k tile kt, step s): W row 32 kt + wrow, chunk
   // 2 s + g = 8 (s / 4) + (2 (s % 4) + g)  ->  ao[s % 4] + kt * 32 rows + 128 (s / 4)
   uint32_t ao[4];
 #pragma unroll
-  for (int s4 = 0; s4 < 4; ++s4) ao[s4] = lds_addr(wk) + lbx_w_off(l32, 2 * s4 + g);
-  const int nsteps = a.np / 16;
+  for (int s4 = 0; s4 < 4; ++s4) ao[s4] = lds_addr(wk) + lbx_w_off(wrow, 2 * s4 + g);
+  const int nsteps = (a.ncols + 15) / 16;  // steps past them multiply zeros
+  // fast steps: those of the leading fast tiles, a multiple of LBX_AHEAD
+  const int ns = nsteps - nf;  // the other steps
   const int64_t units = (a.m + 31) / 32;
   const int64_t stride = (int64_t)gridDim.x * LBX_WAVES;
-  for (int64_t u = (int64_t)blockIdx.x * LBX_WAVES + wave; u < units; u += stride) {
+  const int64_t u0 = (int64_t)blockIdx.x * LBX_WAVES + wave;
+  // the fast-step stream: position s of unit u, then step 0 of unit u + stride
+  bf16x8 bq[LBX_AHEAD];
+#pragma unroll
+  for (int d = 0; d < LBX_AHEAD; ++d)
+    bq[d] = lbx_load_fast(a, d, g, (uint32_t)(u0 * 32 + l32), nf > 0 && u0 < units);
+  if constexpr (STREAM) {
+    // eight empty stores (a zero-length range drops them): the unit loop
+    // is then entered with the same operations in flight as at its back edge
+    // (fragments, then a unit's stores), so the waits of a unit's first
+    // block count the stores and need not wait for them
+    const rsrc_t none = buf_rsrc_n(a.dx, 0u);
+#pragma unroll
+    for (int f = 0; f < 8; ++f) __builtin_amdgcn_raw_buffer_store_b128(u32x4{0u, 0u, 0u, 0u}, none, 16u * f, 0, 0);
+  }
+  f32x16 acc[4] = {};  // zero at the start of every unit
+  for (int64_t u = u0; u < units; u += stride) {
     const int64_t m = u * 32 + l32;
     const bool mok = m < a.m;
-    // this row's x at k = 32 kt + 8 j + 4 g + 0..3 and its statistics (for the epilogue)
-    u32x2 xq[16];
+    // this row's x at k = 32 kt + 16 a + 8 g + 0..7 (xq[2 kt + a]) and its
+    // statistics (for the epilogue).  Every load of the loop is issued
+    // unconditionally (a row past m reads the last row and is zeroed), so the
+    // waits can count them.
+    const int64_t mc = mok ? m : a.m - 1;
+    u32x4 xq[8];
 #pragma unroll
-    for (int f = 0; f < 16; ++f)
-      xq[f] = mok ? *(const u32x2*)(a.x + m * LNL_K + 8 * f + 4 * g) : u32x2{0u, 0u};
-    const float mean = mok ? a.mean[m] : 0.f, rstd = mok ? a.rstd[m] : 0.f;
+    for (int f = 0; f < 8; ++f) {
+      const u32x4 v = *(const u32x4*)(a.x + mc * LNL_K + 16 * f + 8 * g);
+      xq[f] = mok ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+    const float mean0 = a.mean[mc], rstd0 = a.rstd[mc];
+    const float mean = mok ? mean0 : 0.f, rstd = mok ? rstd0 : 0.f;
+    LbxSlow sl[LBX_SLOW_AHEAD];  // the first other steps (a step past the last reads the last)
+#pragma unroll
+    for (int i = 0; i < LBX_SLOW_AHEAD; ++i) sl[i] = lbx_load_slow(a, quad, min(nf + i, nsteps - 1), g, m);
 
-    f32x16 acc[4] = {};
-    bf16x8 bq[LBX_AHEAD];
+    auto mma_step = [&](int s, const bf16x8& b) {
+      const uint32_t ad = lds_addr(wk) + lbx_w_off(wrow, 2 * s + g);
 #pragma unroll
-    for (int d = 0; d < LBX_AHEAD; ++d) bq[d] = d < nsteps ? lbx_load_b(a, quad, d, g, m) : bf16x8{};
-    for (int s0 = 0; s0 < nsteps; s0 += LBX_AHEAD) {
+      for (int kt = 0; kt < 4; ++kt)
+        acc[kt] = Mma<bf16>::mma(lds_load16<bf16x8>(ad + kt * 32 * LBX_PITCH), b, acc[kt]);
+    };
+    const int64_t un = u + stride;
+    auto fast_block = [&](int s0) {  // steps s0 .. s0 + LBX_AHEAD - 1
+      const bool wrap = s0 + LBX_AHEAD >= nf;  // the refills belong to the next unit
+      const uint32_t mrow = (uint32_t)((wrap ? un : u) * 32 + l32);
+      const bool real = !wrap || un < units;
 #pragma unroll
       for (int d = 0; d < LBX_AHEAD; ++d) {
         const int s = s0 + d;
-        if (s < nsteps) {
-          const uint32_t ad = ao[d] + 128 * (s >> 2);
-          const bf16x8 b = bq[d];
-          if (s + LBX_AHEAD < nsteps) bq[d] = lbx_load_b(a, quad, s + LBX_AHEAD, g, m);
+        const uint32_t ad = ao[d % 4] + 128 * (s >> 2);
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
-            acc[kt] = Mma<bf16>::mma(lds_load16<bf16x8>(ad + kt * 32 * LBX_PITCH), b, acc[kt]);
-        }
+        for (int kt = 0; kt < 4; ++kt)
+          acc[kt] = Mma<bf16>::mma(lds_load16<bf16x8>(ad + kt * 32 * LBX_PITCH), bq[d], acc[kt]);
+        // the refill after the use: it can reuse the fragment's registers
+        bq[d] = lbx_load_fast(a, wrap ? d : s + LBX_AHEAD, g, mrow, real);
       }
+    };
+    if constexpr (STREAM) {
+      // at least one block (nf >= LBX_AHEAD), the first outside the loop: its
+      // waits can count this unit's x loads and the last unit's stores as
+      // issued after its fragments, and the waits after the loop know that
+      // the last block's loads were issued after everything else
+      fast_block(0);
+      for (int s0 = LBX_AHEAD; s0 < nf; s0 += LBX_AHEAD) fast_block(s0);
+    } else {
+      for (int s0 = 0; s0 < nf; s0 += LBX_AHEAD) fast_block(s0);
     }
-    // lane (row m, half g) holds do1[m][32 kt + 8 j + 4 g + i] in acc[kt][4 j + i]
+#pragma unroll
+    for (int i = 0; i < LBX_SLOW_AHEAD; ++i)
+      if (i < ns) mma_step(nf + i, lbx_slow_value(sl[i]));
+    if constexpr (!STREAM)
+      for (int i = LBX_SLOW_AHEAD; i < ns; ++i) mma_step(nf + i, lbx_slow_value(lbx_load_slow(a, quad, nf + i, g, m)));
+    // lane (row m, half g) holds do1[m][32 kt + 16 a + 8 g + e] in acc[kt][8 a + e].
+    // gamma is read from LDS per unit: an offset the compiler cannot see
+    // through keeps it from holding all 64 values in registers across the loop.
+    int gz = 8 * g;
+    asm volatile("" : "+v"(gz));
+    const float* const gl = gam + gz;
     float c1 = 0.f, c2 = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const bf16x4 xv = __builtin_bit_cast(bf16x4, xq[4 * kt + j]);
-        const f32x4 gm = *(const f32x4*)(gam + 32 * kt + 8 * j + 4 * g);
+      for (int a2 = 0; a2 < 2; ++a2) {
+        const bf16x8 xv = __builtin_bit_cast(bf16x8, xq[2 * kt + a2]);
+        const f32x4 g0 = *(const f32x4*)(gl + 32 * kt + 16 * a2), g1 = *(const f32x4*)(gl + 32 * kt + 16 * a2 + 4);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float xh = ((float)xv[i] - mean) * rstd;
-          const float wdy = acc[kt][4 * j + i] * gm[i];
+        for (int e = 0; e < 8; ++e) {
+          const float xh = ((float)xv[e] - mean) * rstd;
+          const float wdy = acc[kt][8 * a2 + e] * (e < 4 ? g0[e] : g1[e - 4]);
           c1 = fmaf(xh, wdy, c1);
           c2 += wdy;
         }
       }
     c1 = wave_xor32_sum(c1) * (1.f / LNL_K);
     c2 = wave_xor32_sum(c2) * (1.f / LNL_K);
-    if (mok) {
+    u32x4 pk[8];  // dx of the lane's 64 features, bf16
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const bf16x4 xv = __builtin_bit_cast(bf16x4, xq[4 * kt + j]);
-          const f32x4 gm = *(const f32x4*)(gam + 32 * kt + 8 * j + 4 * g);
-          f32x4 d;
+      for (int a2 = 0; a2 < 2; ++a2) {
+        const bf16x8 xv = __builtin_bit_cast(bf16x8, xq[2 * kt + a2]);
+        const f32x4 g0 = *(const f32x4*)(gl + 32 * kt + 16 * a2), g1 = *(const f32x4*)(gl + 32 * kt + 16 * a2 + 4);
+        bf16x8 d;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float xh = ((float)xv[i] - mean) * rstd;
-            d[i] = rstd * (acc[kt][4 * j + i] * gm[i] - c1 * xh - c2);
-          }
-          store4(a.dx + m * LNL_K + 32 * kt + 8 * j + 4 * g, d);
+        for (int e = 0; e < 8; ++e) {
+          const float xh = ((float)xv[e] - mean) * rstd;
+          d[e] = (bf16)(rstd * (acc[kt][8 * a2 + e] * (e < 4 ? g0[e] : g1[e - 4]) - c1 * xh - c2));
         }
-    }
+        pk[2 * kt + a2] = __builtin_bit_cast(u32x4, d);
+      }
+    // The next unit's accumulators are zeroed before the stores are issued, so
+    // the stores' data never sits in registers written while they are in flight.
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) acc[kt] = f32x16{};
+    asm volatile("" : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]) : : "memory");
+    // every lane stores (the buffer range drops rows past m): no branch, so
+    // the waits of the next unit can count the stores
+    const rsrc_t rdx = buf_rsrc_n(a.dx, (uint32_t)(a.m * LNL_K * 2));
+    const uint32_t vdx = (uint32_t)m * (uint32_t)(LNL_K * 2) + 16u * (uint32_t)g;
+#pragma unroll
+    for (int f = 0; f < 8; ++f) __builtin_amdgcn_raw_buffer_store_b128(pk[f], rdx, vdx + 32u * f, 0, 0);
   }
 }
 
@@ -500,6 +610,44 @@ __device__ inline uint32_t lbg_swz_lane(int lane) {
 }
 __device__ inline uint32_t lbg_swz_off(int p, int col) {  // byte offset of (row p, column col)
   return p * 256 + 16 * ((col >> 3) ^ (4 * (p & 3))) + 2 * (col & 7);
+}
+
+// The A operand's staged reads of a unit, one wait for all: x^T at
+// xa (+ 2048 j, four transposed reads) and the mean and rstd of its
+// positions at sp (runs at + 0, 32, 64, 96 and, for rstd, + 1024).
+__device__ inline void lbg_a_reads(uint32_t xa, uint32_t sp, s16x4 (&xr)[4], f32x4 (&st)[8]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %12\n\tds_read_b64_tr_b16 %1, %12 offset:2048\n\t"
+      "ds_read_b64_tr_b16 %2, %12 offset:4096\n\tds_read_b64_tr_b16 %3, %12 offset:6144\n\t"
+      "ds_read_b128 %4, %13\n\tds_read_b128 %5, %13 offset:32\n\t"
+      "ds_read_b128 %6, %13 offset:1024\n\tds_read_b128 %7, %13 offset:1056\n\t"
+      "ds_read_b128 %8, %13 offset:64\n\tds_read_b128 %9, %13 offset:96\n\t"
+      "ds_read_b128 %10, %13 offset:1088\n\tds_read_b128 %11, %13 offset:1120\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(xr[0]), "=&v"(xr[1]), "=&v"(xr[2]), "=&v"(xr[3]), "=&v"(st[0]), "=&v"(st[1]),
+        "=&v"(st[2]), "=&v"(st[3]), "=&v"(st[4]), "=&v"(st[5]), "=&v"(st[6]), "=&v"(st[7])
+      : "v"(xa), "v"(sp));
+}
+
+// Transposed reads of three B tiles (four each, at b[t] + j s[t]), one wait.
+__device__ inline void lbg_b_reads3(const uint32_t (&b)[3], const uint32_t (&st)[3], s16x4 (&r)[12]) {
+  uint32_t ad[12];
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ad[4 * t + j] = b[t] + j * st[t];
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %12\n\tds_read_b64_tr_b16 %1, %13\n\t"
+      "ds_read_b64_tr_b16 %2, %14\n\tds_read_b64_tr_b16 %3, %15\n\t"
+      "ds_read_b64_tr_b16 %4, %16\n\tds_read_b64_tr_b16 %5, %17\n\t"
+      "ds_read_b64_tr_b16 %6, %18\n\tds_read_b64_tr_b16 %7, %19\n\t"
+      "ds_read_b64_tr_b16 %8, %20\n\tds_read_b64_tr_b16 %9, %21\n\t"
+      "ds_read_b64_tr_b16 %10, %22\n\tds_read_b64_tr_b16 %11, %23\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]),
+        "=&v"(r[6]), "=&v"(r[7]), "=&v"(r[8]), "=&v"(r[9]), "=&v"(r[10]), "=&v"(r[11])
+      : "v"(ad[0]), "v"(ad[1]), "v"(ad[2]), "v"(ad[3]), "v"(ad[4]), "v"(ad[5]), "v"(ad[6]),
+        "v"(ad[7]), "v"(ad[8]), "v"(ad[9]), "v"(ad[10]), "v"(ad[11]));
 }
 
 // s_waitcnt vmcnt(n) for a wave-uniform n in [0, 15].
@@ -607,34 +755,34 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
   const bf16x2 one2 = {(bf16)1.f, (bf16)1.f};
   const int64_t units = (a.m + 31) / 32;
   // this wave's pieces of a unit (the same nw for every unit); the two
-  // statistics pieces need only the unit's 32 x 4 bytes
-  // (the table is read once per unit and its fields made wave-uniform, so the
-  // buffer resources live in scalar registers and each piece is one instruction)
+  // statistics pieces need only the unit's 32 x 4 bytes.  The table is read
+  // once, before the loop, and its fields made wave-uniform, so the buffer
+  // resources live in scalar registers and each piece is one instruction.
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  constexpr int MAXW = LBG_MAXOPS / LBG_WAVES;  // pieces per wave, at most
+  rsrc_t prs[MAXW];
+  uint32_t prow[MAXW], pvo[MAXW], plds[MAXW];
+#pragma unroll
+  for (int i = 0; i < MAXW; ++i) {
+    const LbgOp op = ops[min(wave_u + LBG_WAVES * i, nops - 1)];
+    // (readfirstlane returns int: widen through uint32_t, never sign-extend)
+    const uint64_t src =
+        (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)op.src) |
+        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)((uintptr_t)op.src >> 32))
+         << 32);
+    const uint32_t nbytes = __builtin_amdgcn_readfirstlane(op.nbytes);
+    prs[i] = __builtin_amdgcn_make_buffer_rsrc((void*)(uintptr_t)src, (short)0, (int)nbytes, 0x00020000);
+    prow[i] = __builtin_amdgcn_readfirstlane(op.rowbytes);
+    pvo[i] = __builtin_amdgcn_readfirstlane(op.voff);
+    plds[i] = __builtin_amdgcn_readfirstlane(op.lds);
+  }
   auto issue = [&](int64_t u, int slot) {
     if (u >= units) return;
-    LbgOp op[LBG_MAXOPS / LBG_WAVES];  // read unconditionally: one wait for all
 #pragma unroll
-    for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i)
-      op[i] = ops[min(wave_u + LBG_WAVES * i, nops - 1)];
-#pragma unroll
-    for (int i = 0; i < LBG_MAXOPS / LBG_WAVES; ++i) {
+    for (int i = 0; i < MAXW; ++i) {
       if (i >= nw) break;
-      // (readfirstlane returns int: widen through uint32_t, never sign-extend)
-      const uint64_t src =
-          (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)op[i].src) |
-          ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(
-               (uint32_t)((uintptr_t)op[i].src >> 32))
-           << 32);
-      const uint32_t rowbytes = __builtin_amdgcn_readfirstlane(op[i].rowbytes);
-      const uint32_t pvoff = __builtin_amdgcn_readfirstlane(op[i].voff);
-      const uint32_t plds = __builtin_amdgcn_readfirstlane(op[i].lds);
-      const uint32_t nbytes = __builtin_amdgcn_readfirstlane(op[i].nbytes);
-      const rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void*)(uintptr_t)src, (short)0,
-                                                         (int)nbytes, 0x00020000);
-      const uint32_t voff =
-          (uint32_t)u * 32u * rowbytes + pvoff + (rowbytes == 256 ? lswz : lplain);
-      if (rowbytes != 4 || lane < 8) dma16b(r, voff, stage + slot * sb + plds);
+      const uint32_t voff = (uint32_t)u * 32u * prow[i] + pvo[i] + (prow[i] == 256 ? lswz : lplain);
+      if (prow[i] != 4 || lane < 8) dma16b(prs[i], voff, stage + slot * sb + plds[i]);
     }
   };
   int64_t u = blockIdx.x;
@@ -649,44 +797,55 @@ __global__ __launch_bounds__(64 * LBG_WAVES) void lnl_bwd_g_kernel(LnlBwdArgs a)
     lds_barrier();  // for every wave; and the slot refilled next is free
     issue(u + (int64_t)ahead * gridDim.x, (it + ahead) % nslots);
     const uint32_t so = slot * sb;
-  // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
+    // A = xhat^T: x of positions {4 g + 0..3, 8 + 4 g + 0..3} (+ 16 u) at
     // channels 32 kt + l32, normalised with those positions' statistics
     s16x4 xr[4];
-    tr_read4_wait(xa + so, xa + so + 2048, xa + so + 4096, xa + so + 6144, xr);
+    f32x4 st[8];  // per half h: mean of the two runs of 4, then their rstd
+    lbg_a_reads(xa + so, sa + so + 16 * g, xr, st);
     bf16x8 af[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const bf16x8 xv = tr_frag(xr, h);
-      // mean and rstd of the 8 positions (two runs of 4)
-      f32x4 st[4];
-      const uint32_t sp = sa + so + 4 * (16 * h + 4 * g);
-      b128_read4_wait(sp, sp + 32, sp + 1024, sp + 1024 + 32, st);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        af[h][e] = (bf16)(((float)xv[e] - st[0][e]) * st[2][e]);
-        af[h][4 + e] = (bf16)(((float)xv[4 + e] - st[1][e]) * st[3][e]);
+        af[h][e] = (bf16)(((float)xv[e] - st[4 * h][e]) * st[4 * h + 2][e]);
+        af[h][4 + e] = (bf16)(((float)xv[4 + e] - st[4 * h + 1][e]) * st[4 * h + 3][e]);
       }
     }
+    // the B tiles three at a time (one wait per three)
 #pragma unroll
-    for (int i = 0; i < LBG_TPW; ++i) {
-      if (i < nt_w) {
-        s16x4 br[4];
-        const uint32_t b0 = ba[i] + so, bs = 8 * bp[i];
-        tr_read4_wait(b0, b0 + bs, b0 + 2 * bs, b0 + 3 * bs, br);
+    for (int i0 = 0; i0 < LBG_TPW; i0 += 3) {
+      if (i0 >= nt_w) break;
+      uint32_t b[3], bst[3];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const bf16x8 bf = tr_frag(br, h);
-          acc[i] = Mma<bf16>::mma(af[h], bf, acc[i]);
-          if (i % 4 == kt)  // column sums: each tile by one of its four waves
-          {
-            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 0, 1), one2,
-                                                      ssum[i], false);
-            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 2, 3), one2,
-                                                      ssum[i], false);
-            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 4, 5), one2,
-                                                      ssum[i], false);
-            ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 6, 7), one2,
-                                                      ssum[i], false);
+      for (int t = 0; t < 3; ++t) {
+        const int i = min(i0 + t, LBG_TPW - 1);
+        const bool ok = i0 + t < nt_w;  // else a harmless read of the first tile
+        b[t] = (ok ? ba[i] : ba[i0]) + so;
+        bst[t] = 8 * (ok ? bp[i] : bp[i0]);
+      }
+      s16x4 br[12];
+      lbg_b_reads3(b, bst, br);
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        const int i = i0 + t;
+        if (i < LBG_TPW && i < nt_w) {
+          const s16x4 bt[4] = {br[4 * t], br[4 * t + 1], br[4 * t + 2], br[4 * t + 3]};
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const bf16x8 bf = tr_frag(bt, h);
+            acc[i] = Mma<bf16>::mma(af[h], bf, acc[i]);
+            if (i % 4 == kt)  // column sums: each tile by one of its four waves
+            {
+              ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 0, 1), one2,
+                                                        ssum[i], false);
+              ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 2, 3), one2,
+                                                        ssum[i], false);
+              ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 4, 5), one2,
+                                                        ssum[i], false);
+              ssum[i] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(bf, bf, 6, 7), one2,
+                                                        ssum[i], false);
+            }
           }
         }
       }
@@ -774,7 +933,11 @@ hipError_t launch_lnl_bwd(const LnlBwdArgs& a, hipStream_t s) {
   {
     KernelTimer t(K_LNL_BWD_DX, s);
     const int nwg = (int)std::min<int64_t>(256, (units + LBX_WAVES - 1) / LBX_WAVES);
-    hipLaunchKernelGGL(lnl_bwd_dx_kernel, dim3(nwg), dim3(64 * LBX_WAVES), 0, s, a);
+    const int nf = lbx_fast_steps(a);
+    if (nf >= LBX_AHEAD && lbx_steps(a) - nf <= LBX_SLOW_AHEAD)
+      hipLaunchKernelGGL(lnl_bwd_dx_kernel<true>, dim3(nwg), dim3(64 * LBX_WAVES), 0, s, a, nf);
+    else
+      hipLaunchKernelGGL(lnl_bwd_dx_kernel<false>, dim3(nwg), dim3(64 * LBX_WAVES), 0, s, a, nf);
   }
   {
     KernelTimer t(K_LNL_BWD_G, s);
