@@ -388,11 +388,11 @@ __device__ inline void lnl_quad_table(const int* start, int n_out, bf16* const* 
   }
 }
 
-// Steps [0, nf) of the fast-step stream: the 16-column steps of the leading
-// fast tiles, rounded down to a multiple of LBX_AHEAD (host side).
-// The dx kernel's 16-column steps: those holding a column below N.
+// The dx kernel's 16-column steps: those holding a column below N (host side).
 static int lbx_steps(const LnlBwdArgs& a) { return (a.ncols + 15) / 16; }
 
+// Steps [0, nf) of the fast-step stream: the 16-column steps of the leading
+// fast tiles, rounded down to a multiple of LBX_AHEAD (host side).
 static int lbx_fast_steps(const LnlBwdArgs& a) {
   const int nsteps = lbx_steps(a);
   int nt = 0;
@@ -445,9 +445,8 @@ __global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a
   uint32_t ao[4];
 #pragma unroll
   for (int s4 = 0; s4 < 4; ++s4) ao[s4] = lds_addr(wk) + lbx_w_off(wrow, 2 * s4 + g);
-  const int nsteps = (a.ncols + 15) / 16;  // steps past them multiply zeros
-  // fast steps: those of the leading fast tiles, a multiple of LBX_AHEAD
-  const int ns = nsteps - nf;  // the other steps
+  const int nsteps = (a.ncols + 15) / 16;  // as lbx_steps: later steps would multiply zeros
+  const int ns = nsteps - nf;              // the steps after the fast-step stream (nf: lbx_fast_steps)
   const int64_t units = (a.m + 31) / 32;
   const int64_t stride = (int64_t)gridDim.x * LBX_WAVES;
   const int64_t u0 = (int64_t)blockIdx.x * LBX_WAVES + wave;
@@ -561,8 +560,9 @@ __global__ __launch_bounds__(64 * LBX_WAVES) void lnl_bwd_dx_kernel(LnlBwdArgs a
         }
         pk[2 * kt + a2] = __builtin_bit_cast(u32x4, d);
       }
-    // The next unit's accumulators are zeroed before the stores are issued, so
-    // the stores' data never sits in registers written while they are in flight.
+    // The next unit's accumulators are zeroed (and tied) before the stores are
+    // issued, so the stores' data and the accumulators never share registers:
+    // no write to the accumulators has to wait for a store to read its data.
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) acc[kt] = f32x16{};
     asm volatile("" : "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]) : : "memory");
