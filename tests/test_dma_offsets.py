@@ -16,9 +16,14 @@ def s_pos(node, n, h):
     return h * D if node == 0 else n * h * D
 
 
+def s_row(node, n, h):
+    return n * h * D if node == 0 else h * D
+
+
 def max_offsets(node, n, h):
     """Largest lane byte offset of each DMA stream, per kernel."""
     sp = s_pos(node, n, h)
+    sr = s_row(node, n, h)
     nkt = (n + 31) // 32
     hb = (h - 1) * D  # head offset folded into the lane offset (dkdv, db)
     chunk = 8 * 3  # channel chunk 8 c, c <= 3
@@ -26,8 +31,10 @@ def max_offsets(node, n, h):
         # fwd_dma: K/V tile positions p < 32; bias tiles 0..3 of the query block
         "fwd_dma kv": (31 * sp + chunk) * 2,
         "fwd_dma bias": (3 * nkt * 1024 + 256 * 3) * 4 + 16 * 63,
-        # dq_dma: K/V tile positions p < 32; bias quarters of one tile
-        "dq_dma kv": (31 * sp + chunk) * 2,
+        # dq_dma: K/V tile positions p < 32; when one resource serves a wave's
+        # units, the second row of the group rides in the lane offset (one row
+        # stride, QD_ROWS = 2); bias quarters of one tile
+        "dq_dma kv": (31 * sp + chunk) * 2 + sr * 2,
         "dq_dma bias": 1024 * 3 + 16 * 63,
         # dkdv_dma: query tile positions p < 32 plus the head; bias tiles 0..3
         "dkdv_dma qda": (31 * sp + hb + chunk) * 2,
