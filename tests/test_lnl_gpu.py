@@ -110,10 +110,13 @@ def test_backward_full(m, cols):
     close("dbeta", db, rdb, row_sum=True)
 
 
-def test_backward_attention_inputs_n768_sampled_rows():
-    # the full launch at m = 768^2 with dO2 nonzero on a sample of rows only:
-    # the sums over rows then cover exactly those rows, and dx is zero elsewhere
-    m = 768 * 768
+@pytest.mark.parametrize("m", [768 * 768, 100003])
+def test_backward_attention_widths_sampled_rows(m):
+    # the full launch with dO2 nonzero on a sample of rows only: the sums over
+    # rows then cover exactly those rows, and dx is zero elsewhere.  m = 768^2
+    # is the pair representation at N = 768 (9 row units for every wave of
+    # the persistent dx kernel); m = 100003 gives the waves 1 or 2 units and
+    # a ragged last unit
     t = W.lnl_inputs(m, W.LNL_COLS, seed=7)
     rows = np.unique(np.concatenate([np.arange(0, 64), np.linspace(64, m - 65, 1900).astype(int),
                                      np.arange(m - 64, m)]))
