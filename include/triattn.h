@@ -293,6 +293,13 @@ const char* tri_attn_status_string(int status);
  * is calling the library.  Off by default. */
 int tri_attn_timing_enable(int on);
 
+/* Restricts the per-kernel timing to the kernels whose bit is set in `mask`
+ * (bit i: kernel i in tri_attn_timing_read's numbering); 0, the default,
+ * times every kernel.  Each timed launch records two events, which costs
+ * the stream a little time, so a benchmark can time only the kernel it
+ * needs.  Process-wide, like tri_attn_timing_enable.  Returns TRIATTN_OK. */
+int tri_attn_timing_select(uint64_t mask);
+
 /* Waits for the recorded events of kernel `index` (0, 1, ... in launch-site
  * order; TRIATTN_ERR_INVALID_ARG past the last one) and returns its name
  * (static string), the summed elapsed milliseconds and the launch count

@@ -72,6 +72,7 @@ def lib():
         L.tri_attn_status_string.argtypes = [_int]
         L.tri_attn_status_string.restype = ctypes.c_char_p
         L.tri_attn_timing_enable.argtypes = [_int]
+        L.tri_attn_timing_select.argtypes = [ctypes.c_uint64]
         L.tri_attn_timing_reset.argtypes = []
         L.tri_attn_timing_read.argtypes = [_int, ctypes.POINTER(ctypes.c_char_p),
                                            ctypes.POINTER(ctypes.c_double),
@@ -95,7 +96,7 @@ def lib():
             getattr(L, name).restype = _int
         for name in ("tri_attn_fwd_workspace_bytes", "tri_attn_bwd_workspace_bytes",
                      "tri_attn_fwd", "tri_attn_bwd", "tri_attn_timing_enable",
-                     "tri_attn_timing_reset", "tri_attn_timing_read",
+                     "tri_attn_timing_reset", "tri_attn_timing_read", "tri_attn_timing_select",
                      "tri_ln_linear_fwd", "tri_ln_linear_bwd_workspace_bytes",
                      "tri_ln_linear_bwd", "tri_attn_rows_fwd_workspace_bytes",
                      "tri_attn_rows_bwd_workspace_bytes", "tri_attn_rows_fwd",
@@ -286,6 +287,27 @@ def tri_attn_timing_enable(on: bool) -> None:
     st = lib().tri_attn_timing_enable(1 if on else 0)
     if st != OK:
         raise TriAttnError(st, "tri_attn_timing_enable")
+
+
+def tri_attn_timing_select(names=None) -> None:
+    """Time only the kernels named in `names` (None: every kernel)."""
+    mask = 0
+    if names is not None:
+        index = {}
+        i = 0
+        while True:
+            r = tri_attn_timing_read(i)
+            if r is None:
+                break
+            index[r[0]] = i
+            i += 1
+        for n in names:
+            if n not in index:
+                raise ValueError(f"unknown kernel name {n!r}")
+            mask |= 1 << index[n]
+    st = lib().tri_attn_timing_select(mask)
+    if st != OK:
+        raise TriAttnError(st, "tri_attn_timing_select")
 
 
 def tri_attn_timing_reset() -> None:

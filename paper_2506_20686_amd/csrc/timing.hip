@@ -29,6 +29,7 @@ struct Pending {
 struct State {
   std::mutex mu;
   bool on = false;
+  uint64_t mask = 0;  // kernels timed (bit per KernelId); 0: all
   std::vector<hipEvent_t> pool;  // created events not in use
   std::vector<Pending> pending;  // recorded, not yet read
   double ms[K_COUNT] = {};
@@ -67,7 +68,7 @@ void drain(State& s) {
 
 KernelTimer::KernelTimer(KernelId id, hipStream_t stream) : id_(id), stream_(stream) {
   State& s = st();
-  if (!s.on) return;
+  if (!s.on || (s.mask != 0 && !((s.mask >> id) & 1u))) return;
   std::lock_guard<std::mutex> lock(s.mu);
   if (!take(s, &a_) || !take(s, &b_) || hipEventRecord(a_, stream_) != hipSuccess) {
     s.status = TRIATTN_ERR_HIP;
@@ -96,6 +97,13 @@ int tri_attn_timing_enable(int on) {
   triattn::State& s = triattn::st();
   std::lock_guard<std::mutex> lock(s.mu);
   s.on = on != 0;
+  return TRIATTN_OK;
+}
+
+int tri_attn_timing_select(uint64_t mask) {
+  triattn::State& s = triattn::st();
+  std::lock_guard<std::mutex> lock(s.mu);
+  s.mask = mask;
   return TRIATTN_OK;
 }
 
