@@ -438,13 +438,13 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
   }
   // When the units of every wave come from one source (the K rows, the V rows
   // or one bias tile, of one channel half), one walking resource serves a
-  // wave's units, the rows told apart by their lane offsets.  Otherwise each
-  // unit walks its own.
+  // wave's units, the rows told apart by their lane offsets.  Otherwise (64
+  // channels: six units from two sources per wave) each unit's pointer moves
+  // and its resource is rebuilt per tile: six walking resources held in
+  // scalar registers outgrow them (the spills cost dQ 14% at 64 channels).
   constexpr bool ONE = L::one_source();
-  constexpr int NW = ONE ? 1 : QD_OPS;
-  Walk wk[NW];
-#pragma unroll
-  for (int j = 0; j < NW; ++j) wk[j] = Walk(src[j], srcend[j], adv[j]);
+  Walk wk[1];
+  if constexpr (ONE) wk[0] = Walk(src[0], srcend[0], adv[0]);
   if constexpr (ONE) {
 #pragma unroll
     for (int j = 1; j < QD_OPS; ++j)
@@ -464,8 +464,11 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
     } else {
 #pragma unroll
       for (int j = 0; j < QD_OPS; ++j) {
-        if (dok[j]) dma16b(wk[j].rsrc(real), voff[j], dst[j] + slot * L::SLOT);
-        wk[j].advance();
+        // records from the unit's pointer to its tensor's end (capped at 2^32 - 1)
+        const uint64_t len = real ? (uint64_t)((const char*)srcend[j] - (const char*)src[j]) : 0u;
+        const rsrc_t rs = buf_rsrc_n(src[j], (len >> 32) != 0 ? 0xffffffffu : (uint32_t)len);
+        if (dok[j]) dma16b(rs, voff[j], dst[j] + slot * L::SLOT);
+        if (real) src[j] = (const char*)src[j] + adv[j];
       }
     }
     ++issued;
