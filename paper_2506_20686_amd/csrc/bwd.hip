@@ -830,6 +830,14 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   // or -D (waves 12-15), 128 bytes per wave (lanes 0..7).
   const int r0 = rc * a.rpc, r1 = min(G.nr, r0 + a.rpc);
   const int nr = max(r1 - r0, 0);
+  // One workgroup per CU: a dispatch round is 256 workgroups.  Alternate
+  // rounds walk their chunk's rows in opposite directions, so that a
+  // workgroup starts on the rows that the previous round on its XCD ended
+  // on, while those are still in the L2.  (The direction depends on the
+  // block index only: results stay bitwise reproducible.)
+  const bool back = ((blockIdx.x >> 8) & 1u) != 0u;
+  const int rfirst = back ? r1 - 1 : r0;
+  const int64_t rdir = back ? -1 : 1;
   const int64_t tensor = (int64_t)G.nr * G.n * G.H * D;
   const int hb = h * D;
   const int pp = 16 * (wave & 7) + (lane >> 2);  // position (key or query) of this lane
@@ -855,30 +863,34 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   // with record counts fixed for the loop (see last_row_records; the lse2 /
   // -D rows are whole rows of np floats).
   const int64_t lastr = max(G.nr - 1 - r0, 0);
-  const char* b0 = (const char*)(src0 + (int64_t)r0 * G.sRow + koff);
-  const char* b1 = (const char*)(src1 + (int64_t)r0 * G.sRow + qoff);
-  const char* b2 = lo_op ? (const char*)(a.dalo + (int64_t)r0 * G.sRow + qoff)
-                         : (const char*)(lrow + (int64_t)r0 * G.np);
+  const char* const c0 = (const char*)(src0 + (int64_t)r0 * G.sRow + koff);
+  const char* const c1r = (const char*)(src1 + (int64_t)r0 * G.sRow + qoff);
+  const char* const c2 = lo_op ? (const char*)(a.dalo + (int64_t)r0 * G.sRow + qoff)
+                               : (const char*)(lrow + (int64_t)r0 * G.np);
   const int64_t rs = G.sRow * 2, rs2 = lo_op ? rs : (int64_t)G.np * 4;  // bytes per row
-  const uint32_t n0 = last_row_records(b0 + lastr * rs, src0 + tensor);
-  const uint32_t n1 = last_row_records(b1 + lastr * rs, src1 + tensor);
-  const uint32_t n2 = lo_op ? last_row_records(b2 + lastr * rs, a.dalo + tensor)
+  const uint32_t n0 = last_row_records(c0 + lastr * rs, src0 + tensor);
+  const uint32_t n1 = last_row_records(c1r + lastr * rs, src1 + tensor);
+  const uint32_t n2 = lo_op ? last_row_records(c2 + lastr * rs, a.dalo + tensor)
                             : (uint32_t)G.np * 4;
   const bool op2 = lo_op ? pok : lane < 8;
-  int next = r0;  // the row the next issue copies
+  // op bases at the walk's first row, moved one row per issue
+  const char* b0 = c0 + (int64_t)(rfirst - r0) * rs;
+  const char* b1 = c1r + (int64_t)(rfirst - r0) * rs;
+  const char* b2 = c2 + (int64_t)(rfirst - r0) * rs2;
+  int issued = 0;
   auto issue = [&](int slot) {
-    // rows past the chunk copy nothing (empty resources) but keep the wait
-    // counts uniform
-    const bool real = next < r1;
+    // issues past the chunk's rows copy nothing (empty resources, based on
+    // the chunk's first row) but keep the wait counts uniform
+    const bool real = issued < nr;
     if (pok) {
-      dma16b(buf_rsrc_n(b0, real ? n0 : 0u), voff, dst0 + slot * DBD_SLOT);
-      dma16b(buf_rsrc_n(b1, real ? n1 : 0u), voff, dst1 + slot * DBD_SLOT);
+      dma16b(real ? buf_rsrc_n(b0, n0) : buf_rsrc_n(c0, 0u), voff, dst0 + slot * DBD_SLOT);
+      dma16b(real ? buf_rsrc_n(b1, n1) : buf_rsrc_n(c1r, 0u), voff, dst1 + slot * DBD_SLOT);
     }
-    if (op2) dma16b(buf_rsrc_n(b2, real ? n2 : 0u), voff2, dst2 + slot * DBD_SLOT);
-    b0 += rs;
-    b1 += rs;
-    b2 += rs2;
-    ++next;
+    if (op2) dma16b(real ? buf_rsrc_n(b2, n2) : buf_rsrc_n(c2, 0u), voff2, dst2 + slot * DBD_SLOT);
+    b0 += rdir * rs;
+    b1 += rdir * rs;
+    b2 += rdir * rs2;
+    ++issued;
   };
 
   // ---- LDS read addresses (slot 0)
@@ -966,11 +978,11 @@ __global__ __launch_bounds__(1024) void db_dma_kernel(BwdArgs<bf16> a, int nkb) 
   issue(1);
   auto run = [&](auto full_c) {
     for (int i = 0; i < nr; i += DBD_SLOTS) {
-      step(r0 + i, slot_c<0>{}, full_c);
+      step(rfirst + (int)rdir * i, slot_c<0>{}, full_c);
       if (i + 1 >= nr) break;
-      step(r0 + i + 1, slot_c<1>{}, full_c);
+      step(rfirst + (int)rdir * (i + 1), slot_c<1>{}, full_c);
       if (i + 2 >= nr) break;
-      step(r0 + i + 2, slot_c<2>{}, full_c);
+      step(rfirst + (int)rdir * (i + 2), slot_c<2>{}, full_c);
     }
   };
   if (rows_full)
