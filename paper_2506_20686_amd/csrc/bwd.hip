@@ -441,7 +441,7 @@ __global__ __launch_bounds__(64 * QD_WAVES) __attribute__((amdgpu_waves_per_eu(Q
   // wave's units, the rows told apart by their lane offsets.  Otherwise (64
   // channels: six units from two sources per wave) each unit's pointer moves
   // and its resource is rebuilt per tile: six walking resources held in
-  // scalar registers outgrow them (the spills cost dQ 14% at 64 channels).
+  // scalar registers outgrow them (their spills cost dQ about 10% at 64 channels).
   constexpr bool ONE = L::one_source();
   Walk wk[1];
   if constexpr (ONE) wk[0] = Walk(src[0], srcend[0], adv[0]);
