@@ -214,6 +214,24 @@ def test_workload_dbias_block(node):
     close("dbias", grads[4], rg[4], w.dtype, bsel)
 
 
+@pytest.mark.parametrize("node", [B.STARTING, B.ENDING])
+def test_dbias_many_workgroup_rounds(node):
+    """n = 257 with 32 heads: the bias-gradient kernel runs at least
+    3 x 3 x 32 = 288 workgroups of 128 x 128, more than one per CU, so
+    workgroups of later dispatch rounds (which walk their chunk's rows in the
+    opposite direction) contribute.  Every fourth query of one 128-query
+    block against the oracle, summed over all rows."""
+    n, h = 257, 32
+    t = inputs(n, h, torch.bfloat16, seed=7301 + node, mask_kind="random")
+    print(f"\n[dbias rounds node={node} n={n} h={h}]", flush=True)
+    out, lse, grads = run_gpu(t, node)
+    qs = list(range(128, 256, 4))
+    rg = oracle.bwd(node, t["q"], t["k"], t["v"], t["g"], t["bias"], t["dout"], t["mask"],
+                    rows=[], db_queries=qs)
+    bsel = (qs,) if node == B.STARTING else (slice(None), qs)
+    close("dbias", grads[4], rg[4], torch.bfloat16, bsel)
+
+
 # ---- properties that hold at any size ----------------------------------------------
 
 @pytest.mark.parametrize("name,node", [("tri_start_bf16_n256_pad10", B.STARTING),
