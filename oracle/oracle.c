@@ -8,7 +8,7 @@
  *
  * What it computes (MegaFold, arXiv 2506.20686):
  *   - 3D attention over the pair representation, Section IV-A and the
- *     EvoAttention table in the appendix ("Computations of EvoAttention"):
+ *     appendix table that lists EvoAttention's computations:
  *       S = Q K^T + Bias (bias broadcast over the pair-row axis),
  *       P = softmax(S) over the keys,  A = P V.
  *     The method (online softmax, Section IV-A) reaches this exact result,
