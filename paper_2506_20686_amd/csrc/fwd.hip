@@ -40,6 +40,21 @@ namespace triattn {
 // one head at a time: the block goes through LDS once and leaves as bt tile
 // (qa, kb) and btT tile (kb, qa), both written 16 bytes per thread.
 template <typename T>
+__device__ inline void load_heads4(const T* p, float (&x)[4]);
+template <>
+__device__ inline void load_heads4(const bf16* p, float (&x)[4]) {
+  const bf16x4 v = *(const bf16x4*)p;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = (float)v[j];
+}
+template <>
+__device__ inline void load_heads4(const float* p, float (&x)[4]) {
+  const f32x4 v = *(const f32x4*)p;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = v[j];
+}
+
+template <typename T>
 __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const T* bias,
                                                         float* bt, float* btT) {
   bias = at_sample(bias, G.bBias);
@@ -48,31 +63,50 @@ __global__ __launch_bounds__(256) void prep_bias_kernel(Geom G, int node, const 
   const int nt = G.nkt, n = G.n;
   const int qa = blockIdx.x % nt, kb = blockIdx.x / nt;
   const int tid = threadIdx.x;
-  __shared__ float tl[32][33];  // [query][key] of one head: bias / scale
-  // loads: query r, keys c0 .. c0 + 3 of the block
+  constexpr int HG = 4;  // heads per pass through LDS
+  __shared__ float tl[HG][32][33];  // [head][query][key] of HG heads: bias / scale
+  // loads: query r, keys c0 .. c0 + 3 of the block, HG heads each (one
+  // vector load per key when the head count is a multiple of HG)
   const int r = tid >> 3, c0 = 4 * (tid & 7);
   const int q = 32 * qa + r;
+  const bool vec = G.H % HG == 0;
   // stores: element 4 tid .. 4 tid + 3 of a tile (j = tid / 64, l = tid % 64)
   const int l = tid & 63, x = l & 31, y0 = 8 * (tid >> 6) + 4 * (l >> 5);
-  for (int h = 0; h < G.H; ++h) {
-    float v[4];
+  for (int h0 = 0; h0 < G.H; h0 += HG) {
+    const int hn = min(HG, G.H - h0);
+    float v[4][HG];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int k = 32 * kb + c0 + e;
       const int qc = min(q, n - 1), kc = min(k, n - 1);  // in bounds; zero outside the map
-      const int64_t at = node == 0 ? ((int64_t)qc * n + kc) * G.H + h : ((int64_t)kc * n + qc) * G.H + h;
-      const float b = (float)bias[at];
-      v[e] = q < n && k < n ? b : 0.f;
-    }
-    __syncthreads();  // the previous head's tile has been read
+      const int64_t at = (node == 0 ? (int64_t)qc * n + kc : (int64_t)kc * n + qc) * G.H + h0;
+      if (vec) {
+        load_heads4(bias + at, v[e]);
+      } else {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) tl[r][c0 + e] = v[e] / G.scale;
+        for (int j = 0; j < HG; ++j) v[e][j] = j < hn ? (float)bias[at + j] : 0.f;
+      }
+      if (!(q < n && k < n)) {
+#pragma unroll
+        for (int j = 0; j < HG; ++j) v[e][j] = 0.f;
+      }
+    }
+    __syncthreads();  // the previous heads' tiles have been read
+#pragma unroll
+    for (int j = 0; j < HG; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tl[j][r][c0 + e] = v[e][j] / G.scale;
     __syncthreads();
-    const f32x4 o = {tl[x][y0], tl[x][y0 + 1], tl[x][y0 + 2], tl[x][y0 + 3]};
-    *(f32x4*)(bt + (((int64_t)h * nt + qa) * nt + kb) * 1024 + 4 * tid) = o;
-    if (btT) {
-      const f32x4 p = {tl[y0][x], tl[y0 + 1][x], tl[y0 + 2][x], tl[y0 + 3][x]};
-      *(f32x4*)(btT + (((int64_t)h * nt + kb) * nt + qa) * 1024 + 4 * tid) = p;
+#pragma unroll
+    for (int j = 0; j < HG; ++j) {
+      if (j >= hn) break;
+      const int h = h0 + j;
+      const f32x4 o = {tl[j][x][y0], tl[j][x][y0 + 1], tl[j][x][y0 + 2], tl[j][x][y0 + 3]};
+      *(f32x4*)(bt + (((int64_t)h * nt + qa) * nt + kb) * 1024 + 4 * tid) = o;
+      if (btT) {
+        const f32x4 p = {tl[j][y0][x], tl[j][y0 + 1][x], tl[j][y0 + 2][x], tl[j][y0 + 3][x]};
+        *(f32x4*)(btT + (((int64_t)h * nt + kb) * nt + qa) * 1024 + 4 * tid) = p;
+      }
     }
   }
 }
